@@ -1,0 +1,170 @@
+/*
+ * cr.h -- C ABI of the CacheRoute planner and shadow-replay library (libcr.so, gfx950).
+ *
+ * The library computes, on one MI355X GPU, the data-parallel core of the periodic
+ * routing planner of "CacheRoute: Planned Prefix-Affinity Routing for Large-Scale
+ * LLM Serving" (Section 3.1, Eq. 1, Algorithm 1; Section 3.2) and a shadow replay
+ * of the resulting routing against per-destination prefix caches.
+ *
+ * Conventions for every entry point:
+ *  - Buffers are DEVICE pointers owned by the caller unless marked "host".
+ *  - A call validates its scalar arguments on the host, enqueues kernels on `stream`
+ *    (a hipStream_t passed as void*; NULL = the default stream) and returns. It
+ *    never allocates, frees or synchronises, and keeps no state between calls.
+ *    Calls are thread-compatible: concurrent calls must not share output buffers.
+ *  - Return value: CR_OK, or a negative cr_status. On a negative status nothing
+ *    has been enqueued.
+ *  - Data-dependent problems found on the device (a key >= num_keys, a destination
+ *    >= R, an inconsistent plan spec) never abort a kernel: the offending item is
+ *    skipped as documented per call, and a CR_ERR_* bit is OR-ed into the caller's
+ *    device word `err` (which the caller clears).
+ *  - Keys are dense ids in [0, num_keys); 0xFFFFFFFF is reserved (empty slot).
+ *  - Request i of a stream has global index first_index + i; control intervals are
+ *    given by device offsets off[0..J] with off[0] = 0, off[J] = n, non-decreasing.
+ */
+#ifndef CR_H
+#define CR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t cr_status;
+#define CR_OK 0
+#define CR_EINVAL (-1) /* an argument is out of range or a pointer is NULL   */
+#define CR_ESIZE (-2)  /* the workspace is smaller than the size query says   */
+#define CR_EHIP (-3)   /* a HIP launch or runtime call failed                 */
+
+#define CR_ERR_KEY_RANGE 1u   /* a key >= num_keys was seen                       */
+#define CR_ERR_DEST_RANGE 2u  /* a destination >= R was seen by the replay        */
+#define CR_ERR_SPEC 4u        /* a plan spec disagrees with its counts row         */
+
+#define CR_EMPTY_SLOT 0xFFFFFFFFu /* unused LRU slot / unused key               */
+#define CR_ROUTE_COLD 0xFFFFFFFFu /* route word of a key that is not admitted    */
+#define CR_ROUTE_SINGLE 0x80000000u /* route word flag: k = 1, low 16 bits = dest */
+
+#define CR_MAX_R 1024      /* destinations per plan                            */
+#define CR_MAX_W 512       /* warm slots per destination                       */
+#define CR_MAX_CANDS 256   /* candidate plans per group                        */
+#define CR_MAX_J 65535     /* control intervals per cr_replay call             */
+
+/* One plan problem (Algorithm 1 inputs: rates, R, q_cap, C). Arrays of these live in
+ * DEVICE memory. q_cap = q_num / q_den requests per window, so Eq. 1 is evaluated as
+ * k = max(1, ceil(c * q_den / q_num)) in exact integers; k is clamped to R. */
+typedef struct {
+    uint32_t window;   /* row of counts the plan is built from (< num_windows)      */
+    uint32_t W;        /* warm slots per destination, 1..max_W; C = R * W           */
+    uint64_t n_window; /* requests in that row (its sum)                            */
+    uint64_t q_num;    /* > 0 unless n_window == 0                                  */
+    uint64_t q_den;    /* 1 .. 2^31 - 1                                             */
+} cr_plan_spec;
+
+/* A set of NP plans arranged as NG groups of `cands` candidates: plan p = g*cands + c.
+ * Every plan of group g routes the same requests; the route table is key-major within
+ * a group so one request reads one contiguous row of `cands` words.
+ * Host struct of device pointers; sizes follow from the fields (C_max = R * max_W):
+ *   order      u32 [num_windows][C_max]  nonzero keys by (count desc, key asc), cut at C_max
+ *   n_order    u32 [num_windows]         entries of order used
+ *   num_admitted u32 [NP]                A
+ *   cold       u64 [NP]                  window requests not carried by admitted keys
+ *   clamped    u32 [NP]                  admitted keys whose k was clamped to R
+ *   member_off u32 [NP][C_max + 1]       member list a = members[off[a] .. off[a+1])
+ *   members    u16 [NP][C_max]           T(b) per admitted key, in selection order
+ *   load       f64 [NP][R]               planned loads L after placement
+ *   route      u32 [NG][num_keys][cands] route words: CR_ROUTE_COLD,
+ *                                        CR_ROUTE_SINGLE | dest, or admission index a */
+typedef struct {
+    uint32_t num_plans;   /* NP = NG * cands                                       */
+    uint32_t cands;       /* candidates per group, 1..CR_MAX_CANDS                 */
+    uint32_t R;           /* destinations, 1..CR_MAX_R                             */
+    uint32_t max_W;       /* >= every spec's W, <= CR_MAX_W                        */
+    uint32_t num_keys;    /* K                                                     */
+    uint32_t num_windows; /* rows of counts                                        */
+    const cr_plan_spec* specs; /* [NP]                                             */
+    uint32_t* order;
+    uint32_t* n_order;
+    uint32_t* num_admitted;
+    uint64_t* cold;
+    uint32_t* clamped;
+    uint32_t* member_off;
+    uint16_t* members;
+    double* load;
+    uint32_t* route;
+} cr_plan_set;
+
+/* Rates per key per control interval (Algorithm 1 input "rates"; Appendix A.2: the
+ * planner needs only {(b, lambda_b)}). Rates are kept in requests per window.
+ *   counts[j * num_keys + b] += #{ i in [off[j], off[j+1]) : keys[i] == b }
+ * keys u32 [n]; off u64 [J+1]; counts u32 [J][num_keys] (accumulated, caller zeroes).
+ * A key >= num_keys is not counted and sets CR_ERR_KEY_RANGE. */
+cr_status cr_count_rates(const uint32_t* keys, uint64_t n, const uint64_t* off, uint32_t J,
+                         uint32_t num_keys, uint32_t* counts, uint32_t* err, void* stream);
+
+/* Workspace for cr_admit, in bytes. */
+size_t cr_admit_workspace_bytes(uint32_t num_windows, uint32_t R, uint32_t max_W);
+
+/* Top-rate admission (Eq. 1; Section 3.1 "Warm-set admission"; Algorithm 1 sort/admit).
+ * For every window: order its nonzero keys by (count desc, key asc), cut at C_max.
+ * For every plan: k_b by Eq. 1 (exact integers, clamped to R), then admit the longest
+ * prefix of that order whose k_b sum is <= C = R * W; cold = n_window - admitted counts.
+ * counts u32 [num_windows][num_keys]. Writes order, n_order, num_admitted, cold,
+ * clamped and member_off[0..A] (prefix sums of k). A spec with a window out of range,
+ * q_num == 0 on a nonempty window, or n_window != row sum sets CR_ERR_SPEC (the plan
+ * then admits nothing). */
+cr_status cr_admit(const uint32_t* counts, const cr_plan_set* plans, void* ws, size_t ws_bytes,
+                   uint32_t* err, void* stream);
+
+/* LPT placement (Section 3.1 "Placement and dispatch"; Algorithm 1 placement loop).
+ * Per plan: L[r] = cold / R; admitted keys in admission order take the k smallest
+ * (L[r], r) destinations, listed in that order, each charged count / k (IEEE double,
+ * one rounding per operation, the same order as the definition). Writes members,
+ * load and the whole route table (cold words first, then admitted keys). */
+cr_status cr_place_lpt(const uint32_t* counts, const cr_plan_set* plans, void* stream);
+
+/* Dispatch (Section 3.1 "Placement and dispatch"; Fig. 1), order-independent form.
+ * Request i lies in interval j and uses plan group gmap[j]; for candidate c:
+ *   h = fmix32((u32)g ^ fmix32((u32)(g >> 32) ^ s)), g = first_index + i,
+ *   s = fmix32((u32)seed ^ (u32)(seed >> 32) ^ 0x9E3779B9) (fmix32 = MurmurHash3's finalizer);
+ *   admitted key with members M (k of them): dest = M[((h >> 16) * k) >> 16];
+ *   otherwise d1 = ((h & 0xFFFF) * R) >> 16, d2 = ((h >> 16) * R) >> 16 and
+ *   dest = L[d2] < L[d1] ? d2 : d1 with L the plan's loads (power of two choices).
+ * keys u32 [n]; off u64 [J+1]; gmap u32 [J] (< NG); dest u16 [cands][n].
+ * A key >= num_keys is routed as cold and sets CR_ERR_KEY_RANGE. */
+cr_status cr_route(const uint32_t* keys, uint64_t n, uint64_t first_index, uint64_t seed,
+                   const uint64_t* off, const uint32_t* gmap, uint32_t J, const cr_plan_set* plans,
+                   uint16_t* dest, uint32_t* err, void* stream);
+
+/* Workspace for cr_replay, in bytes. */
+size_t cr_replay_workspace_bytes(uint64_t n, uint32_t P, uint32_t R);
+
+/* Shadow replay (Section 3.2: admitted and cold prefixes share each destination's
+ * cache) against an LRU of W_c whole-prefix slots per destination (the equal-slot model
+ * of Section 3.1), for P candidate routings of the same stream at once.
+ * For candidate c, destination d, requests in arrival order:
+ *   requests += 1; prefill += suffix[i];
+ *   key cached: hits += 1; hit_prefix += prefix_len[key]; key becomes most recent;
+ *   otherwise:  prefill += prefix_len[key]; key inserted as most recent, the least
+ *               recent dropped once W_c would be exceeded.
+ * keys u32 [n]; suffix u16 [n]; prefix_len u32 [num_keys]; dest u16 [P][n]; off u64 [J+1];
+ * W host u32 [P] (1..CR_MAX_W); lru_in / lru_out u32 [P][R][max_W]: carried cache state,
+ * most recent first, CR_EMPTY_SLOT after the used entries (lru_in NULL = all empty;
+ * lru_in and lru_out must not overlap); stats u64 [J][P][R][4] (accumulated) =
+ * {requests, hits, prefill_tokens, hit_prefix_tokens}.
+ * A destination >= R sets CR_ERR_DEST_RANGE and a key >= num_keys sets CR_ERR_KEY_RANGE;
+ * such requests are skipped. */
+cr_status cr_replay(const uint32_t* keys, const uint16_t* suffix, const uint32_t* prefix_len,
+                    uint32_t num_keys, const uint16_t* dest, uint64_t n, const uint64_t* off,
+                    uint32_t J, uint32_t P, uint32_t R, const uint32_t* W, uint32_t max_W,
+                    const uint32_t* lru_in, uint32_t* lru_out, uint64_t* stats, void* ws,
+                    size_t ws_bytes, uint32_t* err, void* stream);
+
+/* Library version string. */
+const char* cr_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* CR_H */

@@ -1,0 +1,163 @@
+"""ctypes binding of libcr.so with the C ABI's names (argument marshalling only).
+
+Every function takes torch tensors that already live on the GPU (device memory and
+the current stream come from PyTorch) and passes their raw pointers to the library.
+Integer buffers use torch's signed dtypes of the same width; the library reads them
+as the unsigned types of the header. Nothing here computes any step of the path, and
+there is no fallback: without the built library every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import torch
+
+from .build import LIB
+
+CR_OK, CR_EINVAL, CR_ESIZE, CR_EHIP = 0, -1, -2, -3
+CR_ERR_KEY_RANGE, CR_ERR_DEST_RANGE, CR_ERR_SPEC = 1, 2, 4
+CR_EMPTY_SLOT = 0xFFFFFFFF
+CR_ROUTE_COLD = 0xFFFFFFFF
+CR_ROUTE_SINGLE = 0x80000000
+CR_MAX_R, CR_MAX_W, CR_MAX_CANDS, CR_MAX_J = 1024, 512, 256, 65535
+
+EXPORTS = ("cr_count_rates", "cr_admit_workspace_bytes", "cr_admit", "cr_place_lpt", "cr_route",
+           "cr_replay_workspace_bytes", "cr_replay", "cr_version")
+
+_u32, _u64, _P = ctypes.c_uint32, ctypes.c_uint64, ctypes.c_void_p
+
+
+class CrPlanSpec(ctypes.Structure):
+    _fields_ = [("window", _u32), ("W", _u32), ("n_window", _u64), ("q_num", _u64), ("q_den", _u64)]
+
+
+class CrPlanSet(ctypes.Structure):
+    _fields_ = [("num_plans", _u32), ("cands", _u32), ("R", _u32), ("max_W", _u32), ("num_keys", _u32),
+                ("num_windows", _u32), ("specs", _P), ("order", _P), ("n_order", _P), ("num_admitted", _P),
+                ("cold", _P), ("clamped", _P), ("member_off", _P), ("members", _P), ("load", _P), ("route", _P)]
+
+
+class CrError(RuntimeError):
+    pass
+
+
+_lib = None
+
+
+def load(path: Optional[str] = None):
+    """Load libcr.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    p = path or LIB
+    if not os.path.exists(p):
+        raise CrError(f"{p} is missing: build it with paper_2608_19677_amd/build.py (no fallback exists)")
+    L = ctypes.CDLL(p)
+    L.cr_count_rates.argtypes = [_P, _u64, _P, _u32, _u32, _P, _P, _P]
+    L.cr_admit_workspace_bytes.argtypes = [_u32, _u32, _u32]
+    L.cr_admit_workspace_bytes.restype = ctypes.c_size_t
+    L.cr_admit.argtypes = [_P, ctypes.POINTER(CrPlanSet), _P, ctypes.c_size_t, _P, _P]
+    L.cr_place_lpt.argtypes = [_P, ctypes.POINTER(CrPlanSet), _P]
+    L.cr_route.argtypes = [_P, _u64, _u64, _u64, _P, _P, _u32, ctypes.POINTER(CrPlanSet), _P, _P, _P]
+    L.cr_replay_workspace_bytes.argtypes = [_u64, _u32, _u32]
+    L.cr_replay_workspace_bytes.restype = ctypes.c_size_t
+    L.cr_replay.argtypes = [_P, _P, _P, _u32, _P, _u64, _P, _u32, _u32, _u32, ctypes.POINTER(_u32), _u32, _P, _P,
+                            _P, _P, ctypes.c_size_t, _P, _P]
+    L.cr_version.restype = ctypes.c_char_p
+    for f in ("cr_count_rates", "cr_admit", "cr_place_lpt", "cr_route", "cr_replay"):
+        getattr(L, f).restype = ctypes.c_int32
+    _lib = L
+    return L
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise CrError("libcr takes device tensors")
+    if not t.is_contiguous():
+        raise CrError("libcr takes contiguous tensors")
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+def _check(rc: int, name: str):
+    if rc != CR_OK:
+        raise CrError(f"{name} returned {rc}")
+
+
+def cr_version() -> str:
+    return load().cr_version().decode()
+
+
+def cr_count_rates(keys, off, J: int, num_keys: int, counts, err, stream=None, n: Optional[int] = None):
+    n = keys.numel() if n is None else n
+    _check(load().cr_count_rates(_ptr(keys), n, _ptr(off), J, num_keys, _ptr(counts), _ptr(err), _stream(stream)),
+           "cr_count_rates")
+
+
+def cr_admit_workspace_bytes(num_windows: int, R: int, max_W: int) -> int:
+    return int(load().cr_admit_workspace_bytes(num_windows, R, max_W))
+
+
+def cr_admit(counts, plans: CrPlanSet, ws, err, stream=None):
+    _check(load().cr_admit(_ptr(counts), ctypes.byref(plans), _ptr(ws), ws.numel() * ws.element_size(), _ptr(err),
+                           _stream(stream)), "cr_admit")
+
+
+def cr_place_lpt(counts, plans: CrPlanSet, stream=None):
+    _check(load().cr_place_lpt(_ptr(counts), ctypes.byref(plans), _stream(stream)), "cr_place_lpt")
+
+
+def cr_route(keys, first_index: int, seed: int, off, gmap, J: int, plans: CrPlanSet, dest, err, stream=None,
+             n: Optional[int] = None):
+    n = keys.numel() if n is None else n
+    _check(load().cr_route(_ptr(keys), n, first_index, seed, _ptr(off), _ptr(gmap), J, ctypes.byref(plans),
+                           _ptr(dest), _ptr(err), _stream(stream)), "cr_route")
+
+
+def cr_replay_workspace_bytes(n: int, P: int, R: int) -> int:
+    return int(load().cr_replay_workspace_bytes(n, P, R))
+
+
+def cr_replay(keys, suffix, prefix_len, num_keys: int, dest, off, J: int, P: int, R: int, W: Sequence[int],
+              max_W: int, lru_in, lru_out, stats, ws, err, stream=None, n: Optional[int] = None):
+    n = keys.numel() if n is None else n
+    Wa = (_u32 * len(W))(*[int(x) for x in W])
+    _check(load().cr_replay(_ptr(keys), _ptr(suffix), _ptr(prefix_len), num_keys, _ptr(dest), n, _ptr(off), J, P, R,
+                            Wa, max_W, _ptr(lru_in), _ptr(lru_out), _ptr(stats), _ptr(ws),
+                            ws.numel() * ws.element_size(), _ptr(err), _stream(stream)), "cr_replay")
+
+
+class PlanSet:
+    """Device buffers of a cr_plan_set (NP = NG * cands plans over num_windows rows)."""
+
+    def __init__(self, specs, cands: int, R: int, max_W: int, num_keys: int, num_windows: int, device):
+        self.num_plans = len(specs)
+        self.cands, self.R, self.max_W, self.num_keys, self.num_windows = cands, R, max_W, num_keys, num_windows
+        cmax = R * max_W
+        self.cmax = cmax
+        NP, NW = self.num_plans, num_windows
+        ng = NP // cands
+        raw = (CrPlanSpec * NP)(*[CrPlanSpec(*s) for s in specs])
+        host = torch.frombuffer(bytearray(bytes(raw)), dtype=torch.uint8)
+        self.specs = host.to(device)
+        i32 = dict(dtype=torch.int32, device=device)
+        self.order = torch.empty((NW, cmax), **i32)
+        self.n_order = torch.empty(NW, **i32)
+        self.num_admitted = torch.empty(NP, **i32)
+        self.cold = torch.empty(NP, dtype=torch.int64, device=device)
+        self.clamped = torch.empty(NP, **i32)
+        self.member_off = torch.empty((NP, cmax + 1), **i32)
+        self.members = torch.empty((NP, cmax), dtype=torch.int16, device=device)
+        self.load = torch.empty((NP, R), dtype=torch.float64, device=device)
+        self.route = torch.empty((ng, num_keys, cands), **i32)
+        self.c = CrPlanSet(NP, cands, R, max_W, num_keys, NW, _ptr(self.specs), _ptr(self.order), _ptr(self.n_order),
+                           _ptr(self.num_admitted), _ptr(self.cold), _ptr(self.clamped), _ptr(self.member_off),
+                           _ptr(self.members), _ptr(self.load), _ptr(self.route))

@@ -1,0 +1,441 @@
+// Plan build: top-rate admission (Eq. 1; Section 3.1 "Warm-set admission"; Algorithm 1)
+// and LPT placement (Section 3.1 "Placement and dispatch"; Algorithm 1 placement loop).
+//
+// Admission is split in two so that every candidate plan built from the same window
+// shares one sort:
+//   k_sort_window  one block per window: radix-select the C_max-th largest count, compact
+//                  the keys at or above it in key order, and stable-LSD-radix-sort them by
+//                  count (descending), which yields (count desc, key asc) exactly;
+//   k_admit_plan   one block per plan: k by Eq. 1 in exact integers, block prefix sum of
+//                  k, and the longest prefix whose sum fits C = R * W.
+// LPT is a dependency chain of sum(k) steps per plan; one wavefront owns one plan and
+// keeps the R loads in registers (lane l holds destinations l, l+64, ...), so each pick
+// is a register scan plus a 6-step cross-lane (L, r) argmin.
+#include <math.h>
+
+#include "cr_common.h"
+
+namespace cr {
+namespace {
+
+constexpr int kSortThreads = 1024;
+constexpr int kSortWaves = kSortThreads / kWave;
+
+__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v)
+{
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+
+__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v)
+{
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v += (uint64_t)__shfl_xor((unsigned long long)v, o, 64);
+    return v;
+}
+
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v)
+{
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        const uint32_t u = __shfl_xor(v, o, 64);
+        v = u > v ? u : v;
+    }
+    return v;
+}
+
+// One block per window. buf: [NW][2][Cmax] (count, key) pairs.
+__global__ __launch_bounds__(kSortThreads) void k_sort_window(const uint32_t* __restrict__ counts, uint32_t K,
+                                                              uint32_t Cmax, uint32_t* __restrict__ order,
+                                                              uint32_t* __restrict__ n_order,
+                                                              uint64_t* __restrict__ row_sum,
+                                                              uint2* __restrict__ buf)
+{
+    __shared__ uint32_t s_hist[256];
+    __shared__ uint32_t s_base[256];
+    __shared__ uint32_t s_wcnt[kSortWaves][256];
+    __shared__ uint32_t s_scan[16];
+    __shared__ uint32_t s_nnz, s_max, s_sel, s_need;
+    __shared__ unsigned long long s_sum;
+
+    const uint32_t w = blockIdx.x, tid = threadIdx.x, bd = blockDim.x, lane = lane_id(), wv = tid >> 6;
+    const uint32_t nwaves = bd >> 6;
+    const uint32_t* __restrict__ row = counts + (uint64_t)w * K;
+    if (tid == 0) {
+        s_nnz = 0;
+        s_max = 0;
+        s_sum = 0;
+    }
+    __syncthreads();
+    {
+        uint32_t nnz = 0, mx = 0;
+        uint64_t sum = 0;
+        for (uint32_t b = tid; b < K; b += bd) {
+            const uint32_t c = row[b];
+            nnz += c != 0;
+            mx = c > mx ? c : mx;
+            sum += c;
+        }
+        nnz = wave_sum_u32(nnz);
+        mx = wave_max_u32(mx);
+        sum = wave_sum_u64(sum);
+        if (lane == 0) {
+            atomicAdd(&s_nnz, nnz);
+            atomicMax(&s_max, mx);
+            atomicAdd(&s_sum, (unsigned long long)sum);
+        }
+    }
+    __syncthreads();
+    const uint32_t nnz = s_nnz, mx = s_max;
+    const uint32_t M = nnz < Cmax ? nnz : Cmax;
+    if (tid == 0) {
+        n_order[w] = M;
+        row_sum[w] = s_sum;
+    }
+    if (M == 0) return;
+
+    // Radix select: t = M-th largest nonzero count; take_eq = how many keys equal to t
+    // (the smallest key ids) complete the top M.
+    uint32_t prefix = 0, pmask = 0, need = M;
+    for (int shift = 24; shift >= 0; shift -= 8) {
+        if ((mx >> shift) == 0) {
+            pmask |= 0xFFu << shift;
+            continue;
+        }
+        for (uint32_t d = tid; d < 256; d += bd) s_hist[d] = 0;
+        __syncthreads();
+        for (uint32_t b = tid; b < K; b += bd) {
+            const uint32_t c = row[b];
+            if (c != 0 && (c & pmask) == prefix) atomicAdd(&s_hist[(c >> shift) & 255u], 1u);
+        }
+        __syncthreads();
+        if (tid == 0) {
+            uint32_t cum = 0, sel = 0;
+            for (int d = 255; d >= 0; --d) {
+                const uint32_t h = s_hist[d];
+                if (cum + h >= need) {
+                    sel = (uint32_t)d;
+                    break;
+                }
+                cum += h;
+            }
+            s_sel = sel;
+            s_need = need - cum;
+        }
+        __syncthreads();
+        prefix |= s_sel << shift;
+        pmask |= 0xFFu << shift;
+        need = s_need;
+        __syncthreads();
+    }
+    const uint32_t t = prefix, take_eq = need;
+
+    // Ordered compaction (key order) of the top M into b0.
+    uint2* __restrict__ b0 = buf + (uint64_t)w * 2u * Cmax;
+    uint2* __restrict__ b1 = b0 + Cmax;
+    uint32_t running = 0, eq_seen = 0;
+    for (uint32_t base = 0; base < K && running < M; base += bd) {
+        const uint32_t b = base + tid;
+        const uint32_t c = b < K ? row[b] : 0u;
+        const bool gt = c > t;
+        const bool eq = c == t;
+        uint32_t eq_tot, sel_tot;
+        const uint32_t eq_rank = block_exscan_u32(eq ? 1u : 0u, s_scan, &eq_tot);
+        const bool sel = gt || (eq && eq_seen + eq_rank < take_eq);
+        const uint32_t pos = block_exscan_u32(sel ? 1u : 0u, s_scan, &sel_tot);
+        if (sel && running + pos < M) b0[running + pos] = make_uint2(c, b);
+        running += sel_tot;
+        eq_seen += eq_tot;
+    }
+    __syncthreads();
+
+    // Stable LSD radix sort by v = mx - count (ascending v = descending count).
+    const uint32_t range = mx - t;
+    const uint32_t bits = range ? 32u - (uint32_t)__clz(range) : 0u;
+    const uint32_t passes = (bits + 7u) / 8u;
+    uint2* src = b0;
+    uint2* dst = b1;
+    for (uint32_t pass = 0; pass < passes; ++pass) {
+        const uint32_t shift = 8u * pass;
+        for (uint32_t d = tid; d < 256; d += bd) {
+            s_hist[d] = 0;
+            for (uint32_t q = 0; q < nwaves; ++q) s_wcnt[q][d] = 0;
+        }
+        __syncthreads();
+        for (uint32_t e = tid; e < M; e += bd) atomicAdd(&s_hist[((mx - src[e].x) >> shift) & 255u], 1u);
+        __syncthreads();
+        if (tid == 0) {
+            uint32_t run = 0;
+            for (int d = 0; d < 256; ++d) {
+                s_base[d] = run;
+                run += s_hist[d];
+            }
+        }
+        __syncthreads();
+        for (uint32_t e0 = 0; e0 < M; e0 += bd) {
+            const uint32_t e = e0 + tid;
+            const bool valid = e < M;
+            const uint2 kv = valid ? src[e] : make_uint2(0u, 0u);
+            const uint32_t d = valid ? ((mx - kv.x) >> shift) & 255u : 0u;
+            uint64_t peers = ballot(valid);
+#pragma unroll
+            for (int bit = 0; bit < 8; ++bit) {
+                const bool on = (d >> bit) & 1u;
+                const uint64_t bb = ballot(on);
+                peers &= on ? bb : ~bb;
+            }
+            const uint32_t rk = (uint32_t)__popcll(peers & lanemask_lt());
+            if (valid && rk == 0) s_wcnt[wv][d] = (uint32_t)__popcll(peers);
+            __syncthreads();
+            if (tid < 256) {
+                uint32_t run = 0;
+                for (uint32_t q = 0; q < nwaves; ++q) {
+                    const uint32_t x = s_wcnt[q][tid];
+                    s_wcnt[q][tid] = run;
+                    run += x;
+                }
+                s_hist[tid] = run;
+            }
+            __syncthreads();
+            if (valid) {
+                const uint32_t at = s_base[d] + s_wcnt[wv][d] + rk;
+                if (at < M) dst[at] = kv;
+            }
+            __syncthreads();
+            if (tid < 256) {
+                s_base[tid] += s_hist[tid];
+                for (uint32_t q = 0; q < nwaves; ++q) s_wcnt[q][tid] = 0;
+            }
+            __syncthreads();
+        }
+        uint2* tmp = src;
+        src = dst;
+        dst = tmp;
+    }
+    uint32_t* __restrict__ ord = order + (uint64_t)w * Cmax;
+    for (uint32_t e = tid; e < M; e += bd) ord[e] = src[e].y;
+}
+
+// One block per plan: Eq. 1 and the prefix admission.
+__global__ __launch_bounds__(kSortThreads) void k_admit_plan(
+    const uint32_t* __restrict__ counts, uint32_t K, uint32_t R, uint32_t Cmax, uint32_t NW,
+    const cr_plan_spec* __restrict__ specs, const uint32_t* __restrict__ order, const uint32_t* __restrict__ n_order,
+    const uint64_t* __restrict__ row_sum, uint32_t* __restrict__ num_admitted, uint64_t* __restrict__ cold,
+    uint32_t* __restrict__ clamped, uint32_t* __restrict__ member_off, uint32_t* __restrict__ err)
+{
+    __shared__ uint32_t s_scan[16];
+    __shared__ unsigned long long s_carried;
+    const uint32_t p = blockIdx.x, tid = threadIdx.x, bd = blockDim.x, lane = lane_id();
+    const cr_plan_spec spec = specs[p];
+    uint32_t* __restrict__ moff = member_off + (uint64_t)p * (Cmax + 1u);
+    bool ok = spec.window < NW && spec.W >= 1 && (uint64_t)R * spec.W <= Cmax;
+    const uint32_t M = ok ? n_order[spec.window] : 0u;
+    if (ok && spec.n_window != row_sum[spec.window]) ok = false;
+    if (ok && M > 0 && (spec.q_num == 0 || spec.q_den == 0 || spec.q_den >= (1ull << 31))) ok = false;
+    if (!ok) {
+        if (tid == 0) {
+            num_admitted[p] = 0;
+            cold[p] = 0;
+            clamped[p] = 0;
+            moff[0] = 0;
+            atomicOr(err, CR_ERR_SPEC);
+        }
+        return;
+    }
+    const uint64_t C = (uint64_t)R * spec.W;
+    const uint32_t* __restrict__ ord = order + (uint64_t)spec.window * Cmax;
+    const uint32_t* __restrict__ row = counts + (uint64_t)spec.window * K;
+    if (tid == 0) s_carried = 0;
+    uint64_t used = 0;
+    uint32_t A = 0, ncl = 0;
+    for (uint32_t base = 0; base < M; base += bd) {
+        const uint32_t a = base + tid;
+        const bool valid = a < M;
+        const uint32_t c = valid ? row[ord[a]] : 0u;
+        uint32_t k = 0;
+        bool cl = false;
+        if (valid) {
+            const uint64_t num = (uint64_t)c * spec.q_den;
+            uint64_t kk = num / spec.q_num + (num % spec.q_num != 0);
+            if (kk < 1) kk = 1;
+            if (kk > R) {
+                kk = R;
+                cl = true;
+            }
+            k = (uint32_t)kk;
+        }
+        uint32_t ktot, ntot, ctot;
+        const uint32_t ex = block_exscan_u32(k, s_scan, &ktot);
+        const bool adm = valid && used + ex + k <= C;
+        if (adm) moff[a] = (uint32_t)(used + ex);
+        const uint32_t kadm_ex = block_exscan_u32(adm ? k : 0u, s_scan, &ntot);
+        (void)kadm_ex;
+        uint32_t nadm;
+        (void)block_exscan_u32(adm ? 1u : 0u, s_scan, &nadm);
+        (void)block_exscan_u32((adm && cl) ? 1u : 0u, s_scan, &ctot);
+        const uint64_t cs = wave_sum_u64(adm ? (uint64_t)c : 0ull);
+        if (lane == 0 && cs) atomicAdd(&s_carried, (unsigned long long)cs);
+        used += ntot;
+        A += nadm;
+        ncl += ctot;
+        const uint32_t nvalid = M - base < bd ? M - base : bd;
+        if (nadm < nvalid) break;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        moff[A] = (uint32_t)used;
+        num_admitted[p] = A;
+        const uint64_t carried = s_carried;
+        cold[p] = spec.n_window >= carried ? spec.n_window - carried : 0ull;
+        clamped[p] = ncl;
+    }
+}
+
+__global__ void k_fill_u32(uint32_t* __restrict__ p, uint64_t n, uint32_t v)
+{
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = v;
+}
+
+// One wavefront (one 64-thread block) per plan. kS = registers of loads per lane.
+template <int kS>
+__global__ __launch_bounds__(64) void k_lpt(const uint32_t* __restrict__ counts, uint32_t K, uint32_t R,
+                                            uint32_t Cmax, uint32_t NW, uint32_t cands,
+                                            const cr_plan_spec* __restrict__ specs,
+                                            const uint32_t* __restrict__ order,
+                                            const uint32_t* __restrict__ num_admitted,
+                                            const uint64_t* __restrict__ cold,
+                                            const uint32_t* __restrict__ member_off, uint16_t* __restrict__ members,
+                                            double* __restrict__ load, uint32_t* __restrict__ route)
+{
+    const uint32_t p = blockIdx.x, lane = lane_id();
+    const cr_plan_spec spec = specs[p];
+    const uint32_t A = num_admitted[p];
+    const uint32_t w = spec.window < NW ? spec.window : 0u;
+    const uint32_t* __restrict__ ord = order + (uint64_t)w * Cmax;
+    const uint32_t* __restrict__ row = counts + (uint64_t)w * K;
+    const uint32_t* __restrict__ moff = member_off + (uint64_t)p * (Cmax + 1u);
+    uint16_t* __restrict__ mem = members + (uint64_t)p * Cmax;
+    const uint32_t g = p / cands, cidx = p % cands;
+    const double init = (double)cold[p] / (double)R;
+    double Lr[kS];
+#pragma unroll
+    for (int s = 0; s < kS; ++s) Lr[s] = (s * 64u + lane < R) ? init : INFINITY;
+    uint32_t taken = 0;
+    for (uint32_t a0 = 0; a0 < A; a0 += 64) {
+        const uint32_t a = a0 + lane;
+        const bool v = a < A;
+        const uint32_t key_l = v ? ord[a] : 0u;
+        const uint32_t cnt_l = v ? row[key_l] : 0u;
+        const uint32_t off_l = v ? moff[a] : 0u;
+        const uint32_t end_l = v ? moff[a + 1] : 0u;
+        const uint32_t nb = A - a0 < 64u ? A - a0 : 64u;
+        for (uint32_t t = 0; t < nb; ++t) {
+            const uint32_t key = rdlane(key_l, t), cnt = rdlane(cnt_l, t);
+            const uint32_t off = rdlane(off_l, t), k = rdlane(end_l, t) - off;
+            const double x = (double)cnt / (double)k;
+            uint32_t first = 0;
+            for (uint32_t m = 0; m < k; ++m) {
+                double bv = INFINITY;
+                uint32_t br = 0xFFFFFFFFu;
+#pragma unroll
+                for (int s = 0; s < kS; ++s) {
+                    const uint32_t r = s * 64u + lane;
+                    if (r < R && !((taken >> s) & 1u) && Lr[s] < bv) {
+                        bv = Lr[s];
+                        br = r;
+                    }
+                }
+#pragma unroll
+                for (int o = 32; o >= 1; o >>= 1) {
+                    const double ov = __shfl_xor(bv, o, 64);
+                    const uint32_t orr = __shfl_xor(br, o, 64);
+                    if (ov < bv || (ov == bv && orr < br)) {
+                        bv = ov;
+                        br = orr;
+                    }
+                }
+                if (lane == 0) mem[off + m] = (uint16_t)br;
+                if ((br & 63u) == lane) taken |= 1u << (br >> 6);
+                if (m == 0) first = br;
+            }
+#pragma unroll
+            for (int s = 0; s < kS; ++s)
+                if ((taken >> s) & 1u) Lr[s] = Lr[s] + x;
+            taken = 0;
+            if (lane == 0)
+                route[((uint64_t)g * K + key) * cands + cidx] = (k == 1) ? (CR_ROUTE_SINGLE | first) : (a0 + t);
+        }
+    }
+#pragma unroll
+    for (int s = 0; s < kS; ++s) {
+        const uint32_t r = s * 64u + lane;
+        if (r < R) load[(uint64_t)p * R + r] = Lr[s];
+    }
+}
+
+bool valid_set(const cr_plan_set* ps)
+{
+    if (!ps) return false;
+    if (ps->num_plans == 0 || ps->cands == 0 || ps->cands > CR_MAX_CANDS || ps->num_plans % ps->cands) return false;
+    if (ps->R == 0 || ps->R > CR_MAX_R || ps->max_W == 0 || ps->max_W > CR_MAX_W) return false;
+    if (ps->num_keys == 0 || ps->num_keys == 0xFFFFFFFFu || ps->num_windows == 0) return false;
+    if (!ps->specs || !ps->order || !ps->n_order || !ps->num_admitted || !ps->cold || !ps->clamped ||
+        !ps->member_off || !ps->members || !ps->load || !ps->route)
+        return false;
+    return true;
+}
+
+}  // namespace
+}  // namespace cr
+
+extern "C" size_t cr_admit_workspace_bytes(uint32_t num_windows, uint32_t R, uint32_t max_W)
+{
+    const uint64_t cmax = (uint64_t)R * max_W;
+    return (size_t)(num_windows * (2u * cmax * sizeof(uint2) + sizeof(uint64_t)) + 256u);
+}
+
+extern "C" cr_status cr_admit(const uint32_t* counts, const cr_plan_set* plans, void* ws, size_t ws_bytes,
+                              uint32_t* err, void* stream)
+{
+    using namespace cr;
+    if (!counts || !valid_set(plans) || !ws || !err) return CR_EINVAL;
+    const uint32_t cmax = plans->R * plans->max_W;
+    if (ws_bytes < cr_admit_workspace_bytes(plans->num_windows, plans->R, plans->max_W)) return CR_ESIZE;
+    uint8_t* base = reinterpret_cast<uint8_t*>(((uintptr_t)ws + 255) & ~(uintptr_t)255);
+    uint2* buf = reinterpret_cast<uint2*>(base);
+    uint64_t* row_sum = reinterpret_cast<uint64_t*>(base + (uint64_t)plans->num_windows * 2u * cmax * sizeof(uint2));
+    const hipStream_t st = as_stream(stream);
+    (void)hipGetLastError();
+    hipLaunchKernelGGL(k_sort_window, dim3(plans->num_windows), dim3(kSortThreads), 0, st, counts, plans->num_keys,
+                       cmax, plans->order, plans->n_order, row_sum, buf);
+    hipLaunchKernelGGL(k_admit_plan, dim3(plans->num_plans), dim3(kSortThreads), 0, st, counts, plans->num_keys,
+                       plans->R, cmax, plans->num_windows, plans->specs, plans->order, plans->n_order, row_sum,
+                       plans->num_admitted, plans->cold, plans->clamped, plans->member_off, err);
+    return hipGetLastError() == hipSuccess ? CR_OK : CR_EHIP;
+}
+
+extern "C" cr_status cr_place_lpt(const uint32_t* counts, const cr_plan_set* plans, void* stream)
+{
+    using namespace cr;
+    if (!counts || !valid_set(plans)) return CR_EINVAL;
+    const uint32_t cmax = plans->R * plans->max_W;
+    const hipStream_t st = as_stream(stream);
+    const uint32_t ng = plans->num_plans / plans->cands;
+    const uint64_t route_words = (uint64_t)ng * plans->num_keys * plans->cands;
+    (void)hipGetLastError();
+    hipLaunchKernelGGL(k_fill_u32, dim3(1024), dim3(256), 0, st, plans->route, route_words, CR_ROUTE_COLD);
+#define CR_LPT(S)                                                                                                   \
+    hipLaunchKernelGGL(k_lpt<S>, dim3(plans->num_plans), dim3(64), 0, st, counts, plans->num_keys, plans->R, cmax, \
+                       plans->num_windows, plans->cands, plans->specs, plans->order, plans->num_admitted,          \
+                       plans->cold, plans->member_off, plans->members, plans->load, plans->route)
+    const uint32_t s = (plans->R + 63) / 64;
+    if (s <= 1) CR_LPT(1);
+    else if (s <= 2) CR_LPT(2);
+    else if (s <= 4) CR_LPT(4);
+    else if (s <= 8) CR_LPT(8);
+    else CR_LPT(16);
+#undef CR_LPT
+    return hipGetLastError() == hipSuccess ? CR_OK : CR_EHIP;
+}

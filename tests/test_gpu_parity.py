@@ -1,0 +1,179 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle, element by element.
+
+Bit-exact: counts, admitted keys in order, k, member lists, cold counts, clamp counts,
+per-request destinations, per-(interval, candidate, destination) replay statistics and
+the carried LRU state. Planned loads: within 1e-9 absolute and, by design, bit-identical.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import pipeline as opipe
+from paper_2608_19677_amd import workload as wl_mod
+from paper_2608_19677_amd.pipeline import Pipeline
+
+from cr_check import compare_all, compare_plan, say
+
+pytestmark = pytest.mark.gpu
+
+
+def _run(wl):
+    say(f"[case] {wl.name} n={wl.n} J={wl.J} K={wl.num_keys} R={wl.R} P={wl.P} "
+        f"W={[c.W for c in wl.candidates]}")
+    gp = Pipeline(wl)
+    gp.step()
+    h = gp.host()
+    orc = opipe.run(wl)
+    compare_all(wl, gp, h, orc)
+    return gp, h, orc
+
+
+SMALL = [
+    # seed, K, n, R, Ws, J, hot, hot_share, qs
+    (1, 50, 3000, 7, [4], 3, 0, 0.0, [(1, 1)]),
+    (2, 1, 5000, 1, [3], 1, 0, 0.0, [(1, 1)]),
+    (3, 200, 20000, 30, [16], 5, 3, 0.5, [(1, 1), (2, 5)]),
+    (4, 1000, 100_003, 64, [64, 65, 130, 300, 512], 4, 2, 0.3, [(1, 1)]),
+    (5, 5000, 50_000, 1024, [8, 100], 2, 4, 0.4, [(1, 1)]),
+    (6, 300, 40_000, 65, [10], 9, 0, 0.0, [(1, 1), (28, 35), (42, 35)]),
+    (7, 100, 10, 30, [16], 3, 0, 0.0, [(1, 1)]),
+    (8, 400, 30_000, 4, [2, 50], 20, 2, 0.9, [(1, 3)]),
+    (9, 2000, 77_777, 16, [128], 6, 8, 0.48, [(2, 5)]),
+    (10, 64, 4096, 128, [1, 63, 64], 2, 0, 0.0, [(1, 1)]),
+]
+
+
+@pytest.mark.parametrize("case", SMALL, ids=[f"s{c[0]}" for c in SMALL])
+def test_small_random_parity(case):
+    seed, K, n, R, Ws, J, hot, share, qs = case
+    wl = wl_mod.small_random(seed, num_keys=K, n=n, R=R, Ws=Ws, J=J, hot=hot, hot_share=share, qs=qs)
+    _run(wl)
+
+
+def test_tiny_shape_parity():
+    gp, h, orc = _run(wl_mod.tiny())
+    pl = gp.plan_of(h, 0, 0)
+    assert len(pl["adm_keys"]) > 400 and pl["adm_k"].max() > 1
+
+
+@pytest.mark.timeout(900)
+def test_llama70b_shape_full_parity():
+    gp, h, orc = _run(wl_mod.llama70b())
+    assert h["num_admitted"].max() > 0
+    assert np.all(np.diff(h["member_off"][:, :2], axis=1) <= 1)  # every k is 1 on this shape
+
+
+@pytest.mark.timeout(900)
+def test_replication_shape_full_parity():
+    gp, h, orc = _run(wl_mod.replication())
+    ks = gp.plan_of(h, 3, 0)["adm_k"]
+    assert ks[:10].tolist() == [4] + [3] * 8 + [2]
+
+
+@pytest.mark.timeout(900)
+def test_burst_shape_full_parity():
+    _run(wl_mod.burst())
+
+
+def test_chunked_stream_equals_whole_stream():
+    # Two chunks split at an interval boundary, the second planned from the first chunk's
+    # last window and starting from its carried cache state, equal the uninterrupted run.
+    wl = wl_mod.small_random(21, num_keys=3000, n=200_000, R=40, Ws=[24, 200], J=6, hot=2, hot_share=0.2)
+    say(f"[case] chunked n={wl.n} J={wl.J}")
+    whole = Pipeline(wl)
+    whole.step()
+    hw = whole.host()
+    cut_j = 3
+    cut = int(wl.offsets[cut_j])
+
+    def part(s, e, js, je, first):
+        off = (wl.offsets[js:je + 1] - wl.offsets[js]).astype(np.uint64)
+        return wl_mod.Workload(name="part", num_keys=wl.num_keys, R=wl.R, candidates=wl.candidates,
+                               keys=wl.keys[s:e], suffix=wl.suffix[s:e], prefix_len=wl.prefix_len, offsets=off,
+                               seed=wl.seed, first_index=first)
+
+    a = part(0, cut, 0, cut_j, 0)
+    b = part(cut, wl.n, cut_j, wl.J, cut)
+    pa = Pipeline(a)
+    pa.step()
+    pb = Pipeline(b, prev_counts=pa.counts[a.J - 1].clone(), prev_n=int(a.offsets[-1] - a.offsets[-2]),
+                  lru_in=pa.lru_out.clone())
+    pb.step()
+    ha, hb = pa.host(), pb.host()
+    np.testing.assert_array_equal(np.concatenate([ha["dest"], hb["dest"]], axis=1), hw["dest"])
+    np.testing.assert_array_equal(np.concatenate([ha["stats"], hb["stats"]], axis=0), hw["stats"])
+    np.testing.assert_array_equal(hb["lru"], hw["lru"])
+    # and the second chunk's plans equal the oracle's chunked driver
+    orc_b = opipe.run(b, lru=[ha["lru"][c, :, :cd.W] for c, cd in enumerate(b.candidates)],
+                      counts_prev=ha["counts"][a.J - 1])
+    assert hb["err"] == 0
+    for (w, c), opl in orc_b["plans"].items():
+        compare_plan(pb.plan_of(hb, w, c), opl, f"chunk plan {w}/{c}")
+    np.testing.assert_array_equal(hb["stats"], orc_b["stats"])
+    np.testing.assert_array_equal(hb["dest"], orc_b["dest"])
+
+
+def test_repeat_runs_are_identical():
+    wl = wl_mod.small_random(31, num_keys=800, n=120_000, R=30, Ws=[32, 96], J=4, hot=3, hot_share=0.3)
+    say(f"[case] determinism n={wl.n}")
+    gp = Pipeline(wl)
+    gp.step()
+    h1 = gp.host()
+    gp.step()
+    h2 = gp.host()
+    for k in ("counts", "order", "members", "load", "route", "dest", "stats", "lru"):
+        assert np.array_equal(np.asarray(h1[k]).view(np.uint8), np.asarray(h2[k]).view(np.uint8)), k
+
+
+@pytest.mark.timeout(900)
+def test_sweep_chunks_sampled_parity():
+    # The 1,024-destination sweep at its full chunk size (1e8 requests, 64 candidates):
+    # counts exact; sampled candidates' plans and routing exact for every request; replay
+    # exact on a sample of destinations (the per-destination caches are independent).
+    from paper_2608_19677_amd import binding as B
+    say("[case] sweep chunk 0, n=1e8, P=64, R=1024")
+    w0 = wl_mod.sweep_chunk(0)
+    gp = Pipeline(w0)
+    gp.step()
+    torch.cuda.synchronize()
+    err = int(gp.err.cpu().numpy().view(np.uint32)[0])
+    assert err == 0
+    counts = gp.counts.cpu().numpy().view(np.uint32)
+    ocounts, _ = oracle.count_rates(w0.keys, w0.offsets, w0.num_keys)
+    np.testing.assert_array_equal(counts, ocounts)
+    row = ocounts[0]
+    n_w = int(row.sum())
+    R = w0.R
+    stats = gp.stats.cpu().numpy().view(np.uint64)
+    lru = gp.lru_out.cpu().numpy().view(np.uint32)
+    dsample = np.array([0, 1, 511, 1023] + list(range(200, 204)))
+    for c in (0, 7, 27, 63):
+        cand = w0.candidates[c]
+        say(f"[case] sweep cand {c} W={cand.W} q={cand.a}/{cand.b}")
+        keys, ks, cold, clamped = oracle.admit(row, R, cand.W, n_w, cand.a * n_w, cand.b * R)
+        members, moff, L = oracle.place_lpt(keys, ks, row, R, cold)
+        h = dict(num_admitted=gp.plans.num_admitted.cpu().numpy().view(np.uint32),
+                 order=gp.plans.order.cpu().numpy().view(np.uint32),
+                 member_off=gp.plans.member_off[c:c + 1].cpu().numpy().view(np.uint32),
+                 members=gp.plans.members[c:c + 1].cpu().numpy().view(np.uint16),
+                 load=gp.plans.load[c:c + 1].cpu().numpy(),
+                 cold=gp.plans.cold[c:c + 1].cpu().numpy().view(np.uint64),
+                 clamped=gp.plans.clamped[c:c + 1].cpu().numpy().view(np.uint32))
+        A = int(h["num_admitted"][c])
+        mo = h["member_off"][0, :A + 1]
+        gpl = dict(adm_keys=h["order"][0, :A], adm_k=np.diff(mo).astype(np.uint32), member_off=mo,
+                   members=h["members"][0, :int(mo[A])], L=h["load"][0], cold=int(h["cold"][0]),
+                   clamped=int(h["clamped"][0]))
+        compare_plan(gpl, dict(adm_keys=keys, adm_k=ks, member_off=moff, members=members, L=L, cold=cold,
+                               clamped=clamped), f"sweep cand {c}")
+        dest_o = oracle.route(w0.keys, w0.first_index, w0.seed, w0.num_keys, R, keys, moff, members, L)
+        dest_g = gp.dest[c].cpu().numpy().view(np.uint16)
+        np.testing.assert_array_equal(dest_g, dest_o, err_msg=f"dest cand {c}")
+        sel = np.isin(dest_o, dsample)
+        st, state = oracle.replay(w0.keys[sel], w0.suffix[sel], w0.prefix_len, dest_o[sel],
+                                  np.array([0, int(sel.sum())], np.uint64), R, cand.W)
+        np.testing.assert_array_equal(stats[0, c, dsample], st[0, dsample], err_msg=f"stats cand {c}")
+        np.testing.assert_array_equal(lru[c, dsample, :cand.W], state[dsample])
+    # every request is accounted for once per candidate
+    assert np.all(stats[0, :, :, 0].sum(axis=1) == w0.n)
