@@ -1,0 +1,164 @@
+"""Benchmark: count -> plan -> route -> LRU replay on one MI355X, plus the CPU oracle baseline.
+
+A step is one pass of the whole path over the 70B-like workload (20,000 keys, Zipf 1.0
+capped at a 0.3 % share, 1e7 requests at 176 QPS in 60-s control intervals = 948
+intervals and 947 plan builds, 30 destinations x 64 LRU slots). Inputs are resident in
+HBM before timing starts. Prints ONE JSON line.
+
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload llama70b|tiny|replication|burst]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+# 32-bit integer VALU: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz = 39,322 G lane-ops/s.
+ALU_PEAK_GOPS = 256 * 4 * 16 * 2.4
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="llama70b")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    return ap.parse_args()
+
+
+def describe(name, wl):
+    return {
+        "workload": {
+            "llama70b": "70B-like: 20,000 keys Zipf(1.0) capped at 0.3% share; 1e7 requests, 176 QPS, "
+                        "60-s intervals; 30 destinations x 64 LRU slots; q_cap = mean load",
+            "tiny": "Tiny: 1,000 keys Zipf(1.1); 1e5 requests, one interval; 30 x 16 slots",
+            "replication": "Replication stress: 5,000 Zipf(1.1) + 8 keys at 6%; 2e7 requests, 60-s intervals; "
+                           "16 x 128 slots; q_cap = 0.4 x mean",
+            "burst": "Burst: 50,000 keys Zipf(1.2), 5% keys 10x for 20 s; 5e7 requests, 100 x 10-s intervals; "
+                     "64 x 64 slots",
+        }.get(name, name),
+        "requests": wl.n, "intervals": wl.J, "plan_builds": None, "keys": wl.num_keys, "destinations": wl.R,
+        "slots": [c.W for c in wl.candidates], "candidates": wl.P,
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "one GPU only: the path runs on a single MI355X and has no multi-GPU "
+                                   "sharding", "n_gpus": args.gpus}), flush=True)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from paper_2608_19677_amd import build as hip_build
+    if not os.path.exists(hip_build.LIB):
+        hip_build.build()
+    from paper_2608_19677_amd import workload
+    from paper_2608_19677_amd.pipeline import Pipeline
+
+    wl = workload.CONFIGS[args.workload]()
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    gp = Pipeline(wl, device="cuda:0")
+    n_plans = gp.plans.num_plans
+    stream = torch.cuda.current_stream()
+
+    stages = Pipeline.STAGES
+    for _ in range(args.warmup):
+        gp.step()
+    torch.cuda.synchronize()
+    ev = {s: [] for s in stages}
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        for s in stages:
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            getattr(gp, s)()
+            b.record(stream)
+            ev[s].append((a, b))
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_step = (t1 - t0) * 1e3 / args.steps
+    stage_ms = {s: float(np.mean([a.elapsed_time(b) for a, b in ev[s]])) for s in stages}
+    h = gp.host()
+    assert h["err"] == 0, f"device error word {h['err']:#x}"
+    tot = h["stats"].sum(axis=(0, 2)).astype(np.float64)
+
+    n, P, R = wl.n, wl.P, wl.R
+    n_adm = int(h["member_off"][np.arange(n_plans), h["num_admitted"].astype(np.int64)].astype(np.int64).sum())
+    # Algorithmic work per launch of the single-kernel calls (the zero fills of stats are
+    # outside the events; count, place, route and lru each launch exactly one kernel here).
+    kern = {
+        "count": dict(kernel="k_count_owner", bound="hbm", unit="GB/s", work=4.0 * n, peak=HBM_PEAK_GBS),
+        "route": dict(kernel="k_route", bound="hbm", unit="GB/s", work=(4.0 + 2.0 * P) * n, peak=HBM_PEAK_GBS),
+        # LPT: every job copy is compared against the R destination loads.
+        "place": dict(kernel="k_lpt_small", bound="alu", unit="Glane-op/s", work=float(n_adm) * R,
+                      peak=ALU_PEAK_GOPS),
+        # LRU: every request compares its key with the W slots and ages the W recency ranks.
+        "lru": dict(kernel="k_replay<%d>" % max({1 if c.W <= 64 else 2 if c.W <= 128 else 4 if c.W <= 256 else 8
+                                                 for c in wl.candidates}), bound="alu", unit="Glane-op/s",
+                    work=float(sum(2.0 * c.W for c in wl.candidates)) * n, peak=ALU_PEAK_GOPS),
+    }
+    for k, v in kern.items():
+        sec = stage_ms[k] * 1e-3
+        v["ms"] = stage_ms[k]
+        v["achieved"] = v["work"] / sec / 1e9
+        v["frac"] = v["achieved"] / v["peak"]
+    dominant = max(kern, key=lambda k: kern[k]["ms"])
+    d = kern[dominant]
+
+    out = {
+        "metric": "requests/sec through count+route+LRU replay",
+        "value": n / (ms_step * 1e-3),
+        "unit": "requests/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u32",
+        "data": "synthetic",
+        "config": describe(args.workload, wl),
+        "roofline": {"bound": d["bound"], "achieved": d["achieved"], "peak": d["peak"], "unit": d["unit"],
+                     "frac": d["frac"], "traffic": None, "kernel": d["kernel"]},
+        "us_per_plan_build": (stage_ms["admit"] + stage_ms["place"]) * 1e3 / n_plans,
+        "stage_ms": stage_ms,
+        "kernels": {k: {kk: vv for kk, vv in v.items() if kk != "work"} for k, v in kern.items()},
+        "hbm_frac": {"count": kern["count"]["frac"], "route": kern["route"]["frac"]},
+        "hit_rate": (tot[:, 1] / tot[:, 0]).tolist(),
+    }
+    out["config"]["plan_builds"] = n_plans
+
+    if not args.no_cpu_baseline:
+        import oracle
+        from oracle import pipeline as opipe
+        times = []
+        t_start = time.perf_counter()
+        while True:
+            s = time.perf_counter()
+            opipe.run(wl)
+            times.append(time.perf_counter() - s)
+            if time.perf_counter() - t_start > args.cpu_seconds or len(times) >= 10:
+                break
+        med = float(np.median(times))
+        out["cpu_baseline"] = {"value": n / med, "unit": "requests/s", "cores": 1, "kind": "oracle",
+                               "sample": f"the full workload, {len(times)} passes, median "
+                                         f"{med:.3f} s per pass (single-threaded C oracle)"}
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

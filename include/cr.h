@@ -67,6 +67,7 @@ typedef struct {
  * a group so one request reads one contiguous row of `cands` words.
  * Host struct of device pointers; sizes follow from the fields (C_max = R * max_W):
  *   order      u32 [num_windows][C_max]  nonzero keys by (count desc, key asc), cut at C_max
+ *   order_count u32 [num_windows][C_max] their counts
  *   n_order    u32 [num_windows]         entries of order used
  *   num_admitted u32 [NP]                A
  *   cold       u64 [NP]                  window requests not carried by admitted keys
@@ -85,6 +86,7 @@ typedef struct {
     uint32_t num_windows; /* rows of counts                                        */
     const cr_plan_spec* specs; /* [NP]                                             */
     uint32_t* order;
+    uint32_t* order_count;
     uint32_t* n_order;
     uint32_t* num_admitted;
     uint64_t* cold;
@@ -97,8 +99,8 @@ typedef struct {
 
 /* Rates per key per control interval (Algorithm 1 input "rates"; Appendix A.2: the
  * planner needs only {(b, lambda_b)}). Rates are kept in requests per window.
- *   counts[j * num_keys + b] += #{ i in [off[j], off[j+1]) : keys[i] == b }
- * keys u32 [n]; off u64 [J+1]; counts u32 [J][num_keys] (accumulated, caller zeroes).
+ *   counts[j * num_keys + b] = #{ i in [off[j], off[j+1]) : keys[i] == b }
+ * keys u32 [n]; off u64 [J+1]; counts u32 [J][num_keys] (overwritten, every row).
  * A key >= num_keys is not counted and sets CR_ERR_KEY_RANGE. */
 cr_status cr_count_rates(const uint32_t* keys, uint64_t n, const uint64_t* off, uint32_t J,
                          uint32_t num_keys, uint32_t* counts, uint32_t* err, void* stream);
@@ -110,8 +112,9 @@ size_t cr_admit_workspace_bytes(uint32_t num_windows, uint32_t R, uint32_t max_W
  * For every window: order its nonzero keys by (count desc, key asc), cut at C_max.
  * For every plan: k_b by Eq. 1 (exact integers, clamped to R), then admit the longest
  * prefix of that order whose k_b sum is <= C = R * W; cold = n_window - admitted counts.
- * counts u32 [num_windows][num_keys]. Writes order, n_order, num_admitted, cold,
- * clamped and member_off[0..A] (prefix sums of k). A spec with a window out of range,
+ * counts u32 [num_windows][num_keys]. Writes order, order_count, n_order, num_admitted,
+ * cold, clamped and member_off[0..A] (prefix sums of k), and resets every route word to
+ * CR_ROUTE_COLD for cr_place_lpt to fill. A spec with a window out of range,
  * q_num == 0 on a nonempty window, or n_window != row sum sets CR_ERR_SPEC (the plan
  * then admits nothing). */
 cr_status cr_admit(const uint32_t* counts, const cr_plan_set* plans, void* ws, size_t ws_bytes,
@@ -121,7 +124,7 @@ cr_status cr_admit(const uint32_t* counts, const cr_plan_set* plans, void* ws, s
  * Per plan: L[r] = cold / R; admitted keys in admission order take the k smallest
  * (L[r], r) destinations, listed in that order, each charged count / k (IEEE double,
  * one rounding per operation, the same order as the definition). Writes members,
- * load and the whole route table (cold words first, then admitted keys). */
+ * load and the route words of admitted keys (cr_admit has reset the others). */
 cr_status cr_place_lpt(const uint32_t* counts, const cr_plan_set* plans, void* stream);
 
 /* Dispatch (Section 3.1 "Placement and dispatch"; Fig. 1), order-independent form.
@@ -137,7 +140,7 @@ cr_status cr_route(const uint32_t* keys, uint64_t n, uint64_t first_index, uint6
                    const uint64_t* off, const uint32_t* gmap, uint32_t J, const cr_plan_set* plans,
                    uint16_t* dest, uint32_t* err, void* stream);
 
-/* Workspace for cr_replay, in bytes. */
+/* Workspace for cr_replay (and for its two phases), in bytes. */
 size_t cr_replay_workspace_bytes(uint64_t n, uint32_t P, uint32_t R);
 
 /* Shadow replay (Section 3.2: admitted and cold prefixes share each destination's
@@ -152,14 +155,30 @@ size_t cr_replay_workspace_bytes(uint64_t n, uint32_t P, uint32_t R);
  * W host u32 [P] (1..CR_MAX_W); lru_in / lru_out u32 [P][R][max_W]: carried cache state,
  * most recent first, CR_EMPTY_SLOT after the used entries (lru_in NULL = all empty;
  * lru_in and lru_out must not overlap); stats u64 [J][P][R][4] (accumulated) =
- * {requests, hits, prefill_tokens, hit_prefix_tokens}.
+ * {requests, hits, prefill_tokens, hit_prefix_tokens}. n < 2^32 - 1.
  * A destination >= R sets CR_ERR_DEST_RANGE and a key >= num_keys sets CR_ERR_KEY_RANGE;
- * such requests are skipped. */
+ * such requests are skipped.
+ * cr_replay = cr_replay_partition followed by cr_replay_lru on the same workspace. */
 cr_status cr_replay(const uint32_t* keys, const uint16_t* suffix, const uint32_t* prefix_len,
                     uint32_t num_keys, const uint16_t* dest, uint64_t n, const uint64_t* off,
                     uint32_t J, uint32_t P, uint32_t R, const uint32_t* W, uint32_t max_W,
                     const uint32_t* lru_in, uint32_t* lru_out, uint64_t* stats, void* ws,
                     size_t ws_bytes, uint32_t* err, void* stream);
+
+/* First phase of cr_replay: groups every candidate's requests by destination in arrival
+ * order (records of key, suffix and interval in the workspace) and cuts each group into
+ * independent segments. Arguments as for cr_replay. */
+cr_status cr_replay_partition(const uint32_t* keys, const uint16_t* suffix, const uint16_t* dest,
+                              uint64_t n, const uint64_t* off, uint32_t J, uint32_t P, uint32_t R,
+                              const uint32_t* W, void* ws, size_t ws_bytes, uint32_t* err,
+                              void* stream);
+
+/* Second phase of cr_replay: replays the partitioned workspace (same n, J, P, R, W)
+ * through the per-destination LRU caches and accumulates stats. */
+cr_status cr_replay_lru(const uint32_t* prefix_len, uint32_t num_keys, uint64_t n, uint32_t J,
+                        uint32_t P, uint32_t R, const uint32_t* W, uint32_t max_W,
+                        const uint32_t* lru_in, uint32_t* lru_out, uint64_t* stats, void* ws,
+                        size_t ws_bytes, uint32_t* err, void* stream);
 
 /* Library version string. */
 const char* cr_version(void);

@@ -24,7 +24,7 @@ CR_ROUTE_SINGLE = 0x80000000
 CR_MAX_R, CR_MAX_W, CR_MAX_CANDS, CR_MAX_J = 1024, 512, 256, 65535
 
 EXPORTS = ("cr_count_rates", "cr_admit_workspace_bytes", "cr_admit", "cr_place_lpt", "cr_route",
-           "cr_replay_workspace_bytes", "cr_replay", "cr_version")
+           "cr_replay_workspace_bytes", "cr_replay", "cr_replay_partition", "cr_replay_lru", "cr_version")
 
 _u32, _u64, _P = ctypes.c_uint32, ctypes.c_uint64, ctypes.c_void_p
 
@@ -35,8 +35,9 @@ class CrPlanSpec(ctypes.Structure):
 
 class CrPlanSet(ctypes.Structure):
     _fields_ = [("num_plans", _u32), ("cands", _u32), ("R", _u32), ("max_W", _u32), ("num_keys", _u32),
-                ("num_windows", _u32), ("specs", _P), ("order", _P), ("n_order", _P), ("num_admitted", _P),
-                ("cold", _P), ("clamped", _P), ("member_off", _P), ("members", _P), ("load", _P), ("route", _P)]
+                ("num_windows", _u32), ("specs", _P), ("order", _P), ("order_count", _P), ("n_order", _P),
+                ("num_admitted", _P), ("cold", _P), ("clamped", _P), ("member_off", _P), ("members", _P),
+                ("load", _P), ("route", _P)]
 
 
 class CrError(RuntimeError):
@@ -65,8 +66,13 @@ def load(path: Optional[str] = None):
     L.cr_replay_workspace_bytes.restype = ctypes.c_size_t
     L.cr_replay.argtypes = [_P, _P, _P, _u32, _P, _u64, _P, _u32, _u32, _u32, ctypes.POINTER(_u32), _u32, _P, _P,
                             _P, _P, ctypes.c_size_t, _P, _P]
+    L.cr_replay_partition.argtypes = [_P, _P, _P, _u64, _P, _u32, _u32, _u32, ctypes.POINTER(_u32), _P,
+                                      ctypes.c_size_t, _P, _P]
+    L.cr_replay_lru.argtypes = [_P, _u32, _u64, _u32, _u32, _u32, ctypes.POINTER(_u32), _u32, _P, _P, _P, _P,
+                                ctypes.c_size_t, _P, _P]
     L.cr_version.restype = ctypes.c_char_p
-    for f in ("cr_count_rates", "cr_admit", "cr_place_lpt", "cr_route", "cr_replay"):
+    for f in ("cr_count_rates", "cr_admit", "cr_place_lpt", "cr_route", "cr_replay", "cr_replay_partition",
+              "cr_replay_lru"):
         getattr(L, f).restype = ctypes.c_int32
     _lib = L
     return L
@@ -135,6 +141,23 @@ def cr_replay(keys, suffix, prefix_len, num_keys: int, dest, off, J: int, P: int
                             ws.numel() * ws.element_size(), _ptr(err), _stream(stream)), "cr_replay")
 
 
+def cr_replay_partition(keys, suffix, dest, off, J: int, P: int, R: int, W: Sequence[int], ws, err, stream=None,
+                        n: Optional[int] = None):
+    n = keys.numel() if n is None else n
+    Wa = (_u32 * len(W))(*[int(x) for x in W])
+    _check(load().cr_replay_partition(_ptr(keys), _ptr(suffix), _ptr(dest), n, _ptr(off), J, P, R, Wa, _ptr(ws),
+                                      ws.numel() * ws.element_size(), _ptr(err), _stream(stream)),
+           "cr_replay_partition")
+
+
+def cr_replay_lru(prefix_len, num_keys: int, n: int, J: int, P: int, R: int, W: Sequence[int], max_W: int, lru_in,
+                  lru_out, stats, ws, err, stream=None):
+    Wa = (_u32 * len(W))(*[int(x) for x in W])
+    _check(load().cr_replay_lru(_ptr(prefix_len), num_keys, n, J, P, R, Wa, max_W, _ptr(lru_in), _ptr(lru_out),
+                                _ptr(stats), _ptr(ws), ws.numel() * ws.element_size(), _ptr(err), _stream(stream)),
+           "cr_replay_lru")
+
+
 class PlanSet:
     """Device buffers of a cr_plan_set (NP = NG * cands plans over num_windows rows)."""
 
@@ -150,6 +173,7 @@ class PlanSet:
         self.specs = host.to(device)
         i32 = dict(dtype=torch.int32, device=device)
         self.order = torch.empty((NW, cmax), **i32)
+        self.order_count = torch.empty((NW, cmax), **i32)
         self.n_order = torch.empty(NW, **i32)
         self.num_admitted = torch.empty(NP, **i32)
         self.cold = torch.empty(NP, dtype=torch.int64, device=device)
@@ -158,6 +182,7 @@ class PlanSet:
         self.members = torch.empty((NP, cmax), dtype=torch.int16, device=device)
         self.load = torch.empty((NP, R), dtype=torch.float64, device=device)
         self.route = torch.empty((ng, num_keys, cands), **i32)
-        self.c = CrPlanSet(NP, cands, R, max_W, num_keys, NW, _ptr(self.specs), _ptr(self.order), _ptr(self.n_order),
+        self.c = CrPlanSet(NP, cands, R, max_W, num_keys, NW, _ptr(self.specs), _ptr(self.order),
+                           _ptr(self.order_count), _ptr(self.n_order),
                            _ptr(self.num_admitted), _ptr(self.cold), _ptr(self.clamped), _ptr(self.member_off),
                            _ptr(self.members), _ptr(self.load), _ptr(self.route))

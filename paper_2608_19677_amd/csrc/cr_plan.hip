@@ -48,6 +48,7 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v)
 // One block per window. buf: [NW][2][Cmax] (count, key) pairs.
 __global__ __launch_bounds__(kSortThreads) void k_sort_window(const uint32_t* __restrict__ counts, uint32_t K,
                                                               uint32_t Cmax, uint32_t* __restrict__ order,
+                                                              uint32_t* __restrict__ order_count,
                                                               uint32_t* __restrict__ n_order,
                                                               uint64_t* __restrict__ row_sum,
                                                               uint2* __restrict__ buf)
@@ -214,14 +215,19 @@ __global__ __launch_bounds__(kSortThreads) void k_sort_window(const uint32_t* __
         dst = tmp;
     }
     uint32_t* __restrict__ ord = order + (uint64_t)w * Cmax;
-    for (uint32_t e = tid; e < M; e += bd) ord[e] = src[e].y;
+    uint32_t* __restrict__ ocnt = order_count + (uint64_t)w * Cmax;
+    for (uint32_t e = tid; e < M; e += bd) {
+        const uint2 kv = src[e];
+        ord[e] = kv.y;
+        ocnt[e] = kv.x;
+    }
 }
 
 // One block per plan: Eq. 1 and the prefix admission.
 __global__ __launch_bounds__(kSortThreads) void k_admit_plan(
-    const uint32_t* __restrict__ counts, uint32_t K, uint32_t R, uint32_t Cmax, uint32_t NW,
-    const cr_plan_spec* __restrict__ specs, const uint32_t* __restrict__ order, const uint32_t* __restrict__ n_order,
-    const uint64_t* __restrict__ row_sum, uint32_t* __restrict__ num_admitted, uint64_t* __restrict__ cold,
+    uint32_t R, uint32_t Cmax, uint32_t NW,
+    const cr_plan_spec* __restrict__ specs, const uint32_t* __restrict__ order_count,
+    const uint32_t* __restrict__ n_order, const uint64_t* __restrict__ row_sum, uint32_t* __restrict__ num_admitted, uint64_t* __restrict__ cold,
     uint32_t* __restrict__ clamped, uint32_t* __restrict__ member_off, uint32_t* __restrict__ err)
 {
     __shared__ uint32_t s_scan[16];
@@ -244,15 +250,14 @@ __global__ __launch_bounds__(kSortThreads) void k_admit_plan(
         return;
     }
     const uint64_t C = (uint64_t)R * spec.W;
-    const uint32_t* __restrict__ ord = order + (uint64_t)spec.window * Cmax;
-    const uint32_t* __restrict__ row = counts + (uint64_t)spec.window * K;
+    const uint32_t* __restrict__ ocnt = order_count + (uint64_t)spec.window * Cmax;
     if (tid == 0) s_carried = 0;
     uint64_t used = 0;
     uint32_t A = 0, ncl = 0;
     for (uint32_t base = 0; base < M; base += bd) {
         const uint32_t a = base + tid;
         const bool valid = a < M;
-        const uint32_t c = valid ? row[ord[a]] : 0u;
+        const uint32_t c = valid ? ocnt[a] : 0u;
         uint32_t k = 0;
         bool cl = false;
         if (valid) {
@@ -298,12 +303,140 @@ __global__ void k_fill_u32(uint32_t* __restrict__ p, uint64_t n, uint32_t v)
     for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = v;
 }
 
-// One wavefront (one 64-thread block) per plan. kS = registers of loads per lane.
+__device__ __forceinline__ uint32_t dpp_shl1(uint32_t old, uint32_t v)  // lane i <- lane i+1
+{
+    return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)v, 0x130, 0xF, 0xF, false);
+}
+
+__device__ __forceinline__ uint32_t dpp_shr1(uint32_t old, uint32_t v)  // lane i <- lane i-1
+{
+    return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)v, 0x138, 0xF, 0xF, false);
+}
+
+__device__ __forceinline__ double dpp_shl1_f64(double v)
+{
+    const uint64_t u = (uint64_t)__double_as_longlong(v);
+    const uint32_t lo = dpp_shl1((uint32_t)u, (uint32_t)u), hi = dpp_shl1((uint32_t)(u >> 32), (uint32_t)(u >> 32));
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+__device__ __forceinline__ double dpp_shr1_f64(double v)
+{
+    const uint64_t u = (uint64_t)__double_as_longlong(v);
+    const uint32_t lo = dpp_shr1((uint32_t)u, (uint32_t)u), hi = dpp_shr1((uint32_t)(u >> 32), (uint32_t)(u >> 32));
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+struct LptBatch {
+    uint32_t key, cnt, off, end;
+};
+
+__device__ __forceinline__ LptBatch lpt_load(const uint32_t* __restrict__ ord, const uint32_t* __restrict__ ocnt,
+                                             const uint32_t* __restrict__ moff, uint32_t a, uint32_t A)
+{
+    LptBatch b{0u, 0u, 0u, 0u};
+    if (a < A) {
+        b.key = ord[a];
+        b.cnt = ocnt[a];
+        b.off = moff[a];
+        b.end = moff[a + 1];
+    }
+    return b;
+}
+
+// R <= 64: lane i holds the i-th smallest (L, r), so the least-loaded destinations are
+// lanes 0..k-1. After charging them, each is re-inserted at its rank among the rest:
+// a ballot + popcount gives the rank, a one-lane DPP shift opens the slot. For k = 1 the
+// pop and the insert fuse into one shift. Stores of a 64-key batch leave in one go.
+__global__ __launch_bounds__(64) void k_lpt_small(uint32_t K, uint32_t R, uint32_t Cmax, uint32_t NW,
+                                                  uint32_t cands, const cr_plan_spec* __restrict__ specs,
+                                                  const uint32_t* __restrict__ order,
+                                                  const uint32_t* __restrict__ order_count,
+                                                  const uint32_t* __restrict__ num_admitted,
+                                                  const uint64_t* __restrict__ cold,
+                                                  const uint32_t* __restrict__ member_off,
+                                                  uint16_t* __restrict__ members, double* __restrict__ load,
+                                                  uint32_t* __restrict__ route)
+{
+    const uint32_t p = blockIdx.x, lane = lane_id();
+    const cr_plan_spec spec = specs[p];
+    const uint32_t A = num_admitted[p];
+    const uint32_t w = spec.window < NW ? spec.window : 0u;
+    const uint32_t* __restrict__ ord = order + (uint64_t)w * Cmax;
+    const uint32_t* __restrict__ ocnt = order_count + (uint64_t)w * Cmax;
+    const uint32_t* __restrict__ moff = member_off + (uint64_t)p * (Cmax + 1u);
+    uint16_t* __restrict__ mem = members + (uint64_t)p * Cmax;
+    const uint64_t rbase = (uint64_t)(p / cands) * K;
+    const uint32_t cidx = p % cands;
+    double Lv = lane < R ? (double)cold[p] / (double)R : INFINITY;
+    uint32_t rv = lane < R ? lane : 0xFFFFu;
+    LptBatch nxt = lpt_load(ord, ocnt, moff, lane, A);
+    for (uint32_t a0 = 0; a0 < A; a0 += 64) {
+        const LptBatch cur = nxt;
+        nxt = lpt_load(ord, ocnt, moff, a0 + 64 + lane, A);
+        const uint32_t nb = A - a0 < 64u ? A - a0 : 64u;
+        const uint32_t k_l = cur.end - cur.off;
+        const double x_l = k_l == 1 ? (double)cur.cnt : (double)cur.cnt / (double)k_l;
+        uint32_t first = 0;  // lane t: least-loaded member chosen for key t of the batch
+        for (uint32_t t = 0; t < nb; ++t) {
+            const uint32_t k = rdlane(k_l, t);
+            const double x = rdlane_f64(x_l, t);
+            const uint32_t r0 = rdlane(rv, 0);
+            first = lane == t ? r0 : first;
+            if (k == 1) {
+                const double v = rdlane_f64(Lv, 0) + x;
+                const bool less = lane != 0 && (Lv < v || (Lv == v && rv < r0));
+                const uint32_t pos = (uint32_t)__popcll(ballot(less));
+                const double sl = dpp_shl1_f64(Lv);
+                const uint32_t sr = dpp_shl1(rv, rv);
+                if (lane < pos) {
+                    Lv = sl;
+                    rv = sr;
+                } else if (lane == pos) {
+                    Lv = v;
+                    rv = r0;
+                }
+            } else {
+                const uint32_t off = rdlane(cur.off, t);
+                if (lane < k) mem[off + lane] = (uint16_t)rv;
+                const double vnew = Lv + x;  // meaningful on lanes < k
+                const uint32_t rnew = rv;
+                const double sL = __shfl(Lv, (int)((lane + k) & 63u), 64);
+                const uint32_t sR = __shfl(rv, (int)((lane + k) & 63u), 64);
+                Lv = lane + k < 64u ? sL : INFINITY;
+                rv = lane + k < 64u ? sR : 0xFFFFu;
+                for (uint32_t u = 0; u < k; ++u) {
+                    const double v = rdlane_f64(vnew, u);
+                    const uint32_t r = rdlane(rnew, u);
+                    const bool less = Lv < v || (Lv == v && rv < r);
+                    const uint32_t pos = (uint32_t)__popcll(ballot(less));
+                    const double up = dpp_shr1_f64(Lv);
+                    const uint32_t upr = dpp_shr1(rv, rv);
+                    if (lane > pos) {
+                        Lv = up;
+                        rv = upr;
+                    } else if (lane == pos) {
+                        Lv = v;
+                        rv = r;
+                    }
+                }
+            }
+        }
+        if (lane < nb) {
+            if (k_l == 1) mem[cur.off] = (uint16_t)first;
+            route[(rbase + cur.key) * cands + cidx] = k_l == 1 ? (CR_ROUTE_SINGLE | first) : (a0 + lane);
+        }
+    }
+    if (lane < R) load[(uint64_t)p * R + rv] = Lv;
+}
+
+// R > 64: lane l holds destinations l, l+64, ... (kS registers); each pick is a register
+// scan plus a cross-lane (L, r) argmin.
 template <int kS>
-__global__ __launch_bounds__(64) void k_lpt(const uint32_t* __restrict__ counts, uint32_t K, uint32_t R,
-                                            uint32_t Cmax, uint32_t NW, uint32_t cands,
+__global__ __launch_bounds__(64) void k_lpt(uint32_t K, uint32_t R, uint32_t Cmax, uint32_t NW, uint32_t cands,
                                             const cr_plan_spec* __restrict__ specs,
                                             const uint32_t* __restrict__ order,
+                                            const uint32_t* __restrict__ order_count,
                                             const uint32_t* __restrict__ num_admitted,
                                             const uint64_t* __restrict__ cold,
                                             const uint32_t* __restrict__ member_off, uint16_t* __restrict__ members,
@@ -314,28 +447,27 @@ __global__ __launch_bounds__(64) void k_lpt(const uint32_t* __restrict__ counts,
     const uint32_t A = num_admitted[p];
     const uint32_t w = spec.window < NW ? spec.window : 0u;
     const uint32_t* __restrict__ ord = order + (uint64_t)w * Cmax;
-    const uint32_t* __restrict__ row = counts + (uint64_t)w * K;
+    const uint32_t* __restrict__ ocnt = order_count + (uint64_t)w * Cmax;
     const uint32_t* __restrict__ moff = member_off + (uint64_t)p * (Cmax + 1u);
     uint16_t* __restrict__ mem = members + (uint64_t)p * Cmax;
-    const uint32_t g = p / cands, cidx = p % cands;
+    const uint64_t rbase = (uint64_t)(p / cands) * K;
+    const uint32_t cidx = p % cands;
     const double init = (double)cold[p] / (double)R;
     double Lr[kS];
 #pragma unroll
     for (int s = 0; s < kS; ++s) Lr[s] = (s * 64u + lane < R) ? init : INFINITY;
     uint32_t taken = 0;
+    LptBatch nxt = lpt_load(ord, ocnt, moff, lane, A);
     for (uint32_t a0 = 0; a0 < A; a0 += 64) {
-        const uint32_t a = a0 + lane;
-        const bool v = a < A;
-        const uint32_t key_l = v ? ord[a] : 0u;
-        const uint32_t cnt_l = v ? row[key_l] : 0u;
-        const uint32_t off_l = v ? moff[a] : 0u;
-        const uint32_t end_l = v ? moff[a + 1] : 0u;
+        const LptBatch cur = nxt;
+        nxt = lpt_load(ord, ocnt, moff, a0 + 64 + lane, A);
         const uint32_t nb = A - a0 < 64u ? A - a0 : 64u;
+        const uint32_t k_l = cur.end - cur.off;
+        const double x_l = k_l == 1 ? (double)cur.cnt : (double)cur.cnt / (double)k_l;
+        uint32_t first = 0;
         for (uint32_t t = 0; t < nb; ++t) {
-            const uint32_t key = rdlane(key_l, t), cnt = rdlane(cnt_l, t);
-            const uint32_t off = rdlane(off_l, t), k = rdlane(end_l, t) - off;
-            const double x = (double)cnt / (double)k;
-            uint32_t first = 0;
+            const uint32_t off = rdlane(cur.off, t), k = rdlane(k_l, t);
+            const double x = rdlane_f64(x_l, t);
             for (uint32_t m = 0; m < k; ++m) {
                 double bv = INFINITY;
                 uint32_t br = 0xFFFFFFFFu;
@@ -356,16 +488,18 @@ __global__ __launch_bounds__(64) void k_lpt(const uint32_t* __restrict__ counts,
                         br = orr;
                     }
                 }
-                if (lane == 0) mem[off + m] = (uint16_t)br;
+                if (k > 1 && lane == 0) mem[off + m] = (uint16_t)br;
                 if ((br & 63u) == lane) taken |= 1u << (br >> 6);
-                if (m == 0) first = br;
+                if (m == 0 && lane == t) first = br;
             }
 #pragma unroll
             for (int s = 0; s < kS; ++s)
                 if ((taken >> s) & 1u) Lr[s] = Lr[s] + x;
             taken = 0;
-            if (lane == 0)
-                route[((uint64_t)g * K + key) * cands + cidx] = (k == 1) ? (CR_ROUTE_SINGLE | first) : (a0 + t);
+        }
+        if (lane < nb) {
+            if (k_l == 1) mem[cur.off] = (uint16_t)first;
+            route[(rbase + cur.key) * cands + cidx] = k_l == 1 ? (CR_ROUTE_SINGLE | first) : (a0 + lane);
         }
     }
 #pragma unroll
@@ -381,7 +515,7 @@ bool valid_set(const cr_plan_set* ps)
     if (ps->num_plans == 0 || ps->cands == 0 || ps->cands > CR_MAX_CANDS || ps->num_plans % ps->cands) return false;
     if (ps->R == 0 || ps->R > CR_MAX_R || ps->max_W == 0 || ps->max_W > CR_MAX_W) return false;
     if (ps->num_keys == 0 || ps->num_keys == 0xFFFFFFFFu || ps->num_windows == 0) return false;
-    if (!ps->specs || !ps->order || !ps->n_order || !ps->num_admitted || !ps->cold || !ps->clamped ||
+    if (!ps->specs || !ps->order || !ps->order_count || !ps->n_order || !ps->num_admitted || !ps->cold || !ps->clamped ||
         !ps->member_off || !ps->members || !ps->load || !ps->route)
         return false;
     return true;
@@ -407,11 +541,14 @@ extern "C" cr_status cr_admit(const uint32_t* counts, const cr_plan_set* plans, 
     uint2* buf = reinterpret_cast<uint2*>(base);
     uint64_t* row_sum = reinterpret_cast<uint64_t*>(base + (uint64_t)plans->num_windows * 2u * cmax * sizeof(uint2));
     const hipStream_t st = as_stream(stream);
+    const uint32_t ng = plans->num_plans / plans->cands;
+    const uint64_t route_words = (uint64_t)ng * plans->num_keys * plans->cands;
     (void)hipGetLastError();
+    hipLaunchKernelGGL(k_fill_u32, dim3(1024), dim3(256), 0, st, plans->route, route_words, CR_ROUTE_COLD);
     hipLaunchKernelGGL(k_sort_window, dim3(plans->num_windows), dim3(kSortThreads), 0, st, counts, plans->num_keys,
-                       cmax, plans->order, plans->n_order, row_sum, buf);
-    hipLaunchKernelGGL(k_admit_plan, dim3(plans->num_plans), dim3(kSortThreads), 0, st, counts, plans->num_keys,
-                       plans->R, cmax, plans->num_windows, plans->specs, plans->order, plans->n_order, row_sum,
+                       cmax, plans->order, plans->order_count, plans->n_order, row_sum, buf);
+    hipLaunchKernelGGL(k_admit_plan, dim3(plans->num_plans), dim3(kSortThreads), 0, st, plans->R, cmax,
+                       plans->num_windows, plans->specs, plans->order_count, plans->n_order, row_sum,
                        plans->num_admitted, plans->cold, plans->clamped, plans->member_off, err);
     return hipGetLastError() == hipSuccess ? CR_OK : CR_EHIP;
 }
@@ -422,17 +559,21 @@ extern "C" cr_status cr_place_lpt(const uint32_t* counts, const cr_plan_set* pla
     if (!counts || !valid_set(plans)) return CR_EINVAL;
     const uint32_t cmax = plans->R * plans->max_W;
     const hipStream_t st = as_stream(stream);
-    const uint32_t ng = plans->num_plans / plans->cands;
-    const uint64_t route_words = (uint64_t)ng * plans->num_keys * plans->cands;
     (void)hipGetLastError();
-    hipLaunchKernelGGL(k_fill_u32, dim3(1024), dim3(256), 0, st, plans->route, route_words, CR_ROUTE_COLD);
+    if (plans->R <= 64) {
+        hipLaunchKernelGGL(k_lpt_small, dim3(plans->num_plans), dim3(64), 0, st, plans->num_keys, plans->R, cmax,
+                           plans->num_windows, plans->cands, plans->specs, plans->order, plans->order_count,
+                           plans->num_admitted, plans->cold, plans->member_off, plans->members, plans->load,
+                           plans->route);
+        return hipGetLastError() == hipSuccess ? CR_OK : CR_EHIP;
+    }
 #define CR_LPT(S)                                                                                                   \
-    hipLaunchKernelGGL(k_lpt<S>, dim3(plans->num_plans), dim3(64), 0, st, counts, plans->num_keys, plans->R, cmax, \
-                       plans->num_windows, plans->cands, plans->specs, plans->order, plans->num_admitted,          \
-                       plans->cold, plans->member_off, plans->members, plans->load, plans->route)
+    hipLaunchKernelGGL(k_lpt<S>, dim3(plans->num_plans), dim3(64), 0, st, plans->num_keys, plans->R, cmax,        \
+                       plans->num_windows, plans->cands, plans->specs, plans->order, plans->order_count,           \
+                       plans->num_admitted, plans->cold, plans->member_off, plans->members, plans->load,           \
+                       plans->route)
     const uint32_t s = (plans->R + 63) / 64;
-    if (s <= 1) CR_LPT(1);
-    else if (s <= 2) CR_LPT(2);
+    if (s <= 2) CR_LPT(2);
     else if (s <= 4) CR_LPT(4);
     else if (s <= 8) CR_LPT(8);
     else CR_LPT(16);

@@ -3,7 +3,7 @@
 // equal-slot model: W whole-prefix slots per destination).
 //
 // Pipeline (all on the caller's stream, workspace from the caller):
-//   k_part_hist / k_part_scan / k_part_scatter
+//   k_part_hist / k_scan_* / k_part_scatter
 //        stable partition of every candidate's requests by destination, preserving
 //        arrival order; each record packs (key, suffix, interval) into 8 bytes;
 //   k_seg_items
@@ -75,40 +75,75 @@ __global__ __launch_bounds__(256) void k_part_hist(const uint16_t* __restrict__ 
     if (bad) atomicOr(err, CR_ERR_DEST_RANGE);
 }
 
-// One block per candidate: exclusive scan of tcnt[c][d][tile] in (d, tile) order.
-__global__ __launch_bounds__(1024) void k_part_scan(uint32_t* __restrict__ tcnt, uint32_t R, uint64_t ntiles,
-                                                    uint32_t* __restrict__ grp_off)
+// Exclusive scan of tcnt[c][d][tile] in (d, tile) order, per candidate, in three phases
+// over chunks of kScanChunk entries: chunk sums, a scan of the chunk sums, and a rescan of
+// every chunk from its offset. The first tile of each destination gives its group offset.
+constexpr uint32_t kScanThreads = 1024;
+constexpr uint32_t kScanChunk = 4 * kScanThreads;
+
+__global__ __launch_bounds__(kScanThreads) void k_scan_reduce(const uint32_t* __restrict__ tcnt, uint64_t len,
+                                                              uint32_t nblk, uint32_t* __restrict__ bsum)
+{
+    __shared__ uint32_t s_scan[16];
+    const uint32_t c = blockIdx.y, blk = blockIdx.x;
+    const uint32_t* __restrict__ t = tcnt + (uint64_t)c * len;
+    const uint64_t e = (uint64_t)blk * kScanChunk + 4u * threadIdx.x;
+    uint32_t s = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) s += e + q < len ? t[e + q] : 0u;
+    uint32_t tot;
+    (void)block_exscan_u32(s, s_scan, &tot);
+    if (threadIdx.x == 0) bsum[(uint64_t)c * nblk + blk] = tot;
+}
+
+__global__ __launch_bounds__(kScanThreads) void k_scan_mid(uint32_t* __restrict__ bsum, uint32_t nblk, uint32_t R,
+                                                           uint32_t* __restrict__ grp_off)
 {
     __shared__ uint32_t s_scan[16];
     const uint32_t c = blockIdx.x;
-    uint32_t* __restrict__ t = tcnt + (uint64_t)c * R * ntiles;
-    const uint64_t len = (uint64_t)R * ntiles;
+    uint32_t* __restrict__ b = bsum + (uint64_t)c * nblk;
     uint32_t carry = 0;
-    for (uint64_t e0 = 0; e0 < len; e0 += 4u * blockDim.x) {
-        const uint64_t e = e0 + 4u * threadIdx.x;
-        uint32_t v[4];
-        uint32_t s = 0;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            v[q] = e + q < len ? t[e + q] : 0u;
-            s += v[q];
-        }
+    for (uint32_t e0 = 0; e0 < nblk; e0 += kScanThreads) {
+        const uint32_t e = e0 + threadIdx.x;
+        const uint32_t v = e < nblk ? b[e] : 0u;
         uint32_t tot;
-        uint32_t ex = block_exscan_u32(s, s_scan, &tot) + carry;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            if (e + q < len) t[e + q] = ex;
-            ex += v[q];
-        }
+        const uint32_t ex = block_exscan_u32(v, s_scan, &tot);
+        if (e < nblk) b[e] = carry + ex;
         carry += tot;
     }
-    __syncthreads();
-    uint32_t* __restrict__ go = grp_off + (uint64_t)c * (R + 1u);
-    for (uint32_t d = threadIdx.x; d < R; d += blockDim.x) go[d] = ntiles ? t[(uint64_t)d * ntiles] : 0u;
-    if (threadIdx.x == 0) go[R] = carry;
+    if (threadIdx.x == 0) grp_off[(uint64_t)c * (R + 1u) + R] = carry;
 }
 
-// One wavefront per (tile, candidate): stable scatter into packed records.
+__global__ __launch_bounds__(kScanThreads) void k_scan_apply(uint32_t* __restrict__ tcnt, uint64_t len,
+                                                             uint64_t ntiles, uint32_t R, uint32_t nblk,
+                                                             const uint32_t* __restrict__ bsum,
+                                                             uint32_t* __restrict__ grp_off)
+{
+    __shared__ uint32_t s_scan[16];
+    const uint32_t c = blockIdx.y, blk = blockIdx.x;
+    uint32_t* __restrict__ t = tcnt + (uint64_t)c * len;
+    const uint64_t e = (uint64_t)blk * kScanChunk + 4u * threadIdx.x;
+    uint32_t v[4], s = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        v[q] = e + q < len ? t[e + q] : 0u;
+        s += v[q];
+    }
+    uint32_t tot;
+    uint32_t ex = block_exscan_u32(s, s_scan, &tot) + bsum[(uint64_t)c * nblk + blk];
+    uint32_t* __restrict__ go = grp_off + (uint64_t)c * (R + 1u);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        if (e + q < len) {
+            t[e + q] = ex;
+            if ((e + q) % ntiles == 0) go[(e + q) / ntiles] = ex;
+        }
+        ex += v[q];
+    }
+}
+
+// One wavefront per (tile, candidate): stable scatter into packed records. The next 64
+// requests are loaded while the current 64 are ranked and written.
 __global__ __launch_bounds__(64) void k_part_scatter(const uint32_t* __restrict__ keys,
                                                      const uint16_t* __restrict__ suffix,
                                                      const uint16_t* __restrict__ dest, uint64_t n,
@@ -125,11 +160,18 @@ __global__ __launch_bounds__(64) void k_part_scatter(const uint32_t* __restrict_
     const uint16_t* __restrict__ dc = dest + (uint64_t)c * n;
     uint64_t* __restrict__ rc = rec + (uint64_t)c * n;
     uint32_t j = find_interval(off, J, t0);
+    uint64_t i = t0 + lane;
+    uint32_t nd = i < t1 ? dc[i] : 0xFFFFu;
+    uint32_t nk = i < t1 ? keys[i] : 0u;
+    uint32_t ns = i < t1 ? suffix[i] : 0u;
     for (uint64_t base = t0; base < t1; base += 64) {
-        const uint64_t i = base + lane;
-        const bool in = i < t1;
-        const uint32_t d = in ? dc[i] : 0xFFFFu;
-        const bool valid = in && d < R;
+        i = base + lane;
+        const uint32_t d = nd, key = nk, sfx = ns;
+        const uint64_t in2 = i + 64;
+        nd = in2 < t1 ? dc[in2] : 0xFFFFu;
+        nk = in2 < t1 ? keys[in2] : 0u;
+        ns = in2 < t1 ? suffix[in2] : 0u;
+        const bool valid = i < t1 && d < R;
         uint32_t jl = j;
         while (jl + 1 < J && off[jl + 1] <= i) ++jl;
         uint64_t peers = ballot(valid);
@@ -141,7 +183,7 @@ __global__ __launch_bounds__(64) void k_part_scatter(const uint32_t* __restrict_
         const uint32_t rk = (uint32_t)__popcll(peers & lanemask_lt());
         if (valid) {
             const uint32_t pos = run[d] + rk;
-            rc[pos] = (uint64_t)keys[i] | ((uint64_t)suffix[i] << 32) | ((uint64_t)jl << 48);
+            rc[pos] = (uint64_t)key | ((uint64_t)sfx << 32) | ((uint64_t)jl << 48);
         }
         __syncthreads();
         if (valid && rk == 0) run[d] += (uint32_t)__popcll(peers);
@@ -202,9 +244,9 @@ __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v)
 template <int SL>
 __global__ __launch_bounds__(kReplayThreads) void k_replay(
     const uint64_t* __restrict__ rec, uint64_t n, const uint32_t* __restrict__ grp_off,
-    const uint32_t* __restrict__ item_off, uint32_t P, uint32_t R, uint32_t K, uint32_t J, const uint32_t* __restrict__ prefix_len,
-    WArg wa, uint32_t max_W, const uint32_t* __restrict__ lru_in, uint32_t* __restrict__ lru_out,
-    uint64_t* __restrict__ stats, uint32_t* __restrict__ err)
+    const uint32_t* __restrict__ item_off, uint32_t P, uint32_t R, uint32_t K, uint32_t J,
+    const uint32_t* __restrict__ prefix_len, WArg wa, uint32_t max_W, const uint32_t* __restrict__ lru_in,
+    uint32_t* __restrict__ lru_out, uint64_t* __restrict__ stats, uint32_t* __restrict__ err)
 {
     const uint32_t lane = lane_id();
     const uint64_t item = (uint64_t)blockIdx.x * (kReplayThreads / 64) + (threadIdx.x >> 6);
@@ -223,7 +265,9 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
     const uint32_t* go = grp_off + (uint64_t)c * (R + 1u);
     const uint32_t gs = go[d], cnt = go[d + 1] - gs;
     const uint32_t S = seg_len(W);
-    const uint32_t s0 = seg * S;
+    const uint64_t s0w = (uint64_t)seg * S;
+    if (s0w > cnt) return;  // only if the partition used other slot counts
+    const uint32_t s0 = (uint32_t)s0w;
     const uint32_t s1 = cnt - s0 < S ? cnt : s0 + S;
     const uint64_t* __restrict__ rl = rec + (uint64_t)c * n + gs;
 
@@ -234,20 +278,28 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
         skey[s] = CR_EMPTY_SLOT;
         srank[s] = idx < W ? idx : 0xFFFFFFFFu;
     }
-    // State before the segment: most recent W distinct keys, newest first.
+    // State before the segment: the most recent W distinct keys, newest first. Records are
+    // read backwards 64 at a time, the next (older) batch in flight while one is scanned.
     uint32_t q = 0;
-    for (uint32_t pos = s0; q < W && pos > 0;) {
-        const uint32_t nb = pos < 64u ? pos : 64u;
-        const uint32_t kl = lane < nb ? (uint32_t)rl[pos - nb + lane] : CR_EMPTY_SLOT;
-        for (int t = (int)nb - 1; t >= 0 && q < W; --t) {
-            const uint32_t kk = rdlane(kl, (uint32_t)t);
-            if (kk >= K) continue;
-            if (!lru_contains<SL>(skey, kk)) {
-                lru_put_slot<SL>(skey, q, kk, lane);
-                ++q;
+    {
+        uint32_t pos = s0;
+        uint32_t nb = pos < 64u ? pos : 64u;
+        uint32_t kl_next = lane < nb ? (uint32_t)rl[pos - nb + lane] : CR_EMPTY_SLOT;
+        while (q < W && pos > 0) {
+            const uint32_t kl = kl_next;
+            const uint32_t cnb = nb;
+            pos -= cnb;
+            nb = pos < 64u ? pos : 64u;
+            kl_next = lane < nb ? (uint32_t)rl[pos - nb + lane] : CR_EMPTY_SLOT;
+            for (int t = (int)cnb - 1; t >= 0 && q < W; --t) {
+                const uint32_t kk = rdlane(kl, (uint32_t)t);
+                if (kk >= K) continue;
+                if (!lru_contains<SL>(skey, kk)) {
+                    lru_put_slot<SL>(skey, q, kk, lane);
+                    ++q;
+                }
             }
         }
-        pos -= nb;
     }
     if (q < W && lru_in) {
         const uint32_t* __restrict__ li = lru_in + ((uint64_t)c * R + d) * max_W;
@@ -286,15 +338,16 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
         }
         a_req = a_hit = a_pre = a_hp = 0;
     };
+    // Forward replay; the next batch of records is in flight while one is replayed.
+    uint64_t rv_next = s0 + lane < s1 ? rl[s0 + lane] : 0ull;
     for (uint32_t b0 = s0; b0 < s1; b0 += 64) {
         const uint32_t nb = s1 - b0 < 64u ? s1 - b0 : 64u;
-        const uint64_t rv = lane < nb ? rl[b0 + lane] : 0ull;
+        const uint64_t rv = rv_next;
+        rv_next = b0 + 64u + lane < s1 ? rl[b0 + 64u + lane] : 0ull;
         const uint32_t kl = lane < nb ? (uint32_t)rv : CR_EMPTY_SLOT;
-        const uint32_t sfx = (uint32_t)(rv >> 32) & 0xFFFFu;
-        const uint32_t ivl = (uint32_t)(rv >> 48);
         const bool vl = lane < nb && kl < K;
         bad |= lane < nb && kl >= K;
-        const uint32_t pl = vl ? prefix_len[kl] : 0u;
+        const uint32_t pl = vl ? prefix_len[kl] : 0u;  // consumed after the batch
         uint64_t hm = 0;
         for (uint32_t t = 0; t < nb; ++t) {
             const uint32_t kk = rdlane(kl, t);
@@ -318,6 +371,8 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
             }
             hm |= (uint64_t)hit << t;
         }
+        const uint32_t sfx = (uint32_t)(rv >> 32) & 0xFFFFu;
+        const uint32_t ivl = (uint32_t)(rv >> 48);
         const bool hl = (hm >> lane) & 1ull;
         uint64_t rem = ballot(vl);
         while (rem) {
@@ -349,36 +404,72 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
     }
 }
 
+__global__ void k_zero32(uint32_t* __restrict__ p, uint64_t n)
+{
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (uint64_t)gridDim.x * blockDim.x)
+        p[i] = 0u;
+}
+
 struct ReplayWs {
     uint64_t* rec;
     uint32_t* tcnt;
+    uint32_t* bsum;
     uint32_t* grp_off;
     uint32_t* item_off;
     size_t bytes;
 };
 
+inline uint32_t scan_blocks(uint64_t n, uint32_t P, uint32_t R)
+{
+    const PartGeom g = part_geom(n, P);
+    return (uint32_t)(((uint64_t)R * g.ntiles + kScanChunk - 1) / kScanChunk);
+}
+
 inline ReplayWs replay_layout(void* base, uint64_t n, uint32_t P, uint32_t R)
 {
     const PartGeom g = part_geom(n, P);
+    const uint32_t nblk = scan_blocks(n, P, R);
     auto up = [](uint64_t x) { return (x + 255) & ~255ull; };
+    uint8_t* b = reinterpret_cast<uint8_t*>(base);
     uint64_t o = 0;
     ReplayWs w{};
-    uint8_t* b = reinterpret_cast<uint8_t*>(base);
-    const uint64_t o_rec = o;
+    w.rec = reinterpret_cast<uint64_t*>(b + o);
     o = up(o + (uint64_t)P * n * 8u);
-    const uint64_t o_t = o;
+    w.tcnt = reinterpret_cast<uint32_t*>(b + o);
     o = up(o + (uint64_t)P * R * g.ntiles * 4u);
-    const uint64_t o_g = o;
+    w.bsum = reinterpret_cast<uint32_t*>(b + o);
+    o = up(o + (uint64_t)P * (nblk + 1u) * 4u);
+    w.grp_off = reinterpret_cast<uint32_t*>(b + o);
     o = up(o + (uint64_t)P * (R + 1u) * 4u);
-    const uint64_t o_i = o;
+    w.item_off = reinterpret_cast<uint32_t*>(b + o);
     o = up(o + ((uint64_t)P * R + 1u) * 4u);
-    w.rec = reinterpret_cast<uint64_t*>(b + o_rec);
-    w.tcnt = reinterpret_cast<uint32_t*>(b + o_t);
-    w.grp_off = reinterpret_cast<uint32_t*>(b + o_g);
-    w.item_off = reinterpret_cast<uint32_t*>(b + o_i);
     w.bytes = (size_t)o + 256u;
     return w;
 }
+
+struct ReplayArgs {
+    WArg wa;
+    uint32_t classes;
+};
+
+inline cr_status replay_args(uint64_t n, uint32_t J, uint32_t P, uint32_t R, const uint32_t* W, uint32_t max_W,
+                             size_t ws_bytes, void* ws, ReplayArgs* ra)
+{
+    if (P == 0 || P > CR_MAX_CANDS || R == 0 || R > CR_MAX_R || J == 0 || J > CR_MAX_J || !W || max_W == 0 ||
+        max_W > CR_MAX_W || !ws || n >= 0xFFFFFFFFull)
+        return CR_EINVAL;
+    ra->wa = WArg{};
+    ra->classes = 0;
+    for (uint32_t c = 0; c < P; ++c) {
+        if (W[c] == 0 || W[c] > max_W) return CR_EINVAL;
+        ra->wa.W[c] = (uint16_t)W[c];
+        ra->classes |= slot_class(W[c]);
+    }
+    if (ws_bytes < replay_layout(nullptr, n, P, R).bytes) return CR_ESIZE;
+    return CR_OK;
+}
+
+inline void* ws_base(void* ws) { return reinterpret_cast<void*>(((uintptr_t)ws + 255) & ~(uintptr_t)255); }
 
 }  // namespace
 }  // namespace cr
@@ -388,32 +479,21 @@ extern "C" size_t cr_replay_workspace_bytes(uint64_t n, uint32_t P, uint32_t R)
     return cr::replay_layout(nullptr, n, P, R).bytes;
 }
 
-extern "C" cr_status cr_replay(const uint32_t* keys, const uint16_t* suffix, const uint32_t* prefix_len,
-                               uint32_t num_keys, const uint16_t* dest, uint64_t n, const uint64_t* off, uint32_t J,
-                               uint32_t P, uint32_t R, const uint32_t* W, uint32_t max_W, const uint32_t* lru_in,
-                               uint32_t* lru_out, uint64_t* stats, void* ws, size_t ws_bytes, uint32_t* err,
-                               void* stream)
+extern "C" cr_status cr_replay_partition(const uint32_t* keys, const uint16_t* suffix, const uint16_t* dest,
+                                         uint64_t n, const uint64_t* off, uint32_t J, uint32_t P, uint32_t R,
+                                         const uint32_t* W, void* ws, size_t ws_bytes, uint32_t* err, void* stream)
 {
     using namespace cr;
-    if (P == 0 || P > CR_MAX_CANDS || R == 0 || R > CR_MAX_R || J == 0 || J > CR_MAX_J || !W || max_W == 0 ||
-        max_W > CR_MAX_W || num_keys == 0 || num_keys == 0xFFFFFFFFu || !off || !lru_out || !stats || !ws || !err ||
-        !prefix_len)
-        return CR_EINVAL;
-    if (n > 0 && (!keys || !suffix || !dest)) return CR_EINVAL;
-    if (n >= 0xFFFFFFFFull) return CR_EINVAL;
-    if (lru_in && lru_in < lru_out + (uint64_t)P * R * max_W && lru_out < lru_in + (uint64_t)P * R * max_W)
-        return CR_EINVAL;
-    WArg wa{};
-    uint32_t classes = 0;
-    for (uint32_t c = 0; c < P; ++c) {
-        if (W[c] == 0 || W[c] > max_W) return CR_EINVAL;
-        wa.W[c] = (uint16_t)W[c];
-        classes |= slot_class(W[c]);
-    }
-    if (ws_bytes < cr_replay_workspace_bytes(n, P, R)) return CR_ESIZE;
-    void* base = reinterpret_cast<void*>(((uintptr_t)ws + 255) & ~(uintptr_t)255);
-    const ReplayWs w = replay_layout(base, n, P, R);
+    ReplayArgs ra;
+    uint32_t mw = 0;
+    for (uint32_t c = 0; W && c < P && c < CR_MAX_CANDS; ++c) mw = W[c] > mw ? W[c] : mw;
+    const cr_status v = replay_args(n, J, P, R, W, mw ? mw : 1u, ws_bytes, ws, &ra);
+    if (v != CR_OK) return v;
+    if (!off || !err || (n > 0 && (!keys || !suffix || !dest))) return CR_EINVAL;
+    const ReplayWs w = replay_layout(ws_base(ws), n, P, R);
     const PartGeom g = part_geom(n, P);
+    const uint32_t nblk = scan_blocks(n, P, R);
+    const uint64_t len = (uint64_t)R * g.ntiles;
     const hipStream_t st = as_stream(stream);
     uint32_t nbits = 0;
     while ((1u << nbits) < R) ++nbits;
@@ -421,24 +501,68 @@ extern "C" cr_status cr_replay(const uint32_t* keys, const uint16_t* suffix, con
     if (g.ntiles) {
         hipLaunchKernelGGL(k_part_hist, dim3((uint32_t)g.ntiles, P), dim3(256), (size_t)R * 4u, st, dest, n, R, g.tile,
                            g.ntiles, w.tcnt, err);
+        hipLaunchKernelGGL(k_scan_reduce, dim3(nblk, P), dim3(kScanThreads), 0, st, w.tcnt, len, nblk, w.bsum);
+    } else {
+        hipLaunchKernelGGL(k_zero32, dim3(64), dim3(256), 0, st, w.grp_off, (uint64_t)P * (R + 1u));
     }
-    hipLaunchKernelGGL(k_part_scan, dim3(P), dim3(1024), 0, st, w.tcnt, R, g.ntiles, w.grp_off);
+    hipLaunchKernelGGL(k_scan_mid, dim3(P), dim3(kScanThreads), 0, st, w.bsum, nblk, R, w.grp_off);
     if (g.ntiles) {
-        hipLaunchKernelGGL(k_part_scatter, dim3((uint32_t)g.ntiles, P), dim3(64), (size_t)R * 4u, st, keys, suffix, dest,
-                           n, off, J, R, nbits, g.tile, g.ntiles, w.tcnt, w.rec);
+        hipLaunchKernelGGL(k_scan_apply, dim3(nblk, P), dim3(kScanThreads), 0, st, w.tcnt, len, g.ntiles, R, nblk,
+                           w.bsum, w.grp_off);
+        hipLaunchKernelGGL(k_part_scatter, dim3((uint32_t)g.ntiles, P), dim3(64), (size_t)R * 4u, st, keys, suffix,
+                           dest, n, off, J, R, nbits, g.tile, g.ntiles, w.tcnt, w.rec);
     }
-    hipLaunchKernelGGL(k_seg_items, dim3(1), dim3(1024), 0, st, w.grp_off, P, R, wa, w.item_off);
+    hipLaunchKernelGGL(k_seg_items, dim3(1), dim3(1024), 0, st, w.grp_off, P, R, ra.wa, w.item_off);
+    return hipGetLastError() == hipSuccess ? CR_OK : CR_EHIP;
+}
+
+extern "C" cr_status cr_replay_lru(const uint32_t* prefix_len, uint32_t num_keys, uint64_t n, uint32_t J,
+                                   uint32_t P, uint32_t R, const uint32_t* W, uint32_t max_W, const uint32_t* lru_in,
+                                   uint32_t* lru_out, uint64_t* stats, void* ws, size_t ws_bytes, uint32_t* err,
+                                   void* stream)
+{
+    using namespace cr;
+    ReplayArgs ra;
+    const cr_status v = replay_args(n, J, P, R, W, max_W, ws_bytes, ws, &ra);
+    if (v != CR_OK) return v;
+    if (num_keys == 0 || num_keys == 0xFFFFFFFFu || !prefix_len || !lru_out || !stats || !err) return CR_EINVAL;
+    if (lru_in && lru_in < lru_out + (uint64_t)P * R * max_W && lru_out < lru_in + (uint64_t)P * R * max_W)
+        return CR_EINVAL;
+    const ReplayWs w = replay_layout(ws_base(ws), n, P, R);
+    const hipStream_t st = as_stream(stream);
     // Upper bound on work items: one per (c, d) plus one per full segment.
     const uint64_t items = (uint64_t)P * R + (uint64_t)P * n / 2048u + 1u;
     const uint64_t blocks = (items + (kReplayThreads / 64) - 1) / (kReplayThreads / 64);
     if (blocks > 0x7FFFFFFFull) return CR_EINVAL;
+    (void)hipGetLastError();
 #define CR_REPLAY(SL)                                                                                               \
     hipLaunchKernelGGL(k_replay<SL>, dim3((uint32_t)blocks), dim3(kReplayThreads), 0, st, w.rec, n, w.grp_off,       \
-                       w.item_off, P, R, num_keys, J, prefix_len, wa, max_W, lru_in, lru_out, stats, err)
-    if (classes & 1u) CR_REPLAY(1);
-    if (classes & 2u) CR_REPLAY(2);
-    if (classes & 4u) CR_REPLAY(4);
-    if (classes & 8u) CR_REPLAY(8);
+                       w.item_off, P, R, num_keys, J, prefix_len, ra.wa, max_W, lru_in, lru_out, stats, err)
+    if (ra.classes & 1u) CR_REPLAY(1);
+    if (ra.classes & 2u) CR_REPLAY(2);
+    if (ra.classes & 4u) CR_REPLAY(4);
+    if (ra.classes & 8u) CR_REPLAY(8);
 #undef CR_REPLAY
     return hipGetLastError() == hipSuccess ? CR_OK : CR_EHIP;
+}
+
+extern "C" cr_status cr_replay(const uint32_t* keys, const uint16_t* suffix, const uint32_t* prefix_len,
+                               uint32_t num_keys, const uint16_t* dest, uint64_t n, const uint64_t* off, uint32_t J,
+                               uint32_t P, uint32_t R, const uint32_t* W, uint32_t max_W, const uint32_t* lru_in,
+                               uint32_t* lru_out, uint64_t* stats, void* ws, size_t ws_bytes, uint32_t* err,
+                               void* stream)
+{
+    using namespace cr;
+    ReplayArgs ra;
+    cr_status v = replay_args(n, J, P, R, W, max_W, ws_bytes, ws, &ra);
+    if (v != CR_OK) return v;
+    if (num_keys == 0 || num_keys == 0xFFFFFFFFu || !prefix_len || !lru_out || !stats || !err || !off ||
+        (n > 0 && (!keys || !suffix || !dest)))
+        return CR_EINVAL;
+    if (lru_in && lru_in < lru_out + (uint64_t)P * R * max_W && lru_out < lru_in + (uint64_t)P * R * max_W)
+        return CR_EINVAL;
+    v = cr_replay_partition(keys, suffix, dest, n, off, J, P, R, W, ws, ws_bytes, err, stream);
+    if (v != CR_OK) return v;
+    return cr_replay_lru(prefix_len, num_keys, n, J, P, R, W, max_W, lru_in, lru_out, stats, ws, ws_bytes, err,
+                         stream);
 }

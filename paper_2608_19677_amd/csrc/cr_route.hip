@@ -3,29 +3,32 @@
 // hash, cold keys use power of two choices on the plan's interval-start loads.
 //
 // HBM-bound stream: 4 B key read + 2 B destination written per request and candidate.
-// The route table of a group is key-major ([key][candidate]) so one request reads one
-// contiguous row; rows of hot keys and the R loads stay in L2.
+// Each thread owns 4 consecutive requests: one 16-byte key load, 4 independent table
+// gathers per candidate (the route table of a group is key-major, [key][candidate], so a
+// request reads one contiguous row; rows of hot keys and the R loads stay in L2), and
+// one 8-byte store of 4 destinations per candidate.
 #include "cr_common.h"
 
 namespace cr {
 namespace {
 
 constexpr int kRouteThreads = 256;
-constexpr int kRouteItems = 8;
+constexpr int kPer = 4;
 
-__device__ __forceinline__ uint16_t route_one(uint32_t word, uint32_t h, uint32_t R, const double* __restrict__ L,
+__device__ __forceinline__ uint32_t route_one(uint32_t word, uint32_t h, uint32_t R, const double* __restrict__ L,
                                               const uint32_t* __restrict__ mo, const uint16_t* __restrict__ mem)
 {
     if (word == CR_ROUTE_COLD) {
         const uint32_t d1 = ((h & 0xFFFFu) * R) >> 16;
         const uint32_t d2 = ((h >> 16) * R) >> 16;
-        return (uint16_t)(L[d2] < L[d1] ? d2 : d1);
+        return L[d2] < L[d1] ? d2 : d1;
     }
-    if (word & CR_ROUTE_SINGLE) return (uint16_t)(word & 0xFFFFu);
+    if (word & CR_ROUTE_SINGLE) return word & 0xFFFFu;
     const uint32_t o = mo[word], k = mo[word + 1] - o;
     return mem[o + (((h >> 16) * k) >> 16)];
 }
 
+template <bool kVec>
 __global__ __launch_bounds__(kRouteThreads) void k_route(
     const uint32_t* __restrict__ keys, uint64_t n, uint64_t first_index, uint32_t smix,
     const uint64_t* __restrict__ off, const uint32_t* __restrict__ gmap, uint32_t J, uint32_t K, uint32_t R,
@@ -34,29 +37,55 @@ __global__ __launch_bounds__(kRouteThreads) void k_route(
     uint16_t* __restrict__ dest, uint32_t* __restrict__ err)
 {
     __shared__ uint32_t s_j0;
-    const uint64_t tile0 = (uint64_t)blockIdx.x * kRouteThreads * kRouteItems;
-    if (tile0 >= n) return;
-    if (threadIdx.x == 0) s_j0 = find_interval(off, J, tile0);
+    const uint64_t bstart = (uint64_t)blockIdx.x * kRouteThreads * kPer;
+    if (bstart >= n) return;
+    if (threadIdx.x == 0) s_j0 = find_interval(off, J, bstart);
     __syncthreads();
+    const uint64_t base = bstart + (uint64_t)threadIdx.x * kPer;
+    if (base >= n) return;
+    const bool full = kVec && base + kPer <= n;
+    uint32_t b[kPer], g[kPer], h[kPer];
+    if (full) {
+        const uint4 q = *reinterpret_cast<const uint4*>(keys + base);
+        b[0] = q.x;
+        b[1] = q.y;
+        b[2] = q.z;
+        b[3] = q.w;
+    } else {
+#pragma unroll
+        for (int t = 0; t < kPer; ++t) b[t] = base + t < n ? keys[base + t] : 0u;
+    }
     uint32_t j = s_j0;
     bool bad = false;
 #pragma unroll
-    for (int it = 0; it < kRouteItems; ++it) {
-        const uint64_t i = tile0 + (uint64_t)it * kRouteThreads + threadIdx.x;
-        if (i >= n) break;
+    for (int t = 0; t < kPer; ++t) {
+        const uint64_t i = base + t;
         while (j + 1 < J && off[j + 1] <= i) ++j;
-        uint32_t g = gmap[j];
-        g = g < NG ? g : NG - 1;
-        const uint32_t b = keys[i];
-        const bool valid = b < K;
+        const uint32_t gg = gmap[j];
+        g[t] = gg < NG ? gg : NG - 1;
+        h[t] = req_hash(smix, first_index + i);
+        const bool valid = i >= n || b[t] < K;
         bad |= !valid;
-        const uint32_t h = req_hash(smix, first_index + i);
-        const uint32_t* __restrict__ rw = route + ((uint64_t)g * K + (valid ? b : 0u)) * cands;
-        for (uint32_t c = 0; c < cands; ++c) {
-            const uint64_t p = (uint64_t)g * cands + c;
-            const uint32_t word = valid ? rw[c] : CR_ROUTE_COLD;
-            dest[(uint64_t)c * n + i] =
-                route_one(word, h, R, load + p * R, member_off + p * mo_stride, members + p * mem_stride);
+        if (!valid) b[t] = 0xFFFFFFFFu;
+    }
+    for (uint32_t c = 0; c < cands; ++c) {
+        uint32_t word[kPer], d[kPer];
+#pragma unroll
+        for (int t = 0; t < kPer; ++t)
+            word[t] = b[t] < K ? route[((uint64_t)g[t] * K + b[t]) * cands + c] : CR_ROUTE_COLD;
+#pragma unroll
+        for (int t = 0; t < kPer; ++t) {
+            const uint64_t p = (uint64_t)g[t] * cands + c;
+            d[t] = route_one(word[t], h[t], R, load + p * R, member_off + p * mo_stride, members + p * mem_stride);
+        }
+        uint16_t* __restrict__ dc = dest + (uint64_t)c * n + base;
+        if (full) {
+            const uint2 v = make_uint2(d[0] | (d[1] << 16), d[2] | (d[3] << 16));
+            *reinterpret_cast<uint2*>(dc) = v;
+        } else {
+#pragma unroll
+            for (int t = 0; t < kPer; ++t)
+                if (base + t < n) dc[t] = (uint16_t)d[t];
         }
     }
     if (bad) atomicOr(err, CR_ERR_KEY_RANGE);
@@ -76,15 +105,21 @@ extern "C" cr_status cr_route(const uint32_t* keys, uint64_t n, uint64_t first_i
         !plans->route || !plans->member_off || !plans->members || !plans->load)
         return CR_EINVAL;
     if (n == 0) return CR_OK;
-    if (!keys || !dest) return CR_EINVAL;
+    if (!keys || !dest || ((uintptr_t)keys & 3u) || ((uintptr_t)dest & 1u)) return CR_EINVAL;
     const uint32_t cmax = plans->R * plans->max_W;
-    const uint64_t per_block = (uint64_t)kRouteThreads * kRouteItems;
+    const uint64_t per_block = (uint64_t)kRouteThreads * kPer;
     const uint64_t blocks = (n + per_block - 1) / per_block;
     if (blocks > 0x7FFFFFFFull) return CR_EINVAL;
+    // 16-byte key loads and 8-byte destination stores need aligned rows.
+    const bool vec = ((uintptr_t)keys & 15u) == 0 && ((uintptr_t)dest & 7u) == 0 && (n & 3u) == 0;
     (void)hipGetLastError();
-    hipLaunchKernelGGL(k_route, dim3((uint32_t)blocks), dim3(kRouteThreads), 0, as_stream(stream), keys, n,
-                       first_index, seed_mix(seed), off, gmap, J, plans->num_keys, plans->R, plans->cands,
-                       plans->num_plans / plans->cands, plans->route, plans->member_off, cmax + 1u, plans->members,
-                       cmax, plans->load, dest, err);
+#define CR_ROUTE_LAUNCH(V)                                                                                         \
+    hipLaunchKernelGGL(k_route<V>, dim3((uint32_t)blocks), dim3(kRouteThreads), 0, as_stream(stream), keys, n,     \
+                       first_index, seed_mix(seed), off, gmap, J, plans->num_keys, plans->R, plans->cands,        \
+                       plans->num_plans / plans->cands, plans->route, plans->member_off, cmax + 1u, plans->members, \
+                       cmax, plans->load, dest, err)
+    if (vec) CR_ROUTE_LAUNCH(true);
+    else CR_ROUTE_LAUNCH(false);
+#undef CR_ROUTE_LAUNCH
     return hipGetLastError() == hipSuccess ? CR_OK : CR_EHIP;
 }

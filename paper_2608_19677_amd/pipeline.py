@@ -56,7 +56,7 @@ class Pipeline:
         self.max_W = max(self.Ws)
         sizes = np.diff(self.inp.off_host.astype(np.int64))
         i32 = dict(dtype=torch.int32, device=device)
-        self.counts = torch.zeros((J, K), **i32)
+        self.counts = torch.empty((J, K), **i32)
         self.err = torch.zeros(1, **i32)
         # plan windows: groups g = 0..NG-1, interval j -> group gmap[j]
         self.prev_counts = prev_counts
@@ -87,20 +87,34 @@ class Pipeline:
 
     # -- the five calls ----------------------------------------------------------------
     def count(self, stream=None):
-        self.counts.zero_()
         B.cr_count_rates(self.inp.keys, self.inp.off, self.J, self.K, self.counts, self.err, stream, n=self.n)
         if self.prev_counts is not None:
             self.win_buf[0].copy_(self.prev_counts)
             if self.J > 1:
                 self.win_buf[1:].copy_(self.counts[: self.J - 1])
 
-    def plan(self, stream=None):
+    def admit(self, stream=None):
         B.cr_admit(self.win_src, self.plans.c, self.ws_admit, self.err, stream)
+
+    def place(self, stream=None):
         B.cr_place_lpt(self.win_src, self.plans.c, stream)
+
+    def plan(self, stream=None):
+        self.admit(stream)
+        self.place(stream)
 
     def route(self, stream=None):
         B.cr_route(self.inp.keys, self.wl.first_index, self.wl.seed, self.inp.off, self.gmap, self.J, self.plans.c,
                    self.dest, self.err, stream, n=self.n)
+
+    def partition(self, stream=None):
+        B.cr_replay_partition(self.inp.keys, self.inp.suffix, self.dest, self.inp.off, self.J, self.P, self.R,
+                              self.Ws, self.ws_replay, self.err, stream, n=self.n)
+
+    def lru(self, stream=None):
+        self.stats.zero_()
+        B.cr_replay_lru(self.inp.prefix_len, self.K, self.n, self.J, self.P, self.R, self.Ws, self.max_W,
+                        self.lru_in, self.lru_out, self.stats, self.ws_replay, self.err, stream)
 
     def replay(self, stream=None):
         self.stats.zero_()
@@ -108,11 +122,11 @@ class Pipeline:
                     self.P, self.R, self.Ws, self.max_W, self.lru_in, self.lru_out, self.stats, self.ws_replay,
                     self.err, stream, n=self.n)
 
+    STAGES = ("count", "admit", "place", "route", "partition", "lru")
+
     def step(self, stream=None):
-        self.count(stream)
-        self.plan(stream)
-        self.route(stream)
-        self.replay(stream)
+        for s in self.STAGES:
+            getattr(self, s)(stream)
 
     # -- host views for checking -------------------------------------------------------
     def host(self) -> dict:

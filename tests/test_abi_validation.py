@@ -1,0 +1,101 @@
+"""Argument validation of the C ABI: every malformed call returns its error code on the
+host before anything is enqueued (runs without a GPU; no pointer is dereferenced)."""
+import ctypes
+import os
+
+import pytest
+
+from paper_2608_19677_amd import binding as B
+
+FAKE = 0x10000  # never dereferenced: every call below fails validation first
+
+
+@pytest.fixture(scope="module")
+def L():
+    from paper_2608_19677_amd import build
+    if not os.path.exists(build.LIB):
+        build.build()
+    return B.load()
+
+
+def _set(**kw):
+    f = dict(num_plans=2, cands=1, R=30, max_W=16, num_keys=100, num_windows=2)
+    f.update(kw)
+    ps = B.CrPlanSet(f["num_plans"], f["cands"], f["R"], f["max_W"], f["num_keys"], f["num_windows"],
+                     *([FAKE] * 11))
+    return ps
+
+
+def test_count_rejects(L):
+    assert L.cr_count_rates(FAKE, 10, FAKE, 0, 100, FAKE, FAKE, None) == B.CR_EINVAL      # J = 0
+    assert L.cr_count_rates(FAKE, 10, FAKE, 1, 0, FAKE, FAKE, None) == B.CR_EINVAL        # no keys
+    assert L.cr_count_rates(FAKE, 10, FAKE, 1, 0xFFFFFFFF, FAKE, FAKE, None) == B.CR_EINVAL
+    assert L.cr_count_rates(None, 10, FAKE, 1, 100, FAKE, FAKE, None) == B.CR_EINVAL      # keys NULL
+    assert L.cr_count_rates(FAKE + 2, 10, FAKE, 1, 100, FAKE, FAKE, None) == B.CR_EINVAL  # misaligned keys
+    assert L.cr_count_rates(FAKE, 10, None, 1, 100, FAKE, FAKE, None) == B.CR_EINVAL
+    assert L.cr_count_rates(FAKE, 10, FAKE, 1, 100, None, FAKE, None) == B.CR_EINVAL
+    assert L.cr_count_rates(FAKE, 10, FAKE, 1, 100, FAKE, None, None) == B.CR_EINVAL
+
+
+@pytest.mark.parametrize("kw", [dict(R=0), dict(R=1025), dict(max_W=0), dict(max_W=513), dict(cands=0),
+                                dict(cands=257, num_plans=257), dict(num_plans=3, cands=2), dict(num_keys=0),
+                                dict(num_windows=0), dict(num_plans=0)])
+def test_plan_set_rejects(L, kw):
+    ps = _set(**kw)
+    assert L.cr_admit(FAKE, ctypes.byref(ps), FAKE, 1 << 40, FAKE, None) == B.CR_EINVAL
+    assert L.cr_place_lpt(FAKE, ctypes.byref(ps), None) == B.CR_EINVAL
+
+
+def test_admit_workspace_too_small(L):
+    ps = _set()
+    need = L.cr_admit_workspace_bytes(2, 30, 16)
+    assert L.cr_admit(FAKE, ctypes.byref(ps), FAKE, need - 1, FAKE, None) == B.CR_ESIZE
+    assert L.cr_admit(FAKE, ctypes.byref(ps), None, need, FAKE, None) == B.CR_EINVAL
+    ps.order_count = None
+    assert L.cr_admit(FAKE, ctypes.byref(ps), FAKE, need, FAKE, None) == B.CR_EINVAL
+
+
+def test_route_rejects(L):
+    ps = _set()
+    assert L.cr_route(FAKE, 10, 0, 1, FAKE, FAKE, 0, ctypes.byref(ps), FAKE, FAKE, None) == B.CR_EINVAL
+    assert L.cr_route(FAKE, 10, 0, 1, None, FAKE, 1, ctypes.byref(ps), FAKE, FAKE, None) == B.CR_EINVAL
+    assert L.cr_route(FAKE, 10, 0, 1, FAKE, None, 1, ctypes.byref(ps), FAKE, FAKE, None) == B.CR_EINVAL
+    assert L.cr_route(FAKE + 1, 10, 0, 1, FAKE, FAKE, 1, ctypes.byref(ps), FAKE, FAKE, None) == B.CR_EINVAL
+    bad = _set(R=2000)
+    assert L.cr_route(FAKE, 10, 0, 1, FAKE, FAKE, 1, ctypes.byref(bad), FAKE, FAKE, None) == B.CR_EINVAL
+    assert L.cr_route(FAKE, 0, 0, 1, FAKE, FAKE, 1, ctypes.byref(ps), FAKE, FAKE, None) == B.CR_OK  # empty: no-op
+
+
+def _W(*v):
+    return (ctypes.c_uint32 * len(v))(*v)
+
+
+def test_replay_rejects(L):
+    need = L.cr_replay_workspace_bytes(1000, 2, 30)
+    ok = dict(keys=FAKE, suffix=FAKE, plen=FAKE, K=100, dest=FAKE, n=1000, off=FAKE, J=1, P=2, R=30,
+              W=_W(16, 8), maxW=16, lin=None, lout=FAKE, stats=FAKE, ws=FAKE, wsb=need, err=FAKE)
+
+    def call(**kw):
+        a = dict(ok)
+        a.update(kw)
+        return L.cr_replay(a["keys"], a["suffix"], a["plen"], a["K"], a["dest"], a["n"], a["off"], a["J"], a["P"],
+                           a["R"], a["W"], a["maxW"], a["lin"], a["lout"], a["stats"], a["ws"], a["wsb"], a["err"],
+                           None)
+
+    assert call(P=0) == B.CR_EINVAL
+    assert call(P=257) == B.CR_EINVAL
+    assert call(R=0) == B.CR_EINVAL
+    assert call(J=0) == B.CR_EINVAL
+    assert call(J=65536) == B.CR_EINVAL
+    assert call(W=_W(16, 0)) == B.CR_EINVAL
+    assert call(W=_W(16, 17)) == B.CR_EINVAL          # W above max_W
+    assert call(maxW=513, W=_W(513, 8)) == B.CR_EINVAL
+    assert call(wsb=need - 1) == B.CR_ESIZE
+    assert call(lout=None) == B.CR_EINVAL
+    assert call(lin=FAKE, lout=FAKE + 64) == B.CR_EINVAL  # overlapping carried state
+    assert call(n=2**32) == B.CR_EINVAL
+    assert call(K=0) == B.CR_EINVAL
+    assert L.cr_replay_partition(FAKE, FAKE, FAKE, 1000, FAKE, 1, 2, 30, _W(16, 8), FAKE, need - 8, FAKE,
+                                 None) == B.CR_ESIZE
+    assert L.cr_replay_lru(FAKE, 100, 1000, 1, 2, 30, _W(16, 8), 8, None, FAKE, FAKE, FAKE, need, FAKE,
+                           None) == B.CR_EINVAL  # max_W below a W
