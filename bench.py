@@ -32,6 +32,9 @@ def parse():
     ap.add_argument("--workload", default="llama70b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--calib-copy-mb", type=int, default=0,
+                    help="after timing, copy this many MiB device-to-device once (a plain copy kernel of known "
+                         "size, to scale the FETCH_SIZE / WRITE_SIZE counters)")
     return ap.parse_args()
 
 
@@ -141,6 +144,16 @@ def main():
         "hit_rate": (tot[:, 1] / tot[:, 0]).tolist(),
     }
     out["config"]["plan_builds"] = n_plans
+
+    if args.calib_copy_mb:
+        nb = args.calib_copy_mb << 20
+        src = torch.empty(nb, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        src.fill_(1)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        out["calib_copy_bytes"] = nb
 
     if not args.no_cpu_baseline:
         import oracle

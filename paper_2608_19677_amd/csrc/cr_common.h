@@ -40,6 +40,14 @@ __device__ __forceinline__ double rdlane_f64(double v, uint32_t l)
 
 __device__ __forceinline__ uint32_t first_lane(uint64_t mask) { return (uint32_t)__builtin_ctzll(mask); }
 
+// v_writelane_b32: returns `old` with lane `lane` replaced by the uniform value `val`.
+__device__ int cr_amdgcn_writelane(int val, int lane, int old) __asm("llvm.amdgcn.writelane.i32");
+
+__device__ __forceinline__ uint32_t wrlane(uint32_t old, uint32_t val, uint32_t lane)
+{
+    return (uint32_t)cr_amdgcn_writelane((int)val, (int)lane, (int)old);
+}
+
 // MurmurHash3's 32-bit finalizer.
 __host__ __device__ __forceinline__ uint32_t fmix32(uint32_t x)
 {
@@ -75,18 +83,31 @@ __device__ __forceinline__ uint32_t find_interval(const uint64_t* __restrict__ o
     return lo;
 }
 
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t v)
+{
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, kCtrl, kRowMask, 0xF, false);
+}
+
+// Inclusive wave64 prefix sum with DPP row shifts and row broadcasts (no LDS traffic).
+__device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t v)
+{
+    v += dpp_u32<0x111, 0xF>(v);  // row_shr:1
+    v += dpp_u32<0x112, 0xF>(v);  // row_shr:2
+    v += dpp_u32<0x114, 0xF>(v);  // row_shr:4
+    v += dpp_u32<0x118, 0xF>(v);  // row_shr:8
+    v += dpp_u32<0x142, 0xA>(v);  // row_bcast:15 into rows 1 and 3
+    v += dpp_u32<0x143, 0xC>(v);  // row_bcast:31 into rows 2 and 3
+    return v;
+}
+
 // Block-wide exclusive scan of 32-bit values (blockDim.x a multiple of 64, <= 1024).
 // `sh` needs 16 words. Returns the exclusive prefix; *total gets the block sum.
 __device__ __forceinline__ uint32_t block_exscan_u32(uint32_t v, uint32_t* sh, uint32_t* total)
 {
-    const uint32_t lane = lane_id(), wv = threadIdx.x >> 6, nw = blockDim.x >> 6;
-    uint32_t x = v;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const uint32_t y = __shfl_up(x, o, 64);
-        if (lane >= (uint32_t)o) x += y;
-    }
-    if (lane == 63) sh[wv] = x;
+    const uint32_t wv = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    const uint32_t x = wave_incl_scan_u32(v);
+    if (lane_id() == 63) sh[wv] = x;
     __syncthreads();
     uint32_t base = 0, tot = 0;
     for (uint32_t w = 0; w < nw; ++w) {
@@ -97,6 +118,42 @@ __device__ __forceinline__ uint32_t block_exscan_u32(uint32_t v, uint32_t* sh, u
     __syncthreads();
     *total = tot;
     return base + x - v;
+}
+
+// Block-wide exclusive count of a predicate (ballot + popcount per wave).
+__device__ __forceinline__ uint32_t block_exscan_flag(bool f, uint32_t* sh, uint32_t* total)
+{
+    const uint32_t wv = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    const uint64_t m = ballot(f);
+    if (lane_id() == 0) sh[wv] = (uint32_t)__popcll(m);
+    __syncthreads();
+    uint32_t base = 0, tot = 0;
+    for (uint32_t w = 0; w < nw; ++w) {
+        const uint32_t t = sh[w];
+        base += (w < wv) ? t : 0u;
+        tot += t;
+    }
+    __syncthreads();
+    *total = tot;
+    return base + (uint32_t)__popcll(m & lanemask_lt());
+}
+
+// Index of this wavefront in its block, as a value the compiler knows is uniform.
+__device__ __forceinline__ uint32_t wave_in_block()
+{
+    return (uint32_t)__builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+}
+
+// Workgroups are dealt to the 8 XCDs round-robin (block b runs on XCD b % 8). A grid
+// rounded up to a multiple of 8 and remapped this way hands every XCD one contiguous
+// eighth of the tiles, so neighbouring tiles share that XCD's L2.
+constexpr uint32_t kXcds = 8;
+
+__host__ __device__ __forceinline__ uint32_t xcd_grid(uint32_t tiles) { return (tiles + kXcds - 1) / kXcds * kXcds; }
+
+__device__ __forceinline__ uint32_t xcd_tile(uint32_t b, uint32_t grid)
+{
+    return (b % kXcds) * (grid / kXcds) + b / kXcds;
 }
 
 inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }

@@ -111,18 +111,16 @@ __global__ __launch_bounds__(kSortThreads) void k_sort_window(const uint32_t* __
             if (c != 0 && (c & pmask) == prefix) atomicAdd(&s_hist[(c >> shift) & 255u], 1u);
         }
         __syncthreads();
-        if (tid == 0) {
-            uint32_t cum = 0, sel = 0;
-            for (int d = 255; d >= 0; --d) {
-                const uint32_t h = s_hist[d];
-                if (cum + h >= need) {
-                    sel = (uint32_t)d;
-                    break;
-                }
-                cum += h;
+        {
+            // counts of digits above d, scanning digits from 255 down: the digit holding the
+            // need-th largest is the one whose running count first reaches need.
+            const uint32_t h = tid < 256 ? s_hist[255 - tid] : 0u;
+            uint32_t tot;
+            const uint32_t above = block_exscan_u32(h, s_scan, &tot);
+            if (tid < 256 && above < need && above + h >= need) {
+                s_sel = 255u - tid;
+                s_need = need - above;
             }
-            s_sel = sel;
-            s_need = need - cum;
         }
         __syncthreads();
         prefix |= s_sel << shift;
@@ -142,9 +140,9 @@ __global__ __launch_bounds__(kSortThreads) void k_sort_window(const uint32_t* __
         const bool gt = c > t;
         const bool eq = c == t;
         uint32_t eq_tot, sel_tot;
-        const uint32_t eq_rank = block_exscan_u32(eq ? 1u : 0u, s_scan, &eq_tot);
+        const uint32_t eq_rank = block_exscan_flag(eq, s_scan, &eq_tot);
         const bool sel = gt || (eq && eq_seen + eq_rank < take_eq);
-        const uint32_t pos = block_exscan_u32(sel ? 1u : 0u, s_scan, &sel_tot);
+        const uint32_t pos = block_exscan_flag(sel, s_scan, &sel_tot);
         if (sel && running + pos < M) b0[running + pos] = make_uint2(c, b);
         running += sel_tot;
         eq_seen += eq_tot;
@@ -166,12 +164,10 @@ __global__ __launch_bounds__(kSortThreads) void k_sort_window(const uint32_t* __
         __syncthreads();
         for (uint32_t e = tid; e < M; e += bd) atomicAdd(&s_hist[((mx - src[e].x) >> shift) & 255u], 1u);
         __syncthreads();
-        if (tid == 0) {
-            uint32_t run = 0;
-            for (int d = 0; d < 256; ++d) {
-                s_base[d] = run;
-                run += s_hist[d];
-            }
+        {
+            uint32_t tot;
+            const uint32_t ex = block_exscan_u32(tid < 256 ? s_hist[tid] : 0u, s_scan, &tot);
+            if (tid < 256) s_base[tid] = ex;
         }
         __syncthreads();
         for (uint32_t e0 = 0; e0 < M; e0 += bd) {
@@ -274,11 +270,10 @@ __global__ __launch_bounds__(kSortThreads) void k_admit_plan(
         const uint32_t ex = block_exscan_u32(k, s_scan, &ktot);
         const bool adm = valid && used + ex + k <= C;
         if (adm) moff[a] = (uint32_t)(used + ex);
-        const uint32_t kadm_ex = block_exscan_u32(adm ? k : 0u, s_scan, &ntot);
-        (void)kadm_ex;
+        (void)block_exscan_u32(adm ? k : 0u, s_scan, &ntot);
         uint32_t nadm;
-        (void)block_exscan_u32(adm ? 1u : 0u, s_scan, &nadm);
-        (void)block_exscan_u32((adm && cl) ? 1u : 0u, s_scan, &ctot);
+        (void)block_exscan_flag(adm, s_scan, &nadm);
+        (void)block_exscan_flag(adm && cl, s_scan, &ctot);
         const uint64_t cs = wave_sum_u64(adm ? (uint64_t)c : 0ull);
         if (lane == 0 && cs) atomicAdd(&s_carried, (unsigned long long)cs);
         used += ntot;
@@ -346,8 +341,13 @@ __device__ __forceinline__ LptBatch lpt_load(const uint32_t* __restrict__ ord, c
 
 // R <= 64: lane i holds the i-th smallest (L, r), so the least-loaded destinations are
 // lanes 0..k-1. After charging them, each is re-inserted at its rank among the rest:
-// a ballot + popcount gives the rank, a one-lane DPP shift opens the slot. For k = 1 the
-// pop and the insert fuse into one shift. Stores of a 64-key batch leave in one go.
+// three compares straight to lane masks give the rank, a one-lane DPP shift opens the
+// slot; for k = 1 the pop and the insert fuse into one shift.
+// A run of at least R equal single-copy jobs whose size exceeds the current spread of
+// the loads (max L < min L + x) is placed as one round: job s of the run goes to lane s,
+// exactly as R sequential picks would choose, and every load gains x at once. The round
+// is taken only if the charged loads stay in (L, r) order; otherwise the picks proceed
+// one by one. Stores of a 64-key batch leave in one go.
 __global__ __launch_bounds__(64) void k_lpt_small(uint32_t K, uint32_t R, uint32_t Cmax, uint32_t NW,
                                                   uint32_t cands, const cr_plan_spec* __restrict__ specs,
                                                   const uint32_t* __restrict__ order,
@@ -360,7 +360,7 @@ __global__ __launch_bounds__(64) void k_lpt_small(uint32_t K, uint32_t R, uint32
 {
     const uint32_t p = blockIdx.x, lane = lane_id();
     const cr_plan_spec spec = specs[p];
-    const uint32_t A = num_admitted[p];
+    const uint32_t A = (uint32_t)__builtin_amdgcn_readfirstlane((int)num_admitted[p]);
     const uint32_t w = spec.window < NW ? spec.window : 0u;
     const uint32_t* __restrict__ ord = order + (uint64_t)w * Cmax;
     const uint32_t* __restrict__ ocnt = order_count + (uint64_t)w * Cmax;
@@ -378,24 +378,44 @@ __global__ __launch_bounds__(64) void k_lpt_small(uint32_t K, uint32_t R, uint32
         const uint32_t k_l = cur.end - cur.off;
         const double x_l = k_l == 1 ? (double)cur.cnt : (double)cur.cnt / (double)k_l;
         uint32_t first = 0;  // lane t: least-loaded member chosen for key t of the batch
-        for (uint32_t t = 0; t < nb; ++t) {
+        for (uint32_t t = 0; t < nb;) {
             const uint32_t k = rdlane(k_l, t);
             const double x = rdlane_f64(x_l, t);
+            if (k == 1 && t + R <= nb) {
+                // length of the run of equal single-copy jobs starting at t
+                const uint64_t same = ballot(k_l == 1 && x_l == x && lane < nb);
+                const uint64_t from_t = ~(same >> t);
+                const uint32_t run = from_t ? (uint32_t)__builtin_ctzll(from_t) : 64u - t;
+                if (run >= R) {
+                    const double lo = rdlane_f64(Lv, 0), hi = rdlane_f64(Lv, R - 1);
+                    if (hi < lo + x) {
+                        const double v = Lv + x;
+                        const double vn = dpp_shl1_f64(v);
+                        const uint32_t rn = dpp_shl1(rv, rv);
+                        const bool bad_pair = lane + 1 < R && vn == v && rn < rv;
+                        if (ballot(bad_pair) == 0) {
+                            const uint32_t src = (lane - t) & 63u;
+                            const uint32_t got = (uint32_t)__shfl((int)rv, (int)src, 64);
+                            if (lane >= t && lane < t + R) first = got;
+                            if (lane < R) Lv = v;
+                            t += R;
+                            continue;
+                        }
+                    }
+                }
+            }
             const uint32_t r0 = rdlane(rv, 0);
-            first = lane == t ? r0 : first;
+            first = wrlane(first, r0, t);
             if (k == 1) {
                 const double v = rdlane_f64(Lv, 0) + x;
-                const bool less = lane != 0 && (Lv < v || (Lv == v && rv < r0));
-                const uint32_t pos = (uint32_t)__popcll(ballot(less));
+                // rank of (v, r0) among lanes 1..: three compares, each straight to a lane mask
+                const uint64_t m_lt = ballot(Lv < v), m_eq = ballot(Lv == v), m_r = ballot(rv < r0);
+                const uint32_t pos = (uint32_t)__popcll((m_lt | (m_eq & m_r)) & ~1ull);
                 const double sl = dpp_shl1_f64(Lv);
                 const uint32_t sr = dpp_shl1(rv, rv);
-                if (lane < pos) {
-                    Lv = sl;
-                    rv = sr;
-                } else if (lane == pos) {
-                    Lv = v;
-                    rv = r0;
-                }
+                const bool lt = lane < pos, eq = lane == pos;
+                Lv = lt ? sl : (eq ? v : Lv);
+                rv = lt ? sr : (eq ? r0 : rv);
             } else {
                 const uint32_t off = rdlane(cur.off, t);
                 if (lane < k) mem[off + lane] = (uint16_t)rv;
@@ -408,19 +428,16 @@ __global__ __launch_bounds__(64) void k_lpt_small(uint32_t K, uint32_t R, uint32
                 for (uint32_t u = 0; u < k; ++u) {
                     const double v = rdlane_f64(vnew, u);
                     const uint32_t r = rdlane(rnew, u);
-                    const bool less = Lv < v || (Lv == v && rv < r);
-                    const uint32_t pos = (uint32_t)__popcll(ballot(less));
+                    const uint64_t m_lt = ballot(Lv < v), m_eq = ballot(Lv == v), m_r = ballot(rv < r);
+                    const uint32_t pos = (uint32_t)__popcll(m_lt | (m_eq & m_r));
                     const double up = dpp_shr1_f64(Lv);
                     const uint32_t upr = dpp_shr1(rv, rv);
-                    if (lane > pos) {
-                        Lv = up;
-                        rv = upr;
-                    } else if (lane == pos) {
-                        Lv = v;
-                        rv = r;
-                    }
+                    const bool gt = lane > pos, eq = lane == pos;
+                    Lv = gt ? up : (eq ? v : Lv);
+                    rv = gt ? upr : (eq ? r : rv);
                 }
             }
+            ++t;
         }
         if (lane < nb) {
             if (k_l == 1) mem[cur.off] = (uint16_t)first;

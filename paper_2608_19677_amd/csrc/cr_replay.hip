@@ -31,7 +31,7 @@ struct WArg {
 __host__ __device__ __forceinline__ uint32_t seg_len(uint32_t W)
 {
     const uint32_t s = 16u * W;
-    return s < 2048u ? 2048u : (s > 16384u ? 16384u : s);
+    return s < 1024u ? 1024u : (s > 16384u ? 16384u : s);
 }
 
 __host__ __device__ __forceinline__ uint32_t slot_class(uint32_t W)
@@ -153,7 +153,8 @@ __global__ __launch_bounds__(64) void k_part_scatter(const uint32_t* __restrict_
 {
     extern __shared__ uint32_t run[];
     const uint32_t c = blockIdx.y, lane = lane_id();
-    const uint64_t t = blockIdx.x;
+    const uint64_t t = xcd_tile(blockIdx.x, gridDim.x);
+    if (t >= ntiles) return;
     const uint64_t t0 = t * tile, t1 = t0 + tile < n ? t0 + tile : n;
     for (uint32_t d = lane; d < R; d += 64) run[d] = tcnt[((uint64_t)c * R + d) * ntiles + t];
     __syncthreads();
@@ -229,9 +230,68 @@ __device__ __forceinline__ bool lru_contains(const uint32_t (&skey)[SL], uint32_
 template <int SL>
 __device__ __forceinline__ void lru_put_slot(uint32_t (&skey)[SL], uint32_t q, uint32_t kk, uint32_t lane)
 {
+    (void)lane;
 #pragma unroll
     for (int s = 0; s < SL; ++s)
-        if ((uint32_t)s == (q >> 6) && lane == (q & 63u)) skey[s] = kk;
+        if ((uint32_t)s == (q >> 6)) skey[s] = wrlane(skey[s], kk, q & 63u);
+}
+
+// One LRU access of key kk; returns true on a hit. The target slot is the hit slot, or
+// on a miss the least recent slot (rank W-1). Every slot more recent than the target
+// ages by one and the target becomes rank 0 holding kk. With one slot per lane the step
+// has no branch: the target's rank is read from its lane either way (W-1 on a miss).
+__device__ __forceinline__ bool lru_step1(uint32_t& skey, uint32_t& srank, uint32_t kk, uint32_t W)
+{
+    const uint64_t m = ballot(skey == kk);
+    const uint64_t v = ballot(srank == W - 1);
+    const bool hit = m != 0;
+    const uint32_t tl = first_lane(hit ? m : v);
+    const uint32_t rh = rdlane(srank, tl);
+    srank += srank < rh ? 1u : 0u;
+    srank = wrlane(srank, 0u, tl);
+    skey = wrlane(skey, kk, tl);
+    return hit;
+}
+
+template <int SL>
+__device__ __forceinline__ bool lru_step(uint32_t (&skey)[SL], uint32_t (&srank)[SL], uint32_t kk, uint32_t W)
+{
+    if (SL == 1) return lru_step1(skey[0], srank[0], kk, W);
+    uint32_t ts = 0, tl = 0;
+    bool hit = false;
+#pragma unroll
+    for (int s = 0; s < SL; ++s) {
+        const uint64_t m = ballot(skey[s] == kk);
+        if (m) {
+            ts = (uint32_t)s;
+            tl = first_lane(m);
+            hit = true;
+        }
+    }
+    if (!hit) {
+#pragma unroll
+        for (int s = 0; s < SL; ++s) {
+            const uint64_t v = ballot(srank[s] == W - 1);
+            if (v) {
+                ts = (uint32_t)s;
+                tl = first_lane(v);
+            }
+        }
+    }
+    uint32_t rh = W - 1;
+#pragma unroll
+    for (int s = 0; s < SL; ++s)
+        if ((uint32_t)s == ts) rh = rdlane(srank[s], tl);
+#pragma unroll
+    for (int s = 0; s < SL; ++s) srank[s] += srank[s] < rh ? 1u : 0u;
+#pragma unroll
+    for (int s = 0; s < SL; ++s) {
+        if ((uint32_t)s == ts) {
+            srank[s] = wrlane(srank[s], 0u, tl);
+            skey[s] = wrlane(skey[s], kk, tl);
+        }
+    }
+    return hit;
 }
 
 __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v)
@@ -249,7 +309,7 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
     uint32_t* __restrict__ lru_out, uint64_t* __restrict__ stats, uint32_t* __restrict__ err)
 {
     const uint32_t lane = lane_id();
-    const uint64_t item = (uint64_t)blockIdx.x * (kReplayThreads / 64) + (threadIdx.x >> 6);
+    const uint64_t item = (uint64_t)blockIdx.x * (kReplayThreads / 64) + wave_in_block();
     const uint32_t ncd = P * R;
     if (item >= item_off[ncd]) return;
     uint32_t lo = 0, hi = ncd;
@@ -322,15 +382,17 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
         }
     }
 
+    // Per-lane sums for the current interval; flushed (one atomic per statistic) when the
+    // interval changes and at the end of the segment.
     uint64_t a_req = 0, a_hit = 0, a_pre = 0, a_hp = 0;
     uint32_t cur = 0xFFFFFFFFu;
     bool bad = false;
-    auto flush = [&](uint32_t iv) {
-        if (iv >= J) return;
+    auto flush = [&]() {
+        if (cur >= J) return;
         const uint64_t r0 = wave_sum_u64(a_req), r1 = wave_sum_u64(a_hit), r2 = wave_sum_u64(a_pre),
                        r3 = wave_sum_u64(a_hp);
         if (lane == 0) {
-            unsigned long long* st = (unsigned long long*)(stats + (((uint64_t)iv * P + c) * R + d) * 4u);
+            unsigned long long* st = (unsigned long long*)(stats + (((uint64_t)cur * P + c) * R + d) * 4u);
             atomicAdd(st + 0, (unsigned long long)r0);
             if (r1) atomicAdd(st + 1, (unsigned long long)r1);
             atomicAdd(st + 2, (unsigned long long)r2);
@@ -338,7 +400,8 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
         }
         a_req = a_hit = a_pre = a_hp = 0;
     };
-    // Forward replay; the next batch of records is in flight while one is replayed.
+    // Forward replay; the next batch of records is in flight while one is replayed. Lane t
+    // of `hitf` records whether record t of the batch hit.
     uint64_t rv_next = s0 + lane < s1 ? rl[s0 + lane] : 0ull;
     for (uint32_t b0 = s0; b0 < s1; b0 += 64) {
         const uint32_t nb = s1 - b0 < 64u ? s1 - b0 : 64u;
@@ -348,37 +411,24 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
         const bool vl = lane < nb && kl < K;
         bad |= lane < nb && kl >= K;
         const uint32_t pl = vl ? prefix_len[kl] : 0u;  // consumed after the batch
-        uint64_t hm = 0;
-        for (uint32_t t = 0; t < nb; ++t) {
-            const uint32_t kk = rdlane(kl, t);
-            if (kk >= K) continue;
-            uint32_t rh = W - 1;
-            bool hit = false;
-#pragma unroll
-            for (int s = 0; s < SL; ++s) {
-                const uint64_t m = ballot(skey[s] == kk);
-                if (m) {
-                    hit = true;
-                    rh = rdlane(srank[s], first_lane(m));
-                }
+        uint32_t hitf = 0;
+        if (ballot(lane < nb && kl >= K) == 0) {
+            for (uint32_t t = 0; t < nb; ++t)
+                hitf = wrlane(hitf, lru_step<SL>(skey, srank, rdlane(kl, t), W) ? 1u : 0u, t);
+        } else {
+            for (uint32_t t = 0; t < nb; ++t) {
+                const uint32_t kk = rdlane(kl, t);
+                if (kk < K) hitf = wrlane(hitf, lru_step<SL>(skey, srank, kk, W) ? 1u : 0u, t);
             }
-#pragma unroll
-            for (int s = 0; s < SL; ++s) {
-                const bool sel = srank[s] == rh;
-                const bool up = srank[s] < rh;
-                skey[s] = sel ? kk : skey[s];
-                srank[s] = sel ? 0u : (up ? srank[s] + 1u : srank[s]);
-            }
-            hm |= (uint64_t)hit << t;
         }
         const uint32_t sfx = (uint32_t)(rv >> 32) & 0xFFFFu;
         const uint32_t ivl = (uint32_t)(rv >> 48);
-        const bool hl = (hm >> lane) & 1ull;
+        const bool hl = hitf != 0;
         uint64_t rem = ballot(vl);
         while (rem) {
             const uint32_t iv = rdlane(ivl, first_lane(rem));
             if (iv != cur) {
-                flush(cur);
+                flush();
                 cur = iv;
             }
             const uint64_t sel = rem & ballot(ivl == iv);
@@ -391,7 +441,7 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
             rem &= ~sel;
         }
     }
-    flush(cur);
+    flush();
     if (ballot(bad) && lane == 0) atomicOr(err, CR_ERR_KEY_RANGE);
     if (s1 == cnt) {
         uint32_t* __restrict__ lo_ = lru_out + ((uint64_t)c * R + d) * max_W;
@@ -509,7 +559,7 @@ extern "C" cr_status cr_replay_partition(const uint32_t* keys, const uint16_t* s
     if (g.ntiles) {
         hipLaunchKernelGGL(k_scan_apply, dim3(nblk, P), dim3(kScanThreads), 0, st, w.tcnt, len, g.ntiles, R, nblk,
                            w.bsum, w.grp_off);
-        hipLaunchKernelGGL(k_part_scatter, dim3((uint32_t)g.ntiles, P), dim3(64), (size_t)R * 4u, st, keys, suffix,
+        hipLaunchKernelGGL(k_part_scatter, dim3(xcd_grid((uint32_t)g.ntiles), P), dim3(64), (size_t)R * 4u, st, keys, suffix,
                            dest, n, off, J, R, nbits, g.tile, g.ntiles, w.tcnt, w.rec);
     }
     hipLaunchKernelGGL(k_seg_items, dim3(1), dim3(1024), 0, st, w.grp_off, P, R, ra.wa, w.item_off);
@@ -531,7 +581,7 @@ extern "C" cr_status cr_replay_lru(const uint32_t* prefix_len, uint32_t num_keys
     const ReplayWs w = replay_layout(ws_base(ws), n, P, R);
     const hipStream_t st = as_stream(stream);
     // Upper bound on work items: one per (c, d) plus one per full segment.
-    const uint64_t items = (uint64_t)P * R + (uint64_t)P * n / 2048u + 1u;
+    const uint64_t items = (uint64_t)P * R + (uint64_t)P * n / 1024u + 1u;
     const uint64_t blocks = (items + (kReplayThreads / 64) - 1) / (kReplayThreads / 64);
     if (blocks > 0x7FFFFFFFull) return CR_EINVAL;
     (void)hipGetLastError();

@@ -37,7 +37,7 @@ __global__ __launch_bounds__(kRouteThreads) void k_route(
     uint16_t* __restrict__ dest, uint32_t* __restrict__ err)
 {
     __shared__ uint32_t s_j0;
-    const uint64_t bstart = (uint64_t)blockIdx.x * kRouteThreads * kPer;
+    const uint64_t bstart = (uint64_t)xcd_tile(blockIdx.x, gridDim.x) * kRouteThreads * kPer;
     if (bstart >= n) return;
     if (threadIdx.x == 0) s_j0 = find_interval(off, J, bstart);
     __syncthreads();
@@ -109,12 +109,12 @@ extern "C" cr_status cr_route(const uint32_t* keys, uint64_t n, uint64_t first_i
     const uint32_t cmax = plans->R * plans->max_W;
     const uint64_t per_block = (uint64_t)kRouteThreads * kPer;
     const uint64_t blocks = (n + per_block - 1) / per_block;
-    if (blocks > 0x7FFFFFFFull) return CR_EINVAL;
+    if (blocks > 0x7FFFFFF0ull) return CR_EINVAL;
     // 16-byte key loads and 8-byte destination stores need aligned rows.
     const bool vec = ((uintptr_t)keys & 15u) == 0 && ((uintptr_t)dest & 7u) == 0 && (n & 3u) == 0;
     (void)hipGetLastError();
 #define CR_ROUTE_LAUNCH(V)                                                                                         \
-    hipLaunchKernelGGL(k_route<V>, dim3((uint32_t)blocks), dim3(kRouteThreads), 0, as_stream(stream), keys, n,     \
+    hipLaunchKernelGGL(k_route<V>, dim3(xcd_grid((uint32_t)blocks)), dim3(kRouteThreads), 0, as_stream(stream), keys, n, \
                        first_index, seed_mix(seed), off, gmap, J, plans->num_keys, plans->R, plans->cands,        \
                        plans->num_plans / plans->cands, plans->route, plans->member_off, cmax + 1u, plans->members, \
                        cmax, plans->load, dest, err)
