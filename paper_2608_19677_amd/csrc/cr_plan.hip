@@ -45,40 +45,89 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v)
     return v;
 }
 
-// One block per window. buf: [NW][2][Cmax] (count, key) pairs.
-__global__ __launch_bounds__(kSortThreads) void k_sort_window(const uint32_t* __restrict__ counts, uint32_t K,
-                                                              uint32_t Cmax, uint32_t* __restrict__ order,
-                                                              uint32_t* __restrict__ order_count,
-                                                              uint32_t* __restrict__ n_order,
-                                                              uint64_t* __restrict__ row_sum,
-                                                              uint2* __restrict__ buf)
+__device__ __forceinline__ uint32_t wave_exscan_u32(uint32_t v, uint32_t* total)
 {
-    __shared__ uint32_t s_hist[256];
-    __shared__ uint32_t s_base[256];
-    __shared__ uint32_t s_wcnt[kSortWaves][256];
-    __shared__ uint32_t s_scan[16];
-    __shared__ uint32_t s_nnz, s_max, s_sel, s_need;
-    __shared__ unsigned long long s_sum;
+    const uint32_t x = wave_incl_scan_u32(v);
+    *total = rdlane(x, 63);
+    return x - v;
+}
 
-    const uint32_t w = blockIdx.x, tid = threadIdx.x, bd = blockDim.x, lane = lane_id(), wv = tid >> 6;
-    const uint32_t nwaves = bd >> 6;
-    const uint32_t* __restrict__ row = counts + (uint64_t)w * K;
+constexpr uint32_t kSortBlock = 1024;                // 16 wavefronts per window
+constexpr uint32_t kSortNW = kSortBlock / 64;
+constexpr uint32_t kSortLdsRowBytes = 96u * 1024u;  // rows up to this size are staged in LDS
+
+// Loads counts[b] for b = base + 4*tid + {0..3} (zero past K), 16 bytes per thread when
+// the row allows it.
+__device__ __forceinline__ uint4 load4(const uint32_t* __restrict__ row, uint32_t K, uint32_t b, bool vec)
+{
+    if (vec && b + 3 < K) return *reinterpret_cast<const uint4*>(row + b);
+    return make_uint4(b < K ? row[b] : 0u, b + 1 < K ? row[b + 1] : 0u, b + 2 < K ? row[b + 2] : 0u,
+                      b + 3 < K ? row[b + 3] : 0u);
+}
+
+// One 1024-thread block per window. The window's nonzero keys are ordered by (count desc,
+// key asc) and cut at C_max in three steps, each with O(1) block barriers:
+//  1. one pass over the row: nnz, max, sum and a histogram of min(count, 255); the
+//     C_max-th largest count t is read off the histogram unless it is >= 255, in which
+//     case an MSB radix select over the row finds it;
+//  2. ordered compaction: every wavefront owns a contiguous slice of the row, counts
+//     what it keeps, takes its offset from the other wavefronts' totals, and writes its
+//     keys in key order (keys equal to t are kept up to the number still needed);
+//  3. stable LSD radix sort by (max - count) over the kept entries, 8 bits per pass, each
+//     wavefront scattering a contiguous slice with ballot-ranked digits.
+// When the row fits, step 1 also stages it in LDS and the later passes read it there.
+template <bool kRowLds>
+__global__ __launch_bounds__(kSortBlock) void k_sort_window(const uint32_t* __restrict__ counts, uint32_t K,
+                                                            uint32_t Cmax, uint32_t* __restrict__ order,
+                                                            uint32_t* __restrict__ order_count,
+                                                            uint32_t* __restrict__ n_order,
+                                                            uint64_t* __restrict__ row_sum, uint2* __restrict__ buf)
+{
+    extern __shared__ uint32_t s_row[];  // [K] when kRowLds
+    __shared__ uint32_t s_hist[kSortNW][256];
+    __shared__ uint32_t s_h256[256];
+    __shared__ uint32_t s_w[kSortNW][4];
+    __shared__ uint32_t s_nnz, s_max, s_t, s_take;
+    __shared__ unsigned long long s_sum;
+    const uint32_t w = blockIdx.x, tid = threadIdx.x, lane = lane_id(), wv = wave_in_block();
+    const uint32_t* __restrict__ grow = counts + (uint64_t)w * K;
+    const bool vec = (((uintptr_t)grow) & 15u) == 0;
+    const uint32_t* row = kRowLds ? s_row : grow;
+    uint2* b0 = buf + (uint64_t)w * 2u * Cmax;
+    uint2* b1 = b0 + Cmax;
+    for (uint32_t d = tid; d < 256; d += kSortBlock) s_h256[d] = 0;
     if (tid == 0) {
         s_nnz = 0;
         s_max = 0;
         s_sum = 0;
     }
     __syncthreads();
+    // 1. statistics and the clamped histogram
     {
         uint32_t nnz = 0, mx = 0;
         uint64_t sum = 0;
-        for (uint32_t b = tid; b < K; b += bd) {
-            const uint32_t c = row[b];
-            nnz += c != 0;
-            mx = c > mx ? c : mx;
-            sum += c;
+        for (uint32_t b = 4 * tid; b < K; b += 4 * kSortBlock * 2) {
+            const uint4 q0 = load4(grow, K, b, vec), q1 = load4(grow, K, b + 4 * kSortBlock, vec);
+            const uint32_t cs[8] = {q0.x, q0.y, q0.z, q0.w, q1.x, q1.y, q1.z, q1.w};
+            if (kRowLds) {
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    if (b + u < K) s_row[b + u] = cs[u];
+                    if (b + 4 * kSortBlock + u < K) s_row[b + 4 * kSortBlock + u] = cs[4 + u];
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const uint32_t c = cs[u];
+                if (c) {
+                    ++nnz;
+                    mx = c > mx ? c : mx;
+                    sum += c;
+                    atomicAdd(&s_h256[c < 255u ? c : 255u], 1u);
+                }
+            }
         }
-        nnz = wave_sum_u32(nnz);
+        nnz = rdlane(wave_incl_scan_u32(nnz), 63);
         mx = wave_max_u32(mx);
         sum = wave_sum_u64(sum);
         if (lane == 0) {
@@ -95,84 +144,168 @@ __global__ __launch_bounds__(kSortThreads) void k_sort_window(const uint32_t* __
         row_sum[w] = s_sum;
     }
     if (M == 0) return;
-
-    // Radix select: t = M-th largest nonzero count; take_eq = how many keys equal to t
-    // (the smallest key ids) complete the top M.
-    uint32_t prefix = 0, pmask = 0, need = M;
-    for (int shift = 24; shift >= 0; shift -= 8) {
-        if ((mx >> shift) == 0) {
-            pmask |= 0xFFu << shift;
-            continue;
+    // threshold from the clamped histogram (wave 0, four bins per lane from 255 down)
+    if (wv == 0) {
+        uint32_t h[4], hs = 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            h[q] = s_h256[255u - 4u * lane - q];
+            hs += h[q];
         }
-        for (uint32_t d = tid; d < 256; d += bd) s_hist[d] = 0;
-        __syncthreads();
-        for (uint32_t b = tid; b < K; b += bd) {
-            const uint32_t c = row[b];
-            if (c != 0 && (c & pmask) == prefix) atomicAdd(&s_hist[(c >> shift) & 255u], 1u);
-        }
-        __syncthreads();
-        {
-            // counts of digits above d, scanning digits from 255 down: the digit holding the
-            // need-th largest is the one whose running count first reaches need.
-            const uint32_t h = tid < 256 ? s_hist[255 - tid] : 0u;
-            uint32_t tot;
-            const uint32_t above = block_exscan_u32(h, s_scan, &tot);
-            if (tid < 256 && above < need && above + h >= need) {
-                s_sel = 255u - tid;
-                s_need = need - above;
+        uint32_t tot;
+        uint32_t above = wave_exscan_u32(hs, &tot);
+        uint32_t sel = 0, need = 0;
+        bool found = false;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            if (!found && above < M && above + h[q] >= M) {
+                sel = 255u - 4u * lane - q;
+                need = M - above;
+                found = true;
             }
+            above += h[q];
+        }
+        const uint32_t fl = first_lane(ballot(found));
+        if (lane == 0) {
+            s_t = rdlane(sel, fl);
+            s_take = rdlane(need, fl);
+        }
+    }
+    __syncthreads();
+    if (s_t == 255u) {
+        // the threshold is at least 255: MSB radix select over the row (rare)
+        uint32_t prefix = 0, pmask = 0, need = M;
+        for (int shift = 24; shift >= 0; shift -= 8) {
+            if ((mx >> shift) == 0) {
+                pmask |= 0xFFu << shift;
+                continue;
+            }
+            __syncthreads();
+            for (uint32_t d = tid; d < 256; d += kSortBlock) s_h256[d] = 0;
+            __syncthreads();
+            for (uint32_t b = tid; b < K; b += kSortBlock) {
+                const uint32_t c = row[b];
+                if (c != 0 && (c & pmask) == prefix) atomicAdd(&s_h256[(c >> shift) & 255u], 1u);
+            }
+            __syncthreads();
+            if (wv == 0) {
+                uint32_t h[4], hs = 0;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    h[q] = s_h256[255u - 4u * lane - q];
+                    hs += h[q];
+                }
+                uint32_t tot;
+                uint32_t above = wave_exscan_u32(hs, &tot);
+                uint32_t sel = 0, nn = 0;
+                bool found = false;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    if (!found && above < need && above + h[q] >= need) {
+                        sel = 255u - 4u * lane - q;
+                        nn = need - above;
+                        found = true;
+                    }
+                    above += h[q];
+                }
+                const uint32_t fl = first_lane(ballot(found));
+                if (lane == 0) {
+                    s_t = rdlane(sel, fl);
+                    s_take = rdlane(nn, fl);
+                }
+            }
+            __syncthreads();
+            prefix |= s_t << shift;
+            pmask |= 0xFFu << shift;
+            need = s_take;
         }
         __syncthreads();
-        prefix |= s_sel << shift;
-        pmask |= 0xFFu << shift;
-        need = s_need;
+        if (tid == 0) {
+            s_t = prefix;
+            s_take = need;
+        }
         __syncthreads();
     }
-    const uint32_t t = prefix, take_eq = need;
+    const uint32_t t = s_t, take_eq = s_take;
 
-    // Ordered compaction (key order) of the top M into b0.
-    uint2* __restrict__ b0 = buf + (uint64_t)w * 2u * Cmax;
-    uint2* __restrict__ b1 = b0 + Cmax;
-    uint32_t running = 0, eq_seen = 0;
-    for (uint32_t base = 0; base < K && running < M; base += bd) {
-        const uint32_t b = base + tid;
-        const uint32_t c = b < K ? row[b] : 0u;
-        const bool gt = c > t;
-        const bool eq = c == t;
-        uint32_t eq_tot, sel_tot;
-        const uint32_t eq_rank = block_exscan_flag(eq, s_scan, &eq_tot);
-        const bool sel = gt || (eq && eq_seen + eq_rank < take_eq);
-        const uint32_t pos = block_exscan_flag(sel, s_scan, &sel_tot);
-        if (sel && running + pos < M) b0[running + pos] = make_uint2(c, b);
-        running += sel_tot;
-        eq_seen += eq_tot;
+    // 2. ordered compaction, one contiguous slice of the row per wavefront
+    const uint32_t span = (((K + kSortNW - 1) / kSortNW) + 63u) & ~63u;
+    const uint32_t lo = wv * span < K ? wv * span : K, hi = lo + span < K ? lo + span : K;
+    {
+        uint32_t gt = 0, eq = 0;
+        for (uint32_t b = lo + lane; b < hi; b += 64) {
+            const uint32_t c = row[b];
+            gt += c > t;
+            eq += c == t;
+        }
+        gt = rdlane(wave_incl_scan_u32(gt), 63);
+        eq = rdlane(wave_incl_scan_u32(eq), 63);
+        if (lane == 0) {
+            s_w[wv][0] = gt;
+            s_w[wv][1] = eq;
+        }
+    }
+    __syncthreads();
+    {
+        uint32_t eq_before = 0, sel_before = 0;
+        for (uint32_t q = 0; q < wv; ++q) {
+            const uint32_t eqq = s_w[q][1];
+            const uint32_t left = take_eq > eq_before ? take_eq - eq_before : 0u;
+            sel_before += s_w[q][0] + (eqq < left ? eqq : left);
+            eq_before += eqq;
+        }
+        uint32_t running = sel_before, eq_seen = eq_before;
+        for (uint32_t base = lo; base < hi; base += 64) {
+            const uint32_t b = base + lane;
+            const uint32_t c = b < hi ? row[b] : 0u;
+            const uint64_t meq = ballot(b < hi && c == t);
+            const uint32_t eq_rank = (uint32_t)__popcll(meq & lanemask_lt());
+            const bool sel = b < hi && (c > t || (c == t && eq_seen + eq_rank < take_eq));
+            const uint64_t ms = ballot(sel);
+            const uint32_t pos = running + (uint32_t)__popcll(ms & lanemask_lt());
+            if (sel && pos < M) b0[pos] = make_uint2(c, b);
+            running += (uint32_t)__popcll(ms);
+            eq_seen += (uint32_t)__popcll(meq);
+        }
     }
     __syncthreads();
 
-    // Stable LSD radix sort by v = mx - count (ascending v = descending count).
+    // 3. stable LSD radix sort by v = mx - count (ascending v = descending count)
     const uint32_t range = mx - t;
     const uint32_t bits = range ? 32u - (uint32_t)__clz(range) : 0u;
     const uint32_t passes = (bits + 7u) / 8u;
+    const uint32_t espan = (((M + kSortNW - 1) / kSortNW) + 63u) & ~63u;
+    const uint32_t elo = wv * espan < M ? wv * espan : M, ehi = elo + espan < M ? elo + espan : M;
     uint2* src = b0;
     uint2* dst = b1;
     for (uint32_t pass = 0; pass < passes; ++pass) {
         const uint32_t shift = 8u * pass;
-        for (uint32_t d = tid; d < 256; d += bd) {
-            s_hist[d] = 0;
-            for (uint32_t q = 0; q < nwaves; ++q) s_wcnt[q][d] = 0;
-        }
+        for (uint32_t d = lane; d < 256; d += 64) s_hist[wv][d] = 0;
+        for (uint32_t e = elo + lane; e < ehi; e += 64) atomicAdd(&s_hist[wv][((mx - src[e].x) >> shift) & 255u], 1u);
         __syncthreads();
-        for (uint32_t e = tid; e < M; e += bd) atomicAdd(&s_hist[((mx - src[e].x) >> shift) & 255u], 1u);
-        __syncthreads();
-        {
+        if (wv == 0) {  // offsets in (digit, wavefront) order
+            uint32_t h[4][kSortNW], hs = 0;
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+#pragma unroll
+                for (uint32_t x = 0; x < kSortNW; ++x) {
+                    h[q][x] = s_hist[x][4u * lane + q];
+                    hs += h[q][x];
+                }
             uint32_t tot;
-            const uint32_t ex = block_exscan_u32(tid < 256 ? s_hist[tid] : 0u, s_scan, &tot);
-            if (tid < 256) s_base[tid] = ex;
+            uint32_t ex = wave_exscan_u32(hs, &tot);
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+#pragma unroll
+                for (uint32_t x = 0; x < kSortNW; ++x) {
+                    s_hist[x][4u * lane + q] = ex;
+                    ex += h[q][x];
+                }
         }
         __syncthreads();
-        for (uint32_t e0 = 0; e0 < M; e0 += bd) {
-            const uint32_t e = e0 + tid;
-            const bool valid = e < M;
+        for (uint32_t e0 = elo; e0 < ehi; e0 += 64) {
+            const uint32_t e = e0 + lane;
+            const bool valid = e < ehi;
             const uint2 kv = valid ? src[e] : make_uint2(0u, 0u);
             const uint32_t d = valid ? ((mx - kv.x) >> shift) & 255u : 0u;
             uint64_t peers = ballot(valid);
@@ -183,36 +316,18 @@ __global__ __launch_bounds__(kSortThreads) void k_sort_window(const uint32_t* __
                 peers &= on ? bb : ~bb;
             }
             const uint32_t rk = (uint32_t)__popcll(peers & lanemask_lt());
-            if (valid && rk == 0) s_wcnt[wv][d] = (uint32_t)__popcll(peers);
-            __syncthreads();
-            if (tid < 256) {
-                uint32_t run = 0;
-                for (uint32_t q = 0; q < nwaves; ++q) {
-                    const uint32_t x = s_wcnt[q][tid];
-                    s_wcnt[q][tid] = run;
-                    run += x;
-                }
-                s_hist[tid] = run;
-            }
-            __syncthreads();
-            if (valid) {
-                const uint32_t at = s_base[d] + s_wcnt[wv][d] + rk;
-                if (at < M) dst[at] = kv;
-            }
-            __syncthreads();
-            if (tid < 256) {
-                s_base[tid] += s_hist[tid];
-                for (uint32_t q = 0; q < nwaves; ++q) s_wcnt[q][tid] = 0;
-            }
-            __syncthreads();
+            const uint32_t at = valid ? s_hist[wv][d] + rk : 0u;
+            if (valid && at < M) dst[at] = kv;
+            if (valid && rk == 0) atomicAdd(&s_hist[wv][d], (uint32_t)__popcll(peers));
         }
+        __syncthreads();
         uint2* tmp = src;
         src = dst;
         dst = tmp;
     }
     uint32_t* __restrict__ ord = order + (uint64_t)w * Cmax;
     uint32_t* __restrict__ ocnt = order_count + (uint64_t)w * Cmax;
-    for (uint32_t e = tid; e < M; e += bd) {
+    for (uint32_t e = tid; e < M; e += kSortBlock) {
         const uint2 kv = src[e];
         ord[e] = kv.y;
         ocnt[e] = kv.x;
@@ -347,7 +462,24 @@ __device__ __forceinline__ LptBatch lpt_load(const uint32_t* __restrict__ ord, c
 // the loads (max L < min L + x) is placed as one round: job s of the run goes to lane s,
 // exactly as R sequential picks would choose, and every load gains x at once. The round
 // is taken only if the charged loads stay in (L, r) order; otherwise the picks proceed
-// one by one. Stores of a 64-key batch leave in one go.
+// one by one. Admitted keys are held in two 64-key batches so a round may straddle the
+// batch boundary; a batch's member and route stores leave when it is retired.
+struct LptLane {
+    LptBatch b;
+    uint32_t k;
+    double x;
+};
+
+__device__ __forceinline__ LptLane lpt_lane(const uint32_t* __restrict__ ord, const uint32_t* __restrict__ ocnt,
+                                            const uint32_t* __restrict__ moff, uint32_t a, uint32_t A)
+{
+    LptLane l;
+    l.b = lpt_load(ord, ocnt, moff, a, A);
+    l.k = a < A ? l.b.end - l.b.off : 0u;
+    l.x = l.k == 1 ? (double)l.b.cnt : (double)l.b.cnt / (double)(l.k ? l.k : 1u);
+    return l;
+}
+
 __global__ __launch_bounds__(64) void k_lpt_small(uint32_t K, uint32_t R, uint32_t Cmax, uint32_t NW,
                                                   uint32_t cands, const cr_plan_spec* __restrict__ specs,
                                                   const uint32_t* __restrict__ order,
@@ -370,79 +502,97 @@ __global__ __launch_bounds__(64) void k_lpt_small(uint32_t K, uint32_t R, uint32
     const uint32_t cidx = p % cands;
     double Lv = lane < R ? (double)cold[p] / (double)R : INFINITY;
     uint32_t rv = lane < R ? lane : 0xFFFFu;
-    LptBatch nxt = lpt_load(ord, ocnt, moff, lane, A);
-    for (uint32_t a0 = 0; a0 < A; a0 += 64) {
-        const LptBatch cur = nxt;
-        nxt = lpt_load(ord, ocnt, moff, a0 + 64 + lane, A);
-        const uint32_t nb = A - a0 < 64u ? A - a0 : 64u;
-        const uint32_t k_l = cur.end - cur.off;
-        const double x_l = k_l == 1 ? (double)cur.cnt : (double)cur.cnt / (double)k_l;
-        uint32_t first = 0;  // lane t: least-loaded member chosen for key t of the batch
-        for (uint32_t t = 0; t < nb;) {
-            const uint32_t k = rdlane(k_l, t);
-            const double x = rdlane_f64(x_l, t);
-            if (k == 1 && t + R <= nb) {
-                // length of the run of equal single-copy jobs starting at t
-                const uint64_t same = ballot(k_l == 1 && x_l == x && lane < nb);
-                const uint64_t from_t = ~(same >> t);
-                const uint32_t run = from_t ? (uint32_t)__builtin_ctzll(from_t) : 64u - t;
-                if (run >= R) {
-                    const double lo = rdlane_f64(Lv, 0), hi = rdlane_f64(Lv, R - 1);
-                    if (hi < lo + x) {
-                        const double v = Lv + x;
-                        const double vn = dpp_shl1_f64(v);
-                        const uint32_t rn = dpp_shl1(rv, rv);
-                        const bool bad_pair = lane + 1 < R && vn == v && rn < rv;
-                        if (ballot(bad_pair) == 0) {
-                            const uint32_t src = (lane - t) & 63u;
-                            const uint32_t got = (uint32_t)__shfl((int)rv, (int)src, 64);
-                            if (lane >= t && lane < t + R) first = got;
-                            if (lane < R) Lv = v;
-                            t += R;
-                            continue;
-                        }
+    LptLane cur = lpt_lane(ord, ocnt, moff, lane, A);
+    LptLane nxt = lpt_lane(ord, ocnt, moff, 64 + lane, A);
+    uint32_t fcur = 0, fnxt = 0;  // lane t: least-loaded member chosen for key t of a batch
+    uint32_t base = 0, t = 0;
+    while (base + t < A) {
+        if (t >= 64) {  // retire the current batch
+            if (base + lane < A) {
+                if (cur.k == 1) mem[cur.b.off] = (uint16_t)fcur;
+                route[(rbase + cur.b.key) * cands + cidx] = cur.k == 1 ? (CR_ROUTE_SINGLE | fcur) : (base + lane);
+            }
+            cur = nxt;
+            fcur = fnxt;
+            fnxt = 0;
+            base += 64;
+            t -= 64;
+            nxt = lpt_lane(ord, ocnt, moff, base + 64 + lane, A);
+            continue;
+        }
+        const uint32_t k = rdlane(cur.k, t);
+        const double x = rdlane_f64(cur.x, t);
+        if (k == 1) {
+            // run of equal single-copy jobs from t, across both batches
+            const uint64_t sc = ballot(cur.k == 1 && cur.x == x) >> t;
+            uint32_t run = ~sc ? (uint32_t)__builtin_ctzll(~sc) : 64u - t;
+            if (run >= 64u - t) {
+                const uint64_t sn = ballot(nxt.k == 1 && nxt.x == x);
+                run = 64u - t + (~sn ? (uint32_t)__builtin_ctzll(~sn) : 64u);
+            }
+            if (run >= R) {
+                const double lo = rdlane_f64(Lv, 0), hi = rdlane_f64(Lv, R - 1);
+                if (hi < lo + x) {
+                    const double v = Lv + x;
+                    const double vn = dpp_shl1_f64(v);
+                    const uint32_t rn = dpp_shl1(rv, rv);
+                    if (ballot(lane + 1 < R && vn == v && rn < rv) == 0) {
+                        const uint32_t gc = (uint32_t)__shfl((int)rv, (int)((lane - t) & 63u), 64);
+                        const uint32_t gn = (uint32_t)__shfl((int)rv, (int)((lane + 64u - t) & 63u), 64);
+                        if (lane >= t && lane - t < R) fcur = gc;
+                        if (lane + 64u - t < R) fnxt = gn;
+                        if (lane < R) Lv = v;
+                        t += R;
+                        continue;
                     }
                 }
             }
+            const double vv = Lv + x;
+            const double v = rdlane_f64(vv, 0);
             const uint32_t r0 = rdlane(rv, 0);
-            first = wrlane(first, r0, t);
-            if (k == 1) {
-                const double v = rdlane_f64(Lv, 0) + x;
-                // rank of (v, r0) among lanes 1..: three compares, each straight to a lane mask
-                const uint64_t m_lt = ballot(Lv < v), m_eq = ballot(Lv == v), m_r = ballot(rv < r0);
-                const uint32_t pos = (uint32_t)__popcll((m_lt | (m_eq & m_r)) & ~1ull);
-                const double sl = dpp_shl1_f64(Lv);
-                const uint32_t sr = dpp_shl1(rv, rv);
-                const bool lt = lane < pos, eq = lane == pos;
-                Lv = lt ? sl : (eq ? v : Lv);
-                rv = lt ? sr : (eq ? r0 : rv);
-            } else {
-                const uint32_t off = rdlane(cur.off, t);
-                if (lane < k) mem[off + lane] = (uint16_t)rv;
-                const double vnew = Lv + x;  // meaningful on lanes < k
-                const uint32_t rnew = rv;
-                const double sL = __shfl(Lv, (int)((lane + k) & 63u), 64);
-                const uint32_t sR = __shfl(rv, (int)((lane + k) & 63u), 64);
-                Lv = lane + k < 64u ? sL : INFINITY;
-                rv = lane + k < 64u ? sR : 0xFFFFu;
-                for (uint32_t u = 0; u < k; ++u) {
-                    const double v = rdlane_f64(vnew, u);
-                    const uint32_t r = rdlane(rnew, u);
-                    const uint64_t m_lt = ballot(Lv < v), m_eq = ballot(Lv == v), m_r = ballot(rv < r);
-                    const uint32_t pos = (uint32_t)__popcll(m_lt | (m_eq & m_r));
-                    const double up = dpp_shr1_f64(Lv);
-                    const uint32_t upr = dpp_shr1(rv, rv);
-                    const bool gt = lane > pos, eq = lane == pos;
-                    Lv = gt ? up : (eq ? v : Lv);
-                    rv = gt ? upr : (eq ? r : rv);
-                }
+            fcur = wrlane(fcur, r0, t);
+            // rank of (v, r0) among lanes 1..: three compares, each straight to a lane mask
+            const uint64_t m_lt = ballot(Lv < v), m_eq = ballot(Lv == v), m_r = ballot(rv < r0);
+            const uint32_t pos = (uint32_t)__popcll((m_lt | (m_eq & m_r)) & ~1ull);
+            const double sl = dpp_shl1_f64(Lv);
+            const uint32_t sr = dpp_shl1(rv, rv);
+            const bool lt = lane < pos, eq = lane == pos;
+            Lv = lt ? sl : (eq ? v : Lv);
+            rv = lt ? sr : (eq ? r0 : rv);
+        } else {
+            const uint32_t r0 = rdlane(rv, 0);
+            fcur = wrlane(fcur, r0, t);
+            const uint32_t off = rdlane(cur.b.off, t);
+            if (lane < k) mem[off + lane] = (uint16_t)rv;
+            const double vnew = Lv + x;  // meaningful on lanes < k
+            const uint32_t rnew = rv;
+            const double sL = __shfl(Lv, (int)((lane + k) & 63u), 64);
+            const uint32_t sR = __shfl(rv, (int)((lane + k) & 63u), 64);
+            Lv = lane + k < 64u ? sL : INFINITY;
+            rv = lane + k < 64u ? sR : 0xFFFFu;
+            for (uint32_t u = 0; u < k; ++u) {
+                const double v = rdlane_f64(vnew, u);
+                const uint32_t r = rdlane(rnew, u);
+                const uint64_t m_lt = ballot(Lv < v), m_eq = ballot(Lv == v), m_r = ballot(rv < r);
+                const uint32_t pos = (uint32_t)__popcll(m_lt | (m_eq & m_r));
+                const double up = dpp_shr1_f64(Lv);
+                const uint32_t upr = dpp_shr1(rv, rv);
+                const bool gt = lane > pos, eq = lane == pos;
+                Lv = gt ? up : (eq ? v : Lv);
+                rv = gt ? upr : (eq ? r : rv);
             }
-            ++t;
         }
-        if (lane < nb) {
-            if (k_l == 1) mem[cur.off] = (uint16_t)first;
-            route[(rbase + cur.key) * cands + cidx] = k_l == 1 ? (CR_ROUTE_SINGLE | first) : (a0 + lane);
-        }
+        ++t;
+    }
+    // retire what is left (the current batch, and the next one if a round reached it)
+    if (base + lane < A) {
+        if (cur.k == 1) mem[cur.b.off] = (uint16_t)fcur;
+        route[(rbase + cur.b.key) * cands + cidx] = cur.k == 1 ? (CR_ROUTE_SINGLE | fcur) : (base + lane);
+    }
+    if (base + 64 + lane < A && t > 64) {
+        if (nxt.k == 1 && lane < t - 64) mem[nxt.b.off] = (uint16_t)fnxt;
+        if (lane < t - 64)
+            route[(rbase + nxt.b.key) * cands + cidx] = nxt.k == 1 ? (CR_ROUTE_SINGLE | fnxt) : (base + 64 + lane);
     }
     if (lane < R) load[(uint64_t)p * R + rv] = Lv;
 }
@@ -562,8 +712,17 @@ extern "C" cr_status cr_admit(const uint32_t* counts, const cr_plan_set* plans, 
     const uint64_t route_words = (uint64_t)ng * plans->num_keys * plans->cands;
     (void)hipGetLastError();
     hipLaunchKernelGGL(k_fill_u32, dim3(1024), dim3(256), 0, st, plans->route, route_words, CR_ROUTE_COLD);
-    hipLaunchKernelGGL(k_sort_window, dim3(plans->num_windows), dim3(kSortThreads), 0, st, counts, plans->num_keys,
-                       cmax, plans->order, plans->order_count, plans->n_order, row_sum, buf);
+    if ((uint64_t)plans->num_keys * 4u <= kSortLdsRowBytes) {
+        const uint32_t lds = plans->num_keys * 4u;
+        if (hipFuncSetAttribute((const void*)k_sort_window<true>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                (int)lds) != hipSuccess)
+            return CR_EHIP;
+        hipLaunchKernelGGL(k_sort_window<true>, dim3(plans->num_windows), dim3(kSortBlock), (size_t)lds, st, counts,
+                           plans->num_keys, cmax, plans->order, plans->order_count, plans->n_order, row_sum, buf);
+    } else {
+        hipLaunchKernelGGL(k_sort_window<false>, dim3(plans->num_windows), dim3(kSortBlock), 0, st, counts,
+                           plans->num_keys, cmax, plans->order, plans->order_count, plans->n_order, row_sum, buf);
+    }
     hipLaunchKernelGGL(k_admit_plan, dim3(plans->num_plans), dim3(kSortThreads), 0, st, plans->R, cmax,
                        plans->num_windows, plans->specs, plans->order_count, plans->n_order, row_sum,
                        plans->num_admitted, plans->cold, plans->clamped, plans->member_off, err);

@@ -161,6 +161,7 @@ __global__ __launch_bounds__(64) void k_part_scatter(const uint32_t* __restrict_
     const uint16_t* __restrict__ dc = dest + (uint64_t)c * n;
     uint64_t* __restrict__ rc = rec + (uint64_t)c * n;
     uint32_t j = find_interval(off, J, t0);
+    uint64_t jend = j + 1 < J ? off[j + 1] : ~0ull;  // first request of the next interval
     uint64_t i = t0 + lane;
     uint32_t nd = i < t1 ? dc[i] : 0xFFFFu;
     uint32_t nk = i < t1 ? keys[i] : 0u;
@@ -174,7 +175,9 @@ __global__ __launch_bounds__(64) void k_part_scatter(const uint32_t* __restrict_
         ns = in2 < t1 ? suffix[in2] : 0u;
         const bool valid = i < t1 && d < R;
         uint32_t jl = j;
-        while (jl + 1 < J && off[jl + 1] <= i) ++jl;
+        if (base + 63 >= jend) {  // an interval boundary falls inside these 64 requests
+            while (jl + 1 < J && off[jl + 1] <= i) ++jl;
+        }
         uint64_t peers = ballot(valid);
         for (uint32_t bit = 0; bit < nbits; ++bit) {
             const bool on = (d >> bit) & 1u;
@@ -189,7 +192,10 @@ __global__ __launch_bounds__(64) void k_part_scatter(const uint32_t* __restrict_
         __syncthreads();
         if (valid && rk == 0) run[d] += (uint32_t)__popcll(peers);
         __syncthreads();
-        j = rdlane(jl, 63);
+        if (base + 63 >= jend) {
+            j = rdlane(jl, 63);
+            jend = j + 1 < J ? off[j + 1] : ~0ull;
+        }
     }
 }
 

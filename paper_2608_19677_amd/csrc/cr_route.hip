@@ -37,9 +37,14 @@ __global__ __launch_bounds__(kRouteThreads) void k_route(
     uint16_t* __restrict__ dest, uint32_t* __restrict__ err)
 {
     __shared__ uint32_t s_j0;
+    __shared__ uint64_t s_bnd[4];  // starts of the next four intervals (~0 past the last)
     const uint64_t bstart = (uint64_t)xcd_tile(blockIdx.x, gridDim.x) * kRouteThreads * kPer;
     if (bstart >= n) return;
-    if (threadIdx.x == 0) s_j0 = find_interval(off, J, bstart);
+    if (threadIdx.x < 64) {
+        const uint32_t j0 = find_interval(off, J, bstart);
+        if (threadIdx.x == 0) s_j0 = j0;
+        if (threadIdx.x < 4) s_bnd[threadIdx.x] = j0 + 1 + threadIdx.x < J ? off[j0 + 1 + threadIdx.x] : ~0ull;
+    }
     __syncthreads();
     const uint64_t base = bstart + (uint64_t)threadIdx.x * kPer;
     if (base >= n) return;
@@ -55,12 +60,15 @@ __global__ __launch_bounds__(kRouteThreads) void k_route(
 #pragma unroll
         for (int t = 0; t < kPer; ++t) b[t] = base + t < n ? keys[base + t] : 0u;
     }
-    uint32_t j = s_j0;
+    const uint32_t j0 = s_j0;
+    const uint64_t e0 = s_bnd[0], e1 = s_bnd[1], e2 = s_bnd[2], e3 = s_bnd[3];
     bool bad = false;
 #pragma unroll
     for (int t = 0; t < kPer; ++t) {
         const uint64_t i = base + t;
-        while (j + 1 < J && off[j + 1] <= i) ++j;
+        uint32_t j = j0 + (i >= e0) + (i >= e1) + (i >= e2) + (i >= e3);
+        if (i >= e3)
+            while (j + 1 < J && off[j + 1] <= i) ++j;
         const uint32_t gg = gmap[j];
         g[t] = gg < NG ? gg : NG - 1;
         h[t] = req_hash(smix, first_index + i);
