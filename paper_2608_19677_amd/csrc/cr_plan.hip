@@ -458,26 +458,41 @@ __device__ __forceinline__ LptBatch lpt_load(const uint32_t* __restrict__ ord, c
 // lanes 0..k-1. After charging them, each is re-inserted at its rank among the rest:
 // three compares straight to lane masks give the rank, a one-lane DPP shift opens the
 // slot; for k = 1 the pop and the insert fuse into one shift.
-// A run of at least R equal single-copy jobs whose size exceeds the current spread of
-// the loads (max L < min L + x) is placed as one round: job s of the run goes to lane s,
-// exactly as R sequential picks would choose, and every load gains x at once. The round
-// is taken only if the charged loads stay in (L, r) order; otherwise the picks proceed
-// one by one. Admitted keys are held in two 64-key batches so a round may straddle the
-// batch boundary; a batch's member and route stores leave when it is retired.
-struct LptLane {
-    LptBatch b;
-    uint32_t k;
-    double x;
+// Runs of equal single-copy jobs are placed several at a time. With v0 = min L + x, every
+// lane below v0 is picked before any charged load can come back into play, so the next
+// m = min(run, #lanes below v0) jobs go to lanes 0..m-1 exactly as m sequential picks
+// would place them. If m = R (a full round) every load gains x in place; otherwise the m
+// charged loads are merged back by counting ranks and one forward lane permutation. A
+// batch is taken only while the charged loads keep their (L, r) order, else the picks
+// proceed one by one. Admitted keys sit in two 64-key batches so a batch of jobs may
+// straddle the boundary; a batch's member and route stores leave when it is retired.
+struct LptRaw {
+    uint32_t key, cnt, off, end;
 };
 
-__device__ __forceinline__ LptLane lpt_lane(const uint32_t* __restrict__ ord, const uint32_t* __restrict__ ocnt,
-                                            const uint32_t* __restrict__ moff, uint32_t a, uint32_t A)
+__device__ __forceinline__ LptRaw lpt_raw(const uint32_t* __restrict__ ord, const uint32_t* __restrict__ ocnt,
+                                          const uint32_t* __restrict__ moff, uint32_t a, uint32_t A)
 {
-    LptLane l;
-    l.b = lpt_load(ord, ocnt, moff, a, A);
-    l.k = a < A ? l.b.end - l.b.off : 0u;
-    l.x = l.k == 1 ? (double)l.b.cnt : (double)l.b.cnt / (double)(l.k ? l.k : 1u);
-    return l;
+    LptRaw r{0u, 0u, 0u, 0u};
+    if (a < A) {
+        r.key = ord[a];
+        r.cnt = ocnt[a];
+        r.off = moff[a];
+        r.end = moff[a + 1];
+    }
+    return r;
+}
+
+__device__ __forceinline__ uint32_t ds_permute_u32(uint32_t dst_lane, uint32_t v)
+{
+    return (uint32_t)__builtin_amdgcn_ds_permute((int)(dst_lane << 2), (int)v);
+}
+
+__device__ __forceinline__ double ds_permute_f64(uint32_t dst_lane, double v)
+{
+    const uint64_t u = (uint64_t)__double_as_longlong(v);
+    const uint32_t lo = ds_permute_u32(dst_lane, (uint32_t)u), hi = ds_permute_u32(dst_lane, (uint32_t)(u >> 32));
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
 }
 
 __global__ __launch_bounds__(64) void k_lpt_small(uint32_t K, uint32_t R, uint32_t Cmax, uint32_t NW,
@@ -502,67 +517,95 @@ __global__ __launch_bounds__(64) void k_lpt_small(uint32_t K, uint32_t R, uint32
     const uint32_t cidx = p % cands;
     double Lv = lane < R ? (double)cold[p] / (double)R : INFINITY;
     uint32_t rv = lane < R ? lane : 0xFFFFu;
-    LptLane cur = lpt_lane(ord, ocnt, moff, lane, A);
-    LptLane nxt = lpt_lane(ord, ocnt, moff, 64 + lane, A);
+    LptRaw cur = lpt_raw(ord, ocnt, moff, lane, A);
+    LptRaw nxt = lpt_raw(ord, ocnt, moff, 64 + lane, A);
+    uint32_t kc = cur.end - cur.off;  // k of the current batch's keys (0 past A)
+    double xc = kc == 1 ? (double)cur.cnt : (double)cur.cnt / (double)(kc ? kc : 1u);
     uint32_t fcur = 0, fnxt = 0;  // lane t: least-loaded member chosen for key t of a batch
     uint32_t base = 0, t = 0;
     while (base + t < A) {
-        if (t >= 64) {  // retire the current batch
+        if (t >= 64) {  // retire the current batch, promote the next one
             if (base + lane < A) {
-                if (cur.k == 1) mem[cur.b.off] = (uint16_t)fcur;
-                route[(rbase + cur.b.key) * cands + cidx] = cur.k == 1 ? (CR_ROUTE_SINGLE | fcur) : (base + lane);
+                if (kc == 1) mem[cur.off] = (uint16_t)fcur;
+                route[(rbase + cur.key) * cands + cidx] = kc == 1 ? (CR_ROUTE_SINGLE | fcur) : (base + lane);
             }
             cur = nxt;
+            kc = cur.end - cur.off;
+            xc = kc == 1 ? (double)cur.cnt : (double)cur.cnt / (double)(kc ? kc : 1u);
             fcur = fnxt;
             fnxt = 0;
             base += 64;
             t -= 64;
-            nxt = lpt_lane(ord, ocnt, moff, base + 64 + lane, A);
+            nxt = lpt_raw(ord, ocnt, moff, base + 64 + lane, A);
             continue;
         }
-        const uint32_t k = rdlane(cur.k, t);
-        const double x = rdlane_f64(cur.x, t);
+        const uint32_t k = rdlane(kc, t);
+        const double x = rdlane_f64(xc, t);
         if (k == 1) {
             // run of equal single-copy jobs from t, across both batches
-            const uint64_t sc = ballot(cur.k == 1 && cur.x == x) >> t;
+            const uint32_t cnt = rdlane(cur.cnt, t);
+            const uint64_t sc = ballot(kc == 1 && cur.cnt == cnt) >> t;
             uint32_t run = ~sc ? (uint32_t)__builtin_ctzll(~sc) : 64u - t;
             if (run >= 64u - t) {
-                const uint64_t sn = ballot(nxt.k == 1 && nxt.x == x);
+                const uint64_t sn = ballot(nxt.end - nxt.off == 1 && nxt.cnt == cnt && base + 64 + lane < A);
                 run = 64u - t + (~sn ? (uint32_t)__builtin_ctzll(~sn) : 64u);
             }
-            if (run >= R) {
-                const double lo = rdlane_f64(Lv, 0), hi = rdlane_f64(Lv, R - 1);
-                if (hi < lo + x) {
-                    const double v = Lv + x;
-                    const double vn = dpp_shl1_f64(v);
-                    const uint32_t rn = dpp_shl1(rv, rv);
-                    if (ballot(lane + 1 < R && vn == v && rn < rv) == 0) {
-                        const uint32_t gc = (uint32_t)__shfl((int)rv, (int)((lane - t) & 63u), 64);
-                        const uint32_t gn = (uint32_t)__shfl((int)rv, (int)((lane + 64u - t) & 63u), 64);
-                        if (lane >= t && lane - t < R) fcur = gc;
-                        if (lane + 64u - t < R) fnxt = gn;
+            const double v = Lv + x;
+            const double v0 = rdlane_f64(v, 0);
+            const uint32_t below = (uint32_t)__popcll(ballot(Lv < v0));
+            const uint32_t m = run < below ? run : below;
+            if (m >= 2) {
+                // the charged loads must keep their (L, r) order
+                const double vn = dpp_shl1_f64(v);
+                const uint32_t rn = dpp_shl1(rv, rv);
+                if (ballot(lane + 1 < m && vn == v && rn < rv) == 0) {
+                    const uint32_t gc = (uint32_t)__shfl((int)rv, (int)((lane - t) & 63u), 64);
+                    const uint32_t gn = (uint32_t)__shfl((int)rv, (int)((lane + 64u - t) & 63u), 64);
+                    if (lane >= t && lane - t < m) fcur = gc;
+                    if (lane + 64u - t < m) fnxt = gn;
+                    if (m >= R) {
                         if (lane < R) Lv = v;
-                        t += R;
-                        continue;
+                    } else {
+                        // Merge: every lane's new place is its index within its own sorted
+                        // set plus the number of lanes of the other set that precede it.
+                        // The loop runs over the smaller set; (L, r) is a strict total order,
+                        // so one compare per lane serves both directions.
+                        const double a = lane < m ? v : Lv;
+                        const bool charged = lane < m;
+                        const bool loop_charged = m <= R - m;
+                        const uint32_t s0 = loop_charged ? 0u : m, s1 = loop_charged ? m : R;
+                        const bool other = lane < R && charged != loop_charged;
+                        uint32_t cnt = 0;
+                        for (uint32_t sl = s0; sl < s1; ++sl) {
+                            const double as = rdlane_f64(a, sl);
+                            const uint32_t rs = rdlane(rv, sl);
+                            const bool s_first = as < a || (as == a && rs < rv);
+                            cnt += (other && s_first) ? 1u : 0u;
+                            const uint32_t before = (uint32_t)__popcll(ballot(other && !s_first));
+                            cnt = wrlane(cnt, before, sl);
+                        }
+                        const uint32_t np = charged ? lane + cnt : (lane < R ? lane - m + cnt : lane);
+                        Lv = ds_permute_f64(np, a);
+                        rv = ds_permute_u32(np, rv);
                     }
+                    t += m;
+                    continue;
                 }
             }
-            const double vv = Lv + x;
-            const double v = rdlane_f64(vv, 0);
             const uint32_t r0 = rdlane(rv, 0);
             fcur = wrlane(fcur, r0, t);
-            // rank of (v, r0) among lanes 1..: three compares, each straight to a lane mask
-            const uint64_t m_lt = ballot(Lv < v), m_eq = ballot(Lv == v), m_r = ballot(rv < r0);
+            // rank of (v0, r0) among lanes 1..: three compares, each straight to a lane mask
+            const uint64_t m_lt = ballot(Lv < v0), m_eq = ballot(Lv == v0), m_r = ballot(rv < r0);
             const uint32_t pos = (uint32_t)__popcll((m_lt | (m_eq & m_r)) & ~1ull);
             const double sl = dpp_shl1_f64(Lv);
             const uint32_t sr = dpp_shl1(rv, rv);
             const bool lt = lane < pos, eq = lane == pos;
-            Lv = lt ? sl : (eq ? v : Lv);
+            Lv = lt ? sl : (eq ? v0 : Lv);
             rv = lt ? sr : (eq ? r0 : rv);
         } else {
             const uint32_t r0 = rdlane(rv, 0);
             fcur = wrlane(fcur, r0, t);
-            const uint32_t off = rdlane(cur.b.off, t);
+            const uint32_t off = rdlane(cur.off, t);
             if (lane < k) mem[off + lane] = (uint16_t)rv;
             const double vnew = Lv + x;  // meaningful on lanes < k
             const uint32_t rnew = rv;
@@ -584,15 +627,15 @@ __global__ __launch_bounds__(64) void k_lpt_small(uint32_t K, uint32_t R, uint32
         }
         ++t;
     }
-    // retire what is left (the current batch, and the next one if a round reached it)
+    // retire what is left (the current batch, and the next one if a batch of jobs reached it)
     if (base + lane < A) {
-        if (cur.k == 1) mem[cur.b.off] = (uint16_t)fcur;
-        route[(rbase + cur.b.key) * cands + cidx] = cur.k == 1 ? (CR_ROUTE_SINGLE | fcur) : (base + lane);
+        if (kc == 1) mem[cur.off] = (uint16_t)fcur;
+        route[(rbase + cur.key) * cands + cidx] = kc == 1 ? (CR_ROUTE_SINGLE | fcur) : (base + lane);
     }
-    if (base + 64 + lane < A && t > 64) {
-        if (nxt.k == 1 && lane < t - 64) mem[nxt.b.off] = (uint16_t)fnxt;
-        if (lane < t - 64)
-            route[(rbase + nxt.b.key) * cands + cidx] = nxt.k == 1 ? (CR_ROUTE_SINGLE | fnxt) : (base + 64 + lane);
+    if (t > 64 && lane < t - 64 && base + 64 + lane < A) {
+        const uint32_t kn = nxt.end - nxt.off;
+        if (kn == 1) mem[nxt.off] = (uint16_t)fnxt;
+        route[(rbase + nxt.key) * cands + cidx] = kn == 1 ? (CR_ROUTE_SINGLE | fnxt) : (base + 64 + lane);
     }
     if (lane < R) load[(uint64_t)p * R + rv] = Lv;
 }
