@@ -14,9 +14,13 @@
 //        wavefront rebuilds it by scanning backwards, then replays its segment. This
 //        turns R*P sequential streams into thousands of independent wavefronts with
 //        results identical to one sequential pass.
-// The LRU lives in registers: slot (s, lane) holds a key and its recency rank (0 = most
-// recent). A lookup is one compare per slot plus a ballot; the update is a rank shift, so
-// no per-request search or reduction is needed.
+// The LRU lives in registers. Up to 64 slots it is a move-to-front list across the lanes:
+// lane i holds the i-th most recent key. A lookup is one compare and a ballot; the first
+// set bit p is the hit depth, and the update shifts lanes 0..p (all lanes on a miss) up
+// by one and writes the key into lane 0, a single select between a lane and its left
+// neighbour under a scalar mask. Above 64 slots, slot (s, lane) holds a key and its
+// recency rank (0 = most recent) and the update is a rank shift; neither form needs a
+// per-request search or reduction.
 #include "cr_common.h"
 
 namespace cr {
@@ -300,6 +304,27 @@ __device__ __forceinline__ bool lru_step(uint32_t (&skey)[SL], uint32_t (&srank)
     return hit;
 }
 
+// First set bit of a wave mask, 0xFFFFFFFF when none (s_ff1_i32_b64).
+__device__ __forceinline__ uint32_t sff1(uint64_t m)
+{
+    uint32_t p;
+    asm("s_ff1_i32_b64 %0, %1" : "=s"(p) : "s"(m));
+    return p;
+}
+
+// Move-to-front access of key kk (lane i = i-th most recent key; lanes outside `wmask`
+// are ignored). Returns the hit depth, or 0xFFFFFFFF on a miss. On a miss the shift runs
+// over every lane, which drops the least recent key of a full list.
+__device__ __forceinline__ uint32_t mtf_step(uint32_t& sk, uint32_t kk, uint64_t wmask)
+{
+    const uint32_t p = sff1(ballot(sk == kk) & wmask);
+    const uint64_t keep = ~1ull << (p & 63u);  // lanes deeper than the hit keep their key
+    const uint32_t up = (uint32_t)__builtin_amdgcn_mov_dpp((int)sk, 0x138, 0xF, 0xF, true);  // wave_shr:1
+    sk = __builtin_amdgcn_inverse_ballot_w64(keep) ? sk : up;
+    sk = wrlane(sk, kk, 0u);
+    return p;
+}
+
 __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v)
 {
 #pragma unroll
@@ -337,6 +362,8 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
     const uint32_t s1 = cnt - s0 < S ? cnt : s0 + S;
     const uint64_t* __restrict__ rl = rec + (uint64_t)c * n + gs;
 
+    // Slot q of the rebuilt state (q = 64 s + lane) is the q-th most recent key, which is
+    // already the move-to-front order; the rank form starts from rank = slot.
     uint32_t skey[SL], srank[SL];
 #pragma unroll
     for (int s = 0; s < SL; ++s) {
@@ -344,6 +371,8 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
         skey[s] = CR_EMPTY_SLOT;
         srank[s] = idx < W ? idx : 0xFFFFFFFFu;
     }
+    const uint64_t wmask = W >= 64u ? ~0ull : ((1ull << W) - 1ull);
+    (void)wmask;
     // State before the segment: the most recent W distinct keys, newest first. Records are
     // read backwards 64 at a time, the next (older) batch in flight while one is scanned.
     uint32_t q = 0;
@@ -417,19 +446,34 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
         const bool vl = lane < nb && kl < K;
         bad |= lane < nb && kl >= K;
         const uint32_t pl = vl ? prefix_len[kl] : 0u;  // consumed after the batch
-        uint32_t hitf = 0;
-        if (ballot(lane < nb && kl >= K) == 0) {
-            for (uint32_t t = 0; t < nb; ++t)
-                hitf = wrlane(hitf, lru_step<SL>(skey, srank, rdlane(kl, t), W) ? 1u : 0u, t);
-        } else {
-            for (uint32_t t = 0; t < nb; ++t) {
-                const uint32_t kk = rdlane(kl, t);
-                if (kk < K) hitf = wrlane(hitf, lru_step<SL>(skey, srank, kk, W) ? 1u : 0u, t);
+        bool hl;
+        if constexpr (SL == 1) {
+            uint32_t depth = 0xFFFFFFFFu;  // lane t: hit depth of record t
+            if (ballot(vl) == ~0ull) {
+#pragma unroll
+                for (uint32_t t = 0; t < 64; ++t) depth = wrlane(depth, mtf_step(skey[0], rdlane(kl, t), wmask), t);
+            } else {
+                for (uint32_t t = 0; t < nb; ++t) {
+                    const uint32_t kk = rdlane(kl, t);
+                    if (kk < K) depth = wrlane(depth, mtf_step(skey[0], kk, wmask), t);
+                }
             }
+            hl = depth != 0xFFFFFFFFu;
+        } else {
+            uint32_t hitf = 0;
+            if (ballot(lane < nb && kl >= K) == 0) {
+                for (uint32_t t = 0; t < nb; ++t)
+                    hitf = wrlane(hitf, lru_step<SL>(skey, srank, rdlane(kl, t), W) ? 1u : 0u, t);
+            } else {
+                for (uint32_t t = 0; t < nb; ++t) {
+                    const uint32_t kk = rdlane(kl, t);
+                    if (kk < K) hitf = wrlane(hitf, lru_step<SL>(skey, srank, kk, W) ? 1u : 0u, t);
+                }
+            }
+            hl = hitf != 0;
         }
         const uint32_t sfx = (uint32_t)(rv >> 32) & 0xFFFFu;
         const uint32_t ivl = (uint32_t)(rv >> 48);
-        const bool hl = hitf != 0;
         uint64_t rem = ballot(vl);
         while (rem) {
             const uint32_t iv = rdlane(ivl, first_lane(rem));
@@ -451,10 +495,14 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
     if (ballot(bad) && lane == 0) atomicOr(err, CR_ERR_KEY_RANGE);
     if (s1 == cnt) {
         uint32_t* __restrict__ lo_ = lru_out + ((uint64_t)c * R + d) * max_W;
+        if constexpr (SL == 1) {
+            if (lane < W) lo_[lane] = skey[0];
+        } else {
 #pragma unroll
-        for (int s = 0; s < SL; ++s) {
-            const uint32_t idx = (uint32_t)s * 64u + lane;
-            if (idx < W && srank[s] < W) lo_[srank[s]] = skey[s];
+            for (int s = 0; s < SL; ++s) {
+                const uint32_t idx = (uint32_t)s * 64u + lane;
+                if (idx < W && srank[s] < W) lo_[srank[s]] = skey[s];
+            }
         }
         for (uint32_t idx = W + lane; idx < max_W; idx += 64) lo_[idx] = CR_EMPTY_SLOT;
     }
