@@ -43,7 +43,6 @@ typedef int32_t cr_status;
 #define CR_ERR_SPEC 4u        /* a plan spec disagrees with its counts row         */
 
 #define CR_EMPTY_SLOT 0xFFFFFFFFu /* unused LRU slot / unused key               */
-#define CR_ROUTE_COLD 0xFFFFFFFFu /* route word of a key that is not admitted    */
 #define CR_ROUTE_SINGLE 0x80000000u /* route word flag: k = 1, low 16 bits = dest */
 
 #define CR_MAX_R 1024      /* destinations per plan                            */
@@ -63,9 +62,13 @@ typedef struct {
 } cr_plan_spec;
 
 /* A set of NP plans arranged as NG groups of `cands` candidates: plan p = g*cands + c.
- * Every plan of group g routes the same requests; the route table is key-major within
- * a group so one request reads one contiguous row of `cands` words.
- * Host struct of device pointers; sizes follow from the fields (C_max = R * max_W):
+ * Every plan of group g routes the same requests. A plan's dispatch table is compact:
+ * key_index marks its admitted keys in a bit mask per 64 keys together with the key rank
+ * (position in key order among the admitted keys) of the first admitted key of those 64,
+ * and route holds one word per admitted key in key-rank order. A lookup is one 16-byte
+ * load and a popcount; a cold key needs nothing more.
+ * Host struct of device pointers; sizes follow from the fields (C_max = R * max_W,
+ * KW = ceil(num_keys / 64)):
  *   order      u32 [num_windows][C_max]  nonzero keys by (count desc, key asc), cut at C_max
  *   order_count u32 [num_windows][C_max] their counts
  *   n_order    u32 [num_windows]         entries of order used
@@ -75,8 +78,10 @@ typedef struct {
  *   member_off u32 [NP][C_max + 1]       member list a = members[off[a] .. off[a+1])
  *   members    u16 [NP][C_max]           T(b) per admitted key, in selection order
  *   load       f64 [NP][R]               planned loads L after placement
- *   route      u32 [NG][num_keys][cands] route words: CR_ROUTE_COLD,
- *                                        CR_ROUTE_SINGLE | dest, or admission index a */
+ *   key_index  u64 [NP][KW][2]          {admitted-key bits of keys 64w..64w+63,
+ *                                        key rank of the first admitted key among them}
+ *   route      u32 [NP][C_max]           by key rank: CR_ROUTE_SINGLE | dest (k = 1)
+ *                                        or the admission index a (k > 1) */
 typedef struct {
     uint32_t num_plans;   /* NP = NG * cands                                       */
     uint32_t cands;       /* candidates per group, 1..CR_MAX_CANDS                 */
@@ -94,6 +99,7 @@ typedef struct {
     uint32_t* member_off;
     uint16_t* members;
     double* load;
+    uint64_t* key_index;
     uint32_t* route;
 } cr_plan_set;
 
@@ -113,8 +119,8 @@ size_t cr_admit_workspace_bytes(uint32_t num_windows, uint32_t R, uint32_t max_W
  * For every plan: k_b by Eq. 1 (exact integers, clamped to R), then admit the longest
  * prefix of that order whose k_b sum is <= C = R * W; cold = n_window - admitted counts.
  * counts u32 [num_windows][num_keys]. Writes order, order_count, n_order, num_admitted,
- * cold, clamped and member_off[0..A] (prefix sums of k), and resets every route word to
- * CR_ROUTE_COLD for cr_place_lpt to fill. A spec with a window out of range,
+ * cold, clamped, member_off[0..A] (prefix sums of k) and the plan's whole key_index
+ * (its admitted keys are order[window][0..A)). A spec with a window out of range,
  * q_num == 0 on a nonempty window, or n_window != row sum sets CR_ERR_SPEC (the plan
  * then admits nothing). */
 cr_status cr_admit(const uint32_t* counts, const cr_plan_set* plans, void* ws, size_t ws_bytes,
@@ -124,7 +130,7 @@ cr_status cr_admit(const uint32_t* counts, const cr_plan_set* plans, void* ws, s
  * Per plan: L[r] = cold / R; admitted keys in admission order take the k smallest
  * (L[r], r) destinations, listed in that order, each charged count / k (IEEE double,
  * one rounding per operation, the same order as the definition). Writes members,
- * load and the route words of admitted keys (cr_admit has reset the others). */
+ * load and route[0..A) (it reads key_index as cr_admit left it). */
 cr_status cr_place_lpt(const uint32_t* counts, const cr_plan_set* plans, void* stream);
 
 /* Dispatch (Section 3.1 "Placement and dispatch"; Fig. 1), order-independent form.

@@ -19,7 +19,6 @@ from .build import LIB
 CR_OK, CR_EINVAL, CR_ESIZE, CR_EHIP = 0, -1, -2, -3
 CR_ERR_KEY_RANGE, CR_ERR_DEST_RANGE, CR_ERR_SPEC = 1, 2, 4
 CR_EMPTY_SLOT = 0xFFFFFFFF
-CR_ROUTE_COLD = 0xFFFFFFFF
 CR_ROUTE_SINGLE = 0x80000000
 CR_MAX_R, CR_MAX_W, CR_MAX_CANDS, CR_MAX_J = 1024, 512, 256, 65535
 
@@ -37,7 +36,7 @@ class CrPlanSet(ctypes.Structure):
     _fields_ = [("num_plans", _u32), ("cands", _u32), ("R", _u32), ("max_W", _u32), ("num_keys", _u32),
                 ("num_windows", _u32), ("specs", _P), ("order", _P), ("order_count", _P), ("n_order", _P),
                 ("num_admitted", _P), ("cold", _P), ("clamped", _P), ("member_off", _P), ("members", _P),
-                ("load", _P), ("route", _P)]
+                ("load", _P), ("key_index", _P), ("route", _P)]
 
 
 class CrError(RuntimeError):
@@ -167,7 +166,6 @@ class PlanSet:
         cmax = R * max_W
         self.cmax = cmax
         NP, NW = self.num_plans, num_windows
-        ng = NP // cands
         raw = (CrPlanSpec * NP)(*[CrPlanSpec(*s) for s in specs])
         host = torch.frombuffer(bytearray(bytes(raw)), dtype=torch.uint8)
         self.specs = host.to(device)
@@ -181,8 +179,9 @@ class PlanSet:
         self.member_off = torch.empty((NP, cmax + 1), **i32)
         self.members = torch.empty((NP, cmax), dtype=torch.int16, device=device)
         self.load = torch.empty((NP, R), dtype=torch.float64, device=device)
-        self.route = torch.empty((ng, num_keys, cands), **i32)
+        self.key_index = torch.empty((NP, (num_keys + 63) // 64, 2), dtype=torch.int64, device=device)
+        self.route = torch.empty((NP, cmax), **i32)
         self.c = CrPlanSet(NP, cands, R, max_W, num_keys, NW, _ptr(self.specs), _ptr(self.order),
                            _ptr(self.order_count), _ptr(self.n_order),
                            _ptr(self.num_admitted), _ptr(self.cold), _ptr(self.clamped), _ptr(self.member_off),
-                           _ptr(self.members), _ptr(self.load), _ptr(self.route))
+                           _ptr(self.members), _ptr(self.load), _ptr(self.key_index), _ptr(self.route))

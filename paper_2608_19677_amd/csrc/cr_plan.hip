@@ -334,18 +334,67 @@ __global__ __launch_bounds__(kSortBlock) void k_sort_window(const uint32_t* __re
     }
 }
 
-// One block per plan: Eq. 1 and the prefix admission.
+// Key index of a plan: bit b % 64 of word b / 64 is set for every admitted key b, and
+// each word carries the key rank of its first admitted key (an exclusive scan of the
+// word popcounts). Built in LDS when the words fit, else with global atomics.
+constexpr uint32_t kKxLdsWords = 4096;  // 32 KB of bits: up to 262,144 keys
+
+__device__ void build_key_index(const uint32_t* __restrict__ ord, uint32_t A, uint32_t KW, uint64_t* __restrict__ kx,
+                                uint64_t* s_bits, uint32_t* s_scan)
+{
+    const uint32_t tid = threadIdx.x, bd = blockDim.x;
+    const bool in_lds = KW <= kKxLdsWords;
+    if (in_lds) {
+        for (uint32_t w = tid; w < KW; w += bd) s_bits[w] = 0ull;
+        __syncthreads();
+        for (uint32_t a = tid; a < A; a += bd) {
+            const uint32_t b = ord[a];
+            atomicOr(reinterpret_cast<unsigned long long*>(&s_bits[b >> 6]), 1ull << (b & 63u));
+        }
+        __syncthreads();
+    } else {
+        for (uint32_t w = tid; w < KW; w += bd) kx[2u * w] = 0ull;
+        __threadfence();
+        __syncthreads();
+        for (uint32_t a = tid; a < A; a += bd) {
+            const uint32_t b = ord[a];
+            atomicOr(reinterpret_cast<unsigned long long*>(&kx[2u * (b >> 6)]), 1ull << (b & 63u));
+        }
+        __threadfence();
+        __syncthreads();
+    }
+    uint32_t carry = 0;
+    for (uint32_t w0 = 0; w0 < KW; w0 += bd) {
+        const uint32_t w = w0 + tid;
+        uint64_t bits = 0;
+        if (w < KW)
+            bits = in_lds ? s_bits[w] : __hip_atomic_load(&kx[2u * w], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        uint32_t tot;
+        const uint32_t ex = block_exscan_u32((uint32_t)__popcll(bits), s_scan, &tot);
+        if (w < KW) {
+            if (in_lds) kx[2u * w] = bits;
+            kx[2u * w + 1u] = carry + ex;
+        }
+        carry += tot;
+    }
+}
+
+// One block per plan: Eq. 1, the prefix admission and the plan's key index.
 __global__ __launch_bounds__(kSortThreads) void k_admit_plan(
-    uint32_t R, uint32_t Cmax, uint32_t NW,
-    const cr_plan_spec* __restrict__ specs, const uint32_t* __restrict__ order_count,
-    const uint32_t* __restrict__ n_order, const uint64_t* __restrict__ row_sum, uint32_t* __restrict__ num_admitted, uint64_t* __restrict__ cold,
-    uint32_t* __restrict__ clamped, uint32_t* __restrict__ member_off, uint32_t* __restrict__ err)
+    uint32_t R, uint32_t Cmax, uint32_t NW, uint32_t KW,
+    const cr_plan_spec* __restrict__ specs, const uint32_t* __restrict__ order,
+    const uint32_t* __restrict__ order_count, const uint32_t* __restrict__ n_order,
+    const uint64_t* __restrict__ row_sum, uint32_t* __restrict__ num_admitted, uint64_t* __restrict__ cold,
+    uint32_t* __restrict__ clamped, uint32_t* __restrict__ member_off, uint64_t* __restrict__ key_index,
+    uint32_t* __restrict__ err)
 {
     __shared__ uint32_t s_scan[16];
     __shared__ unsigned long long s_carried;
+    __shared__ uint64_t s_bits[kKxLdsWords];
     const uint32_t p = blockIdx.x, tid = threadIdx.x, bd = blockDim.x, lane = lane_id();
     const cr_plan_spec spec = specs[p];
     uint32_t* __restrict__ moff = member_off + (uint64_t)p * (Cmax + 1u);
+    uint64_t* __restrict__ kx = key_index + (uint64_t)p * 2u * KW;
     bool ok = spec.window < NW && spec.W >= 1 && (uint64_t)R * spec.W <= Cmax;
     const uint32_t M = ok ? n_order[spec.window] : 0u;
     if (ok && spec.n_window != row_sum[spec.window]) ok = false;
@@ -358,6 +407,7 @@ __global__ __launch_bounds__(kSortThreads) void k_admit_plan(
             moff[0] = 0;
             atomicOr(err, CR_ERR_SPEC);
         }
+        build_key_index(order, 0u, KW, kx, s_bits, s_scan);
         return;
     }
     const uint64_t C = (uint64_t)R * spec.W;
@@ -405,12 +455,7 @@ __global__ __launch_bounds__(kSortThreads) void k_admit_plan(
         cold[p] = spec.n_window >= carried ? spec.n_window - carried : 0ull;
         clamped[p] = ncl;
     }
-}
-
-__global__ void k_fill_u32(uint32_t* __restrict__ p, uint64_t n, uint32_t v)
-{
-    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
-    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = v;
+    build_key_index(order + (uint64_t)spec.window * Cmax, A, KW, kx, s_bits, s_scan);
 }
 
 __device__ __forceinline__ uint32_t dpp_shl1(uint32_t old, uint32_t v)  // lane i <- lane i+1
@@ -454,6 +499,18 @@ __device__ __forceinline__ LptBatch lpt_load(const uint32_t* __restrict__ ord, c
     return b;
 }
 
+// Key index entry of key b ({bits, rank of the word's first admitted key}); the key's
+// rank is entry.y + popcount of the bits below b.
+__device__ __forceinline__ ulonglong2 kx_entry(const uint64_t* __restrict__ kx, uint32_t b, bool valid)
+{
+    return valid ? *reinterpret_cast<const ulonglong2*>(kx + 2u * (b >> 6)) : make_ulonglong2(0ull, 0ull);
+}
+
+__device__ __forceinline__ uint32_t kx_rank(ulonglong2 e, uint32_t b)
+{
+    return (uint32_t)e.y + (uint32_t)__popcll(e.x & ((1ull << (b & 63u)) - 1ull));
+}
+
 // R <= 64: lane i holds the i-th smallest (L, r), so the least-loaded destinations are
 // lanes 0..k-1. After charging them, each is re-inserted at its rank among the rest:
 // three compares straight to lane masks give the rank, a one-lane DPP shift opens the
@@ -495,13 +552,14 @@ __device__ __forceinline__ double ds_permute_f64(uint32_t dst_lane, double v)
     return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
 }
 
-__global__ __launch_bounds__(64) void k_lpt_small(uint32_t K, uint32_t R, uint32_t Cmax, uint32_t NW,
-                                                  uint32_t cands, const cr_plan_spec* __restrict__ specs,
+__global__ __launch_bounds__(64) void k_lpt_small(uint32_t KW, uint32_t R, uint32_t Cmax, uint32_t NW,
+                                                  const cr_plan_spec* __restrict__ specs,
                                                   const uint32_t* __restrict__ order,
                                                   const uint32_t* __restrict__ order_count,
                                                   const uint32_t* __restrict__ num_admitted,
                                                   const uint64_t* __restrict__ cold,
                                                   const uint32_t* __restrict__ member_off,
+                                                  const uint64_t* __restrict__ key_index,
                                                   uint16_t* __restrict__ members, double* __restrict__ load,
                                                   uint32_t* __restrict__ route)
 {
@@ -513,12 +571,13 @@ __global__ __launch_bounds__(64) void k_lpt_small(uint32_t K, uint32_t R, uint32
     const uint32_t* __restrict__ ocnt = order_count + (uint64_t)w * Cmax;
     const uint32_t* __restrict__ moff = member_off + (uint64_t)p * (Cmax + 1u);
     uint16_t* __restrict__ mem = members + (uint64_t)p * Cmax;
-    const uint64_t rbase = (uint64_t)(p / cands) * K;
-    const uint32_t cidx = p % cands;
+    const uint64_t* __restrict__ kx = key_index + (uint64_t)p * 2u * KW;
+    uint32_t* __restrict__ rw = route + (uint64_t)p * Cmax;
     double Lv = lane < R ? (double)cold[p] / (double)R : INFINITY;
     uint32_t rv = lane < R ? lane : 0xFFFFu;
     LptRaw cur = lpt_raw(ord, ocnt, moff, lane, A);
     LptRaw nxt = lpt_raw(ord, ocnt, moff, 64 + lane, A);
+    ulonglong2 kxc = kx_entry(kx, cur.key, lane < A);  // needed when the batch retires
     uint32_t kc = cur.end - cur.off;  // k of the current batch's keys (0 past A)
     double xc = kc == 1 ? (double)cur.cnt : (double)cur.cnt / (double)(kc ? kc : 1u);
     uint32_t fcur = 0, fnxt = 0;  // lane t: least-loaded member chosen for key t of a batch
@@ -527,9 +586,10 @@ __global__ __launch_bounds__(64) void k_lpt_small(uint32_t K, uint32_t R, uint32
         if (t >= 64) {  // retire the current batch, promote the next one
             if (base + lane < A) {
                 if (kc == 1) mem[cur.off] = (uint16_t)fcur;
-                route[(rbase + cur.key) * cands + cidx] = kc == 1 ? (CR_ROUTE_SINGLE | fcur) : (base + lane);
+                rw[kx_rank(kxc, cur.key)] = kc == 1 ? (CR_ROUTE_SINGLE | fcur) : (base + lane);
             }
             cur = nxt;
+            kxc = kx_entry(kx, cur.key, base + 64 + lane < A);
             kc = cur.end - cur.off;
             xc = kc == 1 ? (double)cur.cnt : (double)cur.cnt / (double)(kc ? kc : 1u);
             fcur = fnxt;
@@ -630,12 +690,12 @@ __global__ __launch_bounds__(64) void k_lpt_small(uint32_t K, uint32_t R, uint32
     // retire what is left (the current batch, and the next one if a batch of jobs reached it)
     if (base + lane < A) {
         if (kc == 1) mem[cur.off] = (uint16_t)fcur;
-        route[(rbase + cur.key) * cands + cidx] = kc == 1 ? (CR_ROUTE_SINGLE | fcur) : (base + lane);
+        rw[kx_rank(kxc, cur.key)] = kc == 1 ? (CR_ROUTE_SINGLE | fcur) : (base + lane);
     }
     if (t > 64 && lane < t - 64 && base + 64 + lane < A) {
         const uint32_t kn = nxt.end - nxt.off;
         if (kn == 1) mem[nxt.off] = (uint16_t)fnxt;
-        route[(rbase + nxt.key) * cands + cidx] = kn == 1 ? (CR_ROUTE_SINGLE | fnxt) : (base + 64 + lane);
+        rw[kx_rank(kx_entry(kx, nxt.key, true), nxt.key)] = kn == 1 ? (CR_ROUTE_SINGLE | fnxt) : (base + 64 + lane);
     }
     if (lane < R) load[(uint64_t)p * R + rv] = Lv;
 }
@@ -643,13 +703,14 @@ __global__ __launch_bounds__(64) void k_lpt_small(uint32_t K, uint32_t R, uint32
 // R > 64: lane l holds destinations l, l+64, ... (kS registers); each pick is a register
 // scan plus a cross-lane (L, r) argmin.
 template <int kS>
-__global__ __launch_bounds__(64) void k_lpt(uint32_t K, uint32_t R, uint32_t Cmax, uint32_t NW, uint32_t cands,
+__global__ __launch_bounds__(64) void k_lpt(uint32_t KW, uint32_t R, uint32_t Cmax, uint32_t NW,
                                             const cr_plan_spec* __restrict__ specs,
                                             const uint32_t* __restrict__ order,
                                             const uint32_t* __restrict__ order_count,
                                             const uint32_t* __restrict__ num_admitted,
                                             const uint64_t* __restrict__ cold,
-                                            const uint32_t* __restrict__ member_off, uint16_t* __restrict__ members,
+                                            const uint32_t* __restrict__ member_off,
+                                            const uint64_t* __restrict__ key_index, uint16_t* __restrict__ members,
                                             double* __restrict__ load, uint32_t* __restrict__ route)
 {
     const uint32_t p = blockIdx.x, lane = lane_id();
@@ -660,8 +721,8 @@ __global__ __launch_bounds__(64) void k_lpt(uint32_t K, uint32_t R, uint32_t Cma
     const uint32_t* __restrict__ ocnt = order_count + (uint64_t)w * Cmax;
     const uint32_t* __restrict__ moff = member_off + (uint64_t)p * (Cmax + 1u);
     uint16_t* __restrict__ mem = members + (uint64_t)p * Cmax;
-    const uint64_t rbase = (uint64_t)(p / cands) * K;
-    const uint32_t cidx = p % cands;
+    const uint64_t* __restrict__ kx = key_index + (uint64_t)p * 2u * KW;
+    uint32_t* __restrict__ rw = route + (uint64_t)p * Cmax;
     const double init = (double)cold[p] / (double)R;
     double Lr[kS];
 #pragma unroll
@@ -671,6 +732,7 @@ __global__ __launch_bounds__(64) void k_lpt(uint32_t K, uint32_t R, uint32_t Cma
     for (uint32_t a0 = 0; a0 < A; a0 += 64) {
         const LptBatch cur = nxt;
         nxt = lpt_load(ord, ocnt, moff, a0 + 64 + lane, A);
+        const ulonglong2 kxc = kx_entry(kx, cur.key, a0 + lane < A);  // needed at the end of the batch
         const uint32_t nb = A - a0 < 64u ? A - a0 : 64u;
         const uint32_t k_l = cur.end - cur.off;
         const double x_l = k_l == 1 ? (double)cur.cnt : (double)cur.cnt / (double)k_l;
@@ -709,7 +771,7 @@ __global__ __launch_bounds__(64) void k_lpt(uint32_t K, uint32_t R, uint32_t Cma
         }
         if (lane < nb) {
             if (k_l == 1) mem[cur.off] = (uint16_t)first;
-            route[(rbase + cur.key) * cands + cidx] = k_l == 1 ? (CR_ROUTE_SINGLE | first) : (a0 + lane);
+            rw[kx_rank(kxc, cur.key)] = k_l == 1 ? (CR_ROUTE_SINGLE | first) : (a0 + lane);
         }
     }
 #pragma unroll
@@ -719,6 +781,8 @@ __global__ __launch_bounds__(64) void k_lpt(uint32_t K, uint32_t R, uint32_t Cma
     }
 }
 
+inline uint32_t key_words(uint32_t K) { return (K + 63u) / 64u; }
+
 bool valid_set(const cr_plan_set* ps)
 {
     if (!ps) return false;
@@ -726,7 +790,7 @@ bool valid_set(const cr_plan_set* ps)
     if (ps->R == 0 || ps->R > CR_MAX_R || ps->max_W == 0 || ps->max_W > CR_MAX_W) return false;
     if (ps->num_keys == 0 || ps->num_keys == 0xFFFFFFFFu || ps->num_windows == 0) return false;
     if (!ps->specs || !ps->order || !ps->order_count || !ps->n_order || !ps->num_admitted || !ps->cold || !ps->clamped ||
-        !ps->member_off || !ps->members || !ps->load || !ps->route)
+        !ps->member_off || !ps->members || !ps->load || !ps->key_index || !ps->route)
         return false;
     return true;
 }
@@ -751,10 +815,7 @@ extern "C" cr_status cr_admit(const uint32_t* counts, const cr_plan_set* plans, 
     uint2* buf = reinterpret_cast<uint2*>(base);
     uint64_t* row_sum = reinterpret_cast<uint64_t*>(base + (uint64_t)plans->num_windows * 2u * cmax * sizeof(uint2));
     const hipStream_t st = as_stream(stream);
-    const uint32_t ng = plans->num_plans / plans->cands;
-    const uint64_t route_words = (uint64_t)ng * plans->num_keys * plans->cands;
     (void)hipGetLastError();
-    hipLaunchKernelGGL(k_fill_u32, dim3(1024), dim3(256), 0, st, plans->route, route_words, CR_ROUTE_COLD);
     if ((uint64_t)plans->num_keys * 4u <= kSortLdsRowBytes) {
         const uint32_t lds = plans->num_keys * 4u;
         if (hipFuncSetAttribute((const void*)k_sort_window<true>, hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -767,8 +828,9 @@ extern "C" cr_status cr_admit(const uint32_t* counts, const cr_plan_set* plans, 
                            plans->num_keys, cmax, plans->order, plans->order_count, plans->n_order, row_sum, buf);
     }
     hipLaunchKernelGGL(k_admit_plan, dim3(plans->num_plans), dim3(kSortThreads), 0, st, plans->R, cmax,
-                       plans->num_windows, plans->specs, plans->order_count, plans->n_order, row_sum,
-                       plans->num_admitted, plans->cold, plans->clamped, plans->member_off, err);
+                       plans->num_windows, key_words(plans->num_keys), plans->specs, plans->order, plans->order_count,
+                       plans->n_order, row_sum, plans->num_admitted, plans->cold, plans->clamped, plans->member_off,
+                       plans->key_index, err);
     return hipGetLastError() == hipSuccess ? CR_OK : CR_EHIP;
 }
 
@@ -780,17 +842,17 @@ extern "C" cr_status cr_place_lpt(const uint32_t* counts, const cr_plan_set* pla
     const hipStream_t st = as_stream(stream);
     (void)hipGetLastError();
     if (plans->R <= 64) {
-        hipLaunchKernelGGL(k_lpt_small, dim3(plans->num_plans), dim3(64), 0, st, plans->num_keys, plans->R, cmax,
-                           plans->num_windows, plans->cands, plans->specs, plans->order, plans->order_count,
-                           plans->num_admitted, plans->cold, plans->member_off, plans->members, plans->load,
-                           plans->route);
+        hipLaunchKernelGGL(k_lpt_small, dim3(plans->num_plans), dim3(64), 0, st, key_words(plans->num_keys), plans->R,
+                           cmax, plans->num_windows, plans->specs, plans->order, plans->order_count,
+                           plans->num_admitted, plans->cold, plans->member_off, plans->key_index, plans->members,
+                           plans->load, plans->route);
         return hipGetLastError() == hipSuccess ? CR_OK : CR_EHIP;
     }
 #define CR_LPT(S)                                                                                                   \
-    hipLaunchKernelGGL(k_lpt<S>, dim3(plans->num_plans), dim3(64), 0, st, plans->num_keys, plans->R, cmax,        \
-                       plans->num_windows, plans->cands, plans->specs, plans->order, plans->order_count,           \
-                       plans->num_admitted, plans->cold, plans->member_off, plans->members, plans->load,           \
-                       plans->route)
+    hipLaunchKernelGGL(k_lpt<S>, dim3(plans->num_plans), dim3(64), 0, st, key_words(plans->num_keys), plans->R,   \
+                       cmax, plans->num_windows, plans->specs, plans->order, plans->order_count,                    \
+                       plans->num_admitted, plans->cold, plans->member_off, plans->key_index, plans->members,       \
+                       plans->load, plans->route)
     const uint32_t s = (plans->R + 63) / 64;
     if (s <= 2) CR_LPT(2);
     else if (s <= 4) CR_LPT(4);

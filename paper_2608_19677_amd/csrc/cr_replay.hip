@@ -52,8 +52,8 @@ inline PartGeom part_geom(uint64_t n, uint32_t P)
 {
     const uint64_t target = 8192u / P > 0 ? 8192u / P : 1u;
     uint64_t tile = (n + target - 1) / target;
+    tile = (tile + 1023) & ~1023ull;  // whole sub-tiles of the scatter
     if (tile < 1024) tile = 1024;
-    tile = (tile + 63) & ~63ull;
     return PartGeom{tile, n ? (n + tile - 1) / tile : 0};
 }
 
@@ -146,8 +146,18 @@ __global__ __launch_bounds__(kScanThreads) void k_scan_apply(uint32_t* __restric
     }
 }
 
-// One wavefront per (tile, candidate): stable scatter into packed records. The next 64
-// requests are loaded while the current 64 are ranked and written.
+// One wavefront per (tile, candidate): stable scatter into packed records, kSub requests
+// at a time. Pass one ranks every request among the earlier ones of its destination in
+// the sub-tile (ballots over the destination bits, plus a per-destination counter in
+// LDS); the records are then staged in LDS in destination order and written out so that
+// consecutive lanes store consecutive addresses of one destination's run: whole cache
+// lines instead of a few bytes in each of R streams per instruction.
+constexpr uint32_t kSub = 1024;
+constexpr uint32_t kSubChunks = kSub / 64;
+static_assert(kSub == 1024, "part_geom rounds tiles to 1024 requests");
+
+inline size_t scatter_lds_bytes(uint32_t R) { return (size_t)kSub * 12u + (size_t)R * 12u; }
+
 __global__ __launch_bounds__(64) void k_part_scatter(const uint32_t* __restrict__ keys,
                                                      const uint16_t* __restrict__ suffix,
                                                      const uint16_t* __restrict__ dest, uint64_t n,
@@ -155,51 +165,100 @@ __global__ __launch_bounds__(64) void k_part_scatter(const uint32_t* __restrict_
                                                      uint32_t nbits, uint64_t tile, uint64_t ntiles,
                                                      const uint32_t* __restrict__ tcnt, uint64_t* __restrict__ rec)
 {
-    extern __shared__ uint32_t run[];
+    extern __shared__ uint64_t lds[];
+    uint64_t* srec = lds;                                        // [kSub] staged records
+    uint32_t* spos = reinterpret_cast<uint32_t*>(srec + kSub);  // [kSub] their output positions
+    uint32_t* run = spos + kSub;                                 // [R] next output position
+    uint32_t* lcnt = run + R;                                    // [R] sub-tile count
+    uint32_t* loff = lcnt + R;                                   // [R] sub-tile offset
     const uint32_t c = blockIdx.y, lane = lane_id();
     const uint64_t t = xcd_tile(blockIdx.x, gridDim.x);
     if (t >= ntiles) return;
     const uint64_t t0 = t * tile, t1 = t0 + tile < n ? t0 + tile : n;
-    for (uint32_t d = lane; d < R; d += 64) run[d] = tcnt[((uint64_t)c * R + d) * ntiles + t];
+    for (uint32_t d = lane; d < R; d += 64) {
+        run[d] = tcnt[((uint64_t)c * R + d) * ntiles + t];
+        lcnt[d] = 0;
+    }
     __syncthreads();
     const uint16_t* __restrict__ dc = dest + (uint64_t)c * n;
     uint64_t* __restrict__ rc = rec + (uint64_t)c * n;
+    const uint32_t per = (R + 63u) >> 6;  // destinations per lane in the offset scan
     uint32_t j = find_interval(off, J, t0);
     uint64_t jend = j + 1 < J ? off[j + 1] : ~0ull;  // first request of the next interval
-    uint64_t i = t0 + lane;
-    uint32_t nd = i < t1 ? dc[i] : 0xFFFFu;
-    uint32_t nk = i < t1 ? keys[i] : 0u;
-    uint32_t ns = i < t1 ? suffix[i] : 0u;
-    for (uint64_t base = t0; base < t1; base += 64) {
-        i = base + lane;
-        const uint32_t d = nd, key = nk, sfx = ns;
-        const uint64_t in2 = i + 64;
-        nd = in2 < t1 ? dc[in2] : 0xFFFFu;
-        nk = in2 < t1 ? keys[in2] : 0u;
-        ns = in2 < t1 ? suffix[in2] : 0u;
-        const bool valid = i < t1 && d < R;
-        uint32_t jl = j;
-        if (base + 63 >= jend) {  // an interval boundary falls inside these 64 requests
-            while (jl + 1 < J && off[jl + 1] <= i) ++jl;
+    for (uint64_t sb = t0; sb < t1; sb += kSub) {
+        const uint64_t se = sb + kSub < t1 ? sb + kSub : t1;
+        uint32_t dk[kSubChunks], kv[kSubChunks], mv[kSubChunks];
+#pragma unroll
+        for (uint32_t m = 0; m < kSubChunks; ++m) {
+            const uint64_t i = sb + m * 64u + lane;
+            const bool in = i < se;
+            dk[m] = in ? dc[i] : 0xFFFFu;
+            kv[m] = in ? keys[i] : 0u;
+            mv[m] = in ? suffix[i] : 0u;
         }
-        uint64_t peers = ballot(valid);
-        for (uint32_t bit = 0; bit < nbits; ++bit) {
-            const bool on = (d >> bit) & 1u;
-            const uint64_t bb = ballot(on);
-            peers &= on ? bb : ~bb;
+#pragma unroll
+        for (uint32_t m = 0; m < kSubChunks; ++m) {
+            const uint64_t base = sb + m * 64u;
+            if (base >= se) {  // past the end of the tile: nothing to stage
+                dk[m] = 0xFFFFFFFFu;
+                continue;
+            }
+            const uint64_t i = base + lane;
+            const uint32_t d = dk[m];
+            const bool valid = i < se && d < R;
+            uint32_t jl = j;
+            if (base + 63 >= jend) {  // an interval boundary falls inside these 64 requests
+                while (jl + 1 < J && off[jl + 1] <= i) ++jl;
+                j = rdlane(jl, 63);
+                jend = j + 1 < J ? off[j + 1] : ~0ull;
+            }
+            uint64_t peers = ballot(valid);
+            for (uint32_t bit = 0; bit < nbits; ++bit) {
+                const bool on = (d >> bit) & 1u;
+                const uint64_t bb = ballot(on);
+                peers &= on ? bb : ~bb;
+            }
+            const uint32_t rk = (uint32_t)__popcll(peers & lanemask_lt());
+            const uint32_t lr = valid ? lcnt[d] + rk : 0u;
+            __syncthreads();
+            if (valid && rk == 0) lcnt[d] += (uint32_t)__popcll(peers);
+            __syncthreads();
+            dk[m] = valid ? (d << 16) | lr : 0xFFFFFFFFu;
+            mv[m] |= jl << 16;
         }
-        const uint32_t rk = (uint32_t)__popcll(peers & lanemask_lt());
-        if (valid) {
-            const uint32_t pos = run[d] + rk;
-            rc[pos] = (uint64_t)key | ((uint64_t)sfx << 32) | ((uint64_t)jl << 48);
+        // exclusive offsets of the destinations within the sub-tile
+        uint32_t own = 0;
+        for (uint32_t q = 0; q < per; ++q) {
+            const uint32_t d = lane * per + q;
+            own += d < R ? lcnt[d] : 0u;
+        }
+        uint32_t acc = wave_incl_scan_u32(own) - own;
+        const uint32_t total = rdlane(acc + own, 63);
+        for (uint32_t q = 0; q < per; ++q) {
+            const uint32_t d = lane * per + q;
+            if (d < R) {
+                loff[d] = acc;
+                acc += lcnt[d];
+            }
         }
         __syncthreads();
-        if (valid && rk == 0) run[d] += (uint32_t)__popcll(peers);
-        __syncthreads();
-        if (base + 63 >= jend) {
-            j = rdlane(jl, 63);
-            jend = j + 1 < J ? off[j + 1] : ~0ull;
+#pragma unroll
+        for (uint32_t m = 0; m < kSubChunks; ++m) {
+            if (dk[m] != 0xFFFFFFFFu) {
+                const uint32_t d = dk[m] >> 16, lr = dk[m] & 0xFFFFu;
+                const uint32_t slot = loff[d] + lr;
+                srec[slot] = (uint64_t)kv[m] | ((uint64_t)mv[m] << 32);
+                spos[slot] = run[d] + lr;
+            }
         }
+        __syncthreads();
+        for (uint32_t q = lane; q < total; q += 64) rc[spos[q]] = srec[q];
+        __syncthreads();
+        for (uint32_t d = lane; d < R; d += 64) {
+            run[d] += lcnt[d];
+            lcnt[d] = 0;
+        }
+        __syncthreads();
     }
 }
 
@@ -613,8 +672,8 @@ extern "C" cr_status cr_replay_partition(const uint32_t* keys, const uint16_t* s
     if (g.ntiles) {
         hipLaunchKernelGGL(k_scan_apply, dim3(nblk, P), dim3(kScanThreads), 0, st, w.tcnt, len, g.ntiles, R, nblk,
                            w.bsum, w.grp_off);
-        hipLaunchKernelGGL(k_part_scatter, dim3(xcd_grid((uint32_t)g.ntiles), P), dim3(64), (size_t)R * 4u, st, keys, suffix,
-                           dest, n, off, J, R, nbits, g.tile, g.ntiles, w.tcnt, w.rec);
+        hipLaunchKernelGGL(k_part_scatter, dim3(xcd_grid((uint32_t)g.ntiles), P), dim3(64), scatter_lds_bytes(R), st, keys,
+                           suffix, dest, n, off, J, R, nbits, g.tile, g.ntiles, w.tcnt, w.rec);
     }
     hipLaunchKernelGGL(k_seg_items, dim3(1), dim3(1024), 0, st, w.grp_off, P, R, ra.wa, w.item_off);
     return hipGetLastError() == hipSuccess ? CR_OK : CR_EHIP;

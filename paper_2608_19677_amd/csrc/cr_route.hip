@@ -3,10 +3,11 @@
 // hash, cold keys use power of two choices on the plan's interval-start loads.
 //
 // HBM-bound stream: 4 B key read + 2 B destination written per request and candidate.
-// Each thread owns 4 consecutive requests: one 16-byte key load, 4 independent table
-// gathers per candidate (the route table of a group is key-major, [key][candidate], so a
-// request reads one contiguous row; rows of hot keys and the R loads stay in L2), and
-// one 8-byte store of 4 destinations per candidate.
+// Each thread owns 4 consecutive requests: one 16-byte key load, then per candidate 4
+// independent lookups in the plan's compact table (a 16-byte key-index entry: admitted
+// bits of 64 keys and the key rank of the first; an admitted key reads its route word by
+// rank) and one 8-byte store of 4 destinations. A plan's table is a few KB for tens of
+// thousands of keys, so the lookups stay in cache.
 #include "cr_common.h"
 
 namespace cr {
@@ -15,10 +16,11 @@ namespace {
 constexpr int kRouteThreads = 256;
 constexpr int kPer = 4;
 
-__device__ __forceinline__ uint32_t route_one(uint32_t word, uint32_t h, uint32_t R, const double* __restrict__ L,
-                                              const uint32_t* __restrict__ mo, const uint16_t* __restrict__ mem)
+__device__ __forceinline__ uint32_t route_one(bool admitted, uint32_t word, uint32_t h, uint32_t R,
+                                              const double* __restrict__ L, const uint32_t* __restrict__ mo,
+                                              const uint16_t* __restrict__ mem)
 {
-    if (word == CR_ROUTE_COLD) {
+    if (!admitted) {
         const uint32_t d1 = ((h & 0xFFFFu) * R) >> 16;
         const uint32_t d2 = ((h >> 16) * R) >> 16;
         return L[d2] < L[d1] ? d2 : d1;
@@ -32,9 +34,10 @@ template <bool kVec>
 __global__ __launch_bounds__(kRouteThreads) void k_route(
     const uint32_t* __restrict__ keys, uint64_t n, uint64_t first_index, uint32_t smix,
     const uint64_t* __restrict__ off, const uint32_t* __restrict__ gmap, uint32_t J, uint32_t K, uint32_t R,
-    uint32_t cands, uint32_t NG, const uint32_t* __restrict__ route, const uint32_t* __restrict__ member_off,
-    uint32_t mo_stride, const uint16_t* __restrict__ members, uint32_t mem_stride, const double* __restrict__ load,
-    uint16_t* __restrict__ dest, uint32_t* __restrict__ err)
+    uint32_t cands, uint32_t NG, uint32_t KW, const uint64_t* __restrict__ key_index,
+    const uint32_t* __restrict__ route, const uint32_t* __restrict__ member_off, uint32_t cmax,
+    const uint16_t* __restrict__ members, const double* __restrict__ load, uint16_t* __restrict__ dest,
+    uint32_t* __restrict__ err)
 {
     __shared__ uint32_t s_j0;
     __shared__ uint64_t s_bnd[4];  // starts of the next four intervals (~0 past the last)
@@ -77,14 +80,21 @@ __global__ __launch_bounds__(kRouteThreads) void k_route(
         if (!valid) b[t] = 0xFFFFFFFFu;
     }
     for (uint32_t c = 0; c < cands; ++c) {
-        uint32_t word[kPer], d[kPer];
-#pragma unroll
-        for (int t = 0; t < kPer; ++t)
-            word[t] = b[t] < K ? route[((uint64_t)g[t] * K + b[t]) * cands + c] : CR_ROUTE_COLD;
+        ulonglong2 e[kPer];
+        uint32_t d[kPer];
 #pragma unroll
         for (int t = 0; t < kPer; ++t) {
             const uint64_t p = (uint64_t)g[t] * cands + c;
-            d[t] = route_one(word[t], h[t], R, load + p * R, member_off + p * mo_stride, members + p * mem_stride);
+            e[t] = b[t] < K ? *reinterpret_cast<const ulonglong2*>(key_index + (p * KW + (b[t] >> 6)) * 2u)
+                            : make_ulonglong2(0ull, 0ull);
+        }
+#pragma unroll
+        for (int t = 0; t < kPer; ++t) {
+            const uint64_t p = (uint64_t)g[t] * cands + c;
+            const uint64_t below = e[t].x & ((1ull << (b[t] & 63u)) - 1ull);
+            const bool adm = (e[t].x >> (b[t] & 63u)) & 1ull;
+            const uint32_t word = adm ? route[p * cmax + (uint32_t)e[t].y + (uint32_t)__popcll(below)] : 0u;
+            d[t] = route_one(adm, word, h[t], R, load + p * R, member_off + p * (cmax + 1u), members + p * cmax);
         }
         uint16_t* __restrict__ dc = dest + (uint64_t)c * n + base;
         if (full) {
@@ -110,7 +120,7 @@ extern "C" cr_status cr_route(const uint32_t* keys, uint64_t n, uint64_t first_i
     if (!plans || !off || !gmap || J == 0 || !err) return CR_EINVAL;
     if (plans->cands == 0 || plans->num_plans == 0 || plans->num_plans % plans->cands || plans->R == 0 ||
         plans->R > CR_MAX_R || plans->num_keys == 0 || plans->num_keys == 0xFFFFFFFFu || plans->max_W == 0 ||
-        !plans->route || !plans->member_off || !plans->members || !plans->load)
+        !plans->key_index || !plans->route || !plans->member_off || !plans->members || !plans->load)
         return CR_EINVAL;
     if (n == 0) return CR_OK;
     if (!keys || !dest || ((uintptr_t)keys & 3u) || ((uintptr_t)dest & 1u)) return CR_EINVAL;
@@ -124,8 +134,8 @@ extern "C" cr_status cr_route(const uint32_t* keys, uint64_t n, uint64_t first_i
 #define CR_ROUTE_LAUNCH(V)                                                                                         \
     hipLaunchKernelGGL(k_route<V>, dim3(xcd_grid((uint32_t)blocks)), dim3(kRouteThreads), 0, as_stream(stream), keys, n, \
                        first_index, seed_mix(seed), off, gmap, J, plans->num_keys, plans->R, plans->cands,        \
-                       plans->num_plans / plans->cands, plans->route, plans->member_off, cmax + 1u, plans->members, \
-                       cmax, plans->load, dest, err)
+                       plans->num_plans / plans->cands, (plans->num_keys + 63u) / 64u, plans->key_index, plans->route, \
+                       plans->member_off, cmax, plans->members, plans->load, dest, err)
     if (vec) CR_ROUTE_LAUNCH(true);
     else CR_ROUTE_LAUNCH(false);
 #undef CR_ROUTE_LAUNCH

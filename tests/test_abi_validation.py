@@ -22,7 +22,7 @@ def _set(**kw):
     f = dict(num_plans=2, cands=1, R=30, max_W=16, num_keys=100, num_windows=2)
     f.update(kw)
     ps = B.CrPlanSet(f["num_plans"], f["cands"], f["R"], f["max_W"], f["num_keys"], f["num_windows"],
-                     *([FAKE] * 11))
+                     *([FAKE] * 12))
     return ps
 
 
