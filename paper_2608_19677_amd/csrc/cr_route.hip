@@ -15,21 +15,12 @@ namespace {
 
 constexpr int kRouteThreads = 256;
 constexpr int kPer = 4;
+constexpr uint32_t kBlockReq = kRouteThreads * kPer;
+constexpr int kBnd = 4;  // interval starts cached per block; more boundaries take a slow path
 
-__device__ __forceinline__ uint32_t route_one(bool admitted, uint32_t word, uint32_t h, uint32_t R,
-                                              const double* __restrict__ L, const uint32_t* __restrict__ mo,
-                                              const uint16_t* __restrict__ mem)
-{
-    if (!admitted) {
-        const uint32_t d1 = ((h & 0xFFFFu) * R) >> 16;
-        const uint32_t d2 = ((h >> 16) * R) >> 16;
-        return L[d2] < L[d1] ? d2 : d1;
-    }
-    if (word & CR_ROUTE_SINGLE) return word & 0xFFFFu;
-    const uint32_t o = mo[word], k = mo[word + 1] - o;
-    return mem[o + (((h >> 16) * k) >> 16)];
-}
-
+// Every gather below is unconditional (indices are clamped into range and the results
+// selected afterwards) so the four requests of a thread keep their loads in flight
+// together instead of waiting on each other behind branches.
 template <bool kVec>
 __global__ __launch_bounds__(kRouteThreads) void k_route(
     const uint32_t* __restrict__ keys, uint64_t n, uint64_t first_index, uint32_t smix,
@@ -40,16 +31,27 @@ __global__ __launch_bounds__(kRouteThreads) void k_route(
     uint32_t* __restrict__ err)
 {
     __shared__ uint32_t s_j0;
-    __shared__ uint64_t s_bnd[4];  // starts of the next four intervals (~0 past the last)
-    const uint64_t bstart = (uint64_t)xcd_tile(blockIdx.x, gridDim.x) * kRouteThreads * kPer;
+    __shared__ uint32_t s_rel[kBnd];     // next interval starts relative to the block (clamped)
+    __shared__ uint32_t s_g[kBnd + 1];   // plan groups of intervals j0 .. j0 + kBnd
+    const uint64_t bstart = (uint64_t)xcd_tile(blockIdx.x, gridDim.x) * kBlockReq;
     if (bstart >= n) return;
     if (threadIdx.x < 64) {
         const uint32_t j0 = find_interval(off, J, bstart);
         if (threadIdx.x == 0) s_j0 = j0;
-        if (threadIdx.x < 4) s_bnd[threadIdx.x] = j0 + 1 + threadIdx.x < J ? off[j0 + 1 + threadIdx.x] : ~0ull;
+        if (threadIdx.x < kBnd) {
+            const uint32_t jb = j0 + 1 + threadIdx.x;
+            const uint64_t e = jb < J ? off[jb] : ~0ull;
+            s_rel[threadIdx.x] = e - bstart < kBlockReq ? (uint32_t)(e - bstart) : kBlockReq;
+        }
+        if (threadIdx.x <= kBnd) {
+            const uint32_t jj = j0 + threadIdx.x < J ? j0 + threadIdx.x : J - 1;
+            const uint32_t gg = gmap[jj];
+            s_g[threadIdx.x] = gg < NG ? gg : NG - 1;
+        }
     }
     __syncthreads();
-    const uint64_t base = bstart + (uint64_t)threadIdx.x * kPer;
+    const uint32_t rel0 = threadIdx.x * kPer;
+    const uint64_t base = bstart + rel0;
     if (base >= n) return;
     const bool full = kVec && base + kPer <= n;
     uint32_t b[kPer], g[kPer], h[kPer];
@@ -64,37 +66,71 @@ __global__ __launch_bounds__(kRouteThreads) void k_route(
         for (int t = 0; t < kPer; ++t) b[t] = base + t < n ? keys[base + t] : 0u;
     }
     const uint32_t j0 = s_j0;
-    const uint64_t e0 = s_bnd[0], e1 = s_bnd[1], e2 = s_bnd[2], e3 = s_bnd[3];
+    const uint32_t r0 = s_rel[0], r1 = s_rel[1], r2 = s_rel[2], r3 = s_rel[3];
+    // request hash: the inner mix depends only on the high word of the global index
+    const uint64_t gi0 = first_index + base;
+    const uint32_t inner0 = fmix32((uint32_t)(gi0 >> 32) ^ smix);
     bool bad = false;
 #pragma unroll
     for (int t = 0; t < kPer; ++t) {
-        const uint64_t i = base + t;
-        uint32_t j = j0 + (i >= e0) + (i >= e1) + (i >= e2) + (i >= e3);
-        if (i >= e3)
-            while (j + 1 < J && off[j + 1] <= i) ++j;
-        const uint32_t gg = gmap[j];
-        g[t] = gg < NG ? gg : NG - 1;
-        h[t] = req_hash(smix, first_index + i);
-        const bool valid = i >= n || b[t] < K;
+        const uint32_t rel = rel0 + t;
+        const uint32_t q = (rel >= r0) + (rel >= r1) + (rel >= r2) + (rel >= r3);
+        if (rel >= r3 && r3 < kBlockReq) {  // more than kBnd boundaries in this block
+            uint32_t j = j0 + kBnd;
+            while (j + 1 < J && off[j + 1] <= base + t) ++j;
+            const uint32_t gg = gmap[j];
+            g[t] = gg < NG ? gg : NG - 1;
+        } else {
+            g[t] = s_g[q];
+        }
+        const uint64_t gi = gi0 + t;
+        const uint32_t inner = (uint32_t)(gi >> 32) == (uint32_t)(gi0 >> 32) ? inner0 : fmix32((uint32_t)(gi >> 32) ^ smix);
+        h[t] = fmix32((uint32_t)gi ^ inner);
+        const bool valid = base + t >= n || b[t] < K;
         bad |= !valid;
-        if (!valid) b[t] = 0xFFFFFFFFu;
     }
     for (uint32_t c = 0; c < cands; ++c) {
         ulonglong2 e[kPer];
-        uint32_t d[kPer];
+        double l1[kPer], l2[kPer];
+        uint32_t d1[kPer], d2[kPer], pl[kPer];
 #pragma unroll
         for (int t = 0; t < kPer; ++t) {
-            const uint64_t p = (uint64_t)g[t] * cands + c;
-            e[t] = b[t] < K ? *reinterpret_cast<const ulonglong2*>(key_index + (p * KW + (b[t] >> 6)) * 2u)
-                            : make_ulonglong2(0ull, 0ull);
+            const uint32_t p = g[t] * cands + c;
+            pl[t] = p;
+            const uint32_t bb = b[t] < K ? b[t] : 0u;
+            e[t] = *reinterpret_cast<const ulonglong2*>(key_index + ((uint64_t)p * KW + (bb >> 6)) * 2u);
+            d1[t] = ((h[t] & 0xFFFFu) * R) >> 16;
+            d2[t] = ((h[t] >> 16) * R) >> 16;
+            l1[t] = load[(uint64_t)p * R + d1[t]];
+            l2[t] = load[(uint64_t)p * R + d2[t]];
         }
+        uint32_t word[kPer];
+        bool adm[kPer];
 #pragma unroll
         for (int t = 0; t < kPer; ++t) {
-            const uint64_t p = (uint64_t)g[t] * cands + c;
-            const uint64_t below = e[t].x & ((1ull << (b[t] & 63u)) - 1ull);
-            const bool adm = (e[t].x >> (b[t] & 63u)) & 1ull;
-            const uint32_t word = adm ? route[p * cmax + (uint32_t)e[t].y + (uint32_t)__popcll(below)] : 0u;
-            d[t] = route_one(adm, word, h[t], R, load + p * R, member_off + p * (cmax + 1u), members + p * cmax);
+            const uint32_t sh = b[t] & 63u;
+            adm[t] = b[t] < K && ((e[t].x >> sh) & 1ull);
+            const uint32_t rank = (uint32_t)e[t].y + (uint32_t)__popcll(e[t].x & ((1ull << sh) - 1ull));
+            word[t] = route[(uint64_t)pl[t] * cmax + (adm[t] ? rank : 0u)];
+        }
+        uint32_t d[kPer];
+        bool multi = false;
+#pragma unroll
+        for (int t = 0; t < kPer; ++t) {
+            d[t] = adm[t] ? (word[t] & 0xFFFFu) : (l2[t] < l1[t] ? d2[t] : d1[t]);
+            multi |= adm[t] && !(word[t] & CR_ROUTE_SINGLE);
+        }
+        if (ballot(multi)) {  // some admitted key of this wave has k > 1
+#pragma unroll
+            for (int t = 0; t < kPer; ++t) {
+                const bool m = adm[t] && !(word[t] & CR_ROUTE_SINGLE);
+                const uint32_t a = m ? word[t] : 0u;
+                const uint32_t* __restrict__ mo = member_off + (uint64_t)pl[t] * (cmax + 1u);
+                const uint32_t o = mo[a], k = mo[a + 1] - o;
+                const uint32_t pick = m ? o + (((h[t] >> 16) * k) >> 16) : 0u;
+                const uint32_t dm = members[(uint64_t)pl[t] * cmax + pick];
+                d[t] = m ? dm : d[t];
+            }
         }
         uint16_t* __restrict__ dc = dest + (uint64_t)c * n + base;
         if (full) {
@@ -125,7 +161,7 @@ extern "C" cr_status cr_route(const uint32_t* keys, uint64_t n, uint64_t first_i
     if (n == 0) return CR_OK;
     if (!keys || !dest || ((uintptr_t)keys & 3u) || ((uintptr_t)dest & 1u)) return CR_EINVAL;
     const uint32_t cmax = plans->R * plans->max_W;
-    const uint64_t per_block = (uint64_t)kRouteThreads * kPer;
+    const uint64_t per_block = kBlockReq;
     const uint64_t blocks = (n + per_block - 1) / per_block;
     if (blocks > 0x7FFFFFF0ull) return CR_EINVAL;
     // 16-byte key loads and 8-byte destination stores need aligned rows.
