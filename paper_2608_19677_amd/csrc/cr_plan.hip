@@ -512,17 +512,18 @@ __device__ __forceinline__ uint32_t kx_rank(ulonglong2 e, uint32_t b)
 }
 
 // R <= 64: lane i holds the i-th smallest (L, r), so the least-loaded destinations are
-// lanes 0..k-1. After charging them, each is re-inserted at its rank among the rest:
-// three compares straight to lane masks give the rank, a one-lane DPP shift opens the
-// slot; for k = 1 the pop and the insert fuse into one shift.
-// Runs of equal single-copy jobs are placed several at a time. With v0 = min L + x, every
-// lane below v0 is picked before any charged load can come back into play, so the next
-// m = min(run, #lanes below v0) jobs go to lanes 0..m-1 exactly as m sequential picks
-// would place them. If m = R (a full round) every load gains x in place; otherwise the m
-// charged loads are merged back by counting ranks and one forward lane permutation. A
-// batch is taken only while the charged loads keep their (L, r) order, else the picks
-// proceed one by one. Admitted keys sit in two 64-key batches so a batch of jobs may
-// straddle the boundary; a batch's member and route stores leave when it is retired.
+// lanes 0..k-1.
+// Consecutive single-copy jobs are placed in batches. Job t+q would take lane q exactly as
+// the sequential picks do as long as, for every q, lane q's load is below every charged
+// load L_q' + x_q' of the earlier lanes q' < q (lane q is then the least (L, r) pair when
+// job t+q is placed); an exclusive prefix minimum across the lanes gives the longest such
+// batch M in one pass, ties ending it. The M charged lanes are merged back by rank: one
+// pass over them yields, through ballots, every lane's new position, and one forward lane
+// permutation applies it. A full round (M = R, equal x, order kept) needs no permutation.
+// A batch of one is a single pick: three compares give the insertion rank and a one-lane
+// DPP shift opens the slot; a job with k > 1 pops k lanes and re-inserts each.
+// Admitted keys sit in two 64-key batches so a batch of jobs may straddle the boundary;
+// the member picked for job a is kept in LDS slot a mod 128 until its batch is retired.
 struct LptRaw {
     uint32_t key, cnt, off, end;
 };
@@ -552,6 +553,37 @@ __device__ __forceinline__ double ds_permute_f64(uint32_t dst_lane, double v)
     return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
 }
 
+__device__ __forceinline__ uint32_t ds_bpermute_u32(uint32_t src_lane, uint32_t v)
+{
+    return (uint32_t)__builtin_amdgcn_ds_bpermute((int)(src_lane << 2), (int)v);
+}
+
+// DPP move of a double; lanes whose source is outside the pattern (or whose row is masked
+// off) receive `fill`.
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ double dpp_f64(double v, double fill)
+{
+    const uint64_t u = (uint64_t)__double_as_longlong(v), f = (uint64_t)__double_as_longlong(fill);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp((int)(uint32_t)f, (int)(uint32_t)u, kCtrl, kRowMask, 0xF, false);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp((int)(uint32_t)(f >> 32), (int)(uint32_t)(u >> 32), kCtrl,
+                                                              kRowMask, 0xF, false);
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+// min over lanes 0 .. lane-1 (+inf on lane 0)
+__device__ __forceinline__ double wave_exclusive_min_f64(double v)
+{
+    const double inf = INFINITY;
+    double s = dpp_f64<0x138, 0xF>(v, inf);  // wave_shr:1
+    s = fmin(s, dpp_f64<0x111, 0xF>(s, inf));  // row_shr:1
+    s = fmin(s, dpp_f64<0x112, 0xF>(s, inf));  // row_shr:2
+    s = fmin(s, dpp_f64<0x114, 0xF>(s, inf));  // row_shr:4
+    s = fmin(s, dpp_f64<0x118, 0xF>(s, inf));  // row_shr:8
+    s = fmin(s, dpp_f64<0x142, 0xA>(s, inf));  // row_bcast:15 into rows 1 and 3
+    s = fmin(s, dpp_f64<0x143, 0xC>(s, inf));  // row_bcast:31 into rows 2 and 3
+    return s;
+}
+
 __global__ __launch_bounds__(64) void k_lpt_small(uint32_t KW, uint32_t R, uint32_t Cmax, uint32_t NW,
                                                   const cr_plan_spec* __restrict__ specs,
                                                   const uint32_t* __restrict__ order,
@@ -563,6 +595,7 @@ __global__ __launch_bounds__(64) void k_lpt_small(uint32_t KW, uint32_t R, uint3
                                                   uint16_t* __restrict__ members, double* __restrict__ load,
                                                   uint32_t* __restrict__ route)
 {
+    __shared__ uint32_t s_mem[128];  // member picked for single-copy job a, slot a mod 128
     const uint32_t p = blockIdx.x, lane = lane_id();
     const cr_plan_spec spec = specs[p];
     const uint32_t A = (uint32_t)__builtin_amdgcn_readfirstlane((int)num_admitted[p]);
@@ -578,82 +611,110 @@ __global__ __launch_bounds__(64) void k_lpt_small(uint32_t KW, uint32_t R, uint3
     LptRaw cur = lpt_raw(ord, ocnt, moff, lane, A);
     LptRaw nxt = lpt_raw(ord, ocnt, moff, 64 + lane, A);
     ulonglong2 kxc = kx_entry(kx, cur.key, lane < A);  // needed when the batch retires
-    uint32_t kc = cur.end - cur.off;  // k of the current batch's keys (0 past A)
+    uint32_t kc = cur.end - cur.off;                   // k of the current batch's keys (0 past A)
     double xc = kc == 1 ? (double)cur.cnt : (double)cur.cnt / (double)(kc ? kc : 1u);
-    uint32_t fcur = 0, fnxt = 0;  // lane t: least-loaded member chosen for key t of a batch
+    const uint64_t rmask = R >= 64 ? ~0ull : ((1ull << R) - 1ull);
     uint32_t base = 0, t = 0;
     while (base + t < A) {
         if (t >= 64) {  // retire the current batch, promote the next one
+            const uint32_t fm = s_mem[(base + lane) & 127u];
             if (base + lane < A) {
-                if (kc == 1) mem[cur.off] = (uint16_t)fcur;
-                rw[kx_rank(kxc, cur.key)] = kc == 1 ? (CR_ROUTE_SINGLE | fcur) : (base + lane);
+                if (kc == 1) mem[cur.off] = (uint16_t)fm;
+                rw[kx_rank(kxc, cur.key)] = kc == 1 ? (CR_ROUTE_SINGLE | fm) : (base + lane);
             }
             cur = nxt;
             kxc = kx_entry(kx, cur.key, base + 64 + lane < A);
             kc = cur.end - cur.off;
-            xc = kc == 1 ? (double)cur.cnt : (double)cur.cnt / (double)(kc ? kc : 1u);
-            fcur = fnxt;
-            fnxt = 0;
+            xc = (double)cur.cnt;
+            if (ballot(kc > 1)) xc = kc > 1 ? (double)cur.cnt / (double)kc : xc;
             base += 64;
             t -= 64;
             nxt = lpt_raw(ord, ocnt, moff, base + 64 + lane, A);
             continue;
         }
         const uint32_t k = rdlane(kc, t);
-        const double x = rdlane_f64(xc, t);
         if (k == 1) {
-            // run of equal single-copy jobs from t, across both batches
-            const uint32_t cnt = rdlane(cur.cnt, t);
-            const uint64_t sc = ballot(kc == 1 && cur.cnt == cnt) >> t;
-            uint32_t run = ~sc ? (uint32_t)__builtin_ctzll(~sc) : 64u - t;
-            if (run >= 64u - t) {
-                const uint64_t sn = ballot(nxt.end - nxt.off == 1 && nxt.cnt == cnt && base + 64 + lane < A);
-                run = 64u - t + (~sn ? (uint32_t)__builtin_ctzll(~sn) : 64u);
-            }
-            const double v = Lv + x;
-            const double v0 = rdlane_f64(v, 0);
-            const uint32_t below = (uint32_t)__popcll(ballot(Lv < v0));
-            const uint32_t m = run < below ? run : below;
-            if (m >= 2) {
-                // the charged loads must keep their (L, r) order
-                const double vn = dpp_shl1_f64(v);
-                const uint32_t rn = dpp_shl1(rv, rv);
-                if (ballot(lane + 1 < m && vn == v && rn < rv) == 0) {
-                    const uint32_t gc = (uint32_t)__shfl((int)rv, (int)((lane - t) & 63u), 64);
-                    const uint32_t gn = (uint32_t)__shfl((int)rv, (int)((lane + 64u - t) & 63u), 64);
-                    if (lane >= t && lane - t < m) fcur = gc;
-                    if (lane + 64u - t < m) fnxt = gn;
-                    if (m >= R) {
-                        if (lane < R) Lv = v;
-                    } else {
-                        // Merge: every lane's new place is its index within its own sorted
-                        // set plus the number of lanes of the other set that precede it.
-                        // The loop runs over the smaller set; (L, r) is a strict total order,
-                        // so one compare per lane serves both directions.
-                        const double a = lane < m ? v : Lv;
-                        const bool charged = lane < m;
-                        const bool loop_charged = m <= R - m;
-                        const uint32_t s0 = loop_charged ? 0u : m, s1 = loop_charged ? m : R;
-                        const bool other = lane < R && charged != loop_charged;
-                        uint32_t cnt = 0;
-                        for (uint32_t sl = s0; sl < s1; ++sl) {
-                            const double as = rdlane_f64(a, sl);
-                            const uint32_t rs = rdlane(rv, sl);
-                            const bool s_first = as < a || (as == a && rs < rv);
-                            cnt += (other && s_first) ? 1u : 0u;
-                            const uint32_t before = (uint32_t)__popcll(ballot(other && !s_first));
-                            cnt = wrlane(cnt, before, sl);
-                        }
-                        const uint32_t np = charged ? lane + cnt : (lane < R ? lane - m + cnt : lane);
-                        Lv = ds_permute_f64(np, a);
-                        rv = ds_permute_u32(np, rv);
-                    }
-                    t += m;
-                    continue;
+            // lane q looks at job t+q: its count if it is a single-copy job, else ~0
+            const uint32_t mc = kc == 1 ? cur.cnt : 0xFFFFFFFFu;
+            const uint32_t mn = nxt.end - nxt.off == 1 ? nxt.cnt : 0xFFFFFFFFu;
+            const uint32_t src = (lane + t) & 63u;
+            const uint32_t c1 = ds_bpermute_u32(src, mc), c2 = ds_bpermute_u32(src, mn);
+            const uint32_t cq = lane + t < 64u ? c1 : c2;
+            const bool jq = lane < R && cq != 0xFFFFFFFFu && base + t + lane < A;
+            const double a = Lv + (double)cq;  // lane q's load once charged with job t+q
+            const double pm = wave_exclusive_min_f64(jq ? a : INFINITY);
+            const uint64_t okm = ballot(jq && (lane == 0 || Lv < pm));
+            const uint32_t M = ~okm ? (uint32_t)__builtin_ctzll(~okm) : 64u;
+            if (M >= 2) {
+                if (lane < M) s_mem[(base + t + lane) & 127u] = rv;
+                bool round = false;
+                const uint32_t c0 = rdlane(cq, 0);
+                if (M == R) {
+                    const double an = dpp_shl1_f64(a);
+                    const uint32_t rn = dpp_shl1(rv, rv);
+                    round = ballot(lane < R && cq != c0) == 0 && ballot(lane + 1 < R && an == a && rn < rv) == 0;
                 }
+                if (round) {
+                    if (lane < R) Lv = a;
+                    t += M;
+                    // Further full rounds of the same run: the next R jobs have the same x, so
+                    // the batch test reduces to every load being below min L + x, and the
+                    // order test to the charged loads keeping their (L, r) order.
+                    const uint64_t same_c = ballot(kc == 1 && cur.cnt == c0 && base + lane < A);
+                    const uint64_t same_n = ballot(nxt.end - nxt.off == 1 && nxt.cnt == c0 && base + 64 + lane < A);
+                    const double x0 = (double)c0;
+                    while (t < 64) {
+                        // jobs t .. t+R-1 must all be single-copy jobs of count c0
+                        const uint32_t e = t + R;  // one past the last job of the round (<= 128)
+                        const uint64_t need_c = (e >= 64 ? ~0ull : ((1ull << e) - 1ull)) & ~((1ull << t) - 1ull);
+                        const uint64_t need_n = e > 64 ? (e >= 128 ? ~0ull : ((1ull << (e - 64)) - 1ull)) : 0ull;
+                        if ((same_c & need_c) != need_c || (same_n & need_n) != need_n) break;
+                        const double an = Lv + x0;
+                        const double v0 = rdlane_f64(an, 0);
+                        const double ann = dpp_shl1_f64(an);
+                        const uint32_t rn2 = dpp_shl1(rv, rv);
+                        if (ballot(lane < R && !(Lv < v0)) != 0 || ballot(lane + 1 < R && ann == an && rn2 < rv) != 0)
+                            break;
+                        if (lane < R) {
+                            s_mem[(base + t + lane) & 127u] = rv;
+                            Lv = an;
+                        }
+                        t += R;
+                    }
+                    continue;
+                } else {
+                    const bool charged = lane < M;
+                    const double av = charged ? a : Lv;
+                    uint32_t cnt = 0;
+                    const uint64_t unch = rmask & ~((M >= 64 ? ~0ull : (1ull << M) - 1ull));
+                    // lanes preceding lane q, as a lane mask; uncharged lanes after q count it
+                    auto pass = [&](uint32_t q) {
+                        const double aq = rdlane_f64(av, q);
+                        const uint32_t rq = rdlane(rv, q);
+                        const uint64_t bm = ballot(av < aq) | (ballot(av == aq) & ballot(rv < rq));
+                        cnt += __builtin_amdgcn_inverse_ballot_w64(unch & ~bm) ? 1u : 0u;
+                        return (uint32_t)__popcll(bm & rmask);
+                    };
+                    uint32_t q = 0;
+                    for (; q + 1 < M; q += 2) {
+                        const uint32_t r0 = pass(q), r1 = pass(q + 1);
+                        cnt = wrlane(wrlane(cnt, r0, q), r1, q + 1);
+                    }
+                    if (q < M) {
+                        const uint32_t rl = pass(q);  // before cnt is read: pass() adds to it
+                        cnt = wrlane(cnt, rl, q);
+                    }
+                    const uint32_t np = charged ? cnt : (lane < R ? lane - M + cnt : lane);
+                    Lv = ds_permute_f64(np, av);
+                    rv = ds_permute_u32(np, rv);
+                }
+                t += M;
+                continue;
             }
+            const double x = rdlane_f64(xc, t);
+            const double v0 = rdlane_f64(Lv, 0) + x;
             const uint32_t r0 = rdlane(rv, 0);
-            fcur = wrlane(fcur, r0, t);
+            if (lane == 0) s_mem[(base + t) & 127u] = r0;
             // rank of (v0, r0) among lanes 1..: three compares, each straight to a lane mask
             const uint64_t m_lt = ballot(Lv < v0), m_eq = ballot(Lv == v0), m_r = ballot(rv < r0);
             const uint32_t pos = (uint32_t)__popcll((m_lt | (m_eq & m_r)) & ~1ull);
@@ -663,8 +724,7 @@ __global__ __launch_bounds__(64) void k_lpt_small(uint32_t KW, uint32_t R, uint3
             Lv = lt ? sl : (eq ? v0 : Lv);
             rv = lt ? sr : (eq ? r0 : rv);
         } else {
-            const uint32_t r0 = rdlane(rv, 0);
-            fcur = wrlane(fcur, r0, t);
+            const double x = rdlane_f64(xc, t);
             const uint32_t off = rdlane(cur.off, t);
             if (lane < k) mem[off + lane] = (uint16_t)rv;
             const double vnew = Lv + x;  // meaningful on lanes < k
@@ -688,14 +748,20 @@ __global__ __launch_bounds__(64) void k_lpt_small(uint32_t KW, uint32_t R, uint3
         ++t;
     }
     // retire what is left (the current batch, and the next one if a batch of jobs reached it)
-    if (base + lane < A) {
-        if (kc == 1) mem[cur.off] = (uint16_t)fcur;
-        rw[kx_rank(kxc, cur.key)] = kc == 1 ? (CR_ROUTE_SINGLE | fcur) : (base + lane);
+    {
+        const uint32_t fm = s_mem[(base + lane) & 127u];
+        if (base + lane < A) {
+            if (kc == 1) mem[cur.off] = (uint16_t)fm;
+            rw[kx_rank(kxc, cur.key)] = kc == 1 ? (CR_ROUTE_SINGLE | fm) : (base + lane);
+        }
     }
-    if (t > 64 && lane < t - 64 && base + 64 + lane < A) {
-        const uint32_t kn = nxt.end - nxt.off;
-        if (kn == 1) mem[nxt.off] = (uint16_t)fnxt;
-        rw[kx_rank(kx_entry(kx, nxt.key, true), nxt.key)] = kn == 1 ? (CR_ROUTE_SINGLE | fnxt) : (base + 64 + lane);
+    if (t > 64) {
+        const uint32_t fm = s_mem[(base + 64 + lane) & 127u];
+        if (lane < t - 64 && base + 64 + lane < A) {
+            const uint32_t kn = nxt.end - nxt.off;
+            if (kn == 1) mem[nxt.off] = (uint16_t)fm;
+            rw[kx_rank(kx_entry(kx, nxt.key, true), nxt.key)] = kn == 1 ? (CR_ROUTE_SINGLE | fm) : (base + 64 + lane);
+        }
     }
     if (lane < R) load[(uint64_t)p * R + rv] = Lv;
 }
