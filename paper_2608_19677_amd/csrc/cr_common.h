@@ -156,6 +156,13 @@ __device__ __forceinline__ uint32_t xcd_tile(uint32_t b, uint32_t grid)
     return (b % kXcds) * (grid / kXcds) + b / kXcds;
 }
 
+// Buffer resource over [p, p + bytes) for raw buffer loads: reads outside the range return
+// 0 instead of touching memory (gfx9 buffer addressing; word 3 = 0x00020000 on this family).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), 0, (int)bytes, 0x00020000);
+}
+
 inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
 
 inline int device_max_lds()

@@ -334,6 +334,269 @@ __global__ __launch_bounds__(kSortBlock) void k_sort_window(const uint32_t* __re
     }
 }
 
+// Register-resident variant for rows of up to 1024 * kNpl keys and C_max <= kRegCmax:
+// wavefront wv keeps its contiguous slice of the row in registers (kNpl values per lane,
+// all loads in flight together), so the row is read from memory once and no LDS row copy
+// limits the blocks per CU; the kept entries and both radix buffers live in LDS. Counts
+// 1..3, the bulk of a long-tailed row, are histogrammed by ballots instead of contended
+// LDS atomics. Same three steps and results as k_sort_window.
+constexpr uint32_t kRegCmax = 2048;
+
+template <int kNpl>
+__global__ __launch_bounds__(kSortBlock) void k_sort_window_reg(const uint32_t* __restrict__ counts, uint32_t K,
+                                                                uint32_t Cmax, uint32_t* __restrict__ order,
+                                                                uint32_t* __restrict__ order_count,
+                                                                uint32_t* __restrict__ n_order,
+                                                                uint64_t* __restrict__ row_sum)
+{
+    __shared__ uint2 s_buf[2][kRegCmax];
+    __shared__ uint32_t s_hist[kSortNW][256];
+    __shared__ uint32_t s_h256[256];
+    __shared__ uint32_t s_w[kSortNW][2];
+    __shared__ uint32_t s_nnz, s_max, s_t, s_take;
+    __shared__ unsigned long long s_sum;
+    const uint32_t w = blockIdx.x, tid = threadIdx.x, lane = lane_id(), wv = wave_in_block();
+    const uint32_t* __restrict__ grow = counts + (uint64_t)w * K;
+    const uint32_t span = (((K + kSortNW - 1) / kSortNW) + 63u) & ~63u;  // <= 64 * kNpl
+    const uint32_t lo = wv * span < K ? wv * span : K, hi = lo + span < K ? lo + span : K;
+    uint32_t v[kNpl];
+    {  // the slice through a buffer resource: entries at or past hi read as 0
+        const __amdgpu_buffer_rsrc_t rs = make_rsrc(grow + lo, (hi - lo) * 4u);
+#pragma unroll
+        for (int i = 0; i < kNpl; ++i) v[i] = __builtin_amdgcn_raw_buffer_load_b32(rs, (64u * i + lane) * 4u, 0, 0);
+    }
+    for (uint32_t d = tid; d < 256; d += kSortBlock) s_h256[d] = 0;
+    if (tid == 0) {
+        s_nnz = 0;
+        s_max = 0;
+        s_sum = 0;
+    }
+    __syncthreads();
+    // 1. statistics and the clamped histogram
+    {
+        uint32_t nnz = 0, mx = 0, n1 = 0, n2 = 0, n3 = 0;  // per lane
+        uint64_t sum = 0;
+#pragma unroll
+        for (int i = 0; i < kNpl; ++i) {
+            const uint32_t c = v[i];
+            nnz += c != 0u;
+            n1 += c == 1u;
+            n2 += c == 2u;
+            n3 += c == 3u;
+            mx = c > mx ? c : mx;
+            sum += c;
+            if (c >= 4u) atomicAdd(&s_h256[c < 255u ? c : 255u], 1u);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        nnz = wave_sum_u32(nnz);
+        n1 = wave_sum_u32(n1);
+        n2 = wave_sum_u32(n2);
+        n3 = wave_sum_u32(n3);
+        mx = wave_max_u32(mx);
+        sum = wave_sum_u64(sum);
+        if (lane == 0) {
+            atomicAdd(&s_nnz, nnz);
+            atomicMax(&s_max, mx);
+            atomicAdd(&s_sum, (unsigned long long)sum);
+            if (n1) atomicAdd(&s_h256[1], n1);
+            if (n2) atomicAdd(&s_h256[2], n2);
+            if (n3) atomicAdd(&s_h256[3], n3);
+        }
+    }
+    __syncthreads();
+    const uint32_t nnz = s_nnz, mx = s_max;
+    const uint32_t M = nnz < Cmax ? nnz : Cmax;
+    if (tid == 0) {
+        n_order[w] = M;
+        row_sum[w] = s_sum;
+    }
+    if (M == 0) return;
+    if (wv == 0) {  // threshold from the clamped histogram, four bins per lane from 255 down
+        uint32_t h[4], hs = 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            h[q] = s_h256[255u - 4u * lane - q];
+            hs += h[q];
+        }
+        uint32_t tot;
+        uint32_t above = wave_exscan_u32(hs, &tot);
+        uint32_t sel = 0, need = 0;
+        bool found = false;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            if (!found && above < M && above + h[q] >= M) {
+                sel = 255u - 4u * lane - q;
+                need = M - above;
+                found = true;
+            }
+            above += h[q];
+        }
+        const uint32_t fl = first_lane(ballot(found));
+        if (lane == 0) {
+            s_t = rdlane(sel, fl);
+            s_take = rdlane(need, fl);
+        }
+    }
+    __syncthreads();
+    if (s_t == 255u) {  // the threshold is at least 255: MSB radix select over the registers
+        uint32_t prefix = 0, pmask = 0, need = M;
+        for (int shift = 24; shift >= 0; shift -= 8) {
+            if ((mx >> shift) == 0) {
+                pmask |= 0xFFu << shift;
+                continue;
+            }
+            __syncthreads();
+            for (uint32_t d = tid; d < 256; d += kSortBlock) s_h256[d] = 0;
+            __syncthreads();
+#pragma unroll
+            for (int i = 0; i < kNpl; ++i) {
+                const uint32_t c = v[i];
+                if (c != 0 && (c & pmask) == prefix) atomicAdd(&s_h256[(c >> shift) & 255u], 1u);
+            }
+            __syncthreads();
+            if (wv == 0) {
+                uint32_t h[4], hs = 0;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    h[q] = s_h256[255u - 4u * lane - q];
+                    hs += h[q];
+                }
+                uint32_t tot;
+                uint32_t above = wave_exscan_u32(hs, &tot);
+                uint32_t sel = 0, nn = 0;
+                bool found = false;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    if (!found && above < need && above + h[q] >= need) {
+                        sel = 255u - 4u * lane - q;
+                        nn = need - above;
+                        found = true;
+                    }
+                    above += h[q];
+                }
+                const uint32_t fl = first_lane(ballot(found));
+                if (lane == 0) {
+                    s_t = rdlane(sel, fl);
+                    s_take = rdlane(nn, fl);
+                }
+            }
+            __syncthreads();
+            prefix |= s_t << shift;
+            pmask |= 0xFFu << shift;
+            need = s_take;
+        }
+        __syncthreads();
+        if (tid == 0) {
+            s_t = prefix;
+            s_take = need;
+        }
+        __syncthreads();
+    }
+    const uint32_t t = s_t, take_eq = s_take;
+
+    // 2. ordered compaction from the registers (entry lo + 64 i + lane is in key order)
+    {
+        uint32_t gt = 0, eq = 0;  // per lane
+#pragma unroll
+        for (int i = 0; i < kNpl; ++i) {
+            gt += v[i] > t;
+            eq += v[i] == t;
+        }
+        gt = wave_sum_u32(gt);
+        eq = wave_sum_u32(eq);
+        if (lane == 0) {
+            s_w[wv][0] = gt;
+            s_w[wv][1] = eq;
+        }
+    }
+    __syncthreads();
+    {
+        uint32_t eq_before = 0, sel_before = 0;
+        for (uint32_t q = 0; q < wv; ++q) {
+            const uint32_t eqq = s_w[q][1];
+            const uint32_t left = take_eq > eq_before ? take_eq - eq_before : 0u;
+            sel_before += s_w[q][0] + (eqq < left ? eqq : left);
+            eq_before += eqq;
+        }
+        uint32_t running = sel_before, eq_seen = eq_before;
+        const uint64_t lt = lanemask_lt();
+#pragma unroll
+        for (int i = 0; i < kNpl; ++i) {
+            const uint32_t c = v[i];
+            const uint64_t meq = ballot(c == t);
+            const uint32_t eq_rank = (uint32_t)__popcll(meq & lt);
+            const bool sel = c > t || (c == t && eq_seen + eq_rank < take_eq);
+            const uint64_t ms = ballot(sel);
+            const uint32_t pos = running + (uint32_t)__popcll(ms & lt);
+            if (sel && pos < M) s_buf[0][pos] = make_uint2(c, lo + 64u * i + lane);
+            running += (uint32_t)__popcll(ms);
+            eq_seen += (uint32_t)__popcll(meq);
+            __builtin_amdgcn_sched_barrier(0);  // one element's masks live at a time
+        }
+    }
+    __syncthreads();
+
+    // 3. stable LSD radix sort by v = mx - count in LDS
+    const uint32_t range = mx - t;
+    const uint32_t bits = range ? 32u - (uint32_t)__clz(range) : 0u;
+    const uint32_t passes = (bits + 7u) / 8u;
+    const uint32_t espan = (((M + kSortNW - 1) / kSortNW) + 63u) & ~63u;
+    const uint32_t elo = wv * espan < M ? wv * espan : M, ehi = elo + espan < M ? elo + espan : M;
+    uint32_t sb = 0;
+    for (uint32_t pass = 0; pass < passes; ++pass) {
+        const uint2* src = s_buf[sb];
+        uint2* dst = s_buf[sb ^ 1u];
+        const uint32_t shift = 8u * pass;
+        for (uint32_t d = lane; d < 256; d += 64) s_hist[wv][d] = 0;
+        for (uint32_t e = elo + lane; e < ehi; e += 64) atomicAdd(&s_hist[wv][((mx - src[e].x) >> shift) & 255u], 1u);
+        __syncthreads();
+        {  // offsets in (digit, wavefront) order: thread tid owns digit tid / 4, waves 4 (tid % 4) ..
+            const uint32_t d = tid >> 2, x0 = (tid & 3u) * 4u;
+            uint32_t hv[4], hs = 0;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                hv[q] = s_hist[x0 + q][d];
+                hs += hv[q];
+            }
+            __shared__ uint32_t s_scan[16];
+            uint32_t tot;
+            uint32_t ex = block_exscan_u32(hs, s_scan, &tot);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                s_hist[x0 + q][d] = ex;
+                ex += hv[q];
+            }
+        }
+        __syncthreads();
+        for (uint32_t e0 = elo; e0 < ehi; e0 += 64) {
+            const uint32_t e = e0 + lane;
+            const bool valid = e < ehi;
+            const uint2 kv = valid ? src[e] : make_uint2(0u, 0u);
+            const uint32_t d = valid ? ((mx - kv.x) >> shift) & 255u : 0u;
+            uint64_t peers = ballot(valid);
+#pragma unroll
+            for (int bit = 0; bit < 8; ++bit) {
+                const bool on = (d >> bit) & 1u;
+                const uint64_t bb = ballot(on);
+                peers &= on ? bb : ~bb;
+            }
+            const uint32_t rk = (uint32_t)__popcll(peers & lanemask_lt());
+            const uint32_t at = valid ? s_hist[wv][d] + rk : 0u;
+            if (valid && at < M) dst[at] = kv;
+            if (valid && rk == 0) atomicAdd(&s_hist[wv][d], (uint32_t)__popcll(peers));
+        }
+        __syncthreads();
+        sb ^= 1u;
+    }
+    uint32_t* __restrict__ ord = order + (uint64_t)w * Cmax;
+    uint32_t* __restrict__ ocnt = order_count + (uint64_t)w * Cmax;
+    for (uint32_t e = tid; e < M; e += kSortBlock) {
+        const uint2 kv = s_buf[sb][e];
+        ord[e] = kv.y;
+        ocnt[e] = kv.x;
+    }
+}
+
 // Key index of a plan: bit b % 64 of word b / 64 is set for every admitted key b, and
 // each word carries the key rank of its first admitted key (an exclusive scan of the
 // word popcounts). Built in LDS when the words fit, else with global atomics.
@@ -882,7 +1145,18 @@ extern "C" cr_status cr_admit(const uint32_t* counts, const cr_plan_set* plans, 
     uint64_t* row_sum = reinterpret_cast<uint64_t*>(base + (uint64_t)plans->num_windows * 2u * cmax * sizeof(uint2));
     const hipStream_t st = as_stream(stream);
     (void)hipGetLastError();
-    if ((uint64_t)plans->num_keys * 4u <= kSortLdsRowBytes) {
+    const uint32_t K = plans->num_keys;
+    if (cmax <= kRegCmax && K <= 1024u * 32u) {
+#define CR_SORT_REG(NPL)                                                                                            \
+    hipLaunchKernelGGL(k_sort_window_reg<NPL>, dim3(plans->num_windows), dim3(kSortBlock), 0, st, counts, K, cmax,  \
+                       plans->order, plans->order_count, plans->n_order, row_sum)
+        if (K <= 1024u * 4u) CR_SORT_REG(4);
+        else if (K <= 1024u * 8u) CR_SORT_REG(8);
+        else if (K <= 1024u * 16u) CR_SORT_REG(16);
+        else if (K <= 1024u * 20u) CR_SORT_REG(20);
+        else CR_SORT_REG(32);
+#undef CR_SORT_REG
+    } else if ((uint64_t)plans->num_keys * 4u <= kSortLdsRowBytes) {
         const uint32_t lds = plans->num_keys * 4u;
         if (hipFuncSetAttribute((const void*)k_sort_window<true>, hipFuncAttributeMaxDynamicSharedMemorySize,
                                 (int)lds) != hipSuccess)
