@@ -20,6 +20,10 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "llama70b_hbm_traffic.md")
+KERNEL_SOURCE = {"k_count": "cr_count.hip", "k_sort": "cr_plan.hip", "k_admit": "cr_plan.hip", "k_lpt": "cr_plan.hip",
+                 "k_route": "cr_route.hip", "k_part": "cr_replay.hip", "k_scan": "cr_replay.hip",
+                 "k_seg": "cr_replay.hip", "k_replay": "cr_replay.hip"}
 # 32-bit integer VALU: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz = 39,322 G lane-ops/s.
 ALU_PEAK_GOPS = 256 * 4 * 16 * 2.4
 
@@ -36,6 +40,29 @@ def parse():
                     help="after timing, copy this many MiB device-to-device once (a plain copy kernel of known "
                          "size, to scale the FETCH_SIZE / WRITE_SIZE counters)")
     return ap.parse_args()
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch of `kernel` from the committed FETCH_SIZE / WRITE_SIZE summary
+    (70B-like workload only), or None when the kernel's sources changed since then."""
+    import hashlib
+    if workload != "llama70b" or not os.path.exists(TRAFFIC_PROFILE):
+        return None
+    rec = None
+    with open(TRAFFIC_PROFILE) as f:
+        for line in f:
+            if line.startswith("traffic-json: "):
+                rec = json.loads(line[len("traffic-json: "):])
+    if rec is None or kernel not in rec["bytes_per_launch"]:
+        return None
+    src = next((v for k, v in KERNEL_SOURCE.items() if kernel.startswith(k)), None)
+    if src is None:
+        return None
+    for rel in ("paper_2608_19677_amd/csrc/" + src, "paper_2608_19677_amd/csrc/cr_common.h"):
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            if hashlib.sha256(f.read()).hexdigest() != rec["sources_sha256"].get(rel):
+                return None
+    return rec["bytes_per_launch"][kernel]
 
 
 def describe(name, wl):
@@ -103,12 +130,15 @@ def main():
     # Algorithmic work per launch of the single-kernel calls (the zero fills of stats are
     # outside the events; count, place, route and lru each launch exactly one kernel here).
     kern = {
-        "count": dict(kernel="k_count_owner", bound="hbm", unit="GB/s", work=4.0 * n, peak=HBM_PEAK_GBS),
-        "route": dict(kernel="k_route", bound="hbm", unit="GB/s", work=(4.0 + 2.0 * P) * n, peak=HBM_PEAK_GBS),
+        # counting reads every key and writes the dense [J][K] counts matrix it defines
+        "count": dict(kernel="k_count_owner", bound="hbm", unit="GB/s", work=4.0 * n + 4.0 * wl.J * wl.num_keys,
+                      peak=HBM_PEAK_GBS),
+        "route": dict(kernel="k_route<true>", bound="hbm", unit="GB/s", work=(4.0 + 2.0 * P) * n, peak=HBM_PEAK_GBS),
         # LPT: every job copy is compared against the R destination loads.
         "place": dict(kernel="k_lpt_small", bound="alu", unit="Glane-op/s", work=float(n_adm) * R,
                       peak=ALU_PEAK_GOPS),
-        # LRU: every request compares its key with the W slots and ages the W recency ranks.
+        # LRU: every request compares its key with the W slots and moves up to W of them one
+        # place (a move-to-front list: one compare and one shift per slot).
         "lru": dict(kernel="k_replay<%d>" % max({1 if c.W <= 64 else 2 if c.W <= 128 else 4 if c.W <= 256 else 8
                                                  for c in wl.candidates}), bound="alu", unit="Glane-op/s",
                     work=float(sum(2.0 * c.W for c in wl.candidates)) * n, peak=ALU_PEAK_GOPS),
@@ -136,7 +166,8 @@ def main():
         "data": "synthetic",
         "config": describe(args.workload, wl),
         "roofline": {"bound": d["bound"], "achieved": d["achieved"], "peak": d["peak"], "unit": d["unit"],
-                     "frac": d["frac"], "traffic": None, "kernel": d["kernel"]},
+                     "frac": d["frac"], "traffic": measured_traffic(d["kernel"], args.workload),
+                     "kernel": d["kernel"]},
         "us_per_plan_build": (stage_ms["admit"] + stage_ms["place"]) * 1e3 / n_plans,
         "stage_ms": stage_ms,
         "kernels": {k: {kk: vv for kk, vv in v.items() if kk != "work"} for k, v in kern.items()},
