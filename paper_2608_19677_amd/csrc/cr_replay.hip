@@ -363,11 +363,24 @@ __device__ __forceinline__ bool lru_step(uint32_t (&skey)[SL], uint32_t (&srank)
     return hit;
 }
 
-// First set bit of a wave mask, 0xFFFFFFFF when none (s_ff1_i32_b64).
-__device__ __forceinline__ uint32_t sff1(uint64_t m)
+// Move-to-front update after a lookup whose hit mask is m: p = first set bit of m
+// (0xFFFFFFFF when none); lanes 1..p (every lane on a miss) take their left neighbour's
+// key and deeper lanes keep theirs, by one v_cndmask with a wave_shr:1 DPP source under
+// VCC = ~1 << p. Lane 0 is left undefined for the caller to overwrite with the key. The
+// scalar steps sit in the same block as the select so that no wait states are inserted
+// between them; the DPP read of sk comes at least three instructions after sk's last
+// VALU write (the compare that produced m, s_ff1 and s_lshl), which covers the two wait
+// states such a read needs.
+__device__ __forceinline__ uint32_t mtf_core(uint32_t& sk, uint64_t m)
 {
-    uint32_t p;
-    asm("s_ff1_i32_b64 %0, %1" : "=s"(p) : "s"(m));
+    uint32_t p, out;
+    asm("s_ff1_i32_b64 %1, %3\n\t"
+        "s_lshl_b64 vcc, -2, %1\n\t"
+        "v_cndmask_b32_dpp %0, %2, %2, vcc wave_shr:1 row_mask:0xf bank_mask:0xf"
+        : "=v"(out), "=&s"(p)
+        : "v"(sk), "s"(m)
+        : "vcc");
+    sk = out;
     return p;
 }
 
@@ -376,12 +389,34 @@ __device__ __forceinline__ uint32_t sff1(uint64_t m)
 // over every lane, which drops the least recent key of a full list.
 __device__ __forceinline__ uint32_t mtf_step(uint32_t& sk, uint32_t kk, uint64_t wmask)
 {
-    const uint32_t p = sff1(ballot(sk == kk) & wmask);
-    const uint64_t keep = ~1ull << (p & 63u);  // lanes deeper than the hit keep their key
-    const uint32_t up = (uint32_t)__builtin_amdgcn_mov_dpp((int)sk, 0x138, 0xF, 0xF, true);  // wave_shr:1
-    sk = __builtin_amdgcn_inverse_ballot_w64(keep) ? sk : up;
+    const uint32_t p = mtf_core(sk, ballot(sk == kk) & wmask);
     sk = wrlane(sk, kk, 0u);
     return p;
+}
+
+// 64 records (lane t of kl = key of record t, all valid) through the move-to-front list;
+// returns lane t = hit depth of record t. Keys are read 16 at a time ahead of their use.
+template <bool kMasked>
+__device__ __forceinline__ uint32_t mtf_batch(uint32_t& sk, uint32_t kl, uint64_t wmask)
+{
+    uint32_t depth = 0xFFFFFFFFu;
+#pragma unroll
+    for (uint32_t g = 0; g < 4; ++g) {
+        uint32_t key[16];
+#pragma unroll
+        for (uint32_t t = 0; t < 16; ++t) key[t] = rdlane(kl, 16u * g + t);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (uint32_t t = 0; t < 16; ++t) {
+            uint64_t m = ballot(sk == key[t]);
+            if (kMasked) m &= wmask;
+            const uint32_t p = mtf_core(sk, m);
+            sk = wrlane(sk, key[t], 0u);
+            depth = wrlane(depth, p, 16u * g + t);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    return depth;
 }
 
 __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v)
@@ -509,8 +544,7 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
         if constexpr (SL == 1) {
             uint32_t depth = 0xFFFFFFFFu;  // lane t: hit depth of record t
             if (ballot(vl) == ~0ull) {
-#pragma unroll
-                for (uint32_t t = 0; t < 64; ++t) depth = wrlane(depth, mtf_step(skey[0], rdlane(kl, t), wmask), t);
+                depth = W == 64u ? mtf_batch<false>(skey[0], kl, wmask) : mtf_batch<true>(skey[0], kl, wmask);
             } else {
                 for (uint32_t t = 0; t < nb; ++t) {
                     const uint32_t kk = rdlane(kl, t);
