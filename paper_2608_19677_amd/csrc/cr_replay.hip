@@ -3,11 +3,11 @@
 // equal-slot model: W whole-prefix slots per destination).
 //
 // Pipeline (all on the caller's stream, workspace from the caller):
-//   k_part_hist / k_scan_* / k_part_scatter
+//   k_part_hist / k_scan_dest / k_seg_items / k_part_scatter
 //        stable partition of every candidate's requests by destination, preserving
 //        arrival order; each record packs (key, suffix, interval) into 8 bytes;
-//   k_seg_items
-//        splits every (candidate, destination) stream into segments of S records;
+//        k_seg_items also splits every (candidate, destination) stream into segments of
+//        S records;
 //   k_replay<SL>
 //        one wavefront per segment. The LRU state before a segment is exactly the most
 //        recent W distinct keys seen at that destination (carried state appended), so a
@@ -79,71 +79,36 @@ __global__ __launch_bounds__(256) void k_part_hist(const uint16_t* __restrict__ 
     if (bad) atomicOr(err, CR_ERR_DEST_RANGE);
 }
 
-// Exclusive scan of tcnt[c][d][tile] in (d, tile) order, per candidate, in three phases
-// over chunks of kScanChunk entries: chunk sums, a scan of the chunk sums, and a rescan of
-// every chunk from its offset. The first tile of each destination gives its group offset.
+// One block per (destination, candidate): exclusive scan of that destination's per-tile
+// counts, which are contiguous in tcnt[c][d][tile], in place; the destination's total goes
+// to dtot[c][d]. Destination bases within a candidate are added later (k_seg_items).
 constexpr uint32_t kScanThreads = 1024;
-constexpr uint32_t kScanChunk = 4 * kScanThreads;
 
-__global__ __launch_bounds__(kScanThreads) void k_scan_reduce(const uint32_t* __restrict__ tcnt, uint64_t len,
-                                                              uint32_t nblk, uint32_t* __restrict__ bsum)
+__global__ __launch_bounds__(kScanThreads) void k_scan_dest(uint32_t* __restrict__ tcnt, uint64_t ntiles, uint32_t R,
+                                                            uint32_t* __restrict__ dtot)
 {
     __shared__ uint32_t s_scan[16];
-    const uint32_t c = blockIdx.y, blk = blockIdx.x;
-    const uint32_t* __restrict__ t = tcnt + (uint64_t)c * len;
-    const uint64_t e = (uint64_t)blk * kScanChunk + 4u * threadIdx.x;
-    uint32_t s = 0;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) s += e + q < len ? t[e + q] : 0u;
-    uint32_t tot;
-    (void)block_exscan_u32(s, s_scan, &tot);
-    if (threadIdx.x == 0) bsum[(uint64_t)c * nblk + blk] = tot;
-}
-
-__global__ __launch_bounds__(kScanThreads) void k_scan_mid(uint32_t* __restrict__ bsum, uint32_t nblk, uint32_t R,
-                                                           uint32_t* __restrict__ grp_off)
-{
-    __shared__ uint32_t s_scan[16];
-    const uint32_t c = blockIdx.x;
-    uint32_t* __restrict__ b = bsum + (uint64_t)c * nblk;
+    const uint32_t d = blockIdx.x, c = blockIdx.y;
+    uint32_t* __restrict__ t = tcnt + ((uint64_t)c * R + d) * ntiles;
     uint32_t carry = 0;
-    for (uint32_t e0 = 0; e0 < nblk; e0 += kScanThreads) {
-        const uint32_t e = e0 + threadIdx.x;
-        const uint32_t v = e < nblk ? b[e] : 0u;
+    for (uint64_t e0 = 0; e0 < ntiles; e0 += 4u * kScanThreads) {
+        const uint64_t e = e0 + 4u * threadIdx.x;
+        uint32_t v[4], sum = 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            v[q] = e + q < ntiles ? t[e + q] : 0u;
+            sum += v[q];
+        }
         uint32_t tot;
-        const uint32_t ex = block_exscan_u32(v, s_scan, &tot);
-        if (e < nblk) b[e] = carry + ex;
+        uint32_t ex = block_exscan_u32(sum, s_scan, &tot) + carry;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            if (e + q < ntiles) t[e + q] = ex;
+            ex += v[q];
+        }
         carry += tot;
     }
-    if (threadIdx.x == 0) grp_off[(uint64_t)c * (R + 1u) + R] = carry;
-}
-
-__global__ __launch_bounds__(kScanThreads) void k_scan_apply(uint32_t* __restrict__ tcnt, uint64_t len,
-                                                             uint64_t ntiles, uint32_t R, uint32_t nblk,
-                                                             const uint32_t* __restrict__ bsum,
-                                                             uint32_t* __restrict__ grp_off)
-{
-    __shared__ uint32_t s_scan[16];
-    const uint32_t c = blockIdx.y, blk = blockIdx.x;
-    uint32_t* __restrict__ t = tcnt + (uint64_t)c * len;
-    const uint64_t e = (uint64_t)blk * kScanChunk + 4u * threadIdx.x;
-    uint32_t v[4], s = 0;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        v[q] = e + q < len ? t[e + q] : 0u;
-        s += v[q];
-    }
-    uint32_t tot;
-    uint32_t ex = block_exscan_u32(s, s_scan, &tot) + bsum[(uint64_t)c * nblk + blk];
-    uint32_t* __restrict__ go = grp_off + (uint64_t)c * (R + 1u);
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        if (e + q < len) {
-            t[e + q] = ex;
-            if ((e + q) % ntiles == 0) go[(e + q) / ntiles] = ex;
-        }
-        ex += v[q];
-    }
+    if (threadIdx.x == 0) dtot[(uint64_t)c * R + d] = carry;
 }
 
 // One wavefront per (tile, candidate): stable scatter into packed records, kSub requests
@@ -163,7 +128,8 @@ __global__ __launch_bounds__(64) void k_part_scatter(const uint32_t* __restrict_
                                                      const uint16_t* __restrict__ dest, uint64_t n,
                                                      const uint64_t* __restrict__ off, uint32_t J, uint32_t R,
                                                      uint32_t nbits, uint64_t tile, uint64_t ntiles,
-                                                     const uint32_t* __restrict__ tcnt, uint64_t* __restrict__ rec)
+                                                     const uint32_t* __restrict__ tcnt,
+                                                     const uint32_t* __restrict__ grp_off, uint64_t* __restrict__ rec)
 {
     extern __shared__ uint64_t lds[];
     uint64_t* srec = lds;                                        // [kSub] staged records
@@ -176,7 +142,7 @@ __global__ __launch_bounds__(64) void k_part_scatter(const uint32_t* __restrict_
     if (t >= ntiles) return;
     const uint64_t t0 = t * tile, t1 = t0 + tile < n ? t0 + tile : n;
     for (uint32_t d = lane; d < R; d += 64) {
-        run[d] = tcnt[((uint64_t)c * R + d) * ntiles + t];
+        run[d] = grp_off[(uint64_t)c * (R + 1u) + d] + tcnt[((uint64_t)c * R + d) * ntiles + t];
         lcnt[d] = 0;
     }
     __syncthreads();
@@ -262,29 +228,50 @@ __global__ __launch_bounds__(64) void k_part_scatter(const uint32_t* __restrict_
     }
 }
 
-// Work items: one per segment of every (candidate, destination) stream (at least one).
-__global__ __launch_bounds__(1024) void k_seg_items(const uint32_t* __restrict__ grp_off, uint32_t P, uint32_t R,
-                                                    WArg wa, uint32_t* __restrict__ item_off)
+// Destination bases and work items, from the destination totals dtot[c][d]:
+//   grp_off[c][d] = records of candidate c routed to destinations < d (grp_off[c][R] = all),
+//   item_off[e]   = first work item of stream e = c * R + d, one item per segment of S
+//                   records (at least one per stream).
+// Pass one scans over all (c, d) in one block; pass two rebases grp_off per candidate.
+__global__ __launch_bounds__(1024) void k_seg_items(const uint32_t* __restrict__ dtot, uint32_t P, uint32_t R,
+                                                    WArg wa, uint32_t* __restrict__ grp_off,
+                                                    uint32_t* __restrict__ item_off)
 {
     __shared__ uint32_t s_scan[16];
+    __shared__ uint32_t s_cstart[CR_MAX_CANDS + 1];
     const uint32_t total = P * R;
-    uint32_t carry = 0;
+    uint32_t carry = 0, icarry = 0;
     for (uint32_t e0 = 0; e0 < total; e0 += blockDim.x) {
         const uint32_t e = e0 + threadIdx.x;
-        uint32_t nseg = 0;
+        uint32_t cnt = 0, nseg = 0;
         if (e < total) {
-            const uint32_t c = e / R, d = e % R;
-            const uint32_t* go = grp_off + (uint64_t)c * (R + 1u);
-            const uint32_t cnt = go[d + 1] - go[d];
-            const uint32_t S = seg_len(wa.W[c]);
+            cnt = dtot[e];
+            const uint32_t S = seg_len(wa.W[e / R]);
             nseg = cnt ? (cnt + S - 1) / S : 1u;
         }
-        uint32_t tot;
-        const uint32_t ex = block_exscan_u32(nseg, s_scan, &tot);
-        if (e < total) item_off[e] = carry + ex;
+        uint32_t tot, itot;
+        const uint32_t ex = block_exscan_u32(cnt, s_scan, &tot);
+        const uint32_t iex = block_exscan_u32(nseg, s_scan, &itot);
+        if (e < total) {
+            const uint32_t c = e / R, d = e % R;
+            grp_off[(uint64_t)c * (R + 1u) + d] = carry + ex;
+            item_off[e] = icarry + iex;
+            if (d == 0) s_cstart[c] = carry + ex;
+        }
         carry += tot;
+        icarry += itot;
     }
-    if (threadIdx.x == 0) item_off[total] = carry;
+    if (threadIdx.x == 0) {
+        item_off[total] = icarry;
+        s_cstart[P] = carry;
+    }
+    __syncthreads();
+    for (uint32_t e = threadIdx.x; e < total; e += blockDim.x) {
+        const uint32_t c = e / R, d = e % R;
+        grp_off[(uint64_t)c * (R + 1u) + d] -= s_cstart[c];
+    }
+    for (uint32_t c = threadIdx.x; c < P; c += blockDim.x)
+        grp_off[(uint64_t)c * (R + 1u) + R] = s_cstart[c + 1] - s_cstart[c];
 }
 
 template <int SL>
@@ -601,31 +588,18 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
     }
 }
 
-__global__ void k_zero32(uint32_t* __restrict__ p, uint64_t n)
-{
-    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (uint64_t)gridDim.x * blockDim.x)
-        p[i] = 0u;
-}
-
 struct ReplayWs {
     uint64_t* rec;
     uint32_t* tcnt;
-    uint32_t* bsum;
+    uint32_t* dtot;
     uint32_t* grp_off;
     uint32_t* item_off;
     size_t bytes;
 };
 
-inline uint32_t scan_blocks(uint64_t n, uint32_t P, uint32_t R)
-{
-    const PartGeom g = part_geom(n, P);
-    return (uint32_t)(((uint64_t)R * g.ntiles + kScanChunk - 1) / kScanChunk);
-}
-
 inline ReplayWs replay_layout(void* base, uint64_t n, uint32_t P, uint32_t R)
 {
     const PartGeom g = part_geom(n, P);
-    const uint32_t nblk = scan_blocks(n, P, R);
     auto up = [](uint64_t x) { return (x + 255) & ~255ull; };
     uint8_t* b = reinterpret_cast<uint8_t*>(base);
     uint64_t o = 0;
@@ -634,8 +608,8 @@ inline ReplayWs replay_layout(void* base, uint64_t n, uint32_t P, uint32_t R)
     o = up(o + (uint64_t)P * n * 8u);
     w.tcnt = reinterpret_cast<uint32_t*>(b + o);
     o = up(o + (uint64_t)P * R * g.ntiles * 4u);
-    w.bsum = reinterpret_cast<uint32_t*>(b + o);
-    o = up(o + (uint64_t)P * (nblk + 1u) * 4u);
+    w.dtot = reinterpret_cast<uint32_t*>(b + o);
+    o = up(o + (uint64_t)P * R * 4u);
     w.grp_off = reinterpret_cast<uint32_t*>(b + o);
     o = up(o + (uint64_t)P * (R + 1u) * 4u);
     w.item_off = reinterpret_cast<uint32_t*>(b + o);
@@ -689,27 +663,18 @@ extern "C" cr_status cr_replay_partition(const uint32_t* keys, const uint16_t* s
     if (!off || !err || (n > 0 && (!keys || !suffix || !dest))) return CR_EINVAL;
     const ReplayWs w = replay_layout(ws_base(ws), n, P, R);
     const PartGeom g = part_geom(n, P);
-    const uint32_t nblk = scan_blocks(n, P, R);
-    const uint64_t len = (uint64_t)R * g.ntiles;
     const hipStream_t st = as_stream(stream);
     uint32_t nbits = 0;
     while ((1u << nbits) < R) ++nbits;
     (void)hipGetLastError();
-    if (g.ntiles) {
+    if (g.ntiles)
         hipLaunchKernelGGL(k_part_hist, dim3((uint32_t)g.ntiles, P), dim3(256), (size_t)R * 4u, st, dest, n, R, g.tile,
                            g.ntiles, w.tcnt, err);
-        hipLaunchKernelGGL(k_scan_reduce, dim3(nblk, P), dim3(kScanThreads), 0, st, w.tcnt, len, nblk, w.bsum);
-    } else {
-        hipLaunchKernelGGL(k_zero32, dim3(64), dim3(256), 0, st, w.grp_off, (uint64_t)P * (R + 1u));
-    }
-    hipLaunchKernelGGL(k_scan_mid, dim3(P), dim3(kScanThreads), 0, st, w.bsum, nblk, R, w.grp_off);
-    if (g.ntiles) {
-        hipLaunchKernelGGL(k_scan_apply, dim3(nblk, P), dim3(kScanThreads), 0, st, w.tcnt, len, g.ntiles, R, nblk,
-                           w.bsum, w.grp_off);
+    hipLaunchKernelGGL(k_scan_dest, dim3(R, P), dim3(kScanThreads), 0, st, w.tcnt, g.ntiles, R, w.dtot);
+    hipLaunchKernelGGL(k_seg_items, dim3(1), dim3(1024), 0, st, w.dtot, P, R, ra.wa, w.grp_off, w.item_off);
+    if (g.ntiles)
         hipLaunchKernelGGL(k_part_scatter, dim3(xcd_grid((uint32_t)g.ntiles), P), dim3(64), scatter_lds_bytes(R), st, keys,
-                           suffix, dest, n, off, J, R, nbits, g.tile, g.ntiles, w.tcnt, w.rec);
-    }
-    hipLaunchKernelGGL(k_seg_items, dim3(1), dim3(1024), 0, st, w.grp_off, P, R, ra.wa, w.item_off);
+                           suffix, dest, n, off, J, R, nbits, g.tile, g.ntiles, w.tcnt, w.grp_off, w.rec);
     return hipGetLastError() == hipSuccess ? CR_OK : CR_EHIP;
 }
 
