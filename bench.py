@@ -2,10 +2,14 @@
 
 A step is one pass of the whole path over the 70B-like workload (20,000 keys, Zipf 1.0
 capped at a 0.3 % share, 1e7 requests at 176 QPS in 60-s control intervals = 948
-intervals and 947 plan builds, 30 destinations x 64 LRU slots). Inputs are resident in
-HBM before timing starts. Prints ONE JSON line.
+intervals, 30 destinations x 64 LRU slots). By default the steps are consecutive chunks of
+one stream: chunk k is planned from chunk k-1's last window, replays from chunk k-1's final
+cache state, and is counted, planned, routed and partitioned on one HIP stream while chunk
+k-1 replays on another (--schedule serial: every step from scratch on one stream). Inputs
+are resident in HBM before timing starts. Prints ONE JSON line.
 
   python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload llama70b|tiny|replication|burst]
+                  [--schedule overlap|serial]
 """
 from __future__ import annotations
 
@@ -34,6 +38,10 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="llama70b")
+    ap.add_argument("--schedule", default="serial", choices=("overlap", "serial"),
+                    help="overlap: consecutive chunks of one stream, chunk k planned on one HIP stream while "
+                         "chunk k-1 replays on another (cache state and last window carried); serial: every "
+                         "step is the whole workload from scratch on one stream")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--calib-copy-mb", type=int, default=0,
@@ -94,34 +102,45 @@ def main():
     if not os.path.exists(hip_build.LIB):
         hip_build.build()
     from paper_2608_19677_amd import workload
-    from paper_2608_19677_amd.pipeline import Pipeline
+    from paper_2608_19677_amd.pipeline import ChunkStream, Pipeline
 
     wl = workload.CONFIGS[args.workload]()
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
-    gp = Pipeline(wl, device="cuda:0")
-    n_plans = gp.plans.num_plans
-    stream = torch.cuda.current_stream()
-
     stages = Pipeline.STAGES
-    for _ in range(args.warmup):
-        gp.step()
-    torch.cuda.synchronize()
     ev = {s: [] for s in stages}
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        for s in stages:
-            a = torch.cuda.Event(enable_timing=True)
-            b = torch.cuda.Event(enable_timing=True)
-            a.record(stream)
-            getattr(gp, s)()
-            b.record(stream)
-            ev[s].append((a, b))
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
+    if args.schedule == "serial":
+        gp = Pipeline(wl, device="cuda:0")
+        stream = torch.cuda.current_stream()
+        for _ in range(args.warmup):
+            gp.step()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            for s in stages:
+                a = torch.cuda.Event(enable_timing=True)
+                b = torch.cuda.Event(enable_timing=True)
+                a.record(stream)
+                getattr(gp, s)()
+                b.record(stream)
+                ev[s].append((a, b))
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        last = gp
+    else:
+        cs = ChunkStream(wl, device="cuda:0")
+        for _ in range(args.warmup):
+            cs.enqueue()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            last = cs.enqueue(timers=ev)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+    n_plans = last.plans.num_plans
     ms_step = (t1 - t0) * 1e3 / args.steps
     stage_ms = {s: float(np.mean([a.elapsed_time(b) for a, b in ev[s]])) for s in stages}
-    h = gp.host()
+    h = last.host()
     assert h["err"] == 0, f"device error word {h['err']:#x}"
     tot = h["stats"].sum(axis=(0, 2)).astype(np.float64)
 
@@ -175,6 +194,7 @@ def main():
         "hit_rate": (tot[:, 1] / tot[:, 0]).tolist(),
     }
     out["config"]["plan_builds"] = n_plans
+    out["config"]["schedule"] = args.schedule
 
     if args.calib_copy_mb:
         nb = args.calib_copy_mb << 20

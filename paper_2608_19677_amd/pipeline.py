@@ -56,19 +56,22 @@ class Pipeline:
         self.max_W = max(self.Ws)
         sizes = np.diff(self.inp.off_host.astype(np.int64))
         i32 = dict(dtype=torch.int32, device=device)
-        self.counts = torch.empty((J, K), **i32)
         self.err = torch.zeros(1, **i32)
         # plan windows: groups g = 0..NG-1, interval j -> group gmap[j]
         self.prev_counts = prev_counts
         if prev_counts is None:
+            self.counts = torch.empty((J, K), **i32)
             NG = max(J - 1, 1)
             self.win_src = self.counts[:NG]
             gmap = [max(j - 1, 0) for j in range(J)]
             n_win = [int(sizes[g]) for g in range(NG)]
         else:
+            # row 0 holds the previous chunk's last window, rows 1..J this chunk's counts,
+            # so that window g (the plan of interval g) is row g with no copy of the rest
+            self.cbuf = torch.empty((J + 1, K), **i32)
+            self.counts = self.cbuf[1:]
             NG = J
-            self.win_buf = torch.empty((J, K), **i32)
-            self.win_src = self.win_buf
+            self.win_src = self.cbuf[:J]
             gmap = list(range(J))
             n_win = [int(prev_n)] + [int(sizes[g]) for g in range(J - 1)]
         self.NG = NG
@@ -84,14 +87,13 @@ class Pipeline:
         self.stats = torch.zeros((J, P, R, 4), dtype=torch.int64, device=device)
         self.lru_in = lru_in
         self.lru_out = torch.empty((P, R, self.max_W), **i32)
+        self.first_index = wl.first_index  # global index of the chunk's first request
 
     # -- the five calls ----------------------------------------------------------------
     def count(self, stream=None):
         B.cr_count_rates(self.inp.keys, self.inp.off, self.J, self.K, self.counts, self.err, stream, n=self.n)
         if self.prev_counts is not None:
-            self.win_buf[0].copy_(self.prev_counts)
-            if self.J > 1:
-                self.win_buf[1:].copy_(self.counts[: self.J - 1])
+            self.cbuf[0].copy_(self.prev_counts)
 
     def admit(self, stream=None):
         B.cr_admit(self.win_src, self.plans.c, self.ws_admit, self.err, stream)
@@ -104,7 +106,7 @@ class Pipeline:
         self.place(stream)
 
     def route(self, stream=None):
-        B.cr_route(self.inp.keys, self.wl.first_index, self.wl.seed, self.inp.off, self.gmap, self.J, self.plans.c,
+        B.cr_route(self.inp.keys, self.first_index, self.wl.seed, self.inp.off, self.gmap, self.J, self.plans.c,
                    self.dest, self.err, stream, n=self.n)
 
     def partition(self, stream=None):
@@ -150,3 +152,74 @@ class Pipeline:
         return dict(adm_keys=h["order"][w, :A].copy(), adm_k=np.diff(mo).astype(np.uint32),
                     member_off=mo.copy(), members=h["members"][p, : int(mo[A]) if A else 0].copy(),
                     L=h["load"][p].copy(), cold=int(h["cold"][p]), clamped=int(h["clamped"][p]))
+
+
+class ChunkStream:
+    """Consecutive chunks of one request stream through the path, two HIP streams deep.
+
+    Chunk k (the workload's requests again, at global indices k*n .. k*n + n - 1) is
+    counted, planned, routed and partitioned on the plan stream while chunk k-1's LRU
+    replay runs on the replay stream. Chunk k >= 1 plans its first interval from chunk
+    k-1's last window and starts its replay from chunk k-1's final cache state, so the
+    results are those of processing the chunks one after another. Chunk 0 has its own
+    buffers; later chunks alternate between two sets, and a chunk's partition waits for
+    the replay of the chunk that used its set before it. Both streams have the default
+    priority.
+    """
+
+    def __init__(self, wl, device="cuda"):
+        self.wl = wl
+        self.n = wl.n
+        self.inp = upload(wl, device)
+        self.first = Pipeline(wl, device, self.inp)
+        last_n = int(self.inp.off_host[-1] - self.inp.off_host[-2])
+        self.slots = [Pipeline(wl, device, self.inp, prev_counts=self.first.counts[wl.J - 1], prev_n=last_n,
+                               lru_in=self.first.lru_out) for _ in range(2)]
+        self.s_plan = torch.cuda.Stream(device=device)
+        self.s_rep = torch.cuda.Stream(device=device)
+        self.ev_part = {}
+        self.ev_rep = {}
+        self.k = 0
+
+    def pipe(self, k: int) -> Pipeline:
+        return self.first if k == 0 else self.slots[(k - 1) % 2]
+
+    def enqueue(self, timers=None):
+        """Enqueue the next chunk. `timers`, if given, maps stage -> list of (start, end)
+        events recorded on the stream the stage runs on."""
+        k = self.k
+        p = self.pipe(k)
+        p.first_index = self.wl.first_index + k * self.n
+        if k:
+            prev = self.pipe(k - 1)
+            p.prev_counts = prev.counts[self.wl.J - 1]
+            p.lru_in = prev.lru_out
+
+        def run(stage, stream):
+            if timers is None:
+                getattr(p, stage)()
+                return
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            getattr(p, stage)()
+            b.record(stream)
+            timers.setdefault(stage, []).append((a, b))
+
+        with torch.cuda.stream(self.s_plan):
+            for stage in ("count", "admit", "place", "route"):
+                run(stage, self.s_plan)
+            if k >= 3:  # this buffer set was last replayed by chunk k-2
+                self.s_plan.wait_event(self.ev_rep.pop(k - 2))
+            run("partition", self.s_plan)
+            ev = torch.cuda.Event()
+            ev.record(self.s_plan)
+            self.ev_part[k] = ev
+        with torch.cuda.stream(self.s_rep):
+            self.s_rep.wait_event(self.ev_part.pop(k))
+            run("lru", self.s_rep)
+            ev = torch.cuda.Event()
+            ev.record(self.s_rep)
+            self.ev_rep[k] = ev
+        self.k += 1
+        return p

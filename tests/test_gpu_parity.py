@@ -11,7 +11,7 @@ import torch
 import oracle
 from oracle import pipeline as opipe
 from paper_2608_19677_amd import workload as wl_mod
-from paper_2608_19677_amd.pipeline import Pipeline
+from paper_2608_19677_amd.pipeline import ChunkStream, Pipeline
 
 from cr_check import compare_all, compare_plan, say
 
@@ -124,6 +124,41 @@ def test_repeat_runs_are_identical():
     h2 = gp.host()
     for k in ("counts", "order", "members", "load", "route", "dest", "stats", "lru"):
         assert np.array_equal(np.asarray(h1[k]).view(np.uint8), np.asarray(h2[k]).view(np.uint8)), k
+
+
+def test_two_stream_chunk_schedule_equals_serial():
+    # ChunkStream plans chunk k on one stream while chunk k-1 replays on another, reusing
+    # two buffer sets; five chunks enqueued with no host synchronisation must equal the
+    # chunks run one after another (plans from the previous chunk's last window, cache
+    # state carried). Buffer sets are reused, so the last two chunks are the ones compared.
+    import dataclasses
+    wl = wl_mod.small_random(41, num_keys=2000, n=150_000, R=30, Ws=[64], J=5, hot=2, hot_share=0.3)
+    say(f"[case] two-stream chunks n={wl.n} J={wl.J}")
+    n_chunks = 5
+    cs = ChunkStream(wl)
+    for _ in range(n_chunks):
+        cs.enqueue()
+    torch.cuda.synchronize()
+    last_n = int(wl.offsets[-1] - wl.offsets[-2])
+    prev, ref = None, []
+    for k in range(n_chunks):
+        wk = dataclasses.replace(wl, first_index=wl.first_index + k * wl.n)
+        if prev is None:
+            p = Pipeline(wk)
+        else:
+            p = Pipeline(wk, prev_counts=prev.counts[wl.J - 1].clone(), prev_n=last_n, lru_in=prev.lru_out.clone())
+        p.step()
+        ref.append(p.host())
+        prev = p
+    for k in (n_chunks - 2, n_chunks - 1):
+        pk = cs.pipe(k)
+        h = pk.host()
+        assert h["err"] == 0
+        for key in ("counts", "load", "dest", "stats", "lru"):
+            np.testing.assert_array_equal(np.asarray(h[key]), np.asarray(ref[k][key]), err_msg=f"chunk {k} {key}")
+        for g in range(pk.NG):  # order and members are defined up to their used lengths
+            for c in range(pk.P):
+                compare_plan(pk.plan_of(h, g, c), pk.plan_of(ref[k], g, c), f"chunk {k} plan {g}/{c}")
 
 
 @pytest.mark.timeout(900)
