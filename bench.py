@@ -44,6 +44,8 @@ def parse():
                          "step is the whole workload from scratch on one stream")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-unbatched", action="store_true",
+                    help="skip the single unbatched plan build (keeps a kernel trace to the step's own launches)")
     ap.add_argument("--calib-copy-mb", type=int, default=0,
                     help="after timing, copy this many MiB device-to-device once (a plain copy kernel of known "
                          "size, to scale the FETCH_SIZE / WRITE_SIZE counters)")
@@ -71,6 +73,33 @@ def measured_traffic(kernel: str, workload: str):
             if hashlib.sha256(f.read()).hexdigest() != rec["sources_sha256"].get(rel):
                 return None
     return rec["bytes_per_launch"][kernel]
+
+
+def one_plan_build_us(wl, pipe, torch, reps=20):
+    """One unbatched plan build: cr_admit + cr_place_lpt for a single plan (the first
+    interval's window, first candidate), timed with events on the current stream."""
+    from paper_2608_19677_amd import binding as B
+    cand = wl.candidates[0]
+    n_win = int(wl.offsets[1] - wl.offsets[0])
+    ps = B.PlanSet([(0, cand.W, n_win, cand.a * n_win, cand.b * wl.R)], 1, wl.R, cand.W, wl.num_keys, 1,
+                   pipe.device)
+    ws = torch.empty(B.cr_admit_workspace_bytes(1, wl.R, cand.W), dtype=torch.uint8, device=pipe.device)
+    err = torch.zeros(1, dtype=torch.int32, device=pipe.device)
+    row = pipe.counts[0:1]
+    stream = torch.cuda.current_stream()
+    for _ in range(3):
+        B.cr_admit(row, ps.c, ws, err, None)
+        B.cr_place_lpt(row, ps.c, None)
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for _ in range(reps):
+        B.cr_admit(row, ps.c, ws, err, None)
+        B.cr_place_lpt(row, ps.c, None)
+    b.record(stream)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    return a.elapsed_time(b) * 1e3 / reps
 
 
 def describe(name, wl):
@@ -139,6 +168,7 @@ def main():
         t1 = time.perf_counter()
     n_plans = last.plans.num_plans
     ms_step = (t1 - t0) * 1e3 / args.steps
+    one_build_us = None if args.no_unbatched else one_plan_build_us(wl, last, torch)
     stage_ms = {s: float(np.mean([a.elapsed_time(b) for a, b in ev[s]])) for s in stages}
     h = last.host()
     assert h["err"] == 0, f"device error word {h['err']:#x}"
@@ -146,8 +176,8 @@ def main():
 
     n, P, R = wl.n, wl.P, wl.R
     n_adm = int(h["member_off"][np.arange(n_plans), h["num_admitted"].astype(np.int64)].astype(np.int64).sum())
-    # Algorithmic work per launch of the single-kernel calls (the zero fills of stats are
-    # outside the events; count, place, route and lru each launch exactly one kernel here).
+    # Algorithmic work per launch of the single-kernel calls (the statistics are cleared in
+    # the partition stage; count, place, route and lru each launch exactly one kernel here).
     kern = {
         # counting reads every key and writes the dense [J][K] counts matrix it defines
         "count": dict(kernel="k_count_owner", bound="hbm", unit="GB/s", work=4.0 * n + 4.0 * wl.J * wl.num_keys,
@@ -188,6 +218,7 @@ def main():
                      "frac": d["frac"], "traffic": measured_traffic(d["kernel"], args.workload),
                      "kernel": d["kernel"]},
         "us_per_plan_build": (stage_ms["admit"] + stage_ms["place"]) * 1e3 / n_plans,
+        "us_one_plan_build": one_build_us,
         "stage_ms": stage_ms,
         "kernels": {k: {kk: vv for kk, vv in v.items() if kk != "work"} for k, v in kern.items()},
         "hbm_frac": {"count": kern["count"]["frac"], "route": kern["route"]["frac"]},

@@ -112,9 +112,9 @@ class Pipeline:
     def partition(self, stream=None):
         B.cr_replay_partition(self.inp.keys, self.inp.suffix, self.dest, self.inp.off, self.J, self.P, self.R,
                               self.Ws, self.ws_replay, self.err, stream, n=self.n)
+        self.stats.zero_()  # cr_replay_lru accumulates into it (cleared here so that lru is one kernel)
 
     def lru(self, stream=None):
-        self.stats.zero_()
         B.cr_replay_lru(self.inp.prefix_len, self.K, self.n, self.J, self.P, self.R, self.Ws, self.max_W,
                         self.lru_in, self.lru_out, self.stats, self.ws_replay, self.err, stream)
 
