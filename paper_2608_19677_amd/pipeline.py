@@ -54,7 +54,11 @@ class Pipeline:
         self.J, self.K, self.R, self.P, self.n = J, K, R, P, wl.n
         self.Ws = [c.W for c in wl.candidates]
         self.max_W = max(self.Ws)
-        sizes = np.diff(self.inp.off_host.astype(np.int64))
+        # requests per window that count (keys < num_keys): a window's N_w is its row sum
+        off = self.inp.off_host.astype(np.int64)
+        csum = np.concatenate([[0], np.cumsum(np.asarray(wl.keys) < K, dtype=np.int64)])
+        sizes = csum[off[1:]] - csum[off[:-1]]
+        self.window_sizes = sizes
         i32 = dict(dtype=torch.int32, device=device)
         self.err = torch.zeros(1, **i32)
         # plan windows: groups g = 0..NG-1, interval j -> group gmap[j]
@@ -172,7 +176,7 @@ class ChunkStream:
         self.n = wl.n
         self.inp = upload(wl, device)
         self.first = Pipeline(wl, device, self.inp)
-        last_n = int(self.inp.off_host[-1] - self.inp.off_host[-2])
+        last_n = int(self.first.window_sizes[-1])
         self.slots = [Pipeline(wl, device, self.inp, prev_counts=self.first.counts[wl.J - 1], prev_n=last_n,
                                lru_in=self.first.lru_out) for _ in range(2)]
         self.s_plan = torch.cuda.Stream(device=device)

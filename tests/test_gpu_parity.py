@@ -51,6 +51,43 @@ def test_small_random_parity(case):
     _run(wl)
 
 
+def test_tiny_intervals_parity():
+    # Thousands of intervals of a few requests each (many empty): a 1024-request route block
+    # spans hundreds of interval boundaries, and the partition and replay cross one in
+    # almost every 64-request chunk.
+    _run(wl_mod.small_random(11, num_keys=500, n=50_000, R=30, Ws=[16], J=8000, hot=2, hot_share=0.2))
+
+
+def test_out_of_range_keys_parity():
+    # Keys >= num_keys are not counted, are dispatched as cold, are skipped by the replay
+    # and set CR_ERR_KEY_RANGE; everything else matches the oracle.
+    wl = wl_mod.small_random(12, num_keys=300, n=30_000, R=16, Ws=[8, 32], J=4, hot=2, hot_share=0.3)
+    rng = np.random.default_rng(5)
+    bad = rng.choice(wl.n, size=400, replace=False)
+    wl.keys = wl.keys.copy()
+    wl.keys[bad] = (wl.num_keys + rng.integers(0, 1000, size=bad.size)).astype(np.uint32)
+    wl.keys[bad[:5]] = np.uint32(0xFFFFFFFF)
+    say(f"[case] out-of-range keys n={wl.n} bad={bad.size}")
+    gp = Pipeline(wl)
+    gp.step()
+    h = gp.host()
+    assert h["err"] & 1, "CR_ERR_KEY_RANGE not set"
+    h["err"] = 0
+    compare_all(wl, gp, h, opipe.run(wl))
+
+
+def test_empty_stream_parity():
+    wl = wl_mod.small_random(13, num_keys=100, n=0, R=8, Ws=[4], J=3)
+    _run(wl)
+
+
+def test_max_candidates_parity():
+    # 256 candidate plans (the ABI's maximum) replayed at once
+    Ws = list(range(1, 17))
+    qs = [(a, 8) for a in range(5, 21)]
+    _run(wl_mod.small_random(14, num_keys=300, n=20_000, R=8, Ws=Ws, J=2, qs=qs, hot=1, hot_share=0.2))
+
+
 def test_tiny_shape_parity():
     gp, h, orc = _run(wl_mod.tiny())
     pl = gp.plan_of(h, 0, 0)
