@@ -146,6 +146,21 @@ cr_status cr_route(const uint32_t* keys, uint64_t n, uint64_t first_index, uint6
                    const uint64_t* off, const uint32_t* gmap, uint32_t J, const cr_plan_set* plans,
                    uint16_t* dest, uint32_t* err, void* stream);
 
+/* Churn between pairs of built plans of one set (Section 5.4 "Rate drift and remapping";
+ * Appendix E, table of replan measurements). With S_x = {(b, r) : r in T_x(b)} over plan
+ * x's admitted keys b, pair i = (p, q) = (pairs[2i], pairs[2i+1]) yields
+ *   out[4i+0] = |S_p intersected with S_q|       (key-destination pairs in both plans)
+ *   out[4i+1] = keys admitted by both plans
+ *   out[4i+2] = of those, keys whose k differs
+ *   out[4i+3] = of those, keys whose destination set T is the same.
+ * Cache churn = 1 - out[4i] / (|S_p| + |S_q| - out[4i]) with |S_x| = member_off[x][A_x];
+ * count churn = out[4i+2] / out[4i+1]. Cost per key admitted by both: k_p * k_q compares.
+ * pairs u32 [num_pairs][2]; out u64 [num_pairs][4] (overwritten). The plans must have
+ * been built by cr_admit and cr_place_lpt. A pair naming a plan >= num_plans sets
+ * CR_ERR_SPEC and yields zeros. */
+cr_status cr_plan_churn(const cr_plan_set* plans, const uint32_t* pairs, uint32_t num_pairs, uint64_t* out,
+                        uint32_t* err, void* stream);
+
 /* Workspace for cr_replay (and for its two phases), in bytes. */
 size_t cr_replay_workspace_bytes(uint64_t n, uint32_t P, uint32_t R);
 

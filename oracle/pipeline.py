@@ -6,6 +6,9 @@ Semantics it fixes (each restated from the paper or from the reading noted):
   is built from the counts of interval j-1 (the table stays fixed for an
   interval and is rebuilt from the latest telemetry, Section 3.2); interval 0
   has no earlier window and uses its own.
+* A workload may name the window of every (interval, candidate) plan itself
+  (``plan_windows``), as the replanning study does to compare fresh and stale
+  plans (Section 5.4, Appendix E).
 * Candidate (W, a, b) has C = R W warm slots and q_cap = (a/b) x N_w / R,
   i.e. q_num = a N_w and q_den = b R with N_w the window's request count.
 * The replay's LRU state per (candidate, destination) starts empty and is
@@ -16,7 +19,7 @@ TEST INFRASTRUCTURE: see the package docstring.
 from __future__ import annotations
 
 import time
-from typing import Dict, List, Optional
+from typing import Dict, List, Optional, Tuple
 
 import numpy as np
 
@@ -27,23 +30,23 @@ def plan_window(j: int) -> int:
     return max(j - 1, 0)
 
 
-def build_plans(counts: np.ndarray, R: int, candidates, windows: List[int]) -> Dict:
-    """Plans for every (window, candidate) pair: dict[(w, c)] -> plan dict."""
+def build_plans(counts: np.ndarray, R: int, candidates, pairs: List[Tuple[int, int]]) -> Dict:
+    """The plan of every (window, candidate) pair in ``pairs``: dict[(w, c)] -> plan dict."""
     plans = {}
-    for w in windows:
+    for w, c in pairs:
         row = counts[w]
         n_w = int(row.sum(dtype=np.uint64))
-        for c, cand in enumerate(candidates):
-            q_num, q_den = cand.a * n_w, cand.b * R
-            if n_w == 0:
-                adm_keys = np.zeros(0, np.uint32)
-                adm_k = np.zeros(0, np.uint32)
-                cold, clamped = 0, 0
-            else:
-                adm_keys, adm_k, cold, clamped = admit(row, R, cand.W, n_w, q_num, q_den)
-            members, member_off, L = place_lpt(adm_keys, adm_k, row, R, cold)
-            plans[(w, c)] = dict(adm_keys=adm_keys, adm_k=adm_k, cold=cold, clamped=clamped,
-                                 members=members, member_off=member_off, L=L, n_window=n_w)
+        cand = candidates[c]
+        q_num, q_den = cand.a * n_w, cand.b * R
+        if n_w == 0:
+            adm_keys = np.zeros(0, np.uint32)
+            adm_k = np.zeros(0, np.uint32)
+            cold, clamped = 0, 0
+        else:
+            adm_keys, adm_k, cold, clamped = admit(row, R, cand.W, n_w, q_num, q_den)
+        members, member_off, L = place_lpt(adm_keys, adm_k, row, R, cold)
+        plans[(w, c)] = dict(adm_keys=adm_keys, adm_k=adm_k, cold=cold, clamped=clamped,
+                             members=members, member_off=member_off, L=L, n_window=n_w)
     return plans
 
 
@@ -53,7 +56,9 @@ def run(wl, lru: Optional[List[np.ndarray]] = None, counts_prev: Optional[np.nda
 
     ``counts_prev`` (one row) stands in for the window before interval 0 when a
     stream is processed in chunks; ``lru`` is the carried replay state per
-    candidate.  Returns counts, plans, dest [P][n], stats [J][P][R][4], lru.
+    candidate.  Returns counts, plans, dest [P][n], stats [J][P][R][4] (or
+    [bins][P][R][4] with ``wl.stat_offsets``), lru, and ``win_of[j][c]``, the window
+    of candidate c's plan in interval j.
     """
     t0 = time.perf_counter()
     counts, _ = count_rates(wl.keys, wl.offsets, wl.num_keys)
@@ -61,12 +66,17 @@ def run(wl, lru: Optional[List[np.ndarray]] = None, counts_prev: Optional[np.nda
     J, P, R = wl.J, wl.P, wl.R
     if counts_prev is None:
         src = counts
-        win_of = [plan_window(j) for j in range(J)]
+        if wl.plan_windows is None:
+            win_of = [[plan_window(j)] * P for j in range(J)]
+        else:
+            win_of = [[int(wl.plan_windows[j][c]) for c in range(P)] for j in range(J)]
     else:
+        if wl.plan_windows is not None:
+            raise ValueError("a stream processed in chunks plans every interval from the window before it")
         src = np.concatenate([counts_prev.reshape(1, -1), counts], axis=0)
-        win_of = list(range(J))  # interval j uses row j of src = counts of interval j-1
-    windows = sorted(set(win_of))
-    plans = build_plans(src, R, wl.candidates, windows)
+        win_of = [[j] * P for j in range(J)]  # interval j uses row j of src = counts of interval j-1
+    needed = sorted({(win_of[j][c], c) for j in range(J) for c in range(P)})
+    plans = build_plans(src, R, wl.candidates, needed)
     t2 = time.perf_counter()
     dest = np.zeros((P, wl.n), dtype=np.uint16)
     off = wl.offsets.astype(np.int64)
@@ -75,14 +85,15 @@ def run(wl, lru: Optional[List[np.ndarray]] = None, counts_prev: Optional[np.nda
         if e == s:
             continue
         for c in range(P):
-            pl = plans[(win_of[j], c)]
+            pl = plans[(win_of[j][c], c)]
             dest[c, s:e] = route(wl.keys[s:e], wl.first_index + s, wl.seed, wl.num_keys, R,
                                  pl["adm_keys"], pl["member_off"], pl["members"], pl["L"])
     t3 = time.perf_counter()
-    stats = np.zeros((J, P, R, 4), dtype=np.uint64)
+    soff = wl.offsets if wl.stat_offsets is None else wl.stat_offsets
+    stats = np.zeros((len(soff) - 1, P, R, 4), dtype=np.uint64)
     out_lru = []
     for c, cand in enumerate(wl.candidates):
-        st, state = replay(wl.keys, wl.suffix, wl.prefix_len, dest[c], wl.offsets, R, cand.W,
+        st, state = replay(wl.keys, wl.suffix, wl.prefix_len, dest[c], soff, R, cand.W,
                            None if lru is None else lru[c])
         stats[:, c] = st
         out_lru.append(state)

@@ -11,6 +11,7 @@
 // LPT is a dependency chain of sum(k) steps per plan; one wavefront owns one plan and
 // keeps the R loads in registers (lane l holds destinations l, l+64, ...), so each pick
 // is a register scan plus a 6-step cross-lane (L, r) argmin.
+// k_plan_churn compares pairs of built plans for the replanning study.
 #include <math.h>
 
 #include "cr_common.h"
@@ -1110,6 +1111,79 @@ __global__ __launch_bounds__(64) void k_lpt(uint32_t KW, uint32_t R, uint32_t Cm
     }
 }
 
+// Churn between two plans of a set (Section 5.4; Appendix E, table of replan measurements).
+// One block per pair (p, q): its threads walk p's admitted keys in admission order, look
+// each key up in q's compact dispatch table (one 16-byte key-index load and a popcount)
+// and compare the two member lists; the work per key is k_p * k_q compares.
+constexpr uint32_t kChurnThreads = 256;
+
+__global__ void __launch_bounds__(kChurnThreads)
+    k_plan_churn(uint32_t NP, uint32_t KW, uint32_t Cmax, uint32_t NW, const cr_plan_spec* __restrict__ specs,
+                 const uint32_t* __restrict__ order, const uint32_t* __restrict__ num_admitted,
+                 const uint32_t* __restrict__ member_off, const uint16_t* __restrict__ members,
+                 const uint64_t* __restrict__ key_index, const uint32_t* __restrict__ route,
+                 const uint32_t* __restrict__ pairs, uint64_t* __restrict__ out, uint32_t* __restrict__ err)
+{
+    __shared__ uint64_t s_acc[4][kChurnThreads / kWave];
+    const uint32_t pr = blockIdx.x;
+    const uint32_t p = pairs[2u * pr], q = pairs[2u * pr + 1u];
+    uint64_t common_pairs = 0, both = 0, k_changed = 0, same_set = 0;
+    if (p < NP && q < NP) {
+        const uint32_t A = min(num_admitted[p], Cmax);
+        const uint32_t w = specs[p].window;
+        const uint32_t* ord = order + (uint64_t)min(w, NW - 1u) * Cmax;
+        const uint32_t* mop = member_off + (uint64_t)p * (Cmax + 1u);
+        const uint16_t* mep = members + (uint64_t)p * Cmax;
+        const uint64_t* kxq = key_index + (uint64_t)q * KW * 2u;
+        const uint32_t* rwq = route + (uint64_t)q * Cmax;
+        const uint32_t* moq = member_off + (uint64_t)q * (Cmax + 1u);
+        const uint16_t* meq = members + (uint64_t)q * Cmax;
+        for (uint32_t a = w < NW ? threadIdx.x : A; a < A; a += kChurnThreads) {
+            const uint32_t b = ord[a];
+            const ulonglong2 e = kx_entry(kxq, b, true);
+            if (!((e.x >> (b & 63u)) & 1ull)) continue;  // not admitted by q
+            const uint32_t word = rwq[kx_rank(e, b)];
+            const bool single = (word & CR_ROUTE_SINGLE) != 0u;
+            const uint32_t q0 = single ? 0u : moq[word];
+            const uint32_t kq = single ? 1u : moq[word + 1u] - q0;
+            const uint32_t p0 = mop[a], kp = mop[a + 1u] - p0;
+            uint32_t common = 0;
+            for (uint32_t i = 0; i < kp; ++i) {
+                const uint32_t m = mep[p0 + i];
+                if (single) {
+                    common += m == (word & 0xFFFFu);
+                } else {
+                    for (uint32_t t = 0; t < kq; ++t) common += m == (uint32_t)meq[q0 + t];
+                }
+            }
+            common_pairs += common;
+            both += 1u;
+            k_changed += kp != kq;
+            same_set += kp == kq && common == kp;
+        }
+    } else if (threadIdx.x == 0) {
+        atomicOr(err, CR_ERR_SPEC);
+    }
+    const uint32_t wv = threadIdx.x / kWave;
+    common_pairs = wave_sum_u64(common_pairs);
+    both = wave_sum_u64(both);
+    k_changed = wave_sum_u64(k_changed);
+    same_set = wave_sum_u64(same_set);
+    if ((threadIdx.x & (kWave - 1u)) == 0u) {
+        s_acc[0][wv] = common_pairs;
+        s_acc[1][wv] = both;
+        s_acc[2][wv] = k_changed;
+        s_acc[3][wv] = same_set;
+    }
+    __syncthreads();
+    if (threadIdx.x < 4u) {
+        uint64_t v = 0;
+#pragma unroll
+        for (uint32_t i = 0; i < kChurnThreads / kWave; ++i) v += s_acc[threadIdx.x][i];
+        out[4ull * pr + threadIdx.x] = v;
+    }
+}
+
 inline uint32_t key_words(uint32_t K) { return (K + 63u) / 64u; }
 
 bool valid_set(const cr_plan_set* ps)
@@ -1199,5 +1273,21 @@ extern "C" cr_status cr_place_lpt(const uint32_t* counts, const cr_plan_set* pla
     else if (s <= 8) CR_LPT(8);
     else CR_LPT(16);
 #undef CR_LPT
+    return hipGetLastError() == hipSuccess ? CR_OK : CR_EHIP;
+}
+
+extern "C" cr_status cr_plan_churn(const cr_plan_set* plans, const uint32_t* pairs, uint32_t num_pairs, uint64_t* out,
+                                   uint32_t* err, void* stream)
+{
+    using namespace cr;
+    if (!valid_set(plans) || !err || (num_pairs > 0 && (!pairs || !out))) return CR_EINVAL;
+    if (num_pairs > 0x7FFFFFFFu) return CR_EINVAL;
+    if (num_pairs == 0) return CR_OK;
+    const hipStream_t st = as_stream(stream);
+    (void)hipGetLastError();
+    hipLaunchKernelGGL(k_plan_churn, dim3(num_pairs), dim3(kChurnThreads), 0, st, plans->num_plans,
+                       key_words(plans->num_keys), plans->R * plans->max_W, plans->num_windows, plans->specs,
+                       plans->order, plans->num_admitted, plans->member_off, plans->members, plans->key_index,
+                       plans->route, pairs, out, err);
     return hipGetLastError() == hipSuccess ? CR_OK : CR_EHIP;
 }

@@ -7,7 +7,10 @@ Semantics (the paper's statement of the loop, Sections 3.1-3.2):
   in chunks, from the last window of the previous chunk);
 * candidate (W, a, b) has C = R W warm slots and load target q_cap = (a/b) N_w / R,
   passed to the library as q_num = a N_w, q_den = b R;
-* the replay's per-destination cache state is carried across intervals and chunks.
+* the replay's per-destination cache state is carried across intervals and chunks;
+* a workload may name the window of each (interval, candidate) plan itself, as the
+  replanning study does (Section 5.4, Appendix E): one plan group per interval then,
+  and replay statistics may be kept in bins finer than the intervals.
 
 Inputs are uploaded once by ``prepare``; ``step`` only enqueues the five library calls
 (plus clearing the accumulating outputs) on the current stream.
@@ -61,15 +64,29 @@ class Pipeline:
         self.window_sizes = sizes
         i32 = dict(dtype=torch.int32, device=device)
         self.err = torch.zeros(1, **i32)
-        # plan windows: groups g = 0..NG-1, interval j -> group gmap[j]
+        # plan groups g = 0..NG-1 (interval j -> group gmap[j]); window[g][c] = counts row
+        # that candidate c's plan of group g is built from
         self.prev_counts = prev_counts
-        if prev_counts is None:
+        pw = getattr(wl, "plan_windows", None)
+        if prev_counts is None and pw is None:
             self.counts = torch.empty((J, K), **i32)
             NG = max(J - 1, 1)
             self.win_src = self.counts[:NG]
             gmap = [max(j - 1, 0) for j in range(J)]
+            window = [[g] * P for g in range(NG)]
             n_win = [int(sizes[g]) for g in range(NG)]
+        elif prev_counts is None:
+            self.counts = torch.empty((J, K), **i32)
+            NG = J
+            self.win_src = self.counts
+            gmap = list(range(J))
+            window = [[int(pw[j][c]) for c in range(P)] for j in range(J)]
+            if any(not 0 <= w < J for row in window for w in row):
+                raise ValueError("plan_windows names a window outside the stream")
+            n_win = [int(x) for x in sizes]
         else:
+            if pw is not None:
+                raise ValueError("a stream processed in chunks plans every interval from the window before it")
             # row 0 holds the previous chunk's last window, rows 1..J this chunk's counts,
             # so that window g (the plan of interval g) is row g with no copy of the rest
             self.cbuf = torch.empty((J + 1, K), **i32)
@@ -77,18 +94,35 @@ class Pipeline:
             NG = J
             self.win_src = self.cbuf[:J]
             gmap = list(range(J))
+            window = [[g] * P for g in range(NG)]
             n_win = [int(prev_n)] + [int(sizes[g]) for g in range(J - 1)]
         self.NG = NG
+        self.gmap_host = gmap
         self.gmap = torch.tensor(gmap, dtype=torch.int32, device=device)
+        self.plan_window = [window[g][c] for g in range(NG) for c in range(P)]  # by plan p = g * P + c
         specs = []
         for g in range(NG):
-            for cand in wl.candidates:
-                specs.append((g, cand.W, n_win[g], cand.a * n_win[g], cand.b * R))
-        self.plans = B.PlanSet(specs, P, R, self.max_W, K, NG, device)
-        self.ws_admit = torch.empty(B.cr_admit_workspace_bytes(NG, R, self.max_W), dtype=torch.uint8, device=device)
+            for c, cand in enumerate(wl.candidates):
+                w = window[g][c]
+                specs.append((w, cand.W, n_win[w], cand.a * n_win[w], cand.b * R))
+        self.NW = self.win_src.shape[0]  # counts rows the plans are built from
+        self.plans = B.PlanSet(specs, P, R, self.max_W, K, self.NW, device)
+        self.ws_admit = torch.empty(B.cr_admit_workspace_bytes(self.NW, R, self.max_W), dtype=torch.uint8,
+                                    device=device)
         self.ws_replay = torch.empty(B.cr_replay_workspace_bytes(wl.n, P, R), dtype=torch.uint8, device=device)
         self.dest = torch.empty((P, max(wl.n, 1)), dtype=torch.int16, device=device)
-        self.stats = torch.zeros((J, P, R, 4), dtype=torch.int64, device=device)
+        soff = getattr(wl, "stat_offsets", None)
+        if soff is None:
+            self.stat_off, self.JS = self.inp.off, J
+        else:
+            soff = np.asarray(soff, dtype=np.uint64)
+            if soff.ndim != 1 or soff.shape[0] < 2 or soff[0] != 0 or soff[-1] != wl.n or np.any(np.diff(soff.astype(np.int64)) < 0):
+                raise ValueError("stat_offsets must rise from 0 to n")
+            self.stat_off = torch.from_numpy(soff.view(np.int64).copy()).to(device)
+            self.JS = soff.shape[0] - 1
+        self.stats = torch.zeros((self.JS, P, R, 4), dtype=torch.int64, device=device)
+        self.churn_pairs = None
+        self.churn_out = None
         self.lru_in = lru_in
         self.lru_out = torch.empty((P, R, self.max_W), **i32)
         self.first_index = wl.first_index  # global index of the chunk's first request
@@ -114,19 +148,30 @@ class Pipeline:
                    self.dest, self.err, stream, n=self.n)
 
     def partition(self, stream=None):
-        B.cr_replay_partition(self.inp.keys, self.inp.suffix, self.dest, self.inp.off, self.J, self.P, self.R,
+        B.cr_replay_partition(self.inp.keys, self.inp.suffix, self.dest, self.stat_off, self.JS, self.P, self.R,
                               self.Ws, self.ws_replay, self.err, stream, n=self.n)
         self.stats.zero_()  # cr_replay_lru accumulates into it (cleared here so that lru is one kernel)
 
     def lru(self, stream=None):
-        B.cr_replay_lru(self.inp.prefix_len, self.K, self.n, self.J, self.P, self.R, self.Ws, self.max_W,
+        B.cr_replay_lru(self.inp.prefix_len, self.K, self.n, self.JS, self.P, self.R, self.Ws, self.max_W,
                         self.lru_in, self.lru_out, self.stats, self.ws_replay, self.err, stream)
 
     def replay(self, stream=None):
         self.stats.zero_()
-        B.cr_replay(self.inp.keys, self.inp.suffix, self.inp.prefix_len, self.K, self.dest, self.inp.off, self.J,
+        B.cr_replay(self.inp.keys, self.inp.suffix, self.inp.prefix_len, self.K, self.dest, self.stat_off, self.JS,
                     self.P, self.R, self.Ws, self.max_W, self.lru_in, self.lru_out, self.stats, self.ws_replay,
                     self.err, stream, n=self.n)
+
+    def set_churn_pairs(self, pairs):
+        """Plan pairs (p, q), p = group * P + candidate, whose churn ``churn`` measures."""
+        pr = np.asarray(pairs, dtype=np.int64).reshape(-1, 2)
+        if pr.size and (pr.min() < 0 or pr.max() >= self.plans.num_plans):
+            raise ValueError("churn pair names a plan outside the set")
+        self.churn_pairs = torch.from_numpy(pr.astype(np.int32)).to(self.device)
+        self.churn_out = torch.empty((pr.shape[0], 4), dtype=torch.int64, device=self.device)
+
+    def churn(self, stream=None):
+        B.cr_plan_churn(self.plans.c, self.churn_pairs, self.churn_out, self.err, stream)
 
     STAGES = ("count", "admit", "place", "route", "partition", "lru")
 
@@ -145,13 +190,14 @@ class Pipeline:
                     members=ps.members.cpu().numpy().view(np.uint16), load=ps.load.cpu().numpy(),
                     route=u32(ps.route), dest=self.dest[:, : self.n].cpu().numpy().view(np.uint16),
                     stats=self.stats.cpu().numpy().view(np.uint64), lru=u32(self.lru_out),
-                    err=int(self.err.cpu().numpy().view(np.uint32)[0]))
+                    err=int(self.err.cpu().numpy().view(np.uint32)[0]),
+                    churn=None if self.churn_out is None else self.churn_out.cpu().numpy().view(np.uint64))
 
     def plan_of(self, h: dict, g: int, c: int) -> dict:
         """Admitted keys, k and members of plan (group g, candidate c) from host views."""
         p = g * self.P + c
         A = int(h["num_admitted"][p])
-        w = g
+        w = self.plan_window[p]
         mo = h["member_off"][p, : A + 1]
         return dict(adm_keys=h["order"][w, :A].copy(), adm_k=np.diff(mo).astype(np.uint32),
                     member_off=mo.copy(), members=h["members"][p, : int(mo[A]) if A else 0].copy(),

@@ -28,7 +28,7 @@ from typing import List, Optional, Sequence, Tuple
 import numpy as np
 
 # Stream tags for SeedSequence children (fixed forever: changing them changes inputs).
-_S_PERM, _S_PREFIX, _S_KEYS, _S_SUFFIX, _S_ARRIVAL, _S_BURST = 1, 2, 3, 4, 5, 6
+_S_PERM, _S_PREFIX, _S_KEYS, _S_SUFFIX, _S_ARRIVAL, _S_BURST, _S_DRIFT = 1, 2, 3, 4, 5, 6, 7
 
 SUFFIX_LO, SUFFIX_HI = 50, 400
 
@@ -56,6 +56,11 @@ class Workload:
     seed: int = 1             # P2C / hash seed
     first_index: int = 0      # global index of keys[0] in the whole stream
     meta: dict = field(default_factory=dict)
+    # plan_windows[j][c]: the counting window whose counts build candidate c's plan for
+    # interval j (None = window j-1, and window 0 for interval 0)
+    plan_windows: Optional[np.ndarray] = None
+    # finer boundaries for the replay statistics (None = the control intervals)
+    stat_offsets: Optional[np.ndarray] = None
 
     @property
     def n(self) -> int:
@@ -236,6 +241,48 @@ def burst(seed: int = 2, n: int = 50_000_000, J: int = 100, num_keys: int = 50_0
     return Workload(name=name, num_keys=num_keys, R=R, candidates=[Candidate(W)], keys=keys,
                     suffix=suffix, prefix_len=plen, offsets=offsets, seed=1,
                     meta=dict(interval_s=10.0, seed=seed, burst_keys=bkeys, burst_start=bstart))
+
+
+def drift(seed: int = 2, n_per: int = 1_000_000, steps: int = 6, sigma: float = 0.3,
+          num_keys: int = 20_000, R: int = 30, W: int = 64, bins_per_interval: int = 100) -> Workload:
+    """Rate drift (Section 5.4, Appendix E): the 70B-like key distribution evolves for
+    ``steps`` intervals by a lognormal random walk, w_t(b) = w_{t-1}(b) exp(sigma z),
+    z ~ N(0, 1) per key and step, starting from the base shares; interval t draws
+    ``n_per`` keys iid from w_t / sum(w_t).
+
+    Candidates (all W slots, q_cap = mean load) differ only in the window their plans
+    come from: candidate 0 is fresh (interval j uses window j's own counts, the rate
+    vector of that interval); candidate t >= 1 is the same except that interval t keeps
+    the plan of window t-1, so it shares candidate 0's history up to the boundary and
+    stays warm after it. Replay statistics are kept in ``bins_per_interval`` equal bins
+    per interval so the rewarming transient after each install is visible."""
+    name = "drift"
+    tag = _tag(name)
+    perm = _rng(seed, tag, _S_PERM).permutation(num_keys)
+    w = np.empty(num_keys)
+    w[perm] = water_fill(zipf_probs(num_keys, 1.0), 0.003)  # per key id
+    zr = _rng(seed, tag, _S_DRIFT)
+    krng = _rng(seed, tag, _S_KEYS)
+    n = n_per * steps
+    keys = np.empty(n, dtype=np.uint32)
+    shares = np.empty((steps, num_keys))
+    for t in range(steps):
+        if t:
+            w = w * np.exp(sigma * zr.standard_normal(num_keys))
+        shares[t] = w / w.sum()
+        keys[t * n_per:(t + 1) * n_per] = CategoricalSampler(shares[t]).sample(krng, n_per).astype(np.uint32)
+    offsets = (np.arange(steps + 1, dtype=np.uint64) * np.uint64(n_per))
+    bins = np.linspace(0, n, steps * bins_per_interval + 1)
+    stat_offsets = np.rint(bins).astype(np.uint64)
+    pw = np.tile(np.arange(steps, dtype=np.int64)[:, None], (1, steps))
+    for t in range(1, steps):
+        pw[t, t] = t - 1
+    suffix = _suffixes(_rng(seed, tag, _S_SUFFIX), n)
+    plen = _prefix_lengths(seed, tag, num_keys, 3000.0, 0.7)
+    return Workload(name=name, num_keys=num_keys, R=R, candidates=[Candidate(W) for _ in range(steps)],
+                    keys=keys, suffix=suffix, prefix_len=plen, offsets=offsets, seed=1,
+                    meta=dict(seed=seed, sigma=sigma, shares=shares, bins_per_interval=bins_per_interval),
+                    plan_windows=pw, stat_offsets=stat_offsets)
 
 
 SWEEP_W = (8, 14, 26, 48, 86, 156, 283, 512)

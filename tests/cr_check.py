@@ -28,13 +28,21 @@ def compare_plan(gpl: dict, opl: dict, where: str):
     assert np.array_equal(gpl["L"].view(np.uint64), opl["L"].view(np.uint64)), f"{where}: loads not bit-identical"
 
 
-def compare_all(wl, gp, h: dict, orc: dict, win_to_group=None):
-    """Full element-by-element comparison of a device pipeline run with the oracle's."""
+def compare_all(wl, gp, h: dict, orc: dict):
+    """Full element-by-element comparison of a device pipeline run with the oracle's:
+    every (plan group, candidate) the device routes with against the oracle's plan for
+    the same interval and candidate."""
     assert h["err"] == 0, f"device error word {h['err']:#x}"
     np.testing.assert_array_equal(h["counts"], orc["counts"], err_msg="counts")
-    for (w, c), opl in orc["plans"].items():
-        g = w if win_to_group is None else win_to_group[w]
-        compare_plan(gp.plan_of(h, g, c), opl, f"plan window {w} cand {c}")
+    seen = set()
+    for j in range(wl.J):
+        g = gp.gmap_host[j]
+        for c in range(wl.P):
+            if (g, c) in seen:
+                continue
+            seen.add((g, c))
+            w = orc["win_of"][j][c]
+            compare_plan(gp.plan_of(h, g, c), orc["plans"][(w, c)], f"interval {j} cand {c} (window {w})")
     np.testing.assert_array_equal(h["dest"], orc["dest"], err_msg="dest")
     np.testing.assert_array_equal(h["stats"], orc["stats"], err_msg="replay stats")
     for c, cand in enumerate(wl.candidates):

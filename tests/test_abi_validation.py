@@ -44,6 +44,16 @@ def test_plan_set_rejects(L, kw):
     ps = _set(**kw)
     assert L.cr_admit(FAKE, ctypes.byref(ps), FAKE, 1 << 40, FAKE, None) == B.CR_EINVAL
     assert L.cr_place_lpt(FAKE, ctypes.byref(ps), None) == B.CR_EINVAL
+    assert L.cr_plan_churn(ctypes.byref(ps), FAKE, 1, FAKE, FAKE, None) == B.CR_EINVAL
+
+
+def test_churn_rejects(L):
+    ps = _set()
+    assert L.cr_plan_churn(ctypes.byref(ps), None, 1, FAKE, FAKE, None) == B.CR_EINVAL     # pairs NULL
+    assert L.cr_plan_churn(ctypes.byref(ps), FAKE, 1, None, FAKE, None) == B.CR_EINVAL     # out NULL
+    assert L.cr_plan_churn(ctypes.byref(ps), FAKE, 1, FAKE, None, None) == B.CR_EINVAL     # err NULL
+    assert L.cr_plan_churn(None, FAKE, 1, FAKE, FAKE, None) == B.CR_EINVAL
+    assert L.cr_plan_churn(ctypes.byref(ps), None, 0, None, FAKE, None) == B.CR_OK         # no pairs: no-op
 
 
 def test_admit_workspace_too_small(L):
