@@ -8,8 +8,12 @@ cache state, and is counted, planned, routed and partitioned on one HIP stream w
 k-1 replays on another (--schedule serial: every step from scratch on one stream). Inputs
 are resident in HBM before timing starts. Prints ONE JSON line.
 
-  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload llama70b|tiny|replication|burst]
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload llama70b|tiny|replication|burst|drift]
                   [--schedule overlap|serial]
+
+--workload drift times the replanning study instead (six drift intervals of 1e6 requests,
+fresh and held plans as six candidates, 600 statistics bins, churn between consecutive
+fresh plans) and adds its per-transition report under "study".
 """
 from __future__ import annotations
 
@@ -112,6 +116,9 @@ def describe(name, wl):
                            "16 x 128 slots; q_cap = 0.4 x mean",
             "burst": "Burst: 50,000 keys Zipf(1.2), 5% keys 10x for 20 s; 5e7 requests, 100 x 10-s intervals; "
                      "64 x 64 slots",
+            "drift": "Replanning under drift: 70B-like keys, lognormal random walk sigma 0.3 over 6 intervals "
+                     "of 1e6 requests; 6 candidates (fresh plan, and the plan held one interval at each "
+                     "boundary); 30 x 64 slots; 600 statistics bins; churn of consecutive fresh plans",
         }.get(name, name),
         "requests": wl.n, "intervals": wl.J, "plan_builds": None, "keys": wl.num_keys, "destinations": wl.R,
         "slots": [c.W for c in wl.candidates], "candidates": wl.P,
@@ -136,13 +143,20 @@ def main():
     wl = workload.CONFIGS[args.workload]()
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
+    study = None
     stages = Pipeline.STAGES
+    if args.workload == "drift":
+        from paper_2608_19677_amd.replan import DriftStudy
+        study = DriftStudy(wl, device="cuda:0")
+        stages = DriftStudy.STAGES
+        args.schedule = "serial"  # its plans come from named windows, not from the previous chunk
     ev = {s: [] for s in stages}
     if args.schedule == "serial":
-        gp = Pipeline(wl, device="cuda:0")
+        gp = study.pipe if study is not None else Pipeline(wl, device="cuda:0")
         stream = torch.cuda.current_stream()
         for _ in range(args.warmup):
-            gp.step()
+            for s in stages:
+                getattr(gp, s)()
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         for _ in range(args.steps):
@@ -180,7 +194,7 @@ def main():
     # the partition stage; count, place, route and lru each launch exactly one kernel here).
     kern = {
         # counting reads every key and writes the dense [J][K] counts matrix it defines
-        "count": dict(kernel="k_count_owner", bound="hbm", unit="GB/s", work=4.0 * n + 4.0 * wl.J * wl.num_keys,
+        "count": dict(kernel="k_count_*", bound="hbm", unit="GB/s", work=4.0 * n + 4.0 * wl.J * wl.num_keys,
                       peak=HBM_PEAK_GBS),
         "route": dict(kernel="k_route<true>", bound="hbm", unit="GB/s", work=(4.0 + 2.0 * P) * n, peak=HBM_PEAK_GBS),
         # LPT: every job copy is compared against the R destination loads.
@@ -226,6 +240,9 @@ def main():
     }
     out["config"]["plan_builds"] = n_plans
     out["config"]["schedule"] = args.schedule
+    if study is not None:
+        out["study"] = study.summary()
+        out["kernels"]["churn"] = {"ms": stage_ms["churn"], "kernel": "k_plan_churn"}
 
     if args.calib_copy_mb:
         nb = args.calib_copy_mb << 20

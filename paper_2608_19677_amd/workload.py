@@ -322,6 +322,7 @@ CONFIGS = {
     "llama70b": llama70b,
     "replication": replication,
     "burst": burst,
+    "drift": drift,
 }
 
 
