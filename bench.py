@@ -13,7 +13,9 @@ are resident in HBM before timing starts. Prints ONE JSON line.
 
 --workload drift times the replanning study instead (six drift intervals of 1e6 requests,
 fresh and held plans as six candidates, 600 statistics bins, churn between consecutive
-fresh plans) and adds its per-transition report under "study".
+fresh plans) and adds its per-transition report under "study". --workload ablation times
+the component ablation (the injected-whale stream under the flat, affinity, replicated
+and full plans as four candidates) and adds the hit and imbalance of each under "study".
 """
 from __future__ import annotations
 
@@ -116,6 +118,9 @@ def describe(name, wl):
                            "16 x 128 slots; q_cap = 0.4 x mean",
             "burst": "Burst: 50,000 keys Zipf(1.2), 5% keys 10x for 20 s; 5e7 requests, 100 x 10-s intervals; "
                      "64 x 64 slots",
+            "ablation": "Component ablation: 5,000 Zipf(1.1) + 8 keys at 6%; 2e7 requests, 60-s intervals; "
+                        "16 x 128 slots; q_cap = 0.4 x mean; candidates flat, affinity (k = 1, hash placement), "
+                        "replicated (Eq. 1, hash placement), full (Eq. 1, LPT)",
             "drift": "Replanning under drift: 70B-like keys, lognormal random walk sigma 0.3 over 6 intervals "
                      "of 1e6 requests; 6 candidates (fresh plan, and the plan held one interval at each "
                      "boundary); 30 x 64 slots; 600 statistics bins; churn of consecutive fresh plans",
@@ -243,6 +248,9 @@ def main():
     if study is not None:
         out["study"] = study.summary()
         out["kernels"]["churn"] = {"ms": stage_ms["churn"], "kernel": "k_plan_churn"}
+    if args.workload == "ablation":
+        from paper_2608_19677_amd.report import ablation_summary
+        out["study"] = ablation_summary(wl, h["stats"], h["load"], last.gmap_host)
 
     if args.calib_copy_mb:
         nb = args.calib_copy_mb << 20

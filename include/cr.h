@@ -50,15 +50,33 @@ typedef int32_t cr_status;
 #define CR_MAX_CANDS 256   /* candidate plans per group                        */
 #define CR_MAX_J 65535     /* control intervals per cr_replay call             */
 
+/* Plan variants: the method and the stages of the paper's component ablation (Section 5.2,
+ * 8B component ablation table), each a plan the same dispatch and replay can run.
+ *   CR_PLAN_FULL        Eq. 1 replication and LPT placement (Algorithm 1)
+ *   CR_PLAN_AFFINITY    k = 1 for every admitted key (top C keys), hash placement
+ *   CR_PLAN_REPLICATED  Eq. 1 replication, hash placement
+ *   CR_PLAN_FLAT        nothing admitted: every request takes the cold path, and with
+ *                       uniform planned loads that is plain hashing (load balancing alone)
+ * Hash placement gives key b the k destinations with the smallest (u(b, r), r), listed in
+ * that order, where u(b, r) = fmix32(fmix32(b ^ t) ^ r), t = fmix32(place_seed ^ 0x7F4A7C15):
+ * a uniformly random k-subset per key, independent of the loads. Every variant charges
+ * count / k to each member after L[r] = cold / R, in admission order, as LPT does. */
+#define CR_PLAN_FULL 0u
+#define CR_PLAN_AFFINITY 1u
+#define CR_PLAN_REPLICATED 2u
+#define CR_PLAN_FLAT 3u
+
 /* One plan problem (Algorithm 1 inputs: rates, R, q_cap, C). Arrays of these live in
  * DEVICE memory. q_cap = q_num / q_den requests per window, so Eq. 1 is evaluated as
  * k = max(1, ceil(c * q_den / q_num)) in exact integers; k is clamped to R. */
 typedef struct {
-    uint32_t window;   /* row of counts the plan is built from (< num_windows)      */
-    uint32_t W;        /* warm slots per destination, 1..max_W; C = R * W           */
-    uint64_t n_window; /* requests in that row (its sum)                            */
-    uint64_t q_num;    /* > 0 unless n_window == 0                                  */
-    uint64_t q_den;    /* 1 .. 2^31 - 1                                             */
+    uint32_t window;     /* row of counts the plan is built from (< num_windows)      */
+    uint32_t W;          /* warm slots per destination, 1..max_W; C = R * W           */
+    uint64_t n_window;   /* requests in that row (its sum)                            */
+    uint64_t q_num;      /* > 0 unless n_window == 0 (unused by AFFINITY and FLAT)   */
+    uint64_t q_den;      /* 1 .. 2^31 - 1 (likewise)                                  */
+    uint32_t variant;    /* CR_PLAN_*                                                 */
+    uint32_t place_seed; /* hash placement seed (AFFINITY, REPLICATED)                */
 } cr_plan_spec;
 
 /* A set of NP plans arranged as NG groups of `cands` candidates: plan p = g*cands + c.
@@ -120,9 +138,10 @@ size_t cr_admit_workspace_bytes(uint32_t num_windows, uint32_t R, uint32_t max_W
  * prefix of that order whose k_b sum is <= C = R * W; cold = n_window - admitted counts.
  * counts u32 [num_windows][num_keys]. Writes order, order_count, n_order, num_admitted,
  * cold, clamped, member_off[0..A] (prefix sums of k) and the plan's whole key_index
- * (its admitted keys are order[window][0..A)). A spec with a window out of range,
- * q_num == 0 on a nonempty window, or n_window != row sum sets CR_ERR_SPEC (the plan
- * then admits nothing). */
+ * (its admitted keys are order[window][0..A)). CR_PLAN_AFFINITY takes k = 1 for every key
+ * and CR_PLAN_FLAT admits nothing. A spec with a window out of range, q_num == 0 on a
+ * nonempty window (FULL, REPLICATED), n_window != row sum or an unknown variant sets
+ * CR_ERR_SPEC (the plan then admits nothing). */
 cr_status cr_admit(const uint32_t* counts, const cr_plan_set* plans, void* ws, size_t ws_bytes,
                    uint32_t* err, void* stream);
 
@@ -130,8 +149,16 @@ cr_status cr_admit(const uint32_t* counts, const cr_plan_set* plans, void* ws, s
  * Per plan: L[r] = cold / R; admitted keys in admission order take the k smallest
  * (L[r], r) destinations, listed in that order, each charged count / k (IEEE double,
  * one rounding per operation, the same order as the definition). Writes members,
- * load and route[0..A) (it reads key_index as cr_admit left it). */
+ * load and route[0..A) (it reads key_index as cr_admit left it). Plans of the hash-placed
+ * variants (CR_PLAN_AFFINITY, CR_PLAN_REPLICATED) are left to cr_place_hash. */
 cr_status cr_place_lpt(const uint32_t* counts, const cr_plan_set* plans, void* stream);
+
+/* Hash placement of the ablation variants CR_PLAN_AFFINITY and CR_PLAN_REPLICATED (Section
+ * 5.2): members are each key's k smallest (u(b, r), r) (see CR_PLAN_*), and the loads
+ * L[r] = cold / R + the count / k of every admitted key placed on r, added in admission
+ * order (IEEE double, as cr_place_lpt). Writes members, load and route[0..A) of those plans
+ * and leaves the others untouched. Cost: R hashes per admitted key and k passes over them. */
+cr_status cr_place_hash(const uint32_t* counts, const cr_plan_set* plans, void* stream);
 
 /* Dispatch (Section 3.1 "Placement and dispatch"; Fig. 1), order-independent form.
  * Request i lies in interval j and uses plan group gmap[j]; for candidate c:

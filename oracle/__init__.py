@@ -51,8 +51,11 @@ def lib():
         L.cro_hash.argtypes = [u64, u64]
         L.cro_hash.restype = u32
         L.cro_route.argtypes = [P, u64, u64, u64, u32, u32, P, u32, P, P, P, P, P]
+        L.cro_place_u.argtypes = [u32, u32, u32]
+        L.cro_place_u.restype = u32
+        L.cro_place_hash.argtypes = [P, P, u32, P, u32, u64, u32, P, P, P]
         L.cro_replay.argtypes = [P, P, P, u32, P, u64, P, u32, u32, u32, P, P, P]
-        for f in (L.cro_count_rates, L.cro_admit, L.cro_place_lpt, L.cro_route, L.cro_replay):
+        for f in (L.cro_count_rates, L.cro_admit, L.cro_place_lpt, L.cro_place_hash, L.cro_route, L.cro_replay):
             f.restype = ctypes.c_int
         _lib = L
     return _lib
@@ -111,6 +114,36 @@ def place_lpt(adm_keys, adm_k, counts_row, R: int, cold: int):
     L = np.zeros(R, dtype=np.float64)
     _check(lib().cro_place_lpt(_p(adm_keys), _p(adm_k), A, _p(row), R, cold, _p(members), _p(off), _p(L)),
            "place_lpt")
+    return members[: int(off[A])].copy(), off, L
+
+
+def admit_affinity(counts_row, R: int, W: int, n_window: int):
+    """Admission of the ablation's affinity stage (Section 5.2): every key takes one slot,
+    so the admitted keys are the first min(C, nnz) nonzero keys by (count desc, key asc).
+    Returns (adm_keys, adm_k, cold)."""
+    row = np.asarray(counts_row, dtype=np.int64)
+    nz = np.nonzero(row)[0]
+    order = nz[np.lexsort((nz, -row[nz]))]
+    adm = order[: R * W].astype(np.uint32)
+    cold = int(n_window) - int(row[adm].sum())
+    return adm, np.ones(adm.shape[0], dtype=np.uint32), cold
+
+
+def place_u(seed: int, b: int, r: int) -> int:
+    return int(lib().cro_place_u(seed & 0xFFFFFFFF, b & 0xFFFFFFFF, r & 0xFFFFFFFF))
+
+
+def place_hash(adm_keys, adm_k, counts_row, R: int, cold: int, seed: int):
+    """Hash placement (ablation): returns (members, member_off, L) like place_lpt."""
+    adm_keys = _c(adm_keys, np.uint32)
+    adm_k = _c(adm_k, np.uint32)
+    row = _c(counts_row, np.uint32)
+    A = adm_keys.shape[0]
+    members = np.zeros(max(1, int(adm_k.sum())), dtype=np.uint16)
+    off = np.zeros(A + 1, dtype=np.uint32)
+    L = np.zeros(R, dtype=np.float64)
+    _check(lib().cro_place_hash(_p(adm_keys), _p(adm_k), A, _p(row), R, cold, seed & 0xFFFFFFFF, _p(members),
+                                _p(off), _p(L)), "place_hash")
     return members[: int(off[A])].copy(), off, L
 
 

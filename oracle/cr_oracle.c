@@ -214,6 +214,64 @@ uint32_t cro_hash(uint64_t seed, uint64_t i)
 }
 
 /* ------------------------------------------------------------------------ */
+/* Hash placement, the "random placement" stages of the component ablation */
+/* (Section 5.2, 8B component ablation table). Key b's k members are a      */
+/* uniformly random k-subset of the destinations: the k smallest (u, r) of  */
+/* u(b, r) = fmix32(fmix32(b ^ t) ^ r), t = fmix32(seed ^ 0x7F4A7C15),      */
+/* listed in that order. Loads start at cold / R and each member is charged */
+/* c / k in admission order, as in LPT; only the choice of members differs. */
+/* ------------------------------------------------------------------------ */
+uint32_t cro_place_u(uint32_t seed, uint32_t b, uint32_t r)
+{
+    uint32_t t = cro_fmix32(seed ^ 0x7F4A7C15u);
+    return cro_fmix32(cro_fmix32(b ^ t) ^ r);
+}
+
+int cro_place_hash(const uint32_t* adm_keys, const uint32_t* adm_k, uint32_t A,
+                   const uint32_t* counts_row, uint32_t R, uint64_t cold, uint32_t seed,
+                   uint16_t* members, uint32_t* member_off, double* L)
+{
+    if (R == 0 || R > 65535) return -1;
+    unsigned char* taken = (unsigned char*)calloc(R, 1);
+    if (!taken) return -2;
+    double init = (double)cold / (double)R;
+    for (uint32_t r = 0; r < R; ++r) L[r] = init;
+    uint32_t off = 0;
+    for (uint32_t a = 0; a < A; ++a) {
+        uint32_t b = adm_keys[a], k = adm_k[a];
+        if (k < 1 || k > R) {
+            free(taken);
+            return -1;
+        }
+        double x = (double)counts_row[b] / (double)k;
+        member_off[a] = off;
+        for (uint32_t t = 0; t < k; ++t) {
+            int64_t best = -1;
+            uint32_t ubest = 0;
+            for (uint32_t r = 0; r < R; ++r) {
+                if (taken[r]) continue;
+                uint32_t u = cro_place_u(seed, b, r);
+                if (best < 0 || u < ubest) {
+                    best = r;
+                    ubest = u;
+                }
+            }
+            members[off + t] = (uint16_t)best;
+            taken[best] = 1;
+        }
+        for (uint32_t t = 0; t < k; ++t) {
+            uint32_t r = members[off + t];
+            L[r] = L[r] + x;
+            taken[r] = 0;
+        }
+        off += k;
+    }
+    member_off[A] = off;
+    free(taken);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
 /* Dispatch through one fixed plan (Section 3.1 "Placement and dispatch";   */
 /* Fig. 1). Request i has global index first_index + i and h = hash(seed,   */
 /* that index). Order-independent reading:                                   */

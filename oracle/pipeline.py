@@ -9,6 +9,10 @@ Semantics it fixes (each restated from the paper or from the reading noted):
 * A workload may name the window of every (interval, candidate) plan itself
   (``plan_windows``), as the replanning study does to compare fresh and stale
   plans (Section 5.4, Appendix E).
+* A candidate may be a stage of the component ablation (Section 5.2): "flat"
+  admits nothing, "affinity" admits the top C keys with one copy each and
+  places them by hash, "replicated" keeps Eq. 1 and places by hash, "full" is
+  the method.
 * Candidate (W, a, b) has C = R W warm slots and q_cap = (a/b) x N_w / R,
   i.e. q_num = a N_w and q_den = b R with N_w the window's request count.
 * The replay's LRU state per (candidate, destination) starts empty and is
@@ -23,7 +27,7 @@ from typing import Dict, List, Optional, Tuple
 
 import numpy as np
 
-from . import admit, count_rates, place_lpt, replay, route
+from . import admit, admit_affinity, count_rates, place_hash, place_lpt, replay, route
 
 
 def plan_window(j: int) -> int:
@@ -37,14 +41,23 @@ def build_plans(counts: np.ndarray, R: int, candidates, pairs: List[Tuple[int, i
         row = counts[w]
         n_w = int(row.sum(dtype=np.uint64))
         cand = candidates[c]
+        variant = getattr(cand, "variant", "full")
         q_num, q_den = cand.a * n_w, cand.b * R
-        if n_w == 0:
+        if n_w == 0 or variant == "flat":
             adm_keys = np.zeros(0, np.uint32)
             adm_k = np.zeros(0, np.uint32)
-            cold, clamped = 0, 0
-        else:
+            cold, clamped = n_w, 0
+        elif variant == "affinity":
+            adm_keys, adm_k, cold = admit_affinity(row, R, cand.W, n_w)
+            clamped = 0
+        elif variant in ("full", "replicated"):
             adm_keys, adm_k, cold, clamped = admit(row, R, cand.W, n_w, q_num, q_den)
-        members, member_off, L = place_lpt(adm_keys, adm_k, row, R, cold)
+        else:
+            raise ValueError(f"unknown plan variant {variant!r}")
+        if variant in ("affinity", "replicated"):
+            members, member_off, L = place_hash(adm_keys, adm_k, row, R, cold, cand.place_seed)
+        else:
+            members, member_off, L = place_lpt(adm_keys, adm_k, row, R, cold)
         plans[(w, c)] = dict(adm_keys=adm_keys, adm_k=adm_k, cold=cold, clamped=clamped,
                              members=members, member_off=member_off, L=L, n_window=n_w)
     return plans

@@ -22,14 +22,21 @@ CR_EMPTY_SLOT = 0xFFFFFFFF
 CR_ROUTE_SINGLE = 0x80000000
 CR_MAX_R, CR_MAX_W, CR_MAX_CANDS, CR_MAX_J = 1024, 512, 256, 65535
 
-EXPORTS = ("cr_count_rates", "cr_admit_workspace_bytes", "cr_admit", "cr_place_lpt", "cr_route", "cr_plan_churn",
+EXPORTS = ("cr_count_rates", "cr_admit_workspace_bytes", "cr_admit", "cr_place_lpt", "cr_place_hash", "cr_route",
+           "cr_plan_churn",
            "cr_replay_workspace_bytes", "cr_replay", "cr_replay_partition", "cr_replay_lru", "cr_version")
 
 _u32, _u64, _P = ctypes.c_uint32, ctypes.c_uint64, ctypes.c_void_p
 
 
+CR_PLAN_FULL, CR_PLAN_AFFINITY, CR_PLAN_REPLICATED, CR_PLAN_FLAT = 0, 1, 2, 3
+PLAN_VARIANTS = {"full": CR_PLAN_FULL, "affinity": CR_PLAN_AFFINITY, "replicated": CR_PLAN_REPLICATED,
+                 "flat": CR_PLAN_FLAT}
+
+
 class CrPlanSpec(ctypes.Structure):
-    _fields_ = [("window", _u32), ("W", _u32), ("n_window", _u64), ("q_num", _u64), ("q_den", _u64)]
+    _fields_ = [("window", _u32), ("W", _u32), ("n_window", _u64), ("q_num", _u64), ("q_den", _u64),
+                ("variant", _u32), ("place_seed", _u32)]
 
 
 class CrPlanSet(ctypes.Structure):
@@ -60,6 +67,7 @@ def load(path: Optional[str] = None):
     L.cr_admit_workspace_bytes.restype = ctypes.c_size_t
     L.cr_admit.argtypes = [_P, ctypes.POINTER(CrPlanSet), _P, ctypes.c_size_t, _P, _P]
     L.cr_place_lpt.argtypes = [_P, ctypes.POINTER(CrPlanSet), _P]
+    L.cr_place_hash.argtypes = [_P, ctypes.POINTER(CrPlanSet), _P]
     L.cr_route.argtypes = [_P, _u64, _u64, _u64, _P, _P, _u32, ctypes.POINTER(CrPlanSet), _P, _P, _P]
     L.cr_plan_churn.argtypes = [ctypes.POINTER(CrPlanSet), _P, _u32, _P, _P, _P]
     L.cr_replay_workspace_bytes.argtypes = [_u64, _u32, _u32]
@@ -71,7 +79,7 @@ def load(path: Optional[str] = None):
     L.cr_replay_lru.argtypes = [_P, _u32, _u64, _u32, _u32, _u32, ctypes.POINTER(_u32), _u32, _P, _P, _P, _P,
                                 ctypes.c_size_t, _P, _P]
     L.cr_version.restype = ctypes.c_char_p
-    for f in ("cr_count_rates", "cr_admit", "cr_place_lpt", "cr_route", "cr_plan_churn", "cr_replay",
+    for f in ("cr_count_rates", "cr_admit", "cr_place_lpt", "cr_place_hash", "cr_route", "cr_plan_churn", "cr_replay",
               "cr_replay_partition", "cr_replay_lru"):
         getattr(L, f).restype = ctypes.c_int32
     _lib = L
@@ -119,6 +127,10 @@ def cr_admit(counts, plans: CrPlanSet, ws, err, stream=None):
 
 def cr_place_lpt(counts, plans: CrPlanSet, stream=None):
     _check(load().cr_place_lpt(_ptr(counts), ctypes.byref(plans), _stream(stream)), "cr_place_lpt")
+
+
+def cr_place_hash(counts, plans: CrPlanSet, stream=None):
+    _check(load().cr_place_hash(_ptr(counts), ctypes.byref(plans), _stream(stream)), "cr_place_hash")
 
 
 def cr_route(keys, first_index: int, seed: int, off, gmap, J: int, plans: CrPlanSet, dest, err, stream=None,

@@ -22,6 +22,11 @@ namespace {
 constexpr int kSortThreads = 1024;
 constexpr int kSortWaves = kSortThreads / kWave;
 
+__host__ __device__ __forceinline__ bool hash_placed(uint32_t variant)
+{
+    return variant == CR_PLAN_AFFINITY || variant == CR_PLAN_REPLICATED;
+}
+
 __device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v)
 {
 #pragma unroll
@@ -659,10 +664,12 @@ __global__ __launch_bounds__(kSortThreads) void k_admit_plan(
     const cr_plan_spec spec = specs[p];
     uint32_t* __restrict__ moff = member_off + (uint64_t)p * (Cmax + 1u);
     uint64_t* __restrict__ kx = key_index + (uint64_t)p * 2u * KW;
-    bool ok = spec.window < NW && spec.W >= 1 && (uint64_t)R * spec.W <= Cmax;
-    const uint32_t M = ok ? n_order[spec.window] : 0u;
+    const bool eq1 = spec.variant == CR_PLAN_FULL || spec.variant == CR_PLAN_REPLICATED;
+    bool ok = spec.window < NW && spec.W >= 1 && (uint64_t)R * spec.W <= Cmax && spec.variant <= CR_PLAN_FLAT;
+    // the flat variant admits nothing: its whole window is cold
+    const uint32_t M = ok && spec.variant != CR_PLAN_FLAT ? n_order[spec.window] : 0u;
     if (ok && spec.n_window != row_sum[spec.window]) ok = false;
-    if (ok && M > 0 && (spec.q_num == 0 || spec.q_den == 0 || spec.q_den >= (1ull << 31))) ok = false;
+    if (ok && eq1 && M > 0 && (spec.q_num == 0 || spec.q_den == 0 || spec.q_den >= (1ull << 31))) ok = false;
     if (!ok) {
         if (tid == 0) {
             num_admitted[p] = 0;
@@ -685,7 +692,9 @@ __global__ __launch_bounds__(kSortThreads) void k_admit_plan(
         const uint32_t c = valid ? ocnt[a] : 0u;
         uint32_t k = 0;
         bool cl = false;
-        if (valid) {
+        if (valid && !eq1) {
+            k = 1;  // affinity: one copy per admitted key
+        } else if (valid) {
             const uint64_t num = (uint64_t)c * spec.q_den;
             uint64_t kk = num / spec.q_num + (num % spec.q_num != 0);
             if (kk < 1) kk = 1;
@@ -862,6 +871,7 @@ __global__ __launch_bounds__(64) void k_lpt_small(uint32_t KW, uint32_t R, uint3
     __shared__ uint32_t s_mem[128];  // member picked for single-copy job a, slot a mod 128
     const uint32_t p = blockIdx.x, lane = lane_id();
     const cr_plan_spec spec = specs[p];
+    if (hash_placed(spec.variant)) return;  // placed by cr_place_hash
     const uint32_t A = (uint32_t)__builtin_amdgcn_readfirstlane((int)num_admitted[p]);
     const uint32_t w = spec.window < NW ? spec.window : 0u;
     const uint32_t* __restrict__ ord = order + (uint64_t)w * Cmax;
@@ -1045,6 +1055,7 @@ __global__ __launch_bounds__(64) void k_lpt(uint32_t KW, uint32_t R, uint32_t Cm
 {
     const uint32_t p = blockIdx.x, lane = lane_id();
     const cr_plan_spec spec = specs[p];
+    if (hash_placed(spec.variant)) return;  // placed by cr_place_hash
     const uint32_t A = num_admitted[p];
     const uint32_t w = spec.window < NW ? spec.window : 0u;
     const uint32_t* __restrict__ ord = order + (uint64_t)w * Cmax;
@@ -1102,6 +1113,112 @@ __global__ __launch_bounds__(64) void k_lpt(uint32_t KW, uint32_t R, uint32_t Cm
         if (lane < nb) {
             if (k_l == 1) mem[cur.off] = (uint16_t)first;
             rw[kx_rank(kxc, cur.key)] = k_l == 1 ? (CR_ROUTE_SINGLE | first) : (a0 + lane);
+        }
+    }
+#pragma unroll
+    for (int s = 0; s < kS; ++s) {
+        const uint32_t r = s * 64u + lane;
+        if (r < R) load[(uint64_t)p * R + r] = Lr[s];
+    }
+}
+
+// Hash placement of the ablation variants (Section 5.2, 8B component ablation table).
+// Members do not depend on the loads, so they are found for every admitted key at once
+// (k_hash_members, one thread per key: k passes over the R hashes, each taking the
+// smallest u above the previous pick, since one key's u values are distinct); only the
+// load sums are ordered, and one wavefront per plan adds them in admission order with
+// the destinations spread over its lanes (k_hash_loads).
+constexpr uint32_t kHashThreads = 256;
+
+__device__ __forceinline__ uint32_t place_key_hash(uint32_t seed, uint32_t b)
+{
+    return fmix32(b ^ fmix32(seed ^ 0x7F4A7C15u));
+}
+
+__global__ void __launch_bounds__(kHashThreads)
+    k_hash_members(uint32_t R, uint32_t Cmax, uint32_t NW, uint32_t KW, const cr_plan_spec* __restrict__ specs,
+                   const uint32_t* __restrict__ order, const uint32_t* __restrict__ num_admitted,
+                   const uint32_t* __restrict__ member_off, const uint64_t* __restrict__ key_index,
+                   uint16_t* __restrict__ members, uint32_t* __restrict__ route)
+{
+    const uint32_t p = blockIdx.x;
+    const uint32_t variant = specs[p].variant;
+    if (!hash_placed(variant)) return;
+    const uint32_t A = min(num_admitted[p], Cmax);
+    const uint32_t a = blockIdx.y * kHashThreads + threadIdx.x;
+    if (a >= A) return;
+    const uint32_t w = min(specs[p].window, NW - 1u);  // A > 0 only for a valid window
+    const uint32_t b = order[(uint64_t)w * Cmax + a];
+    const uint32_t* __restrict__ moff = member_off + (uint64_t)p * (Cmax + 1u);
+    const uint32_t o = moff[a], k = moff[a + 1u] - o;
+    const uint32_t kb = place_key_hash(specs[p].place_seed, b);
+    uint16_t* __restrict__ mem = members + (uint64_t)p * Cmax + o;
+    uint32_t prev = 0, first = 0;
+    for (uint32_t t = 0; t < k; ++t) {
+        uint32_t best_u = 0, best_r = R;
+        for (uint32_t r = 0; r < R; ++r) {
+            const uint32_t u = fmix32(kb ^ r);
+            if ((t == 0 || u > prev) && (best_r == R || u < best_u)) {
+                best_u = u;
+                best_r = r;
+            }
+        }
+        mem[t] = (uint16_t)best_r;
+        prev = best_u;
+        if (t == 0) first = best_r;
+    }
+    const ulonglong2 e = kx_entry(key_index + (uint64_t)p * 2u * KW, b, true);
+    route[(uint64_t)p * Cmax + kx_rank(e, b)] = k == 1u ? (CR_ROUTE_SINGLE | first) : a;
+}
+
+template <int kS>
+__global__ void __launch_bounds__(64)
+    k_hash_loads(uint32_t R, uint32_t Cmax, uint32_t NW, const cr_plan_spec* __restrict__ specs,
+                 const uint32_t* __restrict__ order_count, const uint32_t* __restrict__ num_admitted,
+                 const uint64_t* __restrict__ cold, const uint32_t* __restrict__ member_off,
+                 const uint16_t* __restrict__ members, double* __restrict__ load)
+{
+    const uint32_t p = blockIdx.x, lane = lane_id();
+    const cr_plan_spec spec = specs[p];
+    if (!hash_placed(spec.variant)) return;
+    const uint32_t A = min((uint32_t)__builtin_amdgcn_readfirstlane((int)num_admitted[p]), Cmax);
+    const uint32_t w = min(spec.window, NW - 1u);
+    const uint32_t* __restrict__ ocnt = order_count + (uint64_t)w * Cmax;
+    const uint32_t* __restrict__ moff = member_off + (uint64_t)p * (Cmax + 1u);
+    const uint16_t* __restrict__ mem = members + (uint64_t)p * Cmax;
+    const double init = (double)cold[p] / (double)R;
+    double Lr[kS];
+#pragma unroll
+    for (int s = 0; s < kS; ++s) Lr[s] = init;
+    for (uint32_t base = 0; base < A; base += 64u) {
+        // lane j holds job base + j: its charge, copy count, first member and offset
+        const uint32_t a = base + lane;
+        double x = 0.0;
+        uint32_t k = 0, d = 0xFFFFu, o = 0;
+        if (a < A) {
+            o = moff[a];
+            k = moff[a + 1u] - o;
+            x = (double)ocnt[a] / (double)k;
+            d = mem[o];
+        }
+        const uint32_t nb = A - base < 64u ? A - base : 64u;
+        for (uint32_t j = 0; j < nb; ++j) {
+            const double xj = rdlane_f64(x, j);
+            const uint32_t kj = rdlane(k, j);
+            if (kj == 1u) {
+                const uint32_t dj = rdlane(d, j);
+#pragma unroll
+                for (int s = 0; s < kS; ++s)
+                    if (s * 64u + lane == dj) Lr[s] = Lr[s] + xj;
+            } else {
+                const uint32_t oj = rdlane(o, j);
+                for (uint32_t t = 0; t < kj; ++t) {
+                    const uint32_t m = mem[oj + t];
+#pragma unroll
+                    for (int s = 0; s < kS; ++s)
+                        if (s * 64u + lane == m) Lr[s] = Lr[s] + xj;
+                }
+            }
         }
     }
 #pragma unroll
@@ -1289,5 +1406,30 @@ extern "C" cr_status cr_plan_churn(const cr_plan_set* plans, const uint32_t* pai
                        key_words(plans->num_keys), plans->R * plans->max_W, plans->num_windows, plans->specs,
                        plans->order, plans->num_admitted, plans->member_off, plans->members, plans->key_index,
                        plans->route, pairs, out, err);
+    return hipGetLastError() == hipSuccess ? CR_OK : CR_EHIP;
+}
+
+extern "C" cr_status cr_place_hash(const uint32_t* counts, const cr_plan_set* plans, void* stream)
+{
+    using namespace cr;
+    if (!counts || !valid_set(plans)) return CR_EINVAL;
+    const uint32_t cmax = plans->R * plans->max_W;
+    const hipStream_t st = as_stream(stream);
+    (void)hipGetLastError();
+    hipLaunchKernelGGL(k_hash_members, dim3(plans->num_plans, (cmax + kHashThreads - 1) / kHashThreads),
+                       dim3(kHashThreads), 0, st, plans->R, cmax, plans->num_windows, key_words(plans->num_keys),
+                       plans->specs, plans->order, plans->num_admitted, plans->member_off, plans->key_index,
+                       plans->members, plans->route);
+#define CR_HASH_LOADS(S)                                                                                            \
+    hipLaunchKernelGGL(k_hash_loads<S>, dim3(plans->num_plans), dim3(64), 0, st, plans->R, cmax, plans->num_windows, \
+                       plans->specs, plans->order_count, plans->num_admitted, plans->cold, plans->member_off,       \
+                       plans->members, plans->load)
+    const uint32_t s = (plans->R + 63) / 64;
+    if (s <= 1) CR_HASH_LOADS(1);
+    else if (s <= 2) CR_HASH_LOADS(2);
+    else if (s <= 4) CR_HASH_LOADS(4);
+    else if (s <= 8) CR_HASH_LOADS(8);
+    else CR_HASH_LOADS(16);
+#undef CR_HASH_LOADS
     return hipGetLastError() == hipSuccess ? CR_OK : CR_EHIP;
 }

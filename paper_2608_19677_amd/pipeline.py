@@ -104,7 +104,10 @@ class Pipeline:
         for g in range(NG):
             for c, cand in enumerate(wl.candidates):
                 w = window[g][c]
-                specs.append((w, cand.W, n_win[w], cand.a * n_win[w], cand.b * R))
+                v = B.PLAN_VARIANTS[getattr(cand, "variant", "full")]
+                specs.append((w, cand.W, n_win[w], cand.a * n_win[w], cand.b * R, v, getattr(cand, "place_seed", 0)))
+        # hash-placed ablation stages need cr_place_hash after cr_place_lpt
+        self.hash_placed = any(getattr(c, "variant", "full") in ("affinity", "replicated") for c in wl.candidates)
         self.NW = self.win_src.shape[0]  # counts rows the plans are built from
         self.plans = B.PlanSet(specs, P, R, self.max_W, K, self.NW, device)
         self.ws_admit = torch.empty(B.cr_admit_workspace_bytes(self.NW, R, self.max_W), dtype=torch.uint8,
@@ -138,6 +141,8 @@ class Pipeline:
 
     def place(self, stream=None):
         B.cr_place_lpt(self.win_src, self.plans.c, stream)
+        if self.hash_placed:
+            B.cr_place_hash(self.win_src, self.plans.c, stream)
 
     def plan(self, stream=None):
         self.admit(stream)

@@ -33,14 +33,22 @@ _S_PERM, _S_PREFIX, _S_KEYS, _S_SUFFIX, _S_ARRIVAL, _S_BURST, _S_DRIFT = 1, 2, 3
 SUFFIX_LO, SUFFIX_HI = 50, 400
 
 
+VARIANTS = ("full", "affinity", "replicated", "flat")
+
+
 @dataclass
 class Candidate:
     """One candidate plan: W warm slots per destination and load target
-    q_cap = (a / b) x (mean per-destination load of the window)."""
+    q_cap = (a / b) x (mean per-destination load of the window). ``variant`` names a stage
+    of the component ablation (Section 5.2): "full" (the method), "affinity" (one copy
+    per key, hash placement), "replicated" (Eq. 1 copies, hash placement) or "flat"
+    (nothing admitted); ``place_seed`` seeds the hash placement."""
 
     W: int
     a: int = 1
     b: int = 1
+    variant: str = "full"
+    place_seed: int = 0
 
 
 @dataclass
@@ -205,6 +213,18 @@ def replication(seed: int = 2, n: int = 20_000_000) -> Workload:
                      probs_by_rank=p, qps=500.0, interval_s=60.0, seed=seed)
 
 
+def ablation(seed: int = 2, n: int = 20_000_000, place_seed: int = 7) -> Workload:
+    """The component ablation (Section 5.2, 8B component ablation table) on the
+    injected-whale stream of ``replication``: the same requests replayed under four
+    candidates that add the method's parts one at a time, load balancing alone (flat),
+    + affinity (one copy per key, hash placement), + replication (Eq. 1, hash placement)
+    and + LPT (the method), all with 128 slots per destination and q_cap = 0.4 x mean."""
+    wl = replication(seed, n)
+    wl.name = "ablation"
+    wl.candidates = [Candidate(128, 2, 5, v, place_seed) for v in ("flat", "affinity", "replicated", "full")]
+    return wl
+
+
 def burst(seed: int = 2, n: int = 50_000_000, J: int = 100, num_keys: int = 50_000,
           R: int = 64, W: int = 64, burst_frac: float = 0.05, burst_mult: float = 10.0,
           burst_len: int = 2) -> Workload:
@@ -323,6 +343,7 @@ CONFIGS = {
     "replication": replication,
     "burst": burst,
     "drift": drift,
+    "ablation": ablation,
 }
 
 

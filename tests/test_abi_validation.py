@@ -45,6 +45,15 @@ def test_plan_set_rejects(L, kw):
     assert L.cr_admit(FAKE, ctypes.byref(ps), FAKE, 1 << 40, FAKE, None) == B.CR_EINVAL
     assert L.cr_place_lpt(FAKE, ctypes.byref(ps), None) == B.CR_EINVAL
     assert L.cr_plan_churn(ctypes.byref(ps), FAKE, 1, FAKE, FAKE, None) == B.CR_EINVAL
+    assert L.cr_place_hash(FAKE, ctypes.byref(ps), None) == B.CR_EINVAL
+
+
+def test_place_hash_rejects(L):
+    ps = _set()
+    assert L.cr_place_hash(None, ctypes.byref(ps), None) == B.CR_EINVAL
+    assert L.cr_place_hash(FAKE, None, None) == B.CR_EINVAL
+    ps.members = None
+    assert L.cr_place_hash(FAKE, ctypes.byref(ps), None) == B.CR_EINVAL
 
 
 def test_churn_rejects(L):

@@ -21,13 +21,23 @@ MUTANTS = [
     ("admit_tie_key_desc", "return p->b < q->b ? -1 : 1;", "return p->b > q->b ? -1 : 1;", "count_admit"),
     ("admit_cold_sign", "*cold = n_window - carried;", "*cold = carried;", "count_admit"),
     ("lpt_tie_high_index", "L[r] < L[best]", "L[r] <= L[best]", "lpt"),
-    ("lpt_no_cold_init", "double init = (double)cold / (double)R;", "double init = 0.0 * (double)cold;", "lpt"),
-    ("lpt_job_not_split", "/ (double)k;\n        member_off", "* 1.0;\n        member_off", "lpt"),
+    ("lpt_no_cold_init", "double init = (double)cold / (double)R;\n    for (uint32_t r = 0; r < R; ++r) L[r] = init;\n"
+     "    uint32_t off = 0;\n    for (uint32_t a = 0; a < A; ++a) {\n        uint32_t k = adm_k[a];",
+     "double init = 0.0 * (double)cold;\n    for (uint32_t r = 0; r < R; ++r) L[r] = init;\n"
+     "    uint32_t off = 0;\n    for (uint32_t a = 0; a < A; ++a) {\n        uint32_t k = adm_k[a];", "lpt"),
+    ("lpt_job_not_split", "counts_row[adm_keys[a]] / (double)k;", "counts_row[adm_keys[a]] * 1.0;", "lpt"),
     ("fmix_shift", "x ^= x >> 13;", "x ^= x >> 15;", "hash_route"),
     ("hash_seed_mix", "^ 0x9E3779B9u", "^ 0x9E3779B1u", "hash_route"),
     ("p2c_prefers_d2_on_tie", "L[d2] < L[d1] ? d2 : d1", "L[d2] <= L[d1] ? d2 : d1", "hash_route"),
     ("p2c_draws_swapped", "(h & 0xFFFFu) * R) >> 16);\n            uint32_t d2", "(h >> 16) * R) >> 16);\n            uint32_t d2", "hash_route"),
     ("member_pick_low_half", "(uint64_t)(h >> 16) * k) >> 16", "(uint64_t)(h & 0xFFFFu) * k) >> 16", "hash_route"),
+    ("hash_picks_largest", "if (best < 0 || u < ubest) {", "if (best < 0 || u > ubest) {", "ablation"),
+    ("hash_ignores_destination", "return cro_fmix32(cro_fmix32(b ^ t) ^ r);", "return cro_fmix32(cro_fmix32(b ^ t));",
+     "ablation"),
+    ("hash_ignores_key", "return cro_fmix32(cro_fmix32(b ^ t) ^ r);", "return cro_fmix32(cro_fmix32(t) ^ r);",
+     "ablation"),
+    ("hash_no_charge", "double x = (double)counts_row[b] / (double)k;", "double x = 0.0 * (double)counts_row[b];",
+     "ablation"),
     ("replay_hit_not_refreshed", "memmove(row + 1, row, sizeof(uint32_t) * pos);", ";", "replay"),
     ("replay_no_hit_prefix", "s[3] += prefix_len[b];", ";", "replay"),
     ("replay_prefill_on_hit", "s[2] += prefix_len[b];\n            uint32_t keep", "uint32_t keep", "replay"),
