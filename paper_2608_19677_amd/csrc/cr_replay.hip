@@ -18,9 +18,12 @@
 // lane i holds the i-th most recent key. A lookup is one compare and a ballot; the first
 // set bit p is the hit depth, and the update shifts lanes 0..p (all lanes on a miss) up
 // by one and writes the key into lane 0, a single select between a lane and its left
-// neighbour under a scalar mask. Above 64 slots, slot (s, lane) holds a key and its
-// recency rank (0 = most recent) and the update is a rank shift; neither form needs a
-// per-request search or reduction.
+// neighbour under a scalar mask. Above 64 slots the list is interleaved over SL registers
+// (position SL * lane + s in register s), so that moving a position back by one is a copy
+// from register s-1 in the same lane, and only the last register wraps into register 0 of
+// the next lane through a one-lane DPP shift; an access is SL compares and SL selects
+// under scalar masks, without branches. Neither form needs a per-request search or
+// reduction.
 #include "cr_common.h"
 
 namespace cr {
@@ -30,12 +33,21 @@ constexpr int kReplayThreads = 256;
 
 struct WArg {
     uint16_t W[CR_MAX_CANDS];
+    uint32_t seg_min;  // shortest segment for this call's record count
 };
 
-__host__ __device__ __forceinline__ uint32_t seg_len(uint32_t W)
+// Segments the whole replay is cut into, a few rounds of wavefronts over the chip: a
+// wavefront's LRU chain is serial, so several per SIMD hide its latency, and beyond that
+// longer segments only save the backward rebuild of the initial state.
+constexpr uint64_t kSegTarget = 16384;
+
+// Records per segment: at least 16 W (the rebuild scans back to W distinct keys) and at
+// least the share that keeps the number of segments near kSegTarget.
+__host__ __device__ __forceinline__ uint32_t seg_len(uint32_t W, uint32_t seg_min)
 {
-    const uint32_t s = 16u * W;
-    return s < 1024u ? 1024u : (s > 16384u ? 16384u : s);
+    uint32_t s = 16u * W;
+    s = s > seg_min ? s : seg_min;
+    return s < 1024u ? 1024u : (s > 65536u ? 65536u : s);
 }
 
 __host__ __device__ __forceinline__ uint32_t slot_class(uint32_t W)
@@ -246,7 +258,7 @@ __global__ __launch_bounds__(1024) void k_seg_items(const uint32_t* __restrict__
         uint32_t cnt = 0, nseg = 0;
         if (e < total) {
             cnt = dtot[e];
-            const uint32_t S = seg_len(wa.W[e / R]);
+            const uint32_t S = seg_len(wa.W[e / R], wa.seg_min);
             nseg = cnt ? (cnt + S - 1) / S : 1u;
         }
         uint32_t tot, itot;
@@ -283,71 +295,14 @@ __device__ __forceinline__ bool lru_contains(const uint32_t (&skey)[SL], uint32_
     return m != 0;
 }
 
+// Position q of the list is lane q / SL of register q % SL.
 template <int SL>
 __device__ __forceinline__ void lru_put_slot(uint32_t (&skey)[SL], uint32_t q, uint32_t kk, uint32_t lane)
 {
     (void)lane;
 #pragma unroll
     for (int s = 0; s < SL; ++s)
-        if ((uint32_t)s == (q >> 6)) skey[s] = wrlane(skey[s], kk, q & 63u);
-}
-
-// One LRU access of key kk; returns true on a hit. The target slot is the hit slot, or
-// on a miss the least recent slot (rank W-1). Every slot more recent than the target
-// ages by one and the target becomes rank 0 holding kk. With one slot per lane the step
-// has no branch: the target's rank is read from its lane either way (W-1 on a miss).
-__device__ __forceinline__ bool lru_step1(uint32_t& skey, uint32_t& srank, uint32_t kk, uint32_t W)
-{
-    const uint64_t m = ballot(skey == kk);
-    const uint64_t v = ballot(srank == W - 1);
-    const bool hit = m != 0;
-    const uint32_t tl = first_lane(hit ? m : v);
-    const uint32_t rh = rdlane(srank, tl);
-    srank += srank < rh ? 1u : 0u;
-    srank = wrlane(srank, 0u, tl);
-    skey = wrlane(skey, kk, tl);
-    return hit;
-}
-
-template <int SL>
-__device__ __forceinline__ bool lru_step(uint32_t (&skey)[SL], uint32_t (&srank)[SL], uint32_t kk, uint32_t W)
-{
-    if (SL == 1) return lru_step1(skey[0], srank[0], kk, W);
-    uint32_t ts = 0, tl = 0;
-    bool hit = false;
-#pragma unroll
-    for (int s = 0; s < SL; ++s) {
-        const uint64_t m = ballot(skey[s] == kk);
-        if (m) {
-            ts = (uint32_t)s;
-            tl = first_lane(m);
-            hit = true;
-        }
-    }
-    if (!hit) {
-#pragma unroll
-        for (int s = 0; s < SL; ++s) {
-            const uint64_t v = ballot(srank[s] == W - 1);
-            if (v) {
-                ts = (uint32_t)s;
-                tl = first_lane(v);
-            }
-        }
-    }
-    uint32_t rh = W - 1;
-#pragma unroll
-    for (int s = 0; s < SL; ++s)
-        if ((uint32_t)s == ts) rh = rdlane(srank[s], tl);
-#pragma unroll
-    for (int s = 0; s < SL; ++s) srank[s] += srank[s] < rh ? 1u : 0u;
-#pragma unroll
-    for (int s = 0; s < SL; ++s) {
-        if ((uint32_t)s == ts) {
-            srank[s] = wrlane(srank[s], 0u, tl);
-            skey[s] = wrlane(skey[s], kk, tl);
-        }
-    }
-    return hit;
+        if ((uint32_t)s == q % (uint32_t)SL) skey[s] = wrlane(skey[s], kk, q / (uint32_t)SL);
 }
 
 // Move-to-front update after a lookup whose hit mask is m: p = first set bit of m
@@ -379,6 +334,105 @@ __device__ __forceinline__ uint32_t mtf_step(uint32_t& sk, uint32_t kk, uint64_t
     const uint32_t p = mtf_core(sk, ballot(sk == kk) & wmask);
     sk = wrlane(sk, kk, 0u);
     return p;
+}
+
+// Rebuild step over one full batch of 64 valid records (lane t = record t), newest first:
+// every key not yet collected is appended at position q (SL lane + s in register s). Each
+// record is branch-free: the put is a select on lane position == target, with target = q
+// for a new key and no position otherwise. q is compared with W once per 16 records, so up
+// to 15 keys may land past W; positions >= W are ignored everywhere (and positions past
+// the registers are never written). Returns the new q.
+template <int SL>
+__device__ __forceinline__ uint32_t rebuild_batch(uint32_t (&sk)[SL], uint32_t kl, uint32_t q, uint32_t W,
+                                                  uint32_t lane)
+{
+    for (int g = 3; g >= 0 && q < W; --g) {
+        uint32_t key[16];
+#pragma unroll
+        for (uint32_t t = 0; t < 16; ++t) key[t] = rdlane(kl, 16u * (uint32_t)g + 15u - t);
+#pragma unroll
+        for (uint32_t t = 0; t < 16; ++t) {
+            uint64_t m = 0;
+#pragma unroll
+            for (int s = 0; s < SL; ++s) m |= ballot(sk[s] == key[t]);
+            const bool fresh = m == 0;
+            const uint32_t target = fresh ? q : 0xFFFFFFFFu;
+#pragma unroll
+            for (int s = 0; s < SL; ++s) sk[s] = lane * (uint32_t)SL + (uint32_t)s == target ? key[t] : sk[s];
+            q += fresh ? 1u : 0u;
+        }
+    }
+    return q;
+}
+
+// Register 0 of the interleaved list after an access whose combined hit mask is m: with
+// l = first set bit of m (0xFFFFFFFF when none, which shifts by 63 and keeps no lane),
+// keep = ~1 << l and lanes outside keep take the last register's key from the lane before
+// (one v_cndmask with a wave_shr:1 DPP source); lane 0 is left for the caller. The scalar
+// steps precede the select in the same block, which gives the DPP read of `last` the two
+// wait states it needs after that register's last VALU write.
+__device__ __forceinline__ uint32_t il_core(uint32_t first, uint32_t last, uint64_t m, uint64_t& keep, uint32_t& l)
+{
+    uint32_t out;
+    asm("s_ff1_i32_b64 %1, %5\n\t"
+        "s_lshl_b64 %2, -2, %1\n\t"
+        "s_mov_b64 vcc, %2\n\t"
+        "v_cndmask_b32_dpp %0, %4, %3, vcc wave_shr:1 row_mask:0xf bank_mask:0xf"
+        : "=v"(out), "=&s"(l), "=&s"(keep)
+        : "v"(first), "v"(last), "s"(m)
+        : "vcc");
+    return out;
+}
+
+// Move-to-front access of key kk over the interleaved list (position SL lane + s in
+// register s; with kMasked, vm[s] masks the positions < W). Returns the hit position's
+// lane, or 0xFFFFFFFF on a miss. With the hit in lane l of register h, positions up to the
+// hit move back by one: register s > 0 takes register s-1 in lanes <= l (lanes < l when
+// s > h), register 0 takes the last register of the lane before in lanes 1..l, and lane 0
+// of register 0 takes the key. A miss moves every position, dropping the least recent key
+// of a full list.
+template <int SL, bool kMasked>
+__device__ __forceinline__ uint32_t mtf_step_il(uint32_t (&sk)[SL], uint32_t kk, const uint64_t (&vm)[SL])
+{
+    uint64_t mh[SL];
+    uint64_t m = 0;
+#pragma unroll
+    for (int s = 0; s < SL; ++s) {
+        mh[s] = ballot(sk[s] == kk);
+        if (kMasked) mh[s] &= vm[s];
+        m |= mh[s];
+    }
+    uint64_t keep;
+    uint32_t l;
+    const uint32_t r0 = il_core(sk[0], sk[SL - 1], m, keep, l);
+    uint64_t before[SL];  // hit bits of registers before s
+    before[0] = 0;
+#pragma unroll
+    for (int s = 1; s < SL; ++s) before[s] = before[s - 1] | mh[s - 1];
+#pragma unroll
+    for (int s = SL - 1; s >= 1; --s) sk[s] = __builtin_amdgcn_inverse_ballot_w64(keep | before[s]) ? sk[s] : sk[s - 1];
+    sk[0] = wrlane(r0, kk, 0u);
+    return l;
+}
+
+// 64 records (lane t of kl = key of record t, all valid) through the interleaved list;
+// returns lane t = hit lane of record t (0xFFFFFFFF on a miss). Keys are read 16 at a
+// time ahead of use.
+template <int SL, bool kMasked>
+__device__ __forceinline__ uint32_t mtf_batch_il(uint32_t (&sk)[SL], uint32_t kl, const uint64_t (&vm)[SL])
+{
+    uint32_t depth = 0xFFFFFFFFu;
+#pragma unroll
+    for (uint32_t g = 0; g < 4; ++g) {
+        uint32_t key[16];
+#pragma unroll
+        for (uint32_t t = 0; t < 16; ++t) key[t] = rdlane(kl, 16u * g + t);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (uint32_t t = 0; t < 16; ++t) depth = wrlane(depth, mtf_step_il<SL, kMasked>(sk, key[t], vm), 16u * g + t);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    return depth;
 }
 
 // 64 records (lane t of kl = key of record t, all valid) through the move-to-front list;
@@ -436,7 +490,7 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
     const uint32_t seg = (uint32_t)(item - item_off[lo]);
     const uint32_t* go = grp_off + (uint64_t)c * (R + 1u);
     const uint32_t gs = go[d], cnt = go[d + 1] - gs;
-    const uint32_t S = seg_len(W);
+    const uint32_t S = seg_len(W, wa.seg_min);
     const uint64_t s0w = (uint64_t)seg * S;
     if (s0w > cnt) return;  // only if the partition used other slot counts
     const uint32_t s0 = (uint32_t)s0w;
@@ -444,16 +498,16 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
     const uint64_t* __restrict__ rl = rec + (uint64_t)c * n + gs;
 
     // Slot q of the rebuilt state (q = 64 s + lane) is the q-th most recent key, which is
-    // already the move-to-front order; the rank form starts from rank = slot.
-    uint32_t skey[SL], srank[SL];
+    // already the move-to-front order.
+    uint32_t skey[SL];
+    uint64_t vm[SL];  // lanes of register s whose position SL lane + s is < W
 #pragma unroll
     for (int s = 0; s < SL; ++s) {
-        const uint32_t idx = (uint32_t)s * 64u + lane;
         skey[s] = CR_EMPTY_SLOT;
-        srank[s] = idx < W ? idx : 0xFFFFFFFFu;
+        const uint32_t nl = W > (uint32_t)s ? (W - (uint32_t)s + SL - 1u) / (uint32_t)SL : 0u;
+        vm[s] = nl >= 64u ? ~0ull : (1ull << nl) - 1ull;
     }
-    const uint64_t wmask = W >= 64u ? ~0ull : ((1ull << W) - 1ull);
-    (void)wmask;
+    const uint64_t wmask = vm[0];
     // State before the segment: the most recent W distinct keys, newest first. Records are
     // read backwards 64 at a time, the next (older) batch in flight while one is scanned.
     uint32_t q = 0;
@@ -467,6 +521,10 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
             pos -= cnb;
             nb = pos < 64u ? pos : 64u;
             kl_next = lane < nb ? (uint32_t)rl[pos - nb + lane] : CR_EMPTY_SLOT;
+            if (cnb == 64u && ballot(kl < K) == ~0ull) {
+                q = rebuild_batch<SL>(skey, kl, q, W, lane);
+                continue;
+            }
             for (int t = (int)cnb - 1; t >= 0 && q < W; --t) {
                 const uint32_t kk = rdlane(kl, (uint32_t)t);
                 if (kk >= K) continue;
@@ -540,17 +598,16 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
             }
             hl = depth != 0xFFFFFFFFu;
         } else {
-            uint32_t hitf = 0;
-            if (ballot(lane < nb && kl >= K) == 0) {
-                for (uint32_t t = 0; t < nb; ++t)
-                    hitf = wrlane(hitf, lru_step<SL>(skey, srank, rdlane(kl, t), W) ? 1u : 0u, t);
+            uint32_t depth = 0xFFFFFFFFu;  // lane t: hit lane of record t
+            if (ballot(vl) == ~0ull) {
+                depth = W == 64u * SL ? mtf_batch_il<SL, false>(skey, kl, vm) : mtf_batch_il<SL, true>(skey, kl, vm);
             } else {
                 for (uint32_t t = 0; t < nb; ++t) {
                     const uint32_t kk = rdlane(kl, t);
-                    if (kk < K) hitf = wrlane(hitf, lru_step<SL>(skey, srank, kk, W) ? 1u : 0u, t);
+                    if (kk < K) depth = wrlane(depth, mtf_step_il<SL, true>(skey, kk, vm), t);
                 }
             }
-            hl = hitf != 0;
+            hl = depth != 0xFFFFFFFFu;
         }
         const uint32_t sfx = (uint32_t)(rv >> 32) & 0xFFFFu;
         const uint32_t ivl = (uint32_t)(rv >> 48);
@@ -575,14 +632,10 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
     if (ballot(bad) && lane == 0) atomicOr(err, CR_ERR_KEY_RANGE);
     if (s1 == cnt) {
         uint32_t* __restrict__ lo_ = lru_out + ((uint64_t)c * R + d) * max_W;
-        if constexpr (SL == 1) {
-            if (lane < W) lo_[lane] = skey[0];
-        } else {
 #pragma unroll
-            for (int s = 0; s < SL; ++s) {
-                const uint32_t idx = (uint32_t)s * 64u + lane;
-                if (idx < W && srank[s] < W) lo_[srank[s]] = skey[s];
-            }
+        for (int s = 0; s < SL; ++s) {
+            const uint32_t idx = lane * (uint32_t)SL + (uint32_t)s;
+            if (idx < W) lo_[idx] = skey[s];
         }
         for (uint32_t idx = W + lane; idx < max_W; idx += 64) lo_[idx] = CR_EMPTY_SLOT;
     }
@@ -630,6 +683,7 @@ inline cr_status replay_args(uint64_t n, uint32_t J, uint32_t P, uint32_t R, con
         max_W > CR_MAX_W || !ws || n >= 0xFFFFFFFFull)
         return CR_EINVAL;
     ra->wa = WArg{};
+    ra->wa.seg_min = (uint32_t)(((uint64_t)n * P + kSegTarget - 1) / kSegTarget);
     ra->classes = 0;
     for (uint32_t c = 0; c < P; ++c) {
         if (W[c] == 0 || W[c] > max_W) return CR_EINVAL;
