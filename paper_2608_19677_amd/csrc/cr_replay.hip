@@ -339,19 +339,23 @@ __device__ __forceinline__ uint32_t mtf_step(uint32_t& sk, uint32_t kk, uint64_t
 // Rebuild step over one full batch of 64 valid records (lane t = record t), newest first:
 // every key not yet collected is appended at position q (SL lane + s in register s). Each
 // record is branch-free: the put is a select on lane position == target, with target = q
-// for a new key and no position otherwise. q is compared with W once per 16 records, so up
-// to 15 keys may land past W; positions >= W are ignored everywhere (and positions past
+// for a new key and no position otherwise. q is compared with W once per 8 records, so up
+// to 7 keys may land past W; positions >= W are ignored everywhere (and positions past
 // the registers are never written). Returns the new q.
 template <int SL>
-__device__ __forceinline__ uint32_t rebuild_batch(uint32_t (&sk)[SL], uint32_t kl, uint32_t q, uint32_t W,
-                                                  uint32_t lane)
+__device__ __forceinline__ uint32_t rebuild_batch(uint32_t (&sk)[SL], const uint64_t* __restrict__ rb, uint32_t q,
+                                                  uint32_t W, uint32_t lane)
 {
-    for (int g = 3; g >= 0 && q < W; --g) {
-        uint32_t key[16];
+    // keys by scalar loads from the batch's records (rb is uniform), 8 per load
+    for (int g = 7; g >= 0 && q < W; --g) {
+        uint64_t rk[8];
 #pragma unroll
-        for (uint32_t t = 0; t < 16; ++t) key[t] = rdlane(kl, 16u * (uint32_t)g + 15u - t);
+        for (uint32_t t = 0; t < 8; ++t) rk[t] = rb[8u * (uint32_t)g + t];
+        uint32_t key[8];
 #pragma unroll
-        for (uint32_t t = 0; t < 16; ++t) {
+        for (uint32_t t = 0; t < 8; ++t) key[t] = (uint32_t)rk[7u - t];  // newest first
+#pragma unroll
+        for (uint32_t t = 0; t < 8; ++t) {
             uint64_t m = 0;
 #pragma unroll
             for (int s = 0; s < SL; ++s) m |= ballot(sk[s] == key[t]);
@@ -419,18 +423,18 @@ __device__ __forceinline__ uint32_t mtf_step_il(uint32_t (&sk)[SL], uint32_t kk,
 // returns lane t = hit lane of record t (0xFFFFFFFF on a miss). Keys are read 16 at a
 // time ahead of use.
 template <int SL, bool kMasked>
-__device__ __forceinline__ uint32_t mtf_batch_il(uint32_t (&sk)[SL], uint32_t kl, const uint64_t (&vm)[SL])
+__device__ __forceinline__ uint32_t mtf_batch_il(uint32_t (&sk)[SL], const uint64_t* __restrict__ rb,
+                                                 const uint64_t (&vm)[SL])
 {
-    uint32_t depth = 0xFFFFFFFFu;
+    uint32_t depth = 0xFFFFFFFFu;  // keys by scalar loads, 8 records per load (rb is uniform)
 #pragma unroll
-    for (uint32_t g = 0; g < 4; ++g) {
-        uint32_t key[16];
+    for (uint32_t g = 0; g < 8; ++g) {
+        uint64_t rk[8];
 #pragma unroll
-        for (uint32_t t = 0; t < 16; ++t) key[t] = rdlane(kl, 16u * g + t);
-        __builtin_amdgcn_sched_barrier(0);
+        for (uint32_t t = 0; t < 8; ++t) rk[t] = rb[8u * g + t];
 #pragma unroll
-        for (uint32_t t = 0; t < 16; ++t) depth = wrlane(depth, mtf_step_il<SL, kMasked>(sk, key[t], vm), 16u * g + t);
-        __builtin_amdgcn_sched_barrier(0);
+        for (uint32_t t = 0; t < 8; ++t)
+            depth = wrlane(depth, mtf_step_il<SL, kMasked>(sk, (uint32_t)rk[t], vm), 8u * g + t);
     }
     return depth;
 }
@@ -438,24 +442,26 @@ __device__ __forceinline__ uint32_t mtf_batch_il(uint32_t (&sk)[SL], uint32_t kl
 // 64 records (lane t of kl = key of record t, all valid) through the move-to-front list;
 // returns lane t = hit depth of record t. Keys are read 16 at a time ahead of their use.
 template <bool kMasked>
-__device__ __forceinline__ uint32_t mtf_batch(uint32_t& sk, uint32_t kl, uint64_t wmask)
+__device__ __forceinline__ uint32_t mtf_batch(uint32_t& sk, const uint64_t* __restrict__ rb, uint64_t wmask)
 {
+    // The keys come from the batch's records (rb is uniform) by scalar loads, 8 records per
+    // load: no vector instruction moves a key into a scalar register. A wavefront waits for
+    // each load; the other wavefronts of its SIMD cover the wait.
     uint32_t depth = 0xFFFFFFFFu;
 #pragma unroll
-    for (uint32_t g = 0; g < 4; ++g) {
-        uint32_t key[16];
+    for (uint32_t g = 0; g < 8; ++g) {
+        uint64_t rk[8];
 #pragma unroll
-        for (uint32_t t = 0; t < 16; ++t) key[t] = rdlane(kl, 16u * g + t);
-        __builtin_amdgcn_sched_barrier(0);
+        for (uint32_t t = 0; t < 8; ++t) rk[t] = rb[8u * g + t];
 #pragma unroll
-        for (uint32_t t = 0; t < 16; ++t) {
-            uint64_t m = ballot(sk == key[t]);
+        for (uint32_t t = 0; t < 8; ++t) {
+            const uint32_t key = (uint32_t)rk[t];
+            uint64_t m = ballot(sk == key);
             if (kMasked) m &= wmask;
             const uint32_t p = mtf_core(sk, m);
-            sk = wrlane(sk, key[t], 0u);
-            depth = wrlane(depth, p, 16u * g + t);
+            sk = wrlane(sk, key, 0u);
+            depth = wrlane(depth, p, 8u * g + t);
         }
-        __builtin_amdgcn_sched_barrier(0);
     }
     return depth;
 }
@@ -522,7 +528,7 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
             nb = pos < 64u ? pos : 64u;
             kl_next = lane < nb ? (uint32_t)rl[pos - nb + lane] : CR_EMPTY_SLOT;
             if (cnb == 64u && ballot(kl < K) == ~0ull) {
-                q = rebuild_batch<SL>(skey, kl, q, W, lane);
+                q = rebuild_batch<SL>(skey, rl + pos, q, W, lane);
                 continue;
             }
             for (int t = (int)cnb - 1; t >= 0 && q < W; --t) {
@@ -589,7 +595,7 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
         if constexpr (SL == 1) {
             uint32_t depth = 0xFFFFFFFFu;  // lane t: hit depth of record t
             if (ballot(vl) == ~0ull) {
-                depth = W == 64u ? mtf_batch<false>(skey[0], kl, wmask) : mtf_batch<true>(skey[0], kl, wmask);
+                depth = W == 64u ? mtf_batch<false>(skey[0], rl + b0, wmask) : mtf_batch<true>(skey[0], rl + b0, wmask);
             } else {
                 for (uint32_t t = 0; t < nb; ++t) {
                     const uint32_t kk = rdlane(kl, t);
@@ -600,7 +606,8 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
         } else {
             uint32_t depth = 0xFFFFFFFFu;  // lane t: hit lane of record t
             if (ballot(vl) == ~0ull) {
-                depth = W == 64u * SL ? mtf_batch_il<SL, false>(skey, kl, vm) : mtf_batch_il<SL, true>(skey, kl, vm);
+                depth = W == 64u * SL ? mtf_batch_il<SL, false>(skey, rl + b0, vm)
+                                      : mtf_batch_il<SL, true>(skey, rl + b0, vm);
             } else {
                 for (uint32_t t = 0; t < nb; ++t) {
                     const uint32_t kk = rdlane(kl, t);
