@@ -48,6 +48,9 @@ def parse():
                     help="overlap: consecutive chunks of one stream, chunk k planned on one HIP stream while "
                          "chunk k-1 replays on another (cache state and last window carried); serial: every "
                          "step is the whole workload from scratch on one stream")
+    ap.add_argument("--dispatch", default="static", choices=("static", "live"),
+                    help="static: order-independent dispatch on interval-start planned loads; live: least-loaded "
+                         "member and power of two choices on the running loads of each interval")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-unbatched", action="store_true",
@@ -155,9 +158,11 @@ def main():
         study = DriftStudy(wl, device="cuda:0")
         stages = DriftStudy.STAGES
         args.schedule = "serial"  # its plans come from named windows, not from the previous chunk
+    if args.dispatch == "live":
+        args.schedule = "serial"
     ev = {s: [] for s in stages}
     if args.schedule == "serial":
-        gp = study.pipe if study is not None else Pipeline(wl, device="cuda:0")
+        gp = study.pipe if study is not None else Pipeline(wl, device="cuda:0", dispatch=args.dispatch)
         stream = torch.cuda.current_stream()
         for _ in range(args.warmup):
             for s in stages:
@@ -201,7 +206,8 @@ def main():
         # counting reads every key and writes the dense [J][K] counts matrix it defines
         "count": dict(kernel="k_count_*", bound="hbm", unit="GB/s", work=4.0 * n + 4.0 * wl.J * wl.num_keys,
                       peak=HBM_PEAK_GBS),
-        "route": dict(kernel="k_route<true>", bound="hbm", unit="GB/s", work=(4.0 + 2.0 * P) * n, peak=HBM_PEAK_GBS),
+        "route": dict(kernel="k_route<true>" if args.dispatch == "static" else "k_route_live<%s>" % (
+            "false" if R <= 64 else "true"), bound="hbm", unit="GB/s", work=(4.0 + 2.0 * P) * n, peak=HBM_PEAK_GBS),
         # LPT: every job copy is compared against the R destination loads.
         "place": dict(kernel="k_lpt_small", bound="alu", unit="Glane-op/s", work=float(n_adm) * R,
                       peak=ALU_PEAK_GOPS),
@@ -245,6 +251,7 @@ def main():
     }
     out["config"]["plan_builds"] = n_plans
     out["config"]["schedule"] = args.schedule
+    out["config"]["dispatch"] = args.dispatch
     if study is not None:
         out["study"] = study.summary()
         out["kernels"]["churn"] = {"ms": stage_ms["churn"], "kernel": "k_plan_churn"}
@@ -269,7 +276,7 @@ def main():
         t_start = time.perf_counter()
         while True:
             s = time.perf_counter()
-            opipe.run(wl)
+            opipe.run(wl, dispatch=args.dispatch)
             times.append(time.perf_counter() - s)
             if time.perf_counter() - t_start > args.cpu_seconds or len(times) >= 10:
                 break

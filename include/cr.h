@@ -173,6 +173,21 @@ cr_status cr_route(const uint32_t* keys, uint64_t n, uint64_t first_index, uint6
                    const uint64_t* off, const uint32_t* gmap, uint32_t J, const cr_plan_set* plans,
                    uint16_t* dest, uint32_t* err, void* stream);
 
+/* Live-load dispatch (Section 3.1 "Placement and dispatch": during the interval admitted
+ * traffic takes the least-loaded member of its fixed T(b), other traffic power of two
+ * choices; Fig. 1). Load is the number of requests of the current interval already sent to
+ * a destination (zero at every interval start), so each decision depends on all earlier
+ * ones in its interval:
+ *   admitted key: the member of T(b) with the smallest (load, destination);
+ *   otherwise: d1, d2 drawn from the request hash exactly as in cr_route, and d2 only if
+ *   load[d2] < load[d1].
+ * Arguments, layouts and errors as for cr_route (the plans' loads are not read). Intervals
+ * and candidates run in parallel, one serial chain each: the cost is the longest
+ * interval's length, not n. */
+cr_status cr_route_live(const uint32_t* keys, uint64_t n, uint64_t first_index, uint64_t seed,
+                        const uint64_t* off, const uint32_t* gmap, uint32_t J, const cr_plan_set* plans,
+                        uint16_t* dest, uint32_t* err, void* stream);
+
 /* Churn between pairs of built plans of one set (Section 5.4 "Rate drift and remapping";
  * Appendix E, table of replan measurements). With S_x = {(b, r) : r in T_x(b)} over plan
  * x's admitted keys b, pair i = (p, q) = (pairs[2i], pairs[2i+1]) yields

@@ -51,11 +51,13 @@ def lib():
         L.cro_hash.argtypes = [u64, u64]
         L.cro_hash.restype = u32
         L.cro_route.argtypes = [P, u64, u64, u64, u32, u32, P, u32, P, P, P, P, P]
+        L.cro_route_live.argtypes = [P, u64, u64, u64, u32, u32, P, u32, P, P, P, P]
         L.cro_place_u.argtypes = [u32, u32, u32]
         L.cro_place_u.restype = u32
         L.cro_place_hash.argtypes = [P, P, u32, P, u32, u64, u32, P, P, P]
         L.cro_replay.argtypes = [P, P, P, u32, P, u64, P, u32, u32, u32, P, P, P]
-        for f in (L.cro_count_rates, L.cro_admit, L.cro_place_lpt, L.cro_place_hash, L.cro_route, L.cro_replay):
+        for f in (L.cro_count_rates, L.cro_admit, L.cro_place_lpt, L.cro_place_hash, L.cro_route, L.cro_route_live,
+                  L.cro_replay):
             f.restype = ctypes.c_int
         _lib = L
     return _lib
@@ -166,6 +168,19 @@ def route(keys, first_index: int, seed: int, K: int, R: int, adm_keys, member_of
     _check(lib().cro_route(_p(keys), keys.shape[0], first_index, seed, K, R, _p(adm_keys),
                            adm_keys.shape[0], _p(member_off), _p(members), _p(L), _p(dest), _p(bad)),
            "route")
+    return dest
+
+
+def route_live(keys, first_index: int, seed: int, K: int, R: int, adm_keys, member_off, members):
+    """Live-load dispatch of ONE control interval (loads start at zero)."""
+    keys = _c(keys, np.uint32)
+    adm_keys = _c(adm_keys, np.uint32)
+    member_off = _c(member_off, np.uint32)
+    members = _c(members if len(members) else np.zeros(1), np.uint16)
+    dest = np.zeros(keys.shape[0], dtype=np.uint16)
+    bad = np.zeros(1, dtype=np.uint64)
+    _check(lib().cro_route_live(_p(keys), keys.shape[0], first_index, seed, K, R, _p(adm_keys),
+                                adm_keys.shape[0], _p(member_off), _p(members), _p(dest), _p(bad)), "route_live")
     return dest
 
 

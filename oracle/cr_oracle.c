@@ -312,6 +312,62 @@ int cro_route(const uint32_t* keys, uint64_t n, uint64_t first_index, uint64_t s
 }
 
 /* ------------------------------------------------------------------------ */
+/* Live-load dispatch through one fixed plan over ONE control interval      */
+/* (Section 3.1 "Placement and dispatch": during the interval admitted      */
+/* traffic takes the least-loaded member of its fixed T(b), other traffic   */
+/* takes power of two choices; Fig. 1). The load of a destination is read   */
+/* as the number of requests of this interval dispatched to it so far       */
+/* (zero when the interval starts), so every decision depends on all        */
+/* earlier ones:                                                            */
+/*  - admitted key with members M: the member with the smallest            */
+/*    (load, destination) pair (k = 1: the only member);                    */
+/*  - otherwise d1, d2 from hash(seed, first_index + i) as in cro_route,    */
+/*    and d2 only if load[d2] < load[d1];                                   */
+/*  - load[dest] += 1.                                                      */
+/* A key >= K is dispatched as cold and counted in *n_bad.                  */
+/* ------------------------------------------------------------------------ */
+int cro_route_live(const uint32_t* keys, uint64_t n, uint64_t first_index, uint64_t seed, uint32_t K,
+                   uint32_t R, const uint32_t* adm_keys, uint32_t A, const uint32_t* member_off,
+                   const uint16_t* members, uint16_t* dest, uint64_t* n_bad)
+{
+    if (R == 0 || R > 65535 || K == 0) return -1;
+    int64_t* rank = (int64_t*)malloc(sizeof(int64_t) * (size_t)K);
+    uint64_t* load = (uint64_t*)calloc(R, sizeof(uint64_t));
+    if (!rank || !load) {
+        free(rank);
+        free(load);
+        return -2;
+    }
+    for (uint32_t b = 0; b < K; ++b) rank[b] = -1;
+    for (uint32_t a = 0; a < A; ++a) rank[adm_keys[a]] = a;
+    uint64_t bad = 0;
+    for (uint64_t i = 0; i < n; ++i) {
+        uint32_t b = keys[i];
+        uint32_t d;
+        if (b < K && rank[b] >= 0) {
+            uint32_t a = (uint32_t)rank[b];
+            d = members[member_off[a]];
+            for (uint32_t t = member_off[a] + 1; t < member_off[a + 1]; ++t) {
+                uint32_t m = members[t];
+                if (load[m] < load[d] || (load[m] == load[d] && m < d)) d = m;
+            }
+        } else {
+            if (b >= K) bad += 1;
+            uint32_t h = cro_hash(seed, first_index + i);
+            uint32_t d1 = (uint32_t)(((uint64_t)(h & 0xFFFFu) * R) >> 16);
+            uint32_t d2 = (uint32_t)(((uint64_t)(h >> 16) * R) >> 16);
+            d = load[d2] < load[d1] ? d2 : d1;
+        }
+        dest[i] = (uint16_t)d;
+        load[d] += 1;
+    }
+    if (n_bad) *n_bad += bad;
+    free(rank);
+    free(load);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
 /* Shadow replay of one plan's routing (Section 3.2: admitted and cold      */
 /* prefixes share each destination's cache and eviction policy).            */
 /* Model: destination d holds an LRU list of at most W whole prefixes       */

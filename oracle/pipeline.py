@@ -15,6 +15,10 @@ Semantics it fixes (each restated from the paper or from the reading noted):
   the method.
 * Candidate (W, a, b) has C = R W warm slots and q_cap = (a/b) x N_w / R,
   i.e. q_num = a N_w and q_den = b R with N_w the window's request count.
+* Dispatch is static by default (planned interval-start loads, order
+  independent) or live: least-loaded member and power of two choices on the
+  running per-destination counts of the interval (Section 3.1 "Placement and
+  dispatch").
 * The replay's LRU state per (candidate, destination) starts empty and is
   carried across intervals and plan changes (Section 3.2, Appendix E).
 
@@ -27,7 +31,7 @@ from typing import Dict, List, Optional, Tuple
 
 import numpy as np
 
-from . import admit, admit_affinity, count_rates, place_hash, place_lpt, replay, route
+from . import admit, admit_affinity, count_rates, place_hash, place_lpt, replay, route, route_live
 
 
 def plan_window(j: int) -> int:
@@ -64,12 +68,13 @@ def build_plans(counts: np.ndarray, R: int, candidates, pairs: List[Tuple[int, i
 
 
 def run(wl, lru: Optional[List[np.ndarray]] = None, counts_prev: Optional[np.ndarray] = None,
-        timings: Optional[dict] = None) -> Dict:
+        timings: Optional[dict] = None, dispatch: str = "static") -> Dict:
     """Count -> plan -> route -> replay over ``wl`` (a workload.Workload).
 
     ``counts_prev`` (one row) stands in for the window before interval 0 when a
     stream is processed in chunks; ``lru`` is the carried replay state per
-    candidate.  Returns counts, plans, dest [P][n], stats [J][P][R][4] (or
+    candidate; ``dispatch`` is "static" (interval-start planned loads) or "live"
+    (running loads within each interval).  Returns counts, plans, dest [P][n], stats [J][P][R][4] (or
     [bins][P][R][4] with ``wl.stat_offsets``), lru, and ``win_of[j][c]``, the window
     of candidate c's plan in interval j.
     """
@@ -99,8 +104,14 @@ def run(wl, lru: Optional[List[np.ndarray]] = None, counts_prev: Optional[np.nda
             continue
         for c in range(P):
             pl = plans[(win_of[j][c], c)]
-            dest[c, s:e] = route(wl.keys[s:e], wl.first_index + s, wl.seed, wl.num_keys, R,
-                                 pl["adm_keys"], pl["member_off"], pl["members"], pl["L"])
+            if dispatch == "live":
+                dest[c, s:e] = route_live(wl.keys[s:e], wl.first_index + s, wl.seed, wl.num_keys, R,
+                                          pl["adm_keys"], pl["member_off"], pl["members"])
+            elif dispatch == "static":
+                dest[c, s:e] = route(wl.keys[s:e], wl.first_index + s, wl.seed, wl.num_keys, R,
+                                     pl["adm_keys"], pl["member_off"], pl["members"], pl["L"])
+            else:
+                raise ValueError(f"unknown dispatch {dispatch!r}")
     t3 = time.perf_counter()
     soff = wl.offsets if wl.stat_offsets is None else wl.stat_offsets
     stats = np.zeros((len(soff) - 1, P, R, 4), dtype=np.uint64)

@@ -23,7 +23,7 @@ CR_ROUTE_SINGLE = 0x80000000
 CR_MAX_R, CR_MAX_W, CR_MAX_CANDS, CR_MAX_J = 1024, 512, 256, 65535
 
 EXPORTS = ("cr_count_rates", "cr_admit_workspace_bytes", "cr_admit", "cr_place_lpt", "cr_place_hash", "cr_route",
-           "cr_plan_churn",
+           "cr_route_live", "cr_plan_churn",
            "cr_replay_workspace_bytes", "cr_replay", "cr_replay_partition", "cr_replay_lru", "cr_version")
 
 _u32, _u64, _P = ctypes.c_uint32, ctypes.c_uint64, ctypes.c_void_p
@@ -69,6 +69,7 @@ def load(path: Optional[str] = None):
     L.cr_place_lpt.argtypes = [_P, ctypes.POINTER(CrPlanSet), _P]
     L.cr_place_hash.argtypes = [_P, ctypes.POINTER(CrPlanSet), _P]
     L.cr_route.argtypes = [_P, _u64, _u64, _u64, _P, _P, _u32, ctypes.POINTER(CrPlanSet), _P, _P, _P]
+    L.cr_route_live.argtypes = [_P, _u64, _u64, _u64, _P, _P, _u32, ctypes.POINTER(CrPlanSet), _P, _P, _P]
     L.cr_plan_churn.argtypes = [ctypes.POINTER(CrPlanSet), _P, _u32, _P, _P, _P]
     L.cr_replay_workspace_bytes.argtypes = [_u64, _u32, _u32]
     L.cr_replay_workspace_bytes.restype = ctypes.c_size_t
@@ -79,7 +80,8 @@ def load(path: Optional[str] = None):
     L.cr_replay_lru.argtypes = [_P, _u32, _u64, _u32, _u32, _u32, ctypes.POINTER(_u32), _u32, _P, _P, _P, _P,
                                 ctypes.c_size_t, _P, _P]
     L.cr_version.restype = ctypes.c_char_p
-    for f in ("cr_count_rates", "cr_admit", "cr_place_lpt", "cr_place_hash", "cr_route", "cr_plan_churn", "cr_replay",
+    for f in ("cr_count_rates", "cr_admit", "cr_place_lpt", "cr_place_hash", "cr_route", "cr_route_live", "cr_plan_churn",
+              "cr_replay",
               "cr_replay_partition", "cr_replay_lru"):
         getattr(L, f).restype = ctypes.c_int32
     _lib = L
@@ -138,6 +140,13 @@ def cr_route(keys, first_index: int, seed: int, off, gmap, J: int, plans: CrPlan
     n = keys.numel() if n is None else n
     _check(load().cr_route(_ptr(keys), n, first_index, seed, _ptr(off), _ptr(gmap), J, ctypes.byref(plans),
                            _ptr(dest), _ptr(err), _stream(stream)), "cr_route")
+
+
+def cr_route_live(keys, first_index: int, seed: int, off, gmap, J: int, plans: CrPlanSet, dest, err, stream=None,
+                  n: Optional[int] = None):
+    n = keys.numel() if n is None else n
+    _check(load().cr_route_live(_ptr(keys), n, first_index, seed, _ptr(off), _ptr(gmap), J, ctypes.byref(plans),
+                                _ptr(dest), _ptr(err), _stream(stream)), "cr_route_live")
 
 
 def cr_plan_churn(plans: CrPlanSet, pairs, out, err, stream=None):

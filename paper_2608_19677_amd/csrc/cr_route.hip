@@ -1,6 +1,7 @@
-// Request dispatch through fixed plans (Section 3.1 "Placement and dispatch"; Fig. 1),
-// in the order-independent form: admitted keys pick a member of T(b) by the request
-// hash, cold keys use power of two choices on the plan's interval-start loads.
+// Request dispatch through fixed plans (Section 3.1 "Placement and dispatch"; Fig. 1).
+// k_route is the order-independent form: admitted keys pick a member of T(b) by the
+// request hash, cold keys use power of two choices on the plan's interval-start loads.
+// k_route_live is the live-load form, one serial chain per interval (see below).
 //
 // HBM-bound stream: 4 B key read + 2 B destination written per request and candidate.
 // Each thread owns 4 consecutive requests: one 16-byte key load, then per candidate 4
@@ -145,8 +146,150 @@ __global__ __launch_bounds__(kRouteThreads) void k_route(
     if (bad) atomicOr(err, CR_ERR_KEY_RANGE);
 }
 
+// Live-load dispatch (Section 3.1 "Placement and dispatch"; Fig. 1): during an interval,
+// admitted keys take the least-loaded member of T(b) and the rest power of two choices,
+// on the running count of requests each destination has received in the interval. Every
+// decision depends on the earlier ones, so an interval is one serial chain; the chains of
+// different intervals and candidates are independent, one wavefront each. With R <= 64,
+// lane r holds destination r's count and a decision reads it with v_readlane; otherwise the
+// counts sit in LDS. For each batch of 64 requests the lanes look their requests up in
+// parallel (table entry, hash, both draws; a single-copy key is a choice between its
+// member and itself), then the wavefront walks the 64 decisions in order.
+template <bool kLds>
+__global__ __launch_bounds__(64) void k_route_live(
+    const uint32_t* __restrict__ keys, uint64_t n, uint64_t first_index, uint32_t smix,
+    const uint64_t* __restrict__ off, const uint32_t* __restrict__ gmap, uint32_t K, uint32_t R, uint32_t cands,
+    uint32_t NG, uint32_t KW, const uint64_t* __restrict__ key_index, const uint32_t* __restrict__ route,
+    const uint32_t* __restrict__ member_off, uint32_t cmax, const uint16_t* __restrict__ members,
+    uint16_t* __restrict__ dest, uint32_t* __restrict__ err)
+{
+    __shared__ uint32_t s_live[kLds ? CR_MAX_R : 1];
+    const uint32_t lane = threadIdx.x;
+    const uint32_t j = blockIdx.x / cands, c = blockIdx.x % cands;
+    const uint64_t i0 = off[j];
+    uint64_t i1 = off[j + 1];
+    i1 = i1 < n ? i1 : n;
+    if (i1 <= i0) return;
+    const uint32_t g = gmap[j] < NG ? gmap[j] : NG - 1u;
+    const uint32_t p = g * cands + c;
+    const uint64_t* __restrict__ kx = key_index + (uint64_t)p * 2u * KW;
+    const uint32_t* __restrict__ rw = route + (uint64_t)p * cmax;
+    const uint32_t* __restrict__ mo = member_off + (uint64_t)p * (cmax + 1u);
+    const uint16_t* __restrict__ mem = members + (uint64_t)p * cmax;
+    uint16_t* __restrict__ dc = dest + (uint64_t)c * n;
+    uint32_t live = 0;  // lane r: requests of this interval sent to destination r (R <= 64)
+    if (kLds)
+        for (uint32_t r = lane; r < R; r += 64u) s_live[r] = 0;
+    auto load_of = [&](uint32_t d) -> uint32_t {
+        if (kLds) return (uint32_t)__builtin_amdgcn_readfirstlane((int)s_live[d]);
+        return rdlane(live, d);
+    };
+    auto charge = [&](uint32_t d) {
+        if (kLds) {
+            if (lane == 0) s_live[d] = s_live[d] + 1u;
+        } else {
+            live += lane == d ? 1u : 0u;
+        }
+    };
+    bool bad = false;
+    for (uint64_t base = i0; base < i1; base += 64u) {
+        const uint64_t i = base + lane;
+        const bool in = i < i1;
+        const uint32_t b = in ? keys[i] : 0u;
+        const bool valid = in && b < K;
+        bad |= in && b >= K;
+        const ulonglong2 e = valid ? *reinterpret_cast<const ulonglong2*>(kx + 2u * (b >> 6))
+                                   : make_ulonglong2(0ull, 0ull);
+        const bool adm = valid && ((e.x >> (b & 63u)) & 1ull);
+        const uint32_t w =
+            adm ? rw[(uint32_t)e.y + (uint32_t)__popcll(e.x & ((1ull << (b & 63u)) - 1ull))] : 0u;
+        const uint32_t h = req_hash(smix, first_index + i);
+        uint32_t d1 = (uint32_t)(((uint64_t)(h & 0xFFFFu) * R) >> 16);
+        uint32_t d2 = (uint32_t)(((uint64_t)(h >> 16) * R) >> 16);
+        if (adm && (w & CR_ROUTE_SINGLE)) d1 = d2 = w & 0xFFFFu;
+        const uint64_t multi = ballot(adm && !(w & CR_ROUTE_SINGLE));
+        const uint32_t nb = i1 - base < 64u ? (uint32_t)(i1 - base) : 64u;
+        uint32_t out = 0;
+        if (!kLds && multi == 0 && nb == 64u) {
+            // Full batch without multi-copy keys: 64 branch-free decisions, draws read 16 ahead.
+#pragma unroll
+            for (uint32_t gq = 0; gq < 4; ++gq) {
+                uint32_t e1[16], e2[16];
+#pragma unroll
+                for (uint32_t t = 0; t < 16; ++t) {
+                    e1[t] = rdlane(d1, 16u * gq + t);
+                    e2[t] = rdlane(d2, 16u * gq + t);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (uint32_t t = 0; t < 16; ++t) {
+                    const uint32_t d = rdlane(live, e2[t]) < rdlane(live, e1[t]) ? e2[t] : e1[t];
+                    live += lane == d ? 1u : 0u;
+                    out = wrlane(out, d, 16u * gq + t);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            dc[i] = (uint16_t)out;
+            continue;
+        }
+        for (uint32_t t = 0; t < nb; ++t) {
+            uint32_t d;
+            if ((multi >> t) & 1ull) {
+                // least (load, destination) among the members of T(b)
+                const uint32_t a = rdlane(w, t);
+                const uint32_t o0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)mo[a]);
+                const uint32_t o1 = (uint32_t)__builtin_amdgcn_readfirstlane((int)mo[a + 1u]);
+                d = (uint32_t)__builtin_amdgcn_readfirstlane((int)mem[o0]);
+                uint32_t ld = load_of(d);
+                for (uint32_t o = o0 + 1u; o < o1; ++o) {
+                    const uint32_t m = (uint32_t)__builtin_amdgcn_readfirstlane((int)mem[o]);
+                    const uint32_t lm = load_of(m);
+                    if (lm < ld || (lm == ld && m < d)) {
+                        d = m;
+                        ld = lm;
+                    }
+                }
+            } else {
+                const uint32_t e1 = rdlane(d1, t), e2 = rdlane(d2, t);
+                d = load_of(e2) < load_of(e1) ? e2 : e1;
+            }
+            charge(d);
+            out = wrlane(out, d, t);
+        }
+        if (in) dc[i] = (uint16_t)out;
+    }
+    if (ballot(bad) && lane == 0) atomicOr(err, CR_ERR_KEY_RANGE);
+}
+
 }  // namespace
 }  // namespace cr
+
+extern "C" cr_status cr_route_live(const uint32_t* keys, uint64_t n, uint64_t first_index, uint64_t seed,
+                                   const uint64_t* off, const uint32_t* gmap, uint32_t J, const cr_plan_set* plans,
+                                   uint16_t* dest, uint32_t* err, void* stream)
+{
+    using namespace cr;
+    if (!plans || !off || !gmap || J == 0 || !err) return CR_EINVAL;
+    if (plans->cands == 0 || plans->num_plans == 0 || plans->num_plans % plans->cands || plans->R == 0 ||
+        plans->R > CR_MAX_R || plans->num_keys == 0 || plans->num_keys == 0xFFFFFFFFu || plans->max_W == 0 ||
+        !plans->key_index || !plans->route || !plans->member_off || !plans->members)
+        return CR_EINVAL;
+    if (n == 0) return CR_OK;
+    if (!keys || !dest || ((uintptr_t)keys & 3u) || ((uintptr_t)dest & 1u)) return CR_EINVAL;
+    const uint64_t blocks = (uint64_t)J * plans->cands;
+    if (blocks > 0x7FFFFFF0ull) return CR_EINVAL;
+    const uint32_t cmax = plans->R * plans->max_W;
+    (void)hipGetLastError();
+#define CR_LIVE_LAUNCH(L)                                                                                          \
+    hipLaunchKernelGGL(k_route_live<L>, dim3((uint32_t)blocks), dim3(64), 0, as_stream(stream), keys, n, first_index, \
+                       seed_mix(seed), off, gmap, plans->num_keys, plans->R, plans->cands,                          \
+                       plans->num_plans / plans->cands, (plans->num_keys + 63u) / 64u, plans->key_index, plans->route, \
+                       plans->member_off, cmax, plans->members, dest, err)
+    if (plans->R <= 64) CR_LIVE_LAUNCH(false);
+    else CR_LIVE_LAUNCH(true);
+#undef CR_LIVE_LAUNCH
+    return hipGetLastError() == hipSuccess ? CR_OK : CR_EHIP;
+}
 
 extern "C" cr_status cr_route(const uint32_t* keys, uint64_t n, uint64_t first_index, uint64_t seed,
                               const uint64_t* off, const uint32_t* gmap, uint32_t J, const cr_plan_set* plans,

@@ -8,6 +8,8 @@ Semantics (the paper's statement of the loop, Sections 3.1-3.2):
 * candidate (W, a, b) has C = R W warm slots and load target q_cap = (a/b) N_w / R,
   passed to the library as q_num = a N_w, q_den = b R;
 * the replay's per-destination cache state is carried across intervals and chunks;
+* dispatch is static (interval-start planned loads, order independent) or live (running
+  loads of the interval, one serial chain per interval and candidate);
 * a workload may name the window of each (interval, candidate) plan itself, as the
   replanning study does (Section 5.4, Appendix E): one plan group per interval then,
   and replay statistics may be kept in bins finer than the intervals.
@@ -49,7 +51,10 @@ class Pipeline:
 
     def __init__(self, wl, device="cuda", dev_in: Optional[DeviceInputs] = None,
                  prev_counts: Optional[torch.Tensor] = None, prev_n: int = 0,
-                 lru_in: Optional[torch.Tensor] = None):
+                 lru_in: Optional[torch.Tensor] = None, dispatch: str = "static"):
+        if dispatch not in ("static", "live"):
+            raise ValueError(f"unknown dispatch {dispatch!r}")
+        self.dispatch = dispatch
         self.wl = wl
         self.device = device
         self.inp = dev_in if dev_in is not None else upload(wl, device)
@@ -149,8 +154,9 @@ class Pipeline:
         self.place(stream)
 
     def route(self, stream=None):
-        B.cr_route(self.inp.keys, self.first_index, self.wl.seed, self.inp.off, self.gmap, self.J, self.plans.c,
-                   self.dest, self.err, stream, n=self.n)
+        fn = B.cr_route_live if self.dispatch == "live" else B.cr_route
+        fn(self.inp.keys, self.first_index, self.wl.seed, self.inp.off, self.gmap, self.J, self.plans.c, self.dest,
+           self.err, stream, n=self.n)
 
     def partition(self, stream=None):
         B.cr_replay_partition(self.inp.keys, self.inp.suffix, self.dest, self.stat_off, self.JS, self.P, self.R,

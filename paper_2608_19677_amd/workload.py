@@ -153,11 +153,18 @@ def _suffixes(rng: np.random.Generator, n: int) -> np.ndarray:
     return rng.integers(SUFFIX_LO, SUFFIX_HI + 1, size=n, dtype=np.int64).astype(np.uint16)
 
 
-def _exp_intervals(rng: np.random.Generator, n: int, qps: float, interval_s: Optional[float]) -> np.ndarray:
-    """Exponential inter-arrivals at ``qps``; offsets of fixed-length control intervals."""
+def _exp_intervals(rng: np.random.Generator, n: int, qps: float, interval_s: Optional[float],
+                   cv: Optional[float] = None) -> np.ndarray:
+    """Inter-arrivals at ``qps``: exponential, or Gamma with coefficient of variation ``cv``
+    (shape 1 / cv^2, same mean; Section 5.4 "Arrival burstiness"); offsets of fixed-length
+    control intervals."""
     if interval_s is None:
         return np.array([0, n], dtype=np.uint64)
-    t = np.cumsum(rng.exponential(1.0 / qps, size=n))
+    if cv is None:
+        gaps = rng.exponential(1.0 / qps, size=n)
+    else:
+        gaps = rng.gamma(1.0 / (cv * cv), (cv * cv) / qps, size=n)
+    t = np.cumsum(gaps)
     j = np.floor(t / interval_s).astype(np.int64)
     J = int(j[-1]) + 1 if n else 1
     off = np.searchsorted(j, np.arange(J + 1), side="left").astype(np.uint64)
@@ -168,7 +175,7 @@ def _exp_intervals(rng: np.random.Generator, n: int, qps: float, interval_s: Opt
 def synthetic(name: str, *, num_keys: int, n: int, R: int, candidates: Sequence[Candidate],
               probs_by_rank: np.ndarray, qps: float = 100.0, interval_s: Optional[float] = None,
               prefix_median: float = 2000.0, prefix_sigma: float = 0.5, seed: int = 2,
-              p2c_seed: int = 1) -> Workload:
+              p2c_seed: int = 1, cv: Optional[float] = None) -> Workload:
     """A stationary stream: keys iid from ``probs_by_rank`` through a seeded permutation."""
     tag = _tag(name)
     perm = _rng(seed, tag, _S_PERM).permutation(num_keys)
@@ -176,11 +183,11 @@ def synthetic(name: str, *, num_keys: int, n: int, R: int, candidates: Sequence[
     ranks = sampler.sample(_rng(seed, tag, _S_KEYS), n)
     keys = perm[ranks].astype(np.uint32)
     suffix = _suffixes(_rng(seed, tag, _S_SUFFIX), n)
-    offsets = _exp_intervals(_rng(seed, tag, _S_ARRIVAL), n, qps, interval_s)
+    offsets = _exp_intervals(_rng(seed, tag, _S_ARRIVAL), n, qps, interval_s, cv)
     plen = _prefix_lengths(seed, tag, num_keys, prefix_median, prefix_sigma)
     return Workload(name=name, num_keys=num_keys, R=R, candidates=list(candidates), keys=keys,
                     suffix=suffix, prefix_len=plen, offsets=offsets, seed=p2c_seed,
-                    meta=dict(qps=qps, interval_s=interval_s, seed=seed))
+                    meta=dict(qps=qps, interval_s=interval_s, seed=seed, cv=cv))
 
 
 # ---------------------------------------------------------------------------
@@ -195,13 +202,23 @@ def tiny(seed: int = 2, n: int = 100_000) -> Workload:
                      prefix_median=2000.0, prefix_sigma=0.5, seed=seed)
 
 
-def llama70b(seed: int = 2, n: int = 10_000_000) -> Workload:
+def llama70b(seed: int = 2, n: int = 10_000_000, cv: Optional[float] = None) -> Workload:
     """20,000 keys, Zipf 1.0 water-filled to a 0.3 % top share, 176 QPS,
-    60-s control intervals, 30 destinations x 64 slots, prefixes lognormal(3000, 0.7)."""
+    60-s control intervals, 30 destinations x 64 slots, prefixes lognormal(3000, 0.7).
+    ``cv`` replaces the exponential gaps by Gamma gaps of that coefficient of variation
+    (the same keys; only the interval boundaries move)."""
     p = water_fill(zipf_probs(20_000, 1.0), 0.003)
     return synthetic("llama70b", num_keys=20_000, n=n, R=30, candidates=[Candidate(64)],
                      probs_by_rank=p, qps=176.0, interval_s=60.0,
-                     prefix_median=3000.0, prefix_sigma=0.7, seed=seed)
+                     prefix_median=3000.0, prefix_sigma=0.7, seed=seed, cv=cv)
+
+
+def llama70b_gamma(seed: int = 2, n: int = 10_000_000) -> Workload:
+    """The 70B-like stream with Gamma arrivals matched to the workload's marginal
+    inter-arrival CV of 1.9 (Section 5.4 "Arrival burstiness")."""
+    wl = llama70b(seed, n, cv=1.9)
+    wl.name = "llama70b_gamma"
+    return wl
 
 
 def replication(seed: int = 2, n: int = 20_000_000) -> Workload:
@@ -344,6 +361,7 @@ CONFIGS = {
     "burst": burst,
     "drift": drift,
     "ablation": ablation,
+    "llama70b_gamma": llama70b_gamma,
 }
 
 

@@ -74,7 +74,20 @@ def test_admit_workspace_too_small(L):
     assert L.cr_admit(FAKE, ctypes.byref(ps), FAKE, need, FAKE, None) == B.CR_EINVAL
 
 
-def test_route_rejects(L):
+@pytest.mark.parametrize("fn", ["cr_route", "cr_route_live"])
+def test_route_rejects(L, fn):
+    route = getattr(L, fn)
+    ps = _set()
+    assert route(FAKE, 10, 0, 1, FAKE, FAKE, 0, ctypes.byref(ps), FAKE, FAKE, None) == B.CR_EINVAL
+    assert route(FAKE, 10, 0, 1, None, FAKE, 1, ctypes.byref(ps), FAKE, FAKE, None) == B.CR_EINVAL
+    assert route(FAKE, 10, 0, 1, FAKE, None, 1, ctypes.byref(ps), FAKE, FAKE, None) == B.CR_EINVAL
+    assert route(FAKE + 1, 10, 0, 1, FAKE, FAKE, 1, ctypes.byref(ps), FAKE, FAKE, None) == B.CR_EINVAL
+    assert route(FAKE, 10, 0, 1, FAKE, FAKE, 1, ctypes.byref(ps), FAKE + 1, FAKE, None) == B.CR_EINVAL
+    assert route(FAKE, 10, 0, 1, FAKE, FAKE, 1, None, FAKE, FAKE, None) == B.CR_EINVAL
+    assert route(FAKE, 0, 0, 1, FAKE, FAKE, 1, ctypes.byref(ps), FAKE, FAKE, None) == B.CR_OK  # empty: no-op
+
+
+def test_route_static_rejects_more(L):
     ps = _set()
     assert L.cr_route(FAKE, 10, 0, 1, FAKE, FAKE, 0, ctypes.byref(ps), FAKE, FAKE, None) == B.CR_EINVAL
     assert L.cr_route(FAKE, 10, 0, 1, None, FAKE, 1, ctypes.byref(ps), FAKE, FAKE, None) == B.CR_EINVAL

@@ -249,3 +249,34 @@ def test_sweep_chunks_sampled_parity():
         np.testing.assert_array_equal(lru[c, dsample, :cand.W], state[dsample])
     # every request is accounted for once per candidate
     assert np.all(stats[0, :, :, 0].sum(axis=1) == w0.n)
+
+
+LIVE = [
+    # seed, K, n, R, Ws, J, hot, hot_share, qs
+    (41, 300, 30_000, 7, [8], 4, 3, 0.5, [(1, 1)]),
+    (42, 2000, 80_000, 30, [16, 64], 6, 5, 0.4, [(1, 1), (1, 4)]),   # k > 1 members, two candidates
+    (43, 500, 20_000, 1, [40], 3, 0, 0.0, [(1, 1)]),                # one destination
+    (44, 5000, 60_000, 100, [4], 3, 8, 0.5, [(1, 1)]),              # counts in LDS (R > 64)
+    (45, 100, 10, 30, [16], 3, 0, 0.0, [(1, 1)]),                   # intervals shorter than a batch
+    (46, 800, 40_000, 16, [2], 2, 2, 0.9, [(1, 20)]),               # k clamped to R
+]
+
+
+@pytest.mark.parametrize("case", LIVE, ids=[f"l{c[0]}" for c in LIVE])
+def test_live_dispatch_parity(case):
+    # live-load dispatch: every decision on the running loads of its interval
+    seed, K, n, R, Ws, J, hot, share, qs = case
+    wl = wl_mod.small_random(seed, num_keys=K, n=n, R=R, Ws=Ws, J=J, hot=hot, hot_share=share, qs=qs)
+    say(f"[case] live {wl.name} n={wl.n} J={wl.J} R={wl.R} P={wl.P}")
+    gp = Pipeline(wl, dispatch="live")
+    gp.step()
+    compare_all(wl, gp, gp.host(), opipe.run(wl, dispatch="live"))
+
+
+def test_live_dispatch_70b_gamma_full_parity():
+    # the 70B-like stream with Gamma (CV 1.9) arrivals, 1e7 requests, live dispatch
+    wl = wl_mod.llama70b_gamma()
+    say(f"[case] live {wl.name} n={wl.n} J={wl.J}")
+    gp = Pipeline(wl, dispatch="live")
+    gp.step()
+    compare_all(wl, gp, gp.host(), opipe.run(wl, dispatch="live"))

@@ -29,8 +29,15 @@ MUTANTS = [
     ("fmix_shift", "x ^= x >> 13;", "x ^= x >> 15;", "hash_route"),
     ("hash_seed_mix", "^ 0x9E3779B9u", "^ 0x9E3779B1u", "hash_route"),
     ("p2c_prefers_d2_on_tie", "L[d2] < L[d1] ? d2 : d1", "L[d2] <= L[d1] ? d2 : d1", "hash_route"),
-    ("p2c_draws_swapped", "(h & 0xFFFFu) * R) >> 16);\n            uint32_t d2", "(h >> 16) * R) >> 16);\n            uint32_t d2", "hash_route"),
+    ("p2c_draws_swapped", "(h & 0xFFFFu) * R) >> 16);\n            uint32_t d2 = (uint32_t)(((uint64_t)(h >> 16) * R) >> 16);\n            dest[i]",
+     "(h >> 16) * R) >> 16);\n            uint32_t d2 = (uint32_t)(((uint64_t)(h >> 16) * R) >> 16);\n            dest[i]", "hash_route"),
+    ("live_p2c_draws_swapped", "(h & 0xFFFFu) * R) >> 16);\n            uint32_t d2 = (uint32_t)(((uint64_t)(h >> 16) * R) >> 16);\n            d = load",
+     "(h >> 16) * R) >> 16);\n            uint32_t d2 = (uint32_t)(((uint64_t)(h >> 16) * R) >> 16);\n            d = load", "live"),
     ("member_pick_low_half", "(uint64_t)(h >> 16) * k) >> 16", "(uint64_t)(h & 0xFFFFu) * k) >> 16", "hash_route"),
+    ("live_no_increment", "        load[d] += 1;", "        ;", "live"),
+    ("live_member_tie_high", "(load[m] == load[d] && m < d)", "(load[m] == load[d] && m > d)", "live"),
+    ("live_p2c_prefers_d2_on_tie", "d = load[d2] < load[d1] ? d2 : d1;", "d = load[d2] <= load[d1] ? d2 : d1;", "live"),
+    ("live_member_most_loaded", "if (load[m] < load[d] ||", "if (load[m] > load[d] ||", "live"),
     ("hash_picks_largest", "if (best < 0 || u < ubest) {", "if (best < 0 || u > ubest) {", "ablation"),
     ("hash_ignores_destination", "return cro_fmix32(cro_fmix32(b ^ t) ^ r);", "return cro_fmix32(cro_fmix32(b ^ t));",
      "ablation"),
