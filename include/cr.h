@@ -41,8 +41,11 @@ typedef int32_t cr_status;
 #define CR_ERR_KEY_RANGE 1u   /* a key >= num_keys was seen                       */
 #define CR_ERR_DEST_RANGE 2u  /* a destination >= R was seen by the replay        */
 #define CR_ERR_SPEC 4u        /* a plan spec disagrees with its counts row         */
+#define CR_ERR_KEYMAP_FULL 8u /* more distinct opaque ids than the directory holds  */
 
 #define CR_EMPTY_SLOT 0xFFFFFFFFu /* unused LRU slot / unused key               */
+#define CR_NO_KEY 0xFFFFFFFFu     /* not an opaque id; dense index of an unknown id */
+#define CR_KEYMAP_MAX_CAPACITY (1u << 28) /* distinct opaque ids per directory      */
 #define CR_ROUTE_SINGLE 0x80000000u /* route word flag: k = 1, low 16 bits = dest */
 
 #define CR_MAX_R 1024      /* destinations per plan                            */
@@ -242,6 +245,37 @@ cr_status cr_replay_lru(const uint32_t* prefix_len, uint32_t num_keys, uint64_t 
                         uint32_t P, uint32_t R, const uint32_t* W, uint32_t max_W,
                         const uint32_t* lru_in, uint32_t* lru_out, uint64_t* stats, void* ws,
                         size_t ws_bytes, uint32_t* err, void* stream);
+
+/* Opaque-key directory (Appendix A.2 "Data handling": the planner needs only the pairs
+ * (b, lambda_b), and b may be salted or ephemeral; Section 2.1: the workload summaries
+ * carry opaque keys). It maps 32-bit opaque ids to the dense indices the counting rows
+ * need. The dense index of an id is the rank of its first occurrence among the distinct
+ * ids of the build stream (order of first appearance), independent of scheduling.
+ * CR_NO_KEY is not an id.
+ *
+ * Directory size in bytes for up to `capacity` distinct ids (an open-addressing table of
+ * at least 2 * capacity slots, 12 bytes each); device memory owned by the caller. */
+size_t cr_keymap_bytes(uint32_t capacity);
+/* Workspace of cr_keymap_build for a stream of n ids, in bytes (a first-occurrence bitmap
+ * of n bits, its per-word prefix and per-block sums). */
+size_t cr_keymap_workspace_bytes(uint64_t n);
+/* Builds the directory of ids u32 [n] (n < 2^32 - 1) into `table`, replacing its contents.
+ * num_keys u32 [1] (device) receives the number of distinct ids. An id equal to CR_NO_KEY
+ * sets CR_ERR_KEY_RANGE and is skipped. More than `capacity` distinct ids sets
+ * CR_ERR_KEYMAP_FULL and the directory must not be used: once its table is full, ids
+ * that found no slot are missing and the indices are ranks among the ids it holds. 1 <= capacity <=
+ * CR_KEYMAP_MAX_CAPACITY. */
+cr_status cr_keymap_build(const uint32_t* ids, uint64_t n, uint32_t capacity, void* table, size_t table_bytes,
+                          void* ws, size_t ws_bytes, uint32_t* num_keys, uint32_t* err, void* stream);
+/* dense[i] = dense index of ids[i], or CR_NO_KEY for an id the directory does not hold
+ * (later stages skip such keys as out of range). ids, dense u32 [n]; `capacity` as built. */
+cr_status cr_keymap_lookup(const void* table, size_t table_bytes, uint32_t capacity, const uint32_t* ids,
+                           uint64_t n, uint32_t* dense, void* stream);
+/* Per-key attributes given by opaque id, moved to dense order: out[dense(ids[x])] =
+ * values[x] for every x < m whose id the directory holds and whose index is < out_len;
+ * other entries of out are left as they are. ids, values u32 [m]; out u32 [out_len]. */
+cr_status cr_keymap_scatter(const void* table, size_t table_bytes, uint32_t capacity, const uint32_t* ids,
+                            const uint32_t* values, uint64_t m, uint32_t* out, uint32_t out_len, void* stream);
 
 /* Library version string. */
 const char* cr_version(void);

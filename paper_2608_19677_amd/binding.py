@@ -17,13 +17,15 @@ import torch
 from .build import LIB
 
 CR_OK, CR_EINVAL, CR_ESIZE, CR_EHIP = 0, -1, -2, -3
-CR_ERR_KEY_RANGE, CR_ERR_DEST_RANGE, CR_ERR_SPEC = 1, 2, 4
+CR_ERR_KEY_RANGE, CR_ERR_DEST_RANGE, CR_ERR_SPEC, CR_ERR_KEYMAP_FULL = 1, 2, 4, 8
+CR_NO_KEY = 0xFFFFFFFF
 CR_EMPTY_SLOT = 0xFFFFFFFF
 CR_ROUTE_SINGLE = 0x80000000
 CR_MAX_R, CR_MAX_W, CR_MAX_CANDS, CR_MAX_J = 1024, 512, 256, 65535
 
 EXPORTS = ("cr_count_rates", "cr_admit_workspace_bytes", "cr_admit", "cr_place_lpt", "cr_place_hash", "cr_route",
-           "cr_route_live", "cr_plan_churn",
+           "cr_route_live", "cr_plan_churn", "cr_keymap_bytes", "cr_keymap_workspace_bytes", "cr_keymap_build",
+           "cr_keymap_lookup", "cr_keymap_scatter",
            "cr_replay_workspace_bytes", "cr_replay", "cr_replay_partition", "cr_replay_lru", "cr_version")
 
 _u32, _u64, _P = ctypes.c_uint32, ctypes.c_uint64, ctypes.c_void_p
@@ -69,6 +71,13 @@ def load(path: Optional[str] = None):
     L.cr_place_lpt.argtypes = [_P, ctypes.POINTER(CrPlanSet), _P]
     L.cr_place_hash.argtypes = [_P, ctypes.POINTER(CrPlanSet), _P]
     L.cr_route.argtypes = [_P, _u64, _u64, _u64, _P, _P, _u32, ctypes.POINTER(CrPlanSet), _P, _P, _P]
+    L.cr_keymap_bytes.argtypes = [_u32]
+    L.cr_keymap_bytes.restype = ctypes.c_size_t
+    L.cr_keymap_workspace_bytes.argtypes = [_u64]
+    L.cr_keymap_workspace_bytes.restype = ctypes.c_size_t
+    L.cr_keymap_build.argtypes = [_P, _u64, _u32, _P, ctypes.c_size_t, _P, ctypes.c_size_t, _P, _P, _P]
+    L.cr_keymap_lookup.argtypes = [_P, ctypes.c_size_t, _u32, _P, _u64, _P, _P]
+    L.cr_keymap_scatter.argtypes = [_P, ctypes.c_size_t, _u32, _P, _P, _u64, _P, _u32, _P]
     L.cr_route_live.argtypes = [_P, _u64, _u64, _u64, _P, _P, _u32, ctypes.POINTER(CrPlanSet), _P, _P, _P]
     L.cr_plan_churn.argtypes = [ctypes.POINTER(CrPlanSet), _P, _u32, _P, _P, _P]
     L.cr_replay_workspace_bytes.argtypes = [_u64, _u32, _u32]
@@ -81,7 +90,7 @@ def load(path: Optional[str] = None):
                                 ctypes.c_size_t, _P, _P]
     L.cr_version.restype = ctypes.c_char_p
     for f in ("cr_count_rates", "cr_admit", "cr_place_lpt", "cr_place_hash", "cr_route", "cr_route_live", "cr_plan_churn",
-              "cr_replay",
+              "cr_keymap_build", "cr_keymap_lookup", "cr_keymap_scatter", "cr_replay",
               "cr_replay_partition", "cr_replay_lru"):
         getattr(L, f).restype = ctypes.c_int32
     _lib = L
@@ -140,6 +149,35 @@ def cr_route(keys, first_index: int, seed: int, off, gmap, J: int, plans: CrPlan
     n = keys.numel() if n is None else n
     _check(load().cr_route(_ptr(keys), n, first_index, seed, _ptr(off), _ptr(gmap), J, ctypes.byref(plans),
                            _ptr(dest), _ptr(err), _stream(stream)), "cr_route")
+
+
+def cr_keymap_bytes(capacity: int) -> int:
+    return int(load().cr_keymap_bytes(capacity))
+
+
+def cr_keymap_workspace_bytes(n: int) -> int:
+    return int(load().cr_keymap_workspace_bytes(n))
+
+
+def _nbytes(t) -> int:
+    return t.numel() * t.element_size()
+
+
+def cr_keymap_build(ids, capacity: int, table, ws, num_keys, err, stream=None, n: Optional[int] = None):
+    n = ids.numel() if n is None else n
+    _check(load().cr_keymap_build(_ptr(ids), n, capacity, _ptr(table), _nbytes(table), _ptr(ws), _nbytes(ws),
+                                  _ptr(num_keys), _ptr(err), _stream(stream)), "cr_keymap_build")
+
+
+def cr_keymap_lookup(table, capacity: int, ids, dense, stream=None, n: Optional[int] = None):
+    n = ids.numel() if n is None else n
+    _check(load().cr_keymap_lookup(_ptr(table), _nbytes(table), capacity, _ptr(ids), n, _ptr(dense), _stream(stream)),
+           "cr_keymap_lookup")
+
+
+def cr_keymap_scatter(table, capacity: int, ids, values, out, stream=None):
+    _check(load().cr_keymap_scatter(_ptr(table), _nbytes(table), capacity, _ptr(ids), _ptr(values), ids.numel(),
+                                    _ptr(out), out.numel(), _stream(stream)), "cr_keymap_scatter")
 
 
 def cr_route_live(keys, first_index: int, seed: int, off, gmap, J: int, plans: CrPlanSet, dest, err, stream=None,

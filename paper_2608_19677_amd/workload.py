@@ -365,6 +365,31 @@ CONFIGS = {
 }
 
 
+@dataclass
+class OpaqueStream:
+    """A request stream whose keys are opaque 32-bit ids, with the per-key prefix lengths
+    given by id (including ids that never appear in the stream)."""
+
+    ids: np.ndarray           # uint32 [N], never 0xFFFFFFFF
+    attr_ids: np.ndarray      # uint32 [K] every key's id
+    prefix_by_id: np.ndarray  # uint32 [K] prefix length of attr_ids[x]
+
+
+def opaque(wl: Workload, salt: int = 0x5EED1234) -> OpaqueStream:
+    """Salted ids for a workload's dense keys (Appendix A.2: keys may be salted): a fixed
+    odd-multiplier bijection of the 32-bit key space, xor a salt. The ids carry no order
+    of the dense keys; 0xFFFFFFFF is never produced."""
+    def salted(b: np.ndarray) -> np.ndarray:
+        x = (b.astype(np.uint64) * np.uint64(0x9E3779B1) + np.uint64(salt)) & np.uint64(0xFFFFFFFF)
+        x = x.astype(np.uint32) ^ np.uint32((salt * 0x632BE5AB) & 0xFFFFFFFF)
+        return x
+
+    all_ids = salted(np.arange(wl.num_keys, dtype=np.uint32))
+    if np.any(all_ids == 0xFFFFFFFF):
+        raise ValueError("salt maps a key to the reserved id; choose another salt")
+    return OpaqueStream(ids=all_ids[wl.keys], attr_ids=all_ids, prefix_by_id=wl.prefix_len.copy())
+
+
 def small_random(seed: int, *, num_keys: int, n: int, R: int, Ws: Sequence[int],
                  J: int = 1, zipf_s: float = 1.1, qs: Sequence[Tuple[int, int]] = ((1, 1),),
                  hot: int = 0, hot_share: float = 0.0) -> Workload:

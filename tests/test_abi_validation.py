@@ -131,3 +131,27 @@ def test_replay_rejects(L):
                                  None) == B.CR_ESIZE
     assert L.cr_replay_lru(FAKE, 100, 1000, 1, 2, 30, _W(16, 8), 8, None, FAKE, FAKE, FAKE, need, FAKE,
                            None) == B.CR_EINVAL  # max_W below a W
+
+
+def test_keymap_rejects(L):
+    tb = L.cr_keymap_bytes(100)
+    ws = L.cr_keymap_workspace_bytes(1000)
+    assert tb >= 3 * 4 * 200 and L.cr_keymap_bytes(1) >= 3 * 4 * 64
+    assert L.cr_keymap_workspace_bytes(10**6) > ws > 0
+    ok = (FAKE, 1000, 100, FAKE, tb, FAKE, ws, FAKE, FAKE, None)
+    assert L.cr_keymap_build(*ok[:2], 0, *ok[3:]) == B.CR_EINVAL                    # capacity 0
+    assert L.cr_keymap_build(*ok[:2], (1 << 28) + 1, *ok[3:]) == B.CR_EINVAL        # over the limit
+    assert L.cr_keymap_build(*ok[:3], None, *ok[4:]) == B.CR_EINVAL                 # table NULL
+    assert L.cr_keymap_build(*ok[:4], tb - 1, *ok[5:]) == B.CR_ESIZE                # table too small
+    assert L.cr_keymap_build(*ok[:6], ws - 1, *ok[7:]) == B.CR_ESIZE                # workspace too small
+    assert L.cr_keymap_build(None, *ok[1:]) == B.CR_EINVAL                          # ids NULL
+    assert L.cr_keymap_build(FAKE + 2, *ok[1:]) == B.CR_EINVAL                      # misaligned ids
+    assert L.cr_keymap_build(*ok[:7], None, *ok[8:]) == B.CR_EINVAL                 # num_keys NULL
+    assert L.cr_keymap_build(*ok[:8], None, None) == B.CR_EINVAL                    # err NULL
+    assert L.cr_keymap_lookup(FAKE, tb, 0, FAKE, 10, FAKE, None) == B.CR_EINVAL
+    assert L.cr_keymap_lookup(FAKE, tb - 1, 100, FAKE, 10, FAKE, None) == B.CR_ESIZE
+    assert L.cr_keymap_lookup(FAKE, tb, 100, None, 10, FAKE, None) == B.CR_EINVAL
+    assert L.cr_keymap_lookup(FAKE, tb, 100, FAKE, 0, FAKE, None) == B.CR_OK        # empty: no-op
+    assert L.cr_keymap_scatter(FAKE, tb, 100, FAKE, None, 5, FAKE, 10, None) == B.CR_EINVAL
+    assert L.cr_keymap_scatter(FAKE, tb - 1, 100, FAKE, FAKE, 5, FAKE, 10, None) == B.CR_ESIZE
+    assert L.cr_keymap_scatter(FAKE, tb, 100, FAKE, FAKE, 0, FAKE, 10, None) == B.CR_OK
