@@ -51,6 +51,9 @@ def parse():
     ap.add_argument("--dispatch", default="static", choices=("static", "live"),
                     help="static: order-independent dispatch on interval-start planned loads; live: least-loaded "
                          "member and power of two choices on the running loads of each interval")
+    ap.add_argument("--opaque", action="store_true",
+                    help="keys arrive as salted 32-bit ids: every step first builds the device directory and "
+                         "remaps the stream to dense keys (timed as stage 'remap')")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-unbatched", action="store_true",
@@ -160,9 +163,39 @@ def main():
         args.schedule = "serial"  # its plans come from named windows, not from the previous chunk
     if args.dispatch == "live":
         args.schedule = "serial"
+    remap = None
+    if args.opaque:
+        if study is not None:
+            raise SystemExit("--opaque runs the plain path only")
+        from paper_2608_19677_amd.keymap import KeyMap, to_device
+        from paper_2608_19677_amd.pipeline import DeviceInputs
+        args.schedule = "serial"
+        op = workload.opaque(wl)
+        km = KeyMap(wl.num_keys, device="cuda:0")
+        d_ids = to_device(op.ids, "cuda:0")
+        dense = torch.empty_like(d_ids)
+        plen = torch.zeros(wl.num_keys, dtype=torch.int32, device="cuda:0")
+        km_err = torch.zeros(1, dtype=torch.int32, device="cuda:0")
+        km.build(d_ids, km_err)
+        km.scatter(to_device(op.attr_ids, "cuda:0"), to_device(op.prefix_by_id, "cuda:0"), plen)
+        dev_in = DeviceInputs(keys=dense, suffix=torch.from_numpy(wl.suffix.view(np.int16)).to(dev), prefix_len=plen,
+                              off=torch.from_numpy(wl.offsets.view(np.int64)).to(dev),
+                              off_host=wl.offsets.astype(np.uint64))
+
+        class _Remap:
+            def remap(self, stream=None):
+                km.build(d_ids, km_err, stream)
+                km.lookup(d_ids, dense, stream)
+
+        remap = _Remap()
+        stages = ("remap",) + tuple(stages)
     ev = {s: [] for s in stages}
     if args.schedule == "serial":
-        gp = study.pipe if study is not None else Pipeline(wl, device="cuda:0", dispatch=args.dispatch)
+        if remap is not None:
+            gp = Pipeline(wl, device="cuda:0", dev_in=dev_in, dispatch=args.dispatch)
+            gp.remap = remap.remap
+        else:
+            gp = study.pipe if study is not None else Pipeline(wl, device="cuda:0", dispatch=args.dispatch)
         stream = torch.cuda.current_stream()
         for _ in range(args.warmup):
             for s in stages:
@@ -252,6 +285,12 @@ def main():
     out["config"]["plan_builds"] = n_plans
     out["config"]["schedule"] = args.schedule
     out["config"]["dispatch"] = args.dispatch
+    if remap is not None:
+        torch.cuda.synchronize()
+        assert int(km_err.item()) == 0
+        out["config"]["keys"] = "salted 32-bit ids, remapped on the device every step"
+        out["kernels"]["remap"] = {"ms": stage_ms["remap"], "kernel": "k_km_*",
+                                   "achieved_GBps": 12.0 * n / (stage_ms["remap"] * 1e-3) / 1e9}
     if study is not None:
         out["study"] = study.summary()
         out["kernels"]["churn"] = {"ms": stage_ms["churn"], "kernel": "k_plan_churn"}

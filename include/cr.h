@@ -254,7 +254,8 @@ cr_status cr_replay_lru(const uint32_t* prefix_len, uint32_t num_keys, uint64_t 
  * CR_NO_KEY is not an id.
  *
  * Directory size in bytes for up to `capacity` distinct ids (an open-addressing table of
- * at least 2 * capacity slots, 12 bytes each); device memory owned by the caller. */
+ * at least 2 * capacity slots, 16 bytes each); device memory owned by the caller, 16-byte
+ * aligned. */
 size_t cr_keymap_bytes(uint32_t capacity);
 /* Workspace of cr_keymap_build for a stream of n ids, in bytes (a first-occurrence bitmap
  * of n bits, its per-word prefix and per-block sums). */

@@ -8,7 +8,8 @@
 //                first-occurrence bitmap;
 //   k_km_insert  inserts every request's id (linear probing, a compare-and-swap claims a
 //                slot) and keeps the id's first request index with an atomic minimum, which
-//                is skipped when the slot already holds a smaller index;
+//                is skipped when the slot already holds a smaller index (the stream goes in
+//                ranges of growing length so that frequent ids are settled early);
 //   k_km_mark    sets bit `first` of the bitmap for every occupied slot;
 //   k_km_sums / k_km_scan_sums / k_km_assign
 //                exclusive prefix of the bitmap's popcounts (per block, then across blocks),
@@ -32,66 +33,79 @@ __host__ __device__ __forceinline__ uint32_t km_slots(uint32_t capacity)
 
 __device__ __forceinline__ uint32_t km_hash(uint32_t id) { return fmix32(id ^ 0x2545F491u); }
 
+// One slot per 16 bytes, {id, first request index, dense index, unused}, so that a probe
+// is one cache-line access. CR_NO_KEY marks an empty slot.
 struct KmTable {
-    uint32_t* ids;    // [S] CR_NO_KEY when empty
-    uint32_t* first;  // [S] first request index of the slot's id
-    uint32_t* dense;  // [S] dense index (valid after the build)
+    uint4* slot;  // [S]
 };
 
-inline KmTable km_table(void* t, uint32_t S)
-{
-    uint32_t* p = reinterpret_cast<uint32_t*>(t);
-    return KmTable{p, p + S, p + 2u * (uint64_t)S};
-}
+inline KmTable km_table(void* t, uint32_t) { return KmTable{reinterpret_cast<uint4*>(t)}; }
 
 __global__ __launch_bounds__(kKmThreads) void k_km_init(KmTable tab, uint32_t S, uint32_t* __restrict__ bitmap,
                                                         uint64_t words)
 {
     const uint64_t stride = (uint64_t)gridDim.x * kKmThreads;
-    for (uint64_t x = (uint64_t)blockIdx.x * kKmThreads + threadIdx.x; x < S; x += stride) {
-        tab.ids[x] = CR_NO_KEY;
-        tab.first[x] = 0xFFFFFFFFu;
-        tab.dense[x] = CR_NO_KEY;
-    }
+    for (uint64_t x = (uint64_t)blockIdx.x * kKmThreads + threadIdx.x; x < S; x += stride)
+        tab.slot[x] = make_uint4(CR_NO_KEY, 0xFFFFFFFFu, CR_NO_KEY, 0u);
     for (uint64_t x = (uint64_t)blockIdx.x * kKmThreads + threadIdx.x; x < words; x += stride) bitmap[x] = 0;
 }
 
-// Slot of id in the table, or S when the id is absent (insert = false) or the table is full.
+// Slot of id in the table, or S when the id is absent (insert = false) or the table is full;
+// *v receives the slot's contents as read (plain loads: a slot's id only ever goes from
+// empty to one id and its first index only decreases, so a stale copy can only cost an
+// extra compare-and-swap or atomic, never a wrong result).
 template <bool kInsert>
-__device__ __forceinline__ uint32_t km_probe(const KmTable& tab, uint32_t S, uint32_t id)
+__device__ __forceinline__ uint32_t km_probe(const KmTable& tab, uint32_t S, uint32_t id, uint4* v)
 {
     uint32_t h = km_hash(id) & (S - 1u);
     for (uint32_t step = 0; step < S; ++step) {
-        uint32_t cur = tab.ids[h];
-        if (cur == id) return h;
-        if (cur == CR_NO_KEY) {
+        uint4 c = tab.slot[h];
+        if (c.x == id) {
+            *v = c;
+            return h;
+        }
+        if (c.x == CR_NO_KEY) {
             if (!kInsert) return S;
-            cur = atomicCAS(tab.ids + h, CR_NO_KEY, id);
-            if (cur == CR_NO_KEY || cur == id) return h;
+            const uint32_t prev = atomicCAS(&tab.slot[h].x, CR_NO_KEY, id);
+            if (prev == CR_NO_KEY || prev == id) {
+                *v = make_uint4(id, prev == id ? c.y : 0xFFFFFFFFu, CR_NO_KEY, 0u);
+                return h;
+            }
         }
         h = (h + 1u) & (S - 1u);
     }
     return S;
 }
 
-__global__ __launch_bounds__(kKmThreads) void k_km_insert(const uint32_t* __restrict__ ids, uint64_t n, KmTable tab,
-                                                          uint32_t S, uint32_t* __restrict__ err)
+// Requests [lo, hi), kKmPer consecutive ones per thread with their loads in flight
+// together. The host runs the stream in ranges of geometrically growing length: a
+// frequent id gets its first index from the first short range, so the many later
+// requests for it see a smaller index already and issue no atomic (same-address atomics
+// are serialised at the cache).
+constexpr uint32_t kKmPer = 4;
+
+__global__ __launch_bounds__(kKmThreads) void k_km_insert(const uint32_t* __restrict__ ids, uint64_t lo, uint64_t hi,
+                                                          KmTable tab, uint32_t S, uint32_t* __restrict__ err)
 {
-    const uint64_t stride = (uint64_t)gridDim.x * kKmThreads;
+    const uint64_t i0 = lo + ((uint64_t)blockIdx.x * kKmThreads + threadIdx.x) * kKmPer;
+    if (i0 >= hi) return;
+    uint32_t id[kKmPer];
+#pragma unroll
+    for (uint32_t t = 0; t < kKmPer; ++t) id[t] = i0 + t < hi ? ids[i0 + t] : CR_NO_KEY;
     uint32_t e = 0;
-    for (uint64_t i = (uint64_t)blockIdx.x * kKmThreads + threadIdx.x; i < n; i += stride) {
-        const uint32_t id = ids[i];
-        if (id == CR_NO_KEY) {
-            e |= CR_ERR_KEY_RANGE;
+#pragma unroll
+    for (uint32_t t = 0; t < kKmPer; ++t) {
+        if (id[t] == CR_NO_KEY) {
+            e |= i0 + t < hi ? CR_ERR_KEY_RANGE : 0u;
             continue;
         }
-        const uint32_t h = km_probe<true>(tab, S, id);
+        uint4 v;
+        const uint32_t h = km_probe<true>(tab, S, id[t], &v);
         if (h == S) {
             e |= CR_ERR_KEYMAP_FULL;
             continue;
         }
-        if (__hip_atomic_load(tab.first + h, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) > (uint32_t)i)
-            atomicMin(tab.first + h, (uint32_t)i);
+        if (v.y > (uint32_t)(i0 + t)) atomicMin(&tab.slot[h].y, (uint32_t)(i0 + t));
     }
     if (e) atomicOr(err, e);
 }
@@ -99,9 +113,10 @@ __global__ __launch_bounds__(kKmThreads) void k_km_insert(const uint32_t* __rest
 __global__ __launch_bounds__(kKmThreads) void k_km_mark(KmTable tab, uint32_t S, uint32_t* __restrict__ bitmap)
 {
     const uint32_t x = blockIdx.x * kKmThreads + threadIdx.x;
-    if (x >= S || tab.ids[x] == CR_NO_KEY) return;
-    const uint32_t f = tab.first[x];
-    atomicOr(bitmap + (f >> 5), 1u << (f & 31u));
+    if (x >= S) return;
+    const uint4 c = tab.slot[x];
+    if (c.x == CR_NO_KEY) return;
+    atomicOr(bitmap + (c.y >> 5), 1u << (c.y & 31u));
 }
 
 __device__ __forceinline__ uint32_t block_sum_u32(uint32_t v, uint32_t* sh)
@@ -169,20 +184,30 @@ __global__ __launch_bounds__(kKmThreads) void k_km_assign(KmTable tab, uint32_t 
                                                           const uint32_t* __restrict__ prefix)
 {
     const uint32_t x = blockIdx.x * kKmThreads + threadIdx.x;
-    if (x >= S || tab.ids[x] == CR_NO_KEY) return;
-    const uint32_t f = tab.first[x];
-    tab.dense[x] = prefix[f >> 5] + __popc(bitmap[f >> 5] & ((1u << (f & 31u)) - 1u));
+    if (x >= S) return;
+    const uint4 c = tab.slot[x];
+    if (c.x == CR_NO_KEY) return;
+    const uint32_t f = c.y;
+    tab.slot[x].z = prefix[f >> 5] + __popc(bitmap[f >> 5] & ((1u << (f & 31u)) - 1u));
 }
 
 __global__ __launch_bounds__(kKmThreads) void k_km_lookup(const uint32_t* __restrict__ ids, uint64_t n, KmTable tab,
                                                           uint32_t S, uint32_t* __restrict__ dense)
 {
-    const uint64_t stride = (uint64_t)gridDim.x * kKmThreads;
-    for (uint64_t i = (uint64_t)blockIdx.x * kKmThreads + threadIdx.x; i < n; i += stride) {
-        const uint32_t id = ids[i];
-        const uint32_t h = id == CR_NO_KEY ? S : km_probe<false>(tab, S, id);
-        dense[i] = h < S ? tab.dense[h] : CR_NO_KEY;
+    const uint64_t i0 = ((uint64_t)blockIdx.x * kKmThreads + threadIdx.x) * kKmPer;
+    if (i0 >= n) return;
+    uint32_t id[kKmPer], d[kKmPer];
+#pragma unroll
+    for (uint32_t t = 0; t < kKmPer; ++t) id[t] = i0 + t < n ? ids[i0 + t] : CR_NO_KEY;
+#pragma unroll
+    for (uint32_t t = 0; t < kKmPer; ++t) {
+        uint4 v;
+        const uint32_t h = id[t] == CR_NO_KEY ? S : km_probe<false>(tab, S, id[t], &v);
+        d[t] = h < S ? v.z : CR_NO_KEY;
     }
+#pragma unroll
+    for (uint32_t t = 0; t < kKmPer; ++t)
+        if (i0 + t < n) dense[i0 + t] = d[t];
 }
 
 __global__ __launch_bounds__(kKmThreads) void k_km_scatter(KmTable tab, uint32_t S, const uint32_t* __restrict__ ids,
@@ -192,11 +217,9 @@ __global__ __launch_bounds__(kKmThreads) void k_km_scatter(KmTable tab, uint32_t
     const uint64_t stride = (uint64_t)gridDim.x * kKmThreads;
     for (uint64_t x = (uint64_t)blockIdx.x * kKmThreads + threadIdx.x; x < m; x += stride) {
         const uint32_t id = ids[x];
-        const uint32_t h = id == CR_NO_KEY ? S : km_probe<false>(tab, S, id);
-        if (h < S) {
-            const uint32_t k = tab.dense[h];
-            if (k < out_len) out[k] = values[x];
-        }
+        uint4 v;
+        const uint32_t h = id == CR_NO_KEY ? S : km_probe<false>(tab, S, id, &v);
+        if (h < S && v.z < out_len) out[v.z] = values[x];
     }
 }
 
@@ -215,7 +238,7 @@ inline uint64_t km_nsums(uint64_t n) { return (km_words(n) + kKmWordsPerBlock - 
 
 extern "C" size_t cr_keymap_bytes(uint32_t capacity)
 {
-    return (size_t)3u * cr::km_slots(capacity) * sizeof(uint32_t);
+    return (size_t)cr::km_slots(capacity) * sizeof(uint4);
 }
 
 extern "C" size_t cr_keymap_workspace_bytes(uint64_t n)
@@ -233,7 +256,7 @@ extern "C" cr_status cr_keymap_build(const uint32_t* ids, uint64_t n, uint32_t c
         (n > 0 && !ids) || n >= 0xFFFFFFFFull)
         return CR_EINVAL;
     if (table_bytes < cr_keymap_bytes(capacity) || ws_bytes < cr_keymap_workspace_bytes(n)) return CR_ESIZE;
-    if (((uintptr_t)table & 3u) || ((uintptr_t)ws & 3u) || ((uintptr_t)ids & 3u)) return CR_EINVAL;
+    if (((uintptr_t)table & 15u) || ((uintptr_t)ws & 3u) || ((uintptr_t)ids & 3u)) return CR_EINVAL;
     const uint64_t words = km_words(n), nsums = km_nsums(n);
     if (nsums > kKmMaxSums) return CR_EINVAL;
     const uint32_t S = km_slots(capacity);
@@ -244,7 +267,12 @@ extern "C" cr_status cr_keymap_build(const uint32_t* ids, uint64_t n, uint32_t c
     const hipStream_t st = as_stream(stream);
     (void)hipGetLastError();
     hipLaunchKernelGGL(k_km_init, dim3(km_grid(words > S ? words : S)), dim3(kKmThreads), 0, st, tab, S, bitmap, words);
-    if (n) hipLaunchKernelGGL(k_km_insert, dim3(km_grid(n)), dim3(kKmThreads), 0, st, ids, n, tab, S, err);
+    for (uint64_t lo = 0, len = (n + 255) / 256; lo < n; lo += len, len *= 4) {
+        const uint64_t hi = n - lo < len ? n : lo + len;
+        const uint64_t threads = (hi - lo + kKmPer - 1) / kKmPer;
+        hipLaunchKernelGGL(k_km_insert, dim3((uint32_t)((threads + kKmThreads - 1) / kKmThreads)), dim3(kKmThreads), 0,
+                           st, ids, lo, hi, tab, S, err);
+    }
     hipLaunchKernelGGL(k_km_mark, dim3((S + kKmThreads - 1) / kKmThreads), dim3(kKmThreads), 0, st, tab, S, bitmap);
     if (nsums) {
         hipLaunchKernelGGL(k_km_sums, dim3((uint32_t)nsums), dim3(kKmThreads), 0, st, bitmap, words, sums);
@@ -266,9 +294,10 @@ extern "C" cr_status cr_keymap_lookup(const void* table, size_t table_bytes, uin
     if (table_bytes < cr_keymap_bytes(capacity)) return CR_ESIZE;
     if (n == 0) return CR_OK;
     const uint32_t S = km_slots(capacity);
+    const uint64_t threads = (n + kKmPer - 1) / kKmPer;
     (void)hipGetLastError();
-    hipLaunchKernelGGL(k_km_lookup, dim3(km_grid(n)), dim3(kKmThreads), 0, as_stream(stream), ids, n,
-                       km_table(const_cast<void*>(table), S), S, dense);
+    hipLaunchKernelGGL(k_km_lookup, dim3((uint32_t)((threads + kKmThreads - 1) / kKmThreads)), dim3(kKmThreads), 0,
+                       as_stream(stream), ids, n, km_table(const_cast<void*>(table), S), S, dense);
     return hipGetLastError() == hipSuccess ? CR_OK : CR_EHIP;
 }
 

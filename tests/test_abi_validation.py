@@ -136,7 +136,7 @@ def test_replay_rejects(L):
 def test_keymap_rejects(L):
     tb = L.cr_keymap_bytes(100)
     ws = L.cr_keymap_workspace_bytes(1000)
-    assert tb >= 3 * 4 * 200 and L.cr_keymap_bytes(1) >= 3 * 4 * 64
+    assert tb >= 16 * 200 and L.cr_keymap_bytes(1) >= 16 * 64
     assert L.cr_keymap_workspace_bytes(10**6) > ws > 0
     ok = (FAKE, 1000, 100, FAKE, tb, FAKE, ws, FAKE, FAKE, None)
     assert L.cr_keymap_build(*ok[:2], 0, *ok[3:]) == B.CR_EINVAL                    # capacity 0
