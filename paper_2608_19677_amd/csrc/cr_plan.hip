@@ -348,8 +348,10 @@ __global__ __launch_bounds__(kSortBlock) void k_sort_window(const uint32_t* __re
 // LDS atomics. Same three steps and results as k_sort_window.
 constexpr uint32_t kRegCmax = 2048;
 
+// Up to 20 counts per thread the kernel fits 64 VGPRs, which leaves room for two blocks
+// per CU (8 wavefronts per SIMD); the windows are independent, so that halves the rounds.
 template <int kNpl>
-__global__ __launch_bounds__(kSortBlock) void k_sort_window_reg(const uint32_t* __restrict__ counts, uint32_t K,
+__global__ __launch_bounds__(kSortBlock, kNpl <= 20 ? 8 : 1) void k_sort_window_reg(const uint32_t* __restrict__ counts, uint32_t K,
                                                                 uint32_t Cmax, uint32_t* __restrict__ order,
                                                                 uint32_t* __restrict__ order_count,
                                                                 uint32_t* __restrict__ n_order,
