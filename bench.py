@@ -2,20 +2,24 @@
 
 A step is one pass of the whole path over the 70B-like workload (20,000 keys, Zipf 1.0
 capped at a 0.3 % share, 1e7 requests at 176 QPS in 60-s control intervals = 948
-intervals, 30 destinations x 64 LRU slots). By default the steps are consecutive chunks of
-one stream: chunk k is planned from chunk k-1's last window, replays from chunk k-1's final
-cache state, and is counted, planned, routed and partitioned on one HIP stream while chunk
-k-1 replays on another (--schedule serial: every step from scratch on one stream). Inputs
-are resident in HBM before timing starts. Prints ONE JSON line.
+intervals, 30 destinations x 64 LRU slots), from scratch on one stream. The timed steps
+replay that step captured once as a HIP graph (--eager: plain launches); the per-stage
+times and the roofline come from an eager pass with HIP events around each library call.
+--schedule overlap instead runs consecutive chunks of one stream, chunk k planned on one
+HIP stream while chunk k-1 replays on another (cache state and last window carried).
+Inputs are resident in HBM before timing starts. Prints ONE JSON line.
 
-  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload llama70b|tiny|replication|burst|drift]
-                  [--schedule overlap|serial]
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--eager] [--schedule serial|overlap]
+                  [--workload llama70b|tiny|replication|burst|drift|ablation|llama70b_gamma]
+                  [--dispatch static|live] [--opaque]
 
 --workload drift times the replanning study instead (six drift intervals of 1e6 requests,
 fresh and held plans as six candidates, 600 statistics bins, churn between consecutive
 fresh plans) and adds its per-transition report under "study". --workload ablation times
 the component ablation (the injected-whale stream under the flat, affinity, replicated
 and full plans as four candidates) and adds the hit and imbalance of each under "study".
+--dispatch live routes by running loads within each interval; --opaque remaps salted
+32-bit ids to dense keys on the device inside every step.
 """
 from __future__ import annotations
 
@@ -54,6 +58,9 @@ def parse():
     ap.add_argument("--opaque", action="store_true",
                     help="keys arrive as salted 32-bit ids: every step first builds the device directory and "
                          "remaps the stream to dense keys (timed as stage 'remap')")
+    ap.add_argument("--eager", action="store_true",
+                    help="time eager launches instead of replays of the step captured as one HIP graph (the "
+                         "per-stage times always come from an eager pass; studies and --opaque run eagerly)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-unbatched", action="store_true",
@@ -213,6 +220,17 @@ def main():
         torch.cuda.synchronize()
         t1 = time.perf_counter()
         last = gp
+        if not args.eager and study is None and remap is None:
+            # the step as one HIP graph: replays replace the eager launches in the timed region
+            gp.capture()
+            for _ in range(args.warmup):
+                gp.replay_graph()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for _ in range(args.steps):
+                gp.replay_graph()
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
     else:
         cs = ChunkStream(wl, device="cuda:0")
         for _ in range(args.warmup):
@@ -285,6 +303,8 @@ def main():
     out["config"]["plan_builds"] = n_plans
     out["config"]["schedule"] = args.schedule
     out["config"]["dispatch"] = args.dispatch
+    out["config"]["launch"] = "eager" if (args.eager or study is not None or remap is not None
+                                          or args.schedule != "serial") else "hip-graph"
     if remap is not None:
         torch.cuda.synchronize()
         assert int(km_err.item()) == 0

@@ -62,7 +62,7 @@ struct PartGeom {
 
 inline PartGeom part_geom(uint64_t n, uint32_t P)
 {
-    const uint64_t target = 8192u / P > 0 ? 8192u / P : 1u;
+    const uint64_t target = 16384u / P > 0 ? 16384u / P : 1u;
     uint64_t tile = (n + target - 1) / target;
     tile = (tile + 1023) & ~1023ull;  // whole sub-tiles of the scatter
     if (tile < 1024) tile = 1024;

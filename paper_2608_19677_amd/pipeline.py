@@ -190,6 +190,22 @@ class Pipeline:
         for s in self.STAGES:
             getattr(self, s)(stream)
 
+    def capture(self):
+        """Record one step as a HIP graph (every library call only enqueues kernels on the
+        current stream, and the statistics are cleared by a fill kernel, not a memset)."""
+        side = torch.cuda.Stream(device=self.device)
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            self.step()
+        torch.cuda.current_stream().wait_stream(side)
+        self.graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(self.graph):
+            self.step()
+        return self.graph
+
+    def replay_graph(self):
+        self.graph.replay()
+
     # -- host views for checking -------------------------------------------------------
     def host(self) -> dict:
         torch.cuda.synchronize()

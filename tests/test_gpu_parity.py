@@ -280,3 +280,27 @@ def test_live_dispatch_70b_gamma_full_parity():
     gp = Pipeline(wl, dispatch="live")
     gp.step()
     compare_all(wl, gp, gp.host(), opipe.run(wl, dispatch="live"))
+
+
+def test_graph_replays_equal_eager_steps():
+    # one step captured as a HIP graph and replayed three times, with eager work between the
+    # replays; every replay must reproduce the eager step exactly
+    wl = wl_mod.small_random(51, num_keys=900, n=150_000, R=30, Ws=[32, 64], J=6, hot=3, hot_share=0.3)
+    say(f"[case] graph n={wl.n} J={wl.J} P={wl.P}")
+    gp = Pipeline(wl)
+    gp.step()
+    ref = gp.host()
+    other = Pipeline(wl_mod.small_random(52, num_keys=300, n=40_000, R=16, Ws=[8], J=3))
+    gp.capture()
+    torch.cuda.synchronize()
+    for r in range(3):
+        other.step()  # eager work between replays
+        gp.err.zero_()
+        gp.dest.zero_()
+        gp.stats.fill_(7)
+        gp.replay_graph()
+        h = gp.host()
+        for k in ("counts", "order", "num_admitted", "members", "load", "route", "dest", "stats", "lru"):
+            assert np.array_equal(np.asarray(h[k]).view(np.uint8), np.asarray(ref[k]).view(np.uint8)), (r, k)
+        assert h["err"] == 0
+    compare_all(wl, gp, h, opipe.run(wl))
