@@ -870,7 +870,9 @@ __global__ __launch_bounds__(64) void k_lpt_small(uint32_t KW, uint32_t R, uint3
                                                   uint16_t* __restrict__ members, double* __restrict__ load,
                                                   uint32_t* __restrict__ route)
 {
-    __shared__ uint32_t s_mem[128];  // member picked for single-copy job a, slot a mod 128
+    // member picked for single-copy job a in slot a mod 128; slots 128.. take the stores of
+    // lanes >= R so that the round loop needs no divergent branch
+    __shared__ uint32_t s_mem[192];
     const uint32_t p = blockIdx.x, lane = lane_id();
     const cr_plan_spec spec = specs[p];
     if (hash_placed(spec.variant)) return;  // placed by cr_place_hash
@@ -892,6 +894,9 @@ __global__ __launch_bounds__(64) void k_lpt_small(uint32_t KW, uint32_t R, uint3
     const uint64_t rmask = R >= 64 ? ~0ull : ((1ull << R) - 1ull);
     uint32_t base = 0, t = 0;
     while (base + t < A) {
+        // the loop state is uniform; saying so keeps it (and the masks built from it) scalar
+        t = (uint32_t)__builtin_amdgcn_readfirstlane((int)t);
+        base = (uint32_t)__builtin_amdgcn_readfirstlane((int)base);
         if (t >= 64) {  // retire the current batch, promote the next one
             const uint32_t fm = s_mem[(base + lane) & 127u];
             if (base + lane < A) {
@@ -931,7 +936,7 @@ __global__ __launch_bounds__(64) void k_lpt_small(uint32_t KW, uint32_t R, uint3
                     round = ballot(lane < R && cq != c0) == 0 && ballot(lane + 1 < R && an == a && rn < rv) == 0;
                 }
                 if (round) {
-                    if (lane < R) Lv = a;
+                    Lv = lane < R ? a : Lv;
                     t += M;
                     // Further full rounds of the same run: the next R jobs have the same x, so
                     // the batch test reduces to every load being below min L + x, and the
@@ -951,11 +956,10 @@ __global__ __launch_bounds__(64) void k_lpt_small(uint32_t KW, uint32_t R, uint3
                         const uint32_t rn2 = dpp_shl1(rv, rv);
                         if (ballot(lane < R && !(Lv < v0)) != 0 || ballot(lane + 1 < R && ann == an && rn2 < rv) != 0)
                             break;
-                        if (lane < R) {
-                            s_mem[(base + t + lane) & 127u] = rv;
-                            Lv = an;
-                        }
+                        s_mem[lane < R ? ((base + t + lane) & 127u) : 128u + lane] = rv;
+                        Lv = lane < R ? an : Lv;
                         t += R;
+                        t = (uint32_t)__builtin_amdgcn_readfirstlane((int)t);
                     }
                     continue;
                 } else {
