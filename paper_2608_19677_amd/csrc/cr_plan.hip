@@ -650,8 +650,11 @@ __device__ void build_key_index(const uint32_t* __restrict__ ord, uint32_t A, ui
     }
 }
 
-// One block per plan: Eq. 1, the prefix admission and the plan's key index.
-__global__ __launch_bounds__(kSortThreads) void k_admit_plan(
+// One block per plan: Eq. 1, the prefix admission and the plan's key index. Blocks of 8
+// wavefronts: four fit on a CU, so a step's plans run in one round.
+constexpr int kAdmitThreads = 512;
+
+__global__ __launch_bounds__(kAdmitThreads) void k_admit_plan(
     uint32_t R, uint32_t Cmax, uint32_t NW, uint32_t KW,
     const cr_plan_spec* __restrict__ specs, const uint32_t* __restrict__ order,
     const uint32_t* __restrict__ order_count, const uint32_t* __restrict__ n_order,
@@ -1364,7 +1367,7 @@ extern "C" cr_status cr_admit(const uint32_t* counts, const cr_plan_set* plans, 
         hipLaunchKernelGGL(k_sort_window<false>, dim3(plans->num_windows), dim3(kSortBlock), 0, st, counts,
                            plans->num_keys, cmax, plans->order, plans->order_count, plans->n_order, row_sum, buf);
     }
-    hipLaunchKernelGGL(k_admit_plan, dim3(plans->num_plans), dim3(kSortThreads), 0, st, plans->R, cmax,
+    hipLaunchKernelGGL(k_admit_plan, dim3(plans->num_plans), dim3(kAdmitThreads), 0, st, plans->R, cmax,
                        plans->num_windows, key_words(plans->num_keys), plans->specs, plans->order, plans->order_count,
                        plans->n_order, row_sum, plans->num_admitted, plans->cold, plans->clamped, plans->member_off,
                        plans->key_index, err);
