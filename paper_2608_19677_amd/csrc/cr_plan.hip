@@ -795,9 +795,11 @@ __device__ __forceinline__ uint32_t kx_rank(ulonglong2 e, uint32_t b)
 // the sequential picks do as long as, for every q, lane q's load is below every charged
 // load L_q' + x_q' of the earlier lanes q' < q (lane q is then the least (L, r) pair when
 // job t+q is placed); an exclusive prefix minimum across the lanes gives the longest such
-// batch M in one pass, ties ending it. The M charged lanes are merged back by rank: one
-// pass over them yields, through ballots, every lane's new position, and one forward lane
-// permutation applies it. A full round (M = R, equal x, order kept) needs no permutation.
+// batch M in one pass, ties ending it. The M charged lanes are merged back by rank: every
+// lane's new position is the number of lanes with a smaller (L, r), counted either by
+// pairwise exchanges over all lanes (many charged lanes) or by one ballot pass per charged
+// lane (few), and one forward lane permutation applies it. A full round (M = R, equal x,
+// order kept) needs no permutation.
 // A batch of one is a single pick: three compares give the insertion rank and a one-lane
 // DPP shift opens the slot; a job with k > 1 pops k lanes and re-inserts each.
 // Admitted keys sit in two 64-key batches so a batch of jobs may straddle the boundary;
@@ -806,17 +808,29 @@ struct LptRaw {
     uint32_t key, cnt, off, end;
 };
 
+// Unconditional loads (the index is clamped into the plan's rows; entries past A are
+// garbage and every use is masked by a < A): a load under an exec mask merges with a zero
+// default, and that merge makes the wavefront wait for the load on the spot.
 __device__ __forceinline__ LptRaw lpt_raw(const uint32_t* __restrict__ ord, const uint32_t* __restrict__ ocnt,
-                                          const uint32_t* __restrict__ moff, uint32_t a, uint32_t A)
+                                          const uint32_t* __restrict__ moff, uint32_t a, uint32_t Cmax)
 {
-    LptRaw r{0u, 0u, 0u, 0u};
-    if (a < A) {
-        r.key = ord[a];
-        r.cnt = ocnt[a];
-        r.off = moff[a];
-        r.end = moff[a + 1];
-    }
-    return r;
+    const uint32_t i = a < Cmax ? a : Cmax - 1u;
+    return LptRaw{ord[i], ocnt[i], moff[i], moff[i + 1u]};
+}
+
+// The key index entry of key b as {bits lo, bits hi, rank of the word's first admitted key}
+// (12 bytes: a 16-byte load would leave a dead register that the compiler may reuse, and
+// the reuse has to wait for the load). Word indices past KW read word 0.
+__device__ __forceinline__ uint3 kx_entry3(const uint64_t* __restrict__ kx, uint32_t b, uint32_t KW)
+{
+    const uint32_t w = (b >> 6) < KW ? (b >> 6) : 0u;
+    return *reinterpret_cast<const uint3*>(kx + 2u * w);
+}
+
+__device__ __forceinline__ uint32_t kx_rank3(uint3 e, uint32_t b)
+{
+    const uint64_t bits = ((uint64_t)e.y << 32) | e.x;
+    return e.z + (uint32_t)__popcll(bits & ((1ull << (b & 63u)) - 1ull));
 }
 
 __device__ __forceinline__ uint32_t ds_permute_u32(uint32_t dst_lane, uint32_t v)
@@ -834,6 +848,13 @@ __device__ __forceinline__ double ds_permute_f64(uint32_t dst_lane, double v)
 __device__ __forceinline__ uint32_t ds_bpermute_u32(uint32_t src_lane, uint32_t v)
 {
     return (uint32_t)__builtin_amdgcn_ds_bpermute((int)(src_lane << 2), (int)v);
+}
+
+__device__ __forceinline__ double ds_bpermute_f64(uint32_t src_lane, double v)
+{
+    const uint64_t u = (uint64_t)__double_as_longlong(v);
+    const uint32_t lo = ds_bpermute_u32(src_lane, (uint32_t)u), hi = ds_bpermute_u32(src_lane, (uint32_t)(u >> 32));
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
 }
 
 // DPP move of a double; lanes whose source is outside the pattern (or whose row is masked
@@ -889,162 +910,218 @@ __global__ __launch_bounds__(64) void k_lpt_small(uint32_t KW, uint32_t R, uint3
     uint32_t* __restrict__ rw = route + (uint64_t)p * Cmax;
     double Lv = lane < R ? (double)cold[p] / (double)R : INFINITY;
     uint32_t rv = lane < R ? lane : 0xFFFFu;
-    LptRaw cur = lpt_raw(ord, ocnt, moff, lane, A);
-    LptRaw nxt = lpt_raw(ord, ocnt, moff, 64 + lane, A);
-    ulonglong2 kxc = kx_entry(kx, cur.key, lane < A);  // needed when the batch retires
-    uint32_t kc = cur.end - cur.off;                   // k of the current batch's keys (0 past A)
-    double xc = kc == 1 ? (double)cur.cnt : (double)cur.cnt / (double)(kc ? kc : 1u);
+    // Three 64-job batches in registers: the one being placed (cur), the next (nxt: a batch of
+    // jobs may reach into it) and the one after (nx2), loaded a whole batch before it is first
+    // read. The three register sets take these roles in turn (the step below is inlined three
+    // times), so a retired batch's registers are reloaded in place with no copy. What the
+    // placement loop reads of the batches (kc, xc, mc, mn, coff) is derived when the previous
+    // batch retires, before that retire issues its loads: every wait is then for loads issued
+    // a batch earlier, and the loop reads no register a load wrote (a loop that stores and
+    // reads such registers gets a wait for every outstanding load at its entry).
+    LptRaw s0 = lpt_raw(ord, ocnt, moff, lane, Cmax);
+    LptRaw s1 = lpt_raw(ord, ocnt, moff, 64 + lane, Cmax);
+    LptRaw s2 = lpt_raw(ord, ocnt, moff, 128 + lane, Cmax);
+    uint3 kxc = kx_entry3(kx, s0.key, KW);                  // needed when the batch retires
+    uint32_t kc = lane < A ? s0.end - s0.off : 0u;         // k of the current batch's keys (0 past A)
+    double xc = kc == 1 ? (double)s0.cnt : (double)s0.cnt / (double)(kc ? kc : 1u);
+    // lane q: the count of job base+q (mc) or base+64+q (mn) if it is a single-copy job, else
+    // ~0; the current batch's member offsets xor k (coff)
+    uint32_t mc = kc == 1 ? s0.cnt : 0xFFFFFFFFu;
+    uint32_t mn = s1.end - s1.off == 1 ? s1.cnt : 0xFFFFFFFFu;
+    uint32_t coff = s0.off ^ kc;
     const uint64_t rmask = R >= 64 ? ~0ull : ((1ull << R) - 1ull);
+    const uint32_t P2 = R <= 1u ? 1u : 1u << (32 - __builtin_clz(R - 1u));  // power of two >= R
     uint32_t base = 0, t = 0;
-    while (base + t < A) {
-        // the loop state is uniform; saying so keeps it (and the masks built from it) scalar
-        t = (uint32_t)__builtin_amdgcn_readfirstlane((int)t);
-        base = (uint32_t)__builtin_amdgcn_readfirstlane((int)base);
-        if (t >= 64) {  // retire the current batch, promote the next one
+    // Places jobs until the current batch retires (true: cur now holds the batch after nx2,
+    // nxt is current) or every job is placed (false, after the final retire).
+    auto step = [&](LptRaw& cur, const LptRaw& nxt, const LptRaw& nx2) __attribute__((always_inline)) -> bool {
+        while (base + t < A) {
+            // the loop state is uniform; saying so keeps it (and the masks built from it) scalar
+            t = (uint32_t)__builtin_amdgcn_readfirstlane((int)t);
+            base = (uint32_t)__builtin_amdgcn_readfirstlane((int)base);
+            if (t >= 64) {  // retire the current batch; its registers take the batch after nx2
+                const uint32_t fm = s_mem[(base + lane) & 127u];
+                const uint32_t rk = kx_rank3(kxc, cur.key);
+                const bool one = kc == 1, live = base + lane < A;
+                const uint32_t roff = coff ^ kc;
+                kc = base + 64 + lane < A ? nxt.end - nxt.off : 0u;
+                xc = (double)nxt.cnt;
+                if (ballot(kc > 1)) xc = kc > 1 ? (double)nxt.cnt / (double)kc : xc;
+                mc = kc == 1 ? nxt.cnt : 0xFFFFFFFFu;
+                mn = nx2.end - nx2.off == 1 ? nx2.cnt : 0xFFFFFFFFu;
+                coff = nxt.off ^ kc;
+                kxc = kx_entry3(kx, nxt.key, KW);
+                if (live) {
+                    if (one) mem[roff] = (uint16_t)fm;
+                    rw[rk] = one ? (CR_ROUTE_SINGLE | fm) : (base + lane);
+                }
+                base += 64;
+                t -= 64;
+                cur = lpt_raw(ord, ocnt, moff, base + 128 + lane, Cmax);
+                return true;
+            }
+            const uint32_t k = rdlane(kc, t);
+            if (k == 1) {
+                // lane q looks at job t+q: its count if it is a single-copy job, else ~0
+                const uint32_t src = (lane + t) & 63u;
+                const uint32_t c1 = ds_bpermute_u32(src, mc), c2 = ds_bpermute_u32(src, mn);
+                const uint32_t cq = lane + t < 64u ? c1 : c2;
+                const bool jq = lane < R && cq != 0xFFFFFFFFu && base + t + lane < A;
+                const double a = Lv + (double)cq;  // lane q's load once charged with job t+q
+                const double pm = wave_exclusive_min_f64(jq ? a : INFINITY);
+                const uint64_t okm = ballot(jq && (lane == 0 || Lv < pm));
+                const uint32_t M = ~okm ? (uint32_t)__builtin_ctzll(~okm) : 64u;
+                if (M >= 2) {
+                    if (lane < M) s_mem[(base + t + lane) & 127u] = rv;
+                    bool round = false;
+                    const uint32_t c0 = rdlane(cq, 0);
+                    if (M == R) {
+                        const double an = dpp_shl1_f64(a);
+                        const uint32_t rn = dpp_shl1(rv, rv);
+                        round = ballot(lane < R && cq != c0) == 0 && ballot(lane + 1 < R && an == a && rn < rv) == 0;
+                    }
+                    if (round) {
+                        Lv = lane < R ? a : Lv;
+                        t += M;
+                        // Further full rounds of the same run: the next R jobs have the same x, so
+                        // the batch test reduces to every load being below min L + x, and the
+                        // order test to the charged loads keeping their (L, r) order.
+                        // (c0 is a single-copy job's count, never ~0)
+                        const uint64_t same_c = ballot(mc == c0 && base + lane < A);
+                        const uint64_t same_n = ballot(mn == c0 && base + 64 + lane < A);
+                        const double x0 = (double)c0;
+                        while (t < 64) {
+                            // jobs t .. t+R-1 must all be single-copy jobs of count c0
+                            const uint32_t e = t + R;  // one past the last job of the round (<= 128)
+                            const uint64_t need_c = (e >= 64 ? ~0ull : ((1ull << e) - 1ull)) & ~((1ull << t) - 1ull);
+                            const uint64_t need_n = e > 64 ? (e >= 128 ? ~0ull : ((1ull << (e - 64)) - 1ull)) : 0ull;
+                            if ((same_c & need_c) != need_c || (same_n & need_n) != need_n) break;
+                            const double an = Lv + x0;
+                            const double v0 = rdlane_f64(an, 0);
+                            const double ann = dpp_shl1_f64(an);
+                            const uint32_t rn2 = dpp_shl1(rv, rv);
+                            if (ballot(lane < R && !(Lv < v0)) != 0 || ballot(lane + 1 < R && ann == an && rn2 < rv) != 0)
+                                break;
+                            s_mem[lane < R ? ((base + t + lane) & 127u) : 128u + lane] = rv;
+                            Lv = lane < R ? an : Lv;
+                            t += R;
+                            t = (uint32_t)__builtin_amdgcn_readfirstlane((int)t);
+                        }
+                        continue;
+                    } else {
+                        const bool charged = lane < M;
+                        const double av = charged ? a : Lv;
+                        uint32_t np = 0;
+                        if (4u * M > P2) {
+                            // All pairs: lane i counts the lanes with a smaller (L, r) by meeting
+                            // lane i ^ s for s = 1 .. P2-1 (every lane of the power-of-two block
+                            // that holds the R destinations, once). The exchanges are independent
+                            // of one another; lanes >= R hold +inf and count for no one.
+                            // (o, orv) < (av, rv), without branches
+                            auto less = [&](double o, uint32_t orv) {
+                                return (uint32_t)((o < av) | ((o == av) & (orv < rv)));
+                            };
+                            // P2 >= 2 here (M >= 2): s = 1, then 2 .. 3, then four at a time with
+                            // the four exchanges issued before any compare
+                            np = less(ds_bpermute_f64(lane ^ 1u, av), ds_bpermute_u32(lane ^ 1u, rv));
+                            if (P2 >= 4) {
+                                const double o2 = ds_bpermute_f64(lane ^ 2u, av), o3 = ds_bpermute_f64(lane ^ 3u, av);
+                                const uint32_t r2 = ds_bpermute_u32(lane ^ 2u, rv), r3 = ds_bpermute_u32(lane ^ 3u, rv);
+                                np += less(o2, r2) + less(o3, r3);
+                            }
+                            for (uint32_t s = 4; s < P2; s += 4) {
+                                const uint32_t i0 = lane ^ s, i1 = lane ^ (s + 1u), i2 = lane ^ (s + 2u), i3 = lane ^ (s + 3u);
+                                const double o0 = ds_bpermute_f64(i0, av), o1 = ds_bpermute_f64(i1, av);
+                                const double o2 = ds_bpermute_f64(i2, av), o3 = ds_bpermute_f64(i3, av);
+                                const uint32_t r0 = ds_bpermute_u32(i0, rv), r1 = ds_bpermute_u32(i1, rv);
+                                const uint32_t r2 = ds_bpermute_u32(i2, rv), r3 = ds_bpermute_u32(i3, rv);
+                                np += less(o0, r0) + less(o1, r1) + less(o2, r2) + less(o3, r3);
+                            }
+                            np = lane < R ? np : lane;
+                        } else {
+                            // Few charged lanes: one pass per charged lane q. The lanes preceding
+                            // lane q form a lane mask; uncharged lanes after q count it.
+                            uint32_t cnt = 0;
+                            const uint64_t unch = rmask & ~((M >= 64 ? ~0ull : (1ull << M) - 1ull));
+                            auto pass = [&](uint32_t q) {
+                                const double aq = rdlane_f64(av, q);
+                                const uint32_t rq = rdlane(rv, q);
+                                const uint64_t bm = ballot(av < aq) | (ballot(av == aq) & ballot(rv < rq));
+                                cnt += __builtin_amdgcn_inverse_ballot_w64(unch & ~bm) ? 1u : 0u;
+                                return (uint32_t)__popcll(bm & rmask);
+                            };
+                            uint32_t q = 0;
+                            for (; q + 1 < M; q += 2) {
+                                const uint32_t r0 = pass(q), r1 = pass(q + 1);
+                                cnt = wrlane(wrlane(cnt, r0, q), r1, q + 1);
+                            }
+                            if (q < M) {
+                                const uint32_t rl = pass(q);  // before cnt is read: pass() adds to it
+                                cnt = wrlane(cnt, rl, q);
+                            }
+                            np = charged ? cnt : (lane < R ? lane - M + cnt : lane);
+                        }
+                        Lv = ds_permute_f64(np, av);
+                        rv = ds_permute_u32(np, rv);
+                    }
+                    t += M;
+                    continue;
+                }
+                const double x = rdlane_f64(xc, t);
+                const double v0 = rdlane_f64(Lv, 0) + x;
+                const uint32_t r0 = rdlane(rv, 0);
+                if (lane == 0) s_mem[(base + t) & 127u] = r0;
+                // rank of (v0, r0) among lanes 1..: three compares, each straight to a lane mask
+                const uint64_t m_lt = ballot(Lv < v0), m_eq = ballot(Lv == v0), m_r = ballot(rv < r0);
+                const uint32_t pos = (uint32_t)__popcll((m_lt | (m_eq & m_r)) & ~1ull);
+                const double sl = dpp_shl1_f64(Lv);
+                const uint32_t sr = dpp_shl1(rv, rv);
+                const bool lt = lane < pos, eq = lane == pos;
+                Lv = lt ? sl : (eq ? v0 : Lv);
+                rv = lt ? sr : (eq ? r0 : rv);
+            } else {
+                const double x = rdlane_f64(xc, t);
+                const uint32_t off = rdlane(coff, t) ^ k;
+                if (lane < k) mem[off + lane] = (uint16_t)rv;
+                const double vnew = Lv + x;  // meaningful on lanes < k
+                const uint32_t rnew = rv;
+                const double sL = __shfl(Lv, (int)((lane + k) & 63u), 64);
+                const uint32_t sR = __shfl(rv, (int)((lane + k) & 63u), 64);
+                Lv = lane + k < 64u ? sL : INFINITY;
+                rv = lane + k < 64u ? sR : 0xFFFFu;
+                for (uint32_t u = 0; u < k; ++u) {
+                    const double v = rdlane_f64(vnew, u);
+                    const uint32_t r = rdlane(rnew, u);
+                    const uint64_t m_lt = ballot(Lv < v), m_eq = ballot(Lv == v), m_r = ballot(rv < r);
+                    const uint32_t pos = (uint32_t)__popcll(m_lt | (m_eq & m_r));
+                    const double up = dpp_shr1_f64(Lv);
+                    const uint32_t upr = dpp_shr1(rv, rv);
+                    const bool gt = lane > pos, eq = lane == pos;
+                    Lv = gt ? up : (eq ? v : Lv);
+                    rv = gt ? upr : (eq ? r : rv);
+                }
+            }
+            ++t;
+        }
+        // retire what is left (the current batch, and the next one if a batch of jobs reached it)
+        {
             const uint32_t fm = s_mem[(base + lane) & 127u];
             if (base + lane < A) {
                 if (kc == 1) mem[cur.off] = (uint16_t)fm;
-                rw[kx_rank(kxc, cur.key)] = kc == 1 ? (CR_ROUTE_SINGLE | fm) : (base + lane);
-            }
-            cur = nxt;
-            kxc = kx_entry(kx, cur.key, base + 64 + lane < A);
-            kc = cur.end - cur.off;
-            xc = (double)cur.cnt;
-            if (ballot(kc > 1)) xc = kc > 1 ? (double)cur.cnt / (double)kc : xc;
-            base += 64;
-            t -= 64;
-            nxt = lpt_raw(ord, ocnt, moff, base + 64 + lane, A);
-            continue;
-        }
-        const uint32_t k = rdlane(kc, t);
-        if (k == 1) {
-            // lane q looks at job t+q: its count if it is a single-copy job, else ~0
-            const uint32_t mc = kc == 1 ? cur.cnt : 0xFFFFFFFFu;
-            const uint32_t mn = nxt.end - nxt.off == 1 ? nxt.cnt : 0xFFFFFFFFu;
-            const uint32_t src = (lane + t) & 63u;
-            const uint32_t c1 = ds_bpermute_u32(src, mc), c2 = ds_bpermute_u32(src, mn);
-            const uint32_t cq = lane + t < 64u ? c1 : c2;
-            const bool jq = lane < R && cq != 0xFFFFFFFFu && base + t + lane < A;
-            const double a = Lv + (double)cq;  // lane q's load once charged with job t+q
-            const double pm = wave_exclusive_min_f64(jq ? a : INFINITY);
-            const uint64_t okm = ballot(jq && (lane == 0 || Lv < pm));
-            const uint32_t M = ~okm ? (uint32_t)__builtin_ctzll(~okm) : 64u;
-            if (M >= 2) {
-                if (lane < M) s_mem[(base + t + lane) & 127u] = rv;
-                bool round = false;
-                const uint32_t c0 = rdlane(cq, 0);
-                if (M == R) {
-                    const double an = dpp_shl1_f64(a);
-                    const uint32_t rn = dpp_shl1(rv, rv);
-                    round = ballot(lane < R && cq != c0) == 0 && ballot(lane + 1 < R && an == a && rn < rv) == 0;
-                }
-                if (round) {
-                    Lv = lane < R ? a : Lv;
-                    t += M;
-                    // Further full rounds of the same run: the next R jobs have the same x, so
-                    // the batch test reduces to every load being below min L + x, and the
-                    // order test to the charged loads keeping their (L, r) order.
-                    const uint64_t same_c = ballot(kc == 1 && cur.cnt == c0 && base + lane < A);
-                    const uint64_t same_n = ballot(nxt.end - nxt.off == 1 && nxt.cnt == c0 && base + 64 + lane < A);
-                    const double x0 = (double)c0;
-                    while (t < 64) {
-                        // jobs t .. t+R-1 must all be single-copy jobs of count c0
-                        const uint32_t e = t + R;  // one past the last job of the round (<= 128)
-                        const uint64_t need_c = (e >= 64 ? ~0ull : ((1ull << e) - 1ull)) & ~((1ull << t) - 1ull);
-                        const uint64_t need_n = e > 64 ? (e >= 128 ? ~0ull : ((1ull << (e - 64)) - 1ull)) : 0ull;
-                        if ((same_c & need_c) != need_c || (same_n & need_n) != need_n) break;
-                        const double an = Lv + x0;
-                        const double v0 = rdlane_f64(an, 0);
-                        const double ann = dpp_shl1_f64(an);
-                        const uint32_t rn2 = dpp_shl1(rv, rv);
-                        if (ballot(lane < R && !(Lv < v0)) != 0 || ballot(lane + 1 < R && ann == an && rn2 < rv) != 0)
-                            break;
-                        s_mem[lane < R ? ((base + t + lane) & 127u) : 128u + lane] = rv;
-                        Lv = lane < R ? an : Lv;
-                        t += R;
-                        t = (uint32_t)__builtin_amdgcn_readfirstlane((int)t);
-                    }
-                    continue;
-                } else {
-                    const bool charged = lane < M;
-                    const double av = charged ? a : Lv;
-                    uint32_t cnt = 0;
-                    const uint64_t unch = rmask & ~((M >= 64 ? ~0ull : (1ull << M) - 1ull));
-                    // lanes preceding lane q, as a lane mask; uncharged lanes after q count it
-                    auto pass = [&](uint32_t q) {
-                        const double aq = rdlane_f64(av, q);
-                        const uint32_t rq = rdlane(rv, q);
-                        const uint64_t bm = ballot(av < aq) | (ballot(av == aq) & ballot(rv < rq));
-                        cnt += __builtin_amdgcn_inverse_ballot_w64(unch & ~bm) ? 1u : 0u;
-                        return (uint32_t)__popcll(bm & rmask);
-                    };
-                    uint32_t q = 0;
-                    for (; q + 1 < M; q += 2) {
-                        const uint32_t r0 = pass(q), r1 = pass(q + 1);
-                        cnt = wrlane(wrlane(cnt, r0, q), r1, q + 1);
-                    }
-                    if (q < M) {
-                        const uint32_t rl = pass(q);  // before cnt is read: pass() adds to it
-                        cnt = wrlane(cnt, rl, q);
-                    }
-                    const uint32_t np = charged ? cnt : (lane < R ? lane - M + cnt : lane);
-                    Lv = ds_permute_f64(np, av);
-                    rv = ds_permute_u32(np, rv);
-                }
-                t += M;
-                continue;
-            }
-            const double x = rdlane_f64(xc, t);
-            const double v0 = rdlane_f64(Lv, 0) + x;
-            const uint32_t r0 = rdlane(rv, 0);
-            if (lane == 0) s_mem[(base + t) & 127u] = r0;
-            // rank of (v0, r0) among lanes 1..: three compares, each straight to a lane mask
-            const uint64_t m_lt = ballot(Lv < v0), m_eq = ballot(Lv == v0), m_r = ballot(rv < r0);
-            const uint32_t pos = (uint32_t)__popcll((m_lt | (m_eq & m_r)) & ~1ull);
-            const double sl = dpp_shl1_f64(Lv);
-            const uint32_t sr = dpp_shl1(rv, rv);
-            const bool lt = lane < pos, eq = lane == pos;
-            Lv = lt ? sl : (eq ? v0 : Lv);
-            rv = lt ? sr : (eq ? r0 : rv);
-        } else {
-            const double x = rdlane_f64(xc, t);
-            const uint32_t off = rdlane(cur.off, t);
-            if (lane < k) mem[off + lane] = (uint16_t)rv;
-            const double vnew = Lv + x;  // meaningful on lanes < k
-            const uint32_t rnew = rv;
-            const double sL = __shfl(Lv, (int)((lane + k) & 63u), 64);
-            const uint32_t sR = __shfl(rv, (int)((lane + k) & 63u), 64);
-            Lv = lane + k < 64u ? sL : INFINITY;
-            rv = lane + k < 64u ? sR : 0xFFFFu;
-            for (uint32_t u = 0; u < k; ++u) {
-                const double v = rdlane_f64(vnew, u);
-                const uint32_t r = rdlane(rnew, u);
-                const uint64_t m_lt = ballot(Lv < v), m_eq = ballot(Lv == v), m_r = ballot(rv < r);
-                const uint32_t pos = (uint32_t)__popcll(m_lt | (m_eq & m_r));
-                const double up = dpp_shr1_f64(Lv);
-                const uint32_t upr = dpp_shr1(rv, rv);
-                const bool gt = lane > pos, eq = lane == pos;
-                Lv = gt ? up : (eq ? v : Lv);
-                rv = gt ? upr : (eq ? r : rv);
+                rw[kx_rank3(kxc, cur.key)] = kc == 1 ? (CR_ROUTE_SINGLE | fm) : (base + lane);
             }
         }
-        ++t;
-    }
-    // retire what is left (the current batch, and the next one if a batch of jobs reached it)
-    {
-        const uint32_t fm = s_mem[(base + lane) & 127u];
-        if (base + lane < A) {
-            if (kc == 1) mem[cur.off] = (uint16_t)fm;
-            rw[kx_rank(kxc, cur.key)] = kc == 1 ? (CR_ROUTE_SINGLE | fm) : (base + lane);
+        if (t > 64) {
+            const uint32_t fm = s_mem[(base + 64 + lane) & 127u];
+            if (lane < t - 64 && base + 64 + lane < A) {
+                const uint32_t kn = nxt.end - nxt.off;
+                if (kn == 1) mem[nxt.off] = (uint16_t)fm;
+                rw[kx_rank3(kx_entry3(kx, nxt.key, KW), nxt.key)] = kn == 1 ? (CR_ROUTE_SINGLE | fm) : (base + 64 + lane);
+            }
         }
-    }
-    if (t > 64) {
-        const uint32_t fm = s_mem[(base + 64 + lane) & 127u];
-        if (lane < t - 64 && base + 64 + lane < A) {
-            const uint32_t kn = nxt.end - nxt.off;
-            if (kn == 1) mem[nxt.off] = (uint16_t)fm;
-            rw[kx_rank(kx_entry(kx, nxt.key, true), nxt.key)] = kn == 1 ? (CR_ROUTE_SINGLE | fm) : (base + 64 + lane);
-        }
+        return false;
+    };
+    while (step(s0, s1, s2) && step(s1, s2, s0) && step(s2, s0, s1)) {
     }
     if (lane < R) load[(uint64_t)p * R + rv] = Lv;
 }

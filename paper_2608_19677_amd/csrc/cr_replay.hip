@@ -69,9 +69,14 @@ inline PartGeom part_geom(uint64_t n, uint32_t P)
     return PartGeom{tile, n ? (n + tile - 1) / tile : 0};
 }
 
-__global__ __launch_bounds__(256) void k_part_hist(const uint16_t* __restrict__ dest, uint64_t n, uint32_t R,
-                                                   uint64_t tile, uint64_t ntiles, uint32_t* __restrict__ tcnt,
-                                                   uint32_t* __restrict__ err)
+// Per-tile destination counts; with aligned rows (kVec) every thread reads four
+// destinations with one 8-byte load.
+constexpr uint32_t kHistThreads = 256;
+
+template <bool kVec>
+__global__ __launch_bounds__(kHistThreads) void k_part_hist(const uint16_t* __restrict__ dest, uint64_t n, uint32_t R,
+                                                            uint64_t tile, uint64_t ntiles, uint32_t* __restrict__ tcnt,
+                                                            uint32_t* __restrict__ err)
 {
     extern __shared__ uint32_t h[];
     const uint32_t c = blockIdx.y;
@@ -81,11 +86,21 @@ __global__ __launch_bounds__(256) void k_part_hist(const uint16_t* __restrict__ 
     __syncthreads();
     const uint16_t* __restrict__ dc = dest + (uint64_t)c * n;
     bool bad = false;
-    for (uint64_t i = t0 + threadIdx.x; i < t1; i += blockDim.x) {
-        const uint32_t d = dc[i];
+    auto add = [&](uint32_t d) {
         if (d < R) atomicAdd(&h[d], 1u);
         else bad = true;
+    };
+    uint64_t a = t0;
+    if (kVec) {
+        for (; a + 4u * kHistThreads <= t1; a += 4u * kHistThreads) {
+            const uint2 q = *reinterpret_cast<const uint2*>(dc + a + 4u * threadIdx.x);
+            add(q.x & 0xFFFFu);
+            add(q.x >> 16);
+            add(q.y & 0xFFFFu);
+            add(q.y >> 16);
+        }
     }
+    for (uint64_t i = a + threadIdx.x; i < t1; i += blockDim.x) add(dc[i]);
     __syncthreads();
     for (uint32_t d = threadIdx.x; d < R; d += blockDim.x) tcnt[((uint64_t)c * R + d) * ntiles + t] = h[d];
     if (bad) atomicOr(err, CR_ERR_DEST_RANGE);
@@ -236,6 +251,157 @@ __global__ __launch_bounds__(64) void k_part_scatter(const uint32_t* __restrict_
             run[d] += lcnt[d];
             lcnt[d] = 0;
         }
+        __syncthreads();
+    }
+}
+
+// R <= 64: the same scatter with each lane owning a run of kRun consecutive requests of
+// the sub-tile. A lane counts its run's destinations in a private row of 16-bit counters in
+// LDS, in request order, which ranks every request within its run; a prefix sum of the rows
+// across the lanes (packed pairs of counters, one wave scan per pair of destinations) gives
+// each lane's offset per destination. A request's rank within the sub-tile is then its lane's
+// offset plus its rank within the run: no cross-lane matching of destinations at all. With
+// aligned rows (kVec) a lane reads its run with 16-byte loads.
+constexpr uint32_t kRun = kSub / 64;
+
+// Row stride in counters: R rounded up to 8 (16-byte pieces).
+__host__ __device__ __forceinline__ uint32_t scat64_row(uint32_t R) { return (R + 7u) & ~7u; }
+
+inline size_t scatter64_lds_bytes(uint32_t R) { return (size_t)kSub * 12u + 64u * 8u + 64u * scat64_row(R) * 2u; }
+
+template <bool kVec>
+__global__ __launch_bounds__(64) void k_part_scatter64(const uint32_t* __restrict__ keys,
+                                                       const uint16_t* __restrict__ suffix,
+                                                       const uint16_t* __restrict__ dest, uint64_t n,
+                                                       const uint64_t* __restrict__ off, uint32_t J, uint32_t R,
+                                                       uint64_t tile, uint64_t ntiles, const uint32_t* __restrict__ tcnt,
+                                                       const uint32_t* __restrict__ grp_off,
+                                                       uint64_t* __restrict__ rec)
+{
+    extern __shared__ uint64_t lds[];
+    uint64_t* srec = lds;                                            // [kSub] staged records
+    uint32_t* spos = reinterpret_cast<uint32_t*>(srec + kSub);      // [kSub] their output positions
+    uint64_t* sbase = reinterpret_cast<uint64_t*>(spos + kSub);     // [64] {sub-tile offset, output position}
+    uint16_t* rows = reinterpret_cast<uint16_t*>(sbase + 64);       // [64][RW] counters per lane
+    uint32_t* stot = spos;  // [64] sub-tile count per destination (spos is free until staging)
+    const uint32_t RW = scat64_row(R);
+    const uint32_t c = blockIdx.y, lane = lane_id();
+    const uint64_t t = xcd_tile(blockIdx.x, gridDim.x);
+    if (t >= ntiles) return;
+    const uint64_t t0 = t * tile, t1 = t0 + tile < n ? t0 + tile : n;
+    // lane d: next output position of destination d
+    uint32_t run = lane < R ? grp_off[(uint64_t)c * (R + 1u) + lane] + tcnt[((uint64_t)c * R + lane) * ntiles + t] : 0u;
+    const uint16_t* __restrict__ dc = dest + (uint64_t)c * n;
+    uint64_t* __restrict__ rc = rec + (uint64_t)c * n;
+    uint16_t* row = rows + lane * RW;
+    uint32_t jw = find_interval(off, J, t0);  // interval of the sub-tile's first request
+    for (uint64_t sb = t0; sb < t1; sb += kSub) {
+        const uint64_t se = sb + kSub < t1 ? sb + kSub : t1;
+        const uint64_t i0 = sb + (uint64_t)lane * kRun;
+        uint32_t kv[kRun], dv[kRun], mv[kRun];
+        if (kVec && se - sb == kSub) {
+            const uint4* k4 = reinterpret_cast<const uint4*>(keys + i0);
+            const uint4* d4 = reinterpret_cast<const uint4*>(dc + i0);
+            const uint4* m4 = reinterpret_cast<const uint4*>(suffix + i0);
+            uint4 qk[4], qd[2], qm[2];
+#pragma unroll
+            for (uint32_t v = 0; v < 4; ++v) qk[v] = k4[v];
+#pragma unroll
+            for (uint32_t v = 0; v < 2; ++v) {
+                qd[v] = d4[v];
+                qm[v] = m4[v];
+            }
+#pragma unroll
+            for (uint32_t v = 0; v < 4; ++v) {
+                kv[4 * v + 0] = qk[v].x;
+                kv[4 * v + 1] = qk[v].y;
+                kv[4 * v + 2] = qk[v].z;
+                kv[4 * v + 3] = qk[v].w;
+            }
+#pragma unroll
+            for (uint32_t v = 0; v < 2; ++v) {
+                const uint32_t dw[4] = {qd[v].x, qd[v].y, qd[v].z, qd[v].w};
+                const uint32_t mw[4] = {qm[v].x, qm[v].y, qm[v].z, qm[v].w};
+#pragma unroll
+                for (uint32_t h = 0; h < 4; ++h) {
+                    dv[8 * v + 2 * h] = dw[h] & 0xFFFFu;
+                    dv[8 * v + 2 * h + 1] = dw[h] >> 16;
+                    mv[8 * v + 2 * h] = mw[h] & 0xFFFFu;
+                    mv[8 * v + 2 * h + 1] = mw[h] >> 16;
+                }
+            }
+        } else {
+#pragma unroll
+            for (uint32_t v = 0; v < kRun; ++v) {
+                const uint64_t i = i0 + v;
+                const bool in = i < se;
+                dv[v] = in ? dc[i] : 0xFFFFu;
+                kv[v] = in ? keys[i] : 0u;
+                mv[v] = in ? suffix[i] : 0u;
+            }
+        }
+        for (uint32_t w = 0; w < RW; w += 8) *reinterpret_cast<uint4*>(row + w) = make_uint4(0u, 0u, 0u, 0u);
+        // interval of each request: from the sub-tile's, past the boundaries up to it
+        uint32_t jl = jw;
+        uint64_t nb = jl + 1 < J ? off[jl + 1] : ~0ull;  // first request of the next interval
+        // rank of each request within the run: the run's earlier requests to its destination
+#pragma unroll
+        for (uint32_t v = 0; v < kRun; ++v) {
+            const uint64_t i = i0 + v;
+            const bool in = i < se;
+            while (in && i >= nb) {
+                ++jl;
+                nb = jl + 1 < J ? off[jl + 1] : ~0ull;
+            }
+            mv[v] |= jl << 16;
+            const uint32_t d = dv[v];
+            if (in && d < R) {
+                const uint32_t r = row[d];
+                row[d] = (uint16_t)(r + 1u);
+                dv[v] = d | (r << 16);
+            } else {
+                dv[v] = 0xFFFFFFFFu;
+            }
+        }
+        // exclusive prefix of the rows across the lanes; lane 63's inclusive sums are the
+        // sub-tile's counts per destination
+        for (uint32_t w = 0; w < RW; w += 8) {
+            uint4* q = reinterpret_cast<uint4*>(row + w);
+            const uint4 own = *q;
+            const uint4 inc = make_uint4(wave_incl_scan_u32(own.x), wave_incl_scan_u32(own.y),
+                                         wave_incl_scan_u32(own.z), wave_incl_scan_u32(own.w));
+            *q = make_uint4(inc.x - own.x, inc.y - own.y, inc.z - own.z, inc.w - own.w);
+            if (lane == 63) {
+                const uint32_t iw[4] = {inc.x, inc.y, inc.z, inc.w};
+#pragma unroll
+                for (uint32_t h = 0; h < 4; ++h) {
+                    stot[w + 2 * h] = iw[h] & 0xFFFFu;
+                    stot[w + 2 * h + 1] = iw[h] >> 16;
+                }
+            }
+        }
+        __syncthreads();
+        // destination offsets within the sub-tile (lane d)
+        const uint32_t tl = lane < R ? stot[lane] : 0u;
+        const uint32_t ex = wave_incl_scan_u32(tl) - tl;
+        const uint32_t total = rdlane(ex + tl, 63);
+        sbase[lane] = (uint64_t)ex | ((uint64_t)run << 32);
+        __syncthreads();
+#pragma unroll
+        for (uint32_t v = 0; v < kRun; ++v) {
+            if (dv[v] != 0xFFFFFFFFu) {
+                const uint32_t d = dv[v] & 0xFFFFu;
+                const uint32_t lr = row[d] + (dv[v] >> 16);
+                const uint64_t bs = sbase[d];
+                const uint32_t slot = (uint32_t)bs + lr;
+                srec[slot] = (uint64_t)kv[v] | ((uint64_t)mv[v] << 32);
+                spos[slot] = (uint32_t)(bs >> 32) + lr;
+            }
+        }
+        __syncthreads();
+        for (uint32_t q = lane; q < total; q += 64) rc[spos[q]] = srec[q];
+        run += tl;
+        while (jw + 1 < J && off[jw + 1] <= se) ++jw;  // interval of the next sub-tile's first request
         __syncthreads();
     }
 }
@@ -728,12 +894,26 @@ extern "C" cr_status cr_replay_partition(const uint32_t* keys, const uint16_t* s
     uint32_t nbits = 0;
     while ((1u << nbits) < R) ++nbits;
     (void)hipGetLastError();
-    if (g.ntiles)
-        hipLaunchKernelGGL(k_part_hist, dim3((uint32_t)g.ntiles, P), dim3(256), (size_t)R * 4u, st, dest, n, R, g.tile,
-                           g.ntiles, w.tcnt, err);
+    // 16-byte loads of keys, destinations and suffixes need 16-byte aligned rows
+    const bool vec = ((uintptr_t)keys & 15u) == 0 && ((uintptr_t)suffix & 15u) == 0 && ((uintptr_t)dest & 15u) == 0 &&
+                     (n & 7u) == 0;
+    if (g.ntiles && vec)
+        hipLaunchKernelGGL(k_part_hist<true>, dim3((uint32_t)g.ntiles, P), dim3(kHistThreads), (size_t)R * 4u, st, dest,
+                           n, R, g.tile, g.ntiles, w.tcnt, err);
+    else if (g.ntiles)
+        hipLaunchKernelGGL(k_part_hist<false>, dim3((uint32_t)g.ntiles, P), dim3(kHistThreads), (size_t)R * 4u, st, dest,
+                           n, R, g.tile, g.ntiles, w.tcnt, err);
     hipLaunchKernelGGL(k_scan_dest, dim3(R, P), dim3(kScanThreads), 0, st, w.tcnt, g.ntiles, R, w.dtot);
     hipLaunchKernelGGL(k_seg_items, dim3(1), dim3(1024), 0, st, w.dtot, P, R, ra.wa, w.grp_off, w.item_off);
-    if (g.ntiles)
+    if (g.ntiles && R <= 64 && vec)
+        hipLaunchKernelGGL(k_part_scatter64<true>, dim3(xcd_grid((uint32_t)g.ntiles), P), dim3(64),
+                           scatter64_lds_bytes(R), st, keys, suffix, dest, n, off, J, R, g.tile, g.ntiles, w.tcnt,
+                           w.grp_off, w.rec);
+    else if (g.ntiles && R <= 64)
+        hipLaunchKernelGGL(k_part_scatter64<false>, dim3(xcd_grid((uint32_t)g.ntiles), P), dim3(64),
+                           scatter64_lds_bytes(R), st, keys, suffix, dest, n, off, J, R, g.tile, g.ntiles, w.tcnt,
+                           w.grp_off, w.rec);
+    else if (g.ntiles)
         hipLaunchKernelGGL(k_part_scatter, dim3(xcd_grid((uint32_t)g.ntiles), P), dim3(64), scatter_lds_bytes(R), st, keys,
                            suffix, dest, n, off, J, R, nbits, g.tile, g.ntiles, w.tcnt, w.grp_off, w.rec);
     return hipGetLastError() == hipSuccess ? CR_OK : CR_EHIP;

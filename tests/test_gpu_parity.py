@@ -41,6 +41,8 @@ SMALL = [
     (8, 400, 30_000, 4, [2, 50], 20, 2, 0.9, [(1, 3)]),
     (9, 2000, 77_777, 16, [128], 6, 8, 0.48, [(2, 5)]),
     (10, 64, 4096, 128, [1, 63, 64], 2, 0, 0.0, [(1, 1)]),
+    (11, 300, 20_000, 2, [8, 30], 3, 2, 0.5, [(1, 1)]),         # two destinations: one exchange per merge
+    (12, 600, 40_000, 33, [6, 12], 4, 3, 0.4, [(1, 2)]),        # 31 idle lanes in the 64-lane merge
 ]
 
 
