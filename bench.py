@@ -1,12 +1,15 @@
 """Benchmark: count -> plan -> route -> LRU replay on one MI355X, plus the CPU oracle baseline.
 
-A step is one pass of the whole path over the 70B-like workload (20,000 keys, Zipf 1.0
-capped at a 0.3 % share, 1e7 requests at 176 QPS in 60-s control intervals = 948
-intervals, 30 destinations x 64 LRU slots), from scratch on one stream. The timed steps
-replay that step captured once as a HIP graph (--eager: plain launches); the per-stage
-times and the roofline come from an eager pass with HIP events around each library call.
---schedule overlap instead runs consecutive chunks of one stream, chunk k planned on one
-HIP stream while chunk k-1 replays on another (cache state and last window carried).
+A step is one pass of the whole path over one batch of the 70B-like workload (20,000 keys,
+Zipf 1.0 capped at a 0.3 % share, 1e7 requests at 176 QPS in 60-s control intervals = 948
+intervals, 30 destinations x 64 LRU slots). By default (--schedule overlap) consecutive
+batches run as chunks of one stream, two HIP streams deep: chunk k is counted and admitted,
+then placed, routed and partitioned on one stream while chunk k-1 replays on the other
+(cache state and last window carried), and the timed steps replay that steady state
+captured as two HIP graphs (one per buffer set), one chunk per step. --schedule serial runs
+every step from scratch on one stream (one HIP graph). --eager times plain launches. The
+per-stage times and the roofline come from an eager pass of the same schedule with HIP
+events around each library call.
 Inputs are resident in HBM before timing starts. Prints ONE JSON line.
 
   python bench.py [--gpus 1] [--steps K] [--warmup W] [--eager] [--schedule serial|overlap]
@@ -48,10 +51,11 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="llama70b")
-    ap.add_argument("--schedule", default="serial", choices=("overlap", "serial"),
-                    help="overlap: consecutive chunks of one stream, chunk k planned on one HIP stream while "
-                         "chunk k-1 replays on another (cache state and last window carried); serial: every "
-                         "step is the whole workload from scratch on one stream")
+    ap.add_argument("--schedule", default="overlap", choices=("overlap", "serial"),
+                    help="overlap: consecutive chunks of one stream, chunk k counted and admitted, then placed, "
+                         "routed and partitioned on one HIP stream while chunk k-1 replays on another (cache "
+                         "state and last window carried); serial: every step is the whole workload from scratch "
+                         "on one stream. The drift study, live dispatch and --opaque run serial")
     ap.add_argument("--dispatch", default="static", choices=("static", "live"),
                     help="static: order-independent dispatch on interval-start planned loads; live: least-loaded "
                          "member and power of two choices on the running loads of each interval")
@@ -235,12 +239,27 @@ def main():
         cs = ChunkStream(wl, device="cuda:0")
         for _ in range(args.warmup):
             cs.enqueue()
+        cs.flush()
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         for _ in range(args.steps):
             last = cs.enqueue(timers=ev)
+        cs.flush(timers=ev)
         torch.cuda.synchronize()
         t1 = time.perf_counter()
+        if not args.eager:
+            # the steady state as two HIP graphs (one per buffer set), replayed in turn: each
+            # replay plans, routes and partitions one chunk beside the previous chunk's replay
+            gs = ChunkStream(wl, device="cuda:0")
+            gs.capture()
+            for _ in range(args.warmup):
+                gs.replay_graph()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for _ in range(args.steps):
+                gs.replay_graph()
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
     n_plans = last.plans.num_plans
     ms_step = (t1 - t0) * 1e3 / args.steps
     one_build_us = None if args.no_unbatched else one_plan_build_us(wl, last, torch)
@@ -303,8 +322,7 @@ def main():
     out["config"]["plan_builds"] = n_plans
     out["config"]["schedule"] = args.schedule
     out["config"]["dispatch"] = args.dispatch
-    out["config"]["launch"] = "eager" if (args.eager or study is not None or remap is not None
-                                          or args.schedule != "serial") else "hip-graph"
+    out["config"]["launch"] = "eager" if (args.eager or study is not None or remap is not None) else "hip-graph"
     if remap is not None:
         torch.cuda.synchronize()
         assert int(km_err.item()) == 0

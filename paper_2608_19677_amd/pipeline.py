@@ -235,8 +235,10 @@ class ChunkStream:
     """Consecutive chunks of one request stream through the path, two HIP streams deep.
 
     Chunk k (the workload's requests again, at global indices k*n .. k*n + n - 1) is
-    counted, planned, routed and partitioned on the plan stream while chunk k-1's LRU
-    replay runs on the replay stream. Chunk k >= 1 plans its first interval from chunk
+    counted, planned, routed and partitioned on the plan stream; chunk k-1's LRU replay
+    runs on the replay stream from the end of chunk k's admission, beside chunk k's
+    placement, routing and partition. `flush()` enqueues the last chunk's replay, which has
+    no next chunk to wait for. Chunk k >= 1 plans its first interval from chunk
     k-1's last window and starts its replay from chunk k-1's final cache state, so the
     results are those of processing the chunks one after another. Chunk 0 has its own
     buffers; later chunks alternate between two sets, and a chunk's partition waits for
@@ -257,13 +259,44 @@ class ChunkStream:
         self.ev_part = {}
         self.ev_rep = {}
         self.k = 0
+        self.pending = None  # chunk whose replay is not enqueued yet
 
     def pipe(self, k: int) -> Pipeline:
         return self.first if k == 0 else self.slots[(k - 1) % 2]
 
+    def _run(self, p, stage, stream, timers):
+        if timers is None:
+            getattr(p, stage)()
+            return
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        getattr(p, stage)()
+        b.record(stream)
+        timers.setdefault(stage, []).append((a, b))
+
+    def _replay(self, after, timers):
+        """Enqueue the pending chunk's replay on the replay stream, after its partition and
+        (if given) the event `after`."""
+        j = self.pending
+        if j is None:
+            return
+        with torch.cuda.stream(self.s_rep):
+            self.s_rep.wait_event(self.ev_part.pop(j))
+            if after is not None:
+                self.s_rep.wait_event(after)
+            self._run(self.pipe(j), "lru", self.s_rep, timers)
+            ev = torch.cuda.Event()
+            ev.record(self.s_rep)
+            self.ev_rep[j] = ev
+        self.pending = None
+
     def enqueue(self, timers=None):
         """Enqueue the next chunk. `timers`, if given, maps stage -> list of (start, end)
-        events recorded on the stream the stage runs on."""
+        events recorded on the stream the stage runs on. The previous chunk's replay is
+        enqueued once this chunk's admission is queued, so that it runs beside this chunk's
+        placement, routing and partition (placement is a few hundred latency-bound
+        wavefronts that leave most of the chip idle) rather than ahead of its counting."""
         k = self.k
         p = self.pipe(k)
         p.first_index = self.wl.first_index + k * self.n
@@ -271,32 +304,78 @@ class ChunkStream:
             prev = self.pipe(k - 1)
             p.prev_counts = prev.counts[self.wl.J - 1]
             p.lru_in = prev.lru_out
-
-        def run(stage, stream):
-            if timers is None:
-                getattr(p, stage)()
-                return
-            a = torch.cuda.Event(enable_timing=True)
-            b = torch.cuda.Event(enable_timing=True)
-            a.record(stream)
-            getattr(p, stage)()
-            b.record(stream)
-            timers.setdefault(stage, []).append((a, b))
-
         with torch.cuda.stream(self.s_plan):
-            for stage in ("count", "admit", "place", "route"):
-                run(stage, self.s_plan)
+            for stage in ("count", "admit"):
+                self._run(p, stage, self.s_plan, timers)
+            adm = torch.cuda.Event()
+            adm.record(self.s_plan)
+        self._replay(adm, timers)
+        with torch.cuda.stream(self.s_plan):
+            for stage in ("place", "route"):
+                self._run(p, stage, self.s_plan, timers)
             if k >= 3:  # this buffer set was last replayed by chunk k-2
                 self.s_plan.wait_event(self.ev_rep.pop(k - 2))
-            run("partition", self.s_plan)
+            self._run(p, "partition", self.s_plan, timers)
             ev = torch.cuda.Event()
             ev.record(self.s_plan)
             self.ev_part[k] = ev
-        with torch.cuda.stream(self.s_rep):
-            self.s_rep.wait_event(self.ev_part.pop(k))
-            run("lru", self.s_rep)
-            ev = torch.cuda.Event()
-            ev.record(self.s_rep)
-            self.ev_rep[k] = ev
+        self.pending = k
         self.k += 1
         return p
+
+    def flush(self, timers=None):
+        """Enqueue the last chunk's replay (it has no next chunk to wait for)."""
+        self._replay(None, timers)
+
+    def capture(self):
+        """Record the steady state as two HIP graphs, one per buffer set. Graph x runs the
+        next chunk into set x (count and admission, then placement, routing and partition)
+        and, forked onto the replay stream after the admission, the replay of the chunk
+        before it, which sits in the other set; the replay stream joins the capture stream
+        at the end. Graph launches on one stream run one after another, which orders each
+        partition after the replay that last used its set. Replaying the graphs in turn
+        continues the chunk sequence; each graph keeps the global indices of the chunk it
+        was recorded with. Returns the chunk indices the two graphs were recorded for."""
+        while self.k < 3:
+            self.enqueue()
+        torch.cuda.synchronize()  # chunk k-1's replay is left pending: the first graph runs it
+        self.graphs = []
+        recorded = []
+        for _ in range(2):
+            k = self.k
+            p, prev = self.pipe(k), self.pipe(k - 1)
+            p.first_index = self.wl.first_index + k * self.n
+            p.prev_counts = prev.counts[self.wl.J - 1]
+            p.lru_in = prev.lru_out
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                cap = torch.cuda.current_stream()
+                p.count()
+                p.admit()
+                self.s_rep.wait_stream(cap)
+                with torch.cuda.stream(self.s_rep):
+                    prev.lru()
+                p.place()
+                p.route()
+                p.partition()
+                cap.wait_stream(self.s_rep)
+            self.graphs.append(g)
+            recorded.append(k)
+            self.k += 1
+        self.pending = None
+        self.turn = 0
+        return recorded
+
+    def replay_graph(self):
+        """One step of the captured steady state: the next graph in turn."""
+        self.graphs[self.turn].replay()
+        self.turn ^= 1
+
+    def graph_pending(self) -> "Pipeline":
+        """The buffer set whose chunk was planned by the last graph replay and has not been
+        replayed yet (the next graph, or `replay_pending`, replays it)."""
+        return self.pipe(self.k - 1 - self.turn)
+
+    def replay_pending(self):
+        """Replay, eagerly on the current stream, the chunk the last graph planned."""
+        self.graph_pending().lru()

@@ -165,6 +165,50 @@ def test_repeat_runs_are_identical():
         assert np.array_equal(np.asarray(h1[k]).view(np.uint8), np.asarray(h2[k]).view(np.uint8)), k
 
 
+def test_two_stream_chunk_graphs_equal_eager_chunks():
+    # the steady state of the two-stream schedule captured as two HIP graphs (one per buffer
+    # set), replayed in turn four times with eager reads and synchronisations in between;
+    # every replay's planned chunk and every replayed chunk must equal a serial chain of
+    # eager chunks with the same global indices (each graph keeps the indices of the chunk
+    # it was recorded with) and the carried cache state
+    import dataclasses
+    wl = wl_mod.small_random(43, num_keys=1500, n=120_000, R=30, Ws=[32], J=4, hot=2, hot_share=0.3)
+    say(f"[case] two-stream chunk graphs n={wl.n} J={wl.J}")
+    cs = ChunkStream(wl)
+    k0, k1 = cs.capture()
+    firsts = [0, 1, 2, k0, k1, k0, k1]  # chunk index whose global indices each chunk uses
+    last_n = int(wl.offsets[-1] - wl.offsets[-2])
+    ref, prev = [], None
+    for f in firsts:
+        wk = dataclasses.replace(wl, first_index=wl.first_index + f * wl.n)
+        if prev is None:
+            p = Pipeline(wk)
+        else:
+            p = Pipeline(wk, prev_counts=prev.counts[wl.J - 1].clone(), prev_n=last_n, lru_in=prev.lru_out.clone())
+        p.step()
+        ref.append(p.host())
+        prev = p
+    for r in range(4):
+        cs.replay_graph()
+        torch.cuda.synchronize()
+        planned = cs.graph_pending()  # chunk 3 + r, planned by this replay
+        h = planned.host()
+        assert h["err"] == 0
+        for key in ("counts", "load", "dest"):
+            np.testing.assert_array_equal(np.asarray(h[key]), np.asarray(ref[3 + r][key]), err_msg=f"replay {r} {key}")
+        if r:  # the chunk planned by the previous replay has been replayed by this one
+            done = cs.pipe(cs.k - 1 - (cs.turn ^ 1))
+            hd = done.host()
+            for key in ("stats", "lru"):
+                np.testing.assert_array_equal(np.asarray(hd[key]), np.asarray(ref[2 + r][key]),
+                                              err_msg=f"replay {r} chunk {2 + r} {key}")
+    cs.replay_pending()
+    torch.cuda.synchronize()
+    hl = cs.graph_pending().host()
+    for key in ("stats", "lru"):
+        np.testing.assert_array_equal(np.asarray(hl[key]), np.asarray(ref[6][key]), err_msg=f"last chunk {key}")
+
+
 def test_two_stream_chunk_schedule_equals_serial():
     # ChunkStream plans chunk k on one stream while chunk k-1 replays on another, reusing
     # two buffer sets; five chunks enqueued with no host synchronisation must equal the
@@ -177,6 +221,7 @@ def test_two_stream_chunk_schedule_equals_serial():
     cs = ChunkStream(wl)
     for _ in range(n_chunks):
         cs.enqueue()
+    cs.flush()
     torch.cuda.synchronize()
     last_n = int(wl.offsets[-1] - wl.offsets[-2])
     prev, ref = None, []
