@@ -379,3 +379,124 @@ class ChunkStream:
     def replay_pending(self):
         """Replay, eagerly on the current stream, the chunk the last graph planned."""
         self.graph_pending().lru()
+
+
+class ChunkStream3:
+    """Consecutive chunks of one request stream, three HIP streams deep.
+
+    A chunk goes through three phases: A (count and admission), B (placement, routing and
+    partition) and C (LRU replay). Step s runs A of chunk s, B of chunk s-1 and C of chunk
+    s-2 at the same time, one HIP stream each. Chunks 1, 2, ... take three buffer sets in
+    turn (chunk 0 has its own), so the three phases of a step touch disjoint buffers: A
+    writes its set's counts and plans, B its set's destinations, records and cleared
+    statistics, C its set's statistics and final cache state (it reads the cache state the
+    chunk before left in another set). Across steps, eager enqueues order each phase after
+    the phases it reads (A of chunk s-1 before B of chunk s-1, B before C) and after the
+    phases that last used its buffers (B of chunk s-3 before A of chunk s, C of chunk s-4
+    before B of chunk s-1); captured steps run one after another, which gives the same
+    order. Chunk k >= 1 plans its first interval from chunk k-1's last window and starts
+    its replay from chunk k-1's final cache state, as if the chunks ran one by one.
+    """
+
+    def __init__(self, wl, device="cuda"):
+        self.wl = wl
+        self.n = wl.n
+        self.inp = upload(wl, device)
+        self.first = Pipeline(wl, device, self.inp)
+        last_n = int(self.first.window_sizes[-1])
+        self.slots = [Pipeline(wl, device, self.inp, prev_counts=self.first.counts[wl.J - 1], prev_n=last_n,
+                               lru_in=self.first.lru_out) for _ in range(3)]
+        self.streams = [torch.cuda.Stream(device=device) for _ in range(3)]
+        self.ev = {}  # (phase, chunk) -> event recorded after that phase
+        self.s = 0    # next step
+
+    def pipe(self, k: int) -> Pipeline:
+        return self.first if k == 0 else self.slots[(k - 1) % 3]
+
+    PHASES = {"A": ("count", "admit"), "B": ("place", "route", "partition"), "C": ("lru",)}
+
+    def _phase(self, ph, k, stream, waits, timers, capturing=False):
+        if k < 0 or k >= self.limit:
+            return
+        p = self.pipe(k)
+        with torch.cuda.stream(stream):
+            for key in waits:
+                e = self.ev.get(key)
+                if e is not None:
+                    stream.wait_event(e)
+            if ph == "A":
+                p.first_index = self.wl.first_index + k * self.n
+                if k:
+                    prev = self.pipe(k - 1)
+                    p.prev_counts = prev.counts[self.wl.J - 1]
+                    p.lru_in = prev.lru_out
+            for stage in self.PHASES[ph]:
+                if timers is None:
+                    getattr(p, stage)()
+                else:
+                    a = torch.cuda.Event(enable_timing=True)
+                    b = torch.cuda.Event(enable_timing=True)
+                    a.record(stream)
+                    getattr(p, stage)()
+                    b.record(stream)
+                    timers.setdefault(stage, []).append((a, b))
+            if not capturing:
+                e = torch.cuda.Event()
+                e.record(stream)
+                self.ev[(ph, k)] = e
+
+    limit = 1 << 62  # chunks from this one on are not started (set by drain)
+
+    def step(self, timers=None):
+        """Enqueue step s: A of chunk s, B of chunk s-1, C of chunk s-2. Returns the chunk
+        whose replay this step enqueued (None before step 2)."""
+        s = self.s
+        sa, sb, sc = self.streams
+        self._phase("A", s, sa, [("B", s - 3)], timers)
+        self._phase("B", s - 1, sb, [("A", s - 1), ("C", s - 4)], timers)
+        self._phase("C", s - 2, sc, [("B", s - 2)], timers)
+        # events no later enqueue waits for: A(k) is read by B(k) (step k+1), B(k) by C(k)
+        # and A(k+3) (steps k+2, k+3), C(k) by B(k+3) (step k+4)
+        for key in (("A", s - 1), ("B", s - 3), ("C", s - 4)):
+            self.ev.pop(key, None)
+        self.s += 1
+        return self.pipe(s - 2) if 0 <= s - 2 < self.limit else None
+
+    def drain(self, timers=None):
+        """Finish the chunks already started (no new chunk is counted)."""
+        self.limit = self.s
+        while self.s < self.limit + 2:
+            self.step(timers)
+
+    def capture(self):
+        """Record the steady state as three HIP graphs (one per step modulo 3), each with the
+        three phases forked onto their streams and joined at the end. Returns the step
+        numbers the graphs were recorded for."""
+        while self.s < 4:
+            self.step()
+        torch.cuda.synchronize()
+        self.ev.clear()
+        self.graphs = []
+        recorded = []
+        for _ in range(3):
+            s = self.s
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                cap = torch.cuda.current_stream()
+                for st in self.streams:
+                    st.wait_stream(cap)
+                self._phase("A", s, self.streams[0], [], None, capturing=True)
+                self._phase("B", s - 1, self.streams[1], [], None, capturing=True)
+                self._phase("C", s - 2, self.streams[2], [], None, capturing=True)
+                for st in self.streams:
+                    cap.wait_stream(st)
+            self.graphs.append(g)
+            recorded.append(s)
+            self.s += 1
+        self.turn = 0
+        return recorded
+
+    def replay_graph(self):
+        """One step of the captured steady state: the next graph in turn."""
+        self.graphs[self.turn].replay()
+        self.turn = (self.turn + 1) % 3

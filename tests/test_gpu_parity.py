@@ -11,7 +11,7 @@ import torch
 import oracle
 from oracle import pipeline as opipe
 from paper_2608_19677_amd import workload as wl_mod
-from paper_2608_19677_amd.pipeline import ChunkStream, Pipeline
+from paper_2608_19677_amd.pipeline import ChunkStream, ChunkStream3, Pipeline
 
 from cr_check import compare_all, compare_plan, say
 
@@ -163,6 +163,71 @@ def test_repeat_runs_are_identical():
     h2 = gp.host()
     for k in ("counts", "order", "members", "load", "route", "dest", "stats", "lru"):
         assert np.array_equal(np.asarray(h1[k]).view(np.uint8), np.asarray(h2[k]).view(np.uint8)), k
+
+
+def _chunk_chain(wl, firsts):
+    """Host results of chunks run one by one, chunk i with the global indices of chunk
+    firsts[i], each planned from the previous chunk's last window with its cache state."""
+    import dataclasses
+    last_n = int(wl.offsets[-1] - wl.offsets[-2])
+    ref, prev = [], None
+    for f in firsts:
+        wk = dataclasses.replace(wl, first_index=wl.first_index + f * wl.n)
+        if prev is None:
+            p = Pipeline(wk)
+        else:
+            p = Pipeline(wk, prev_counts=prev.counts[wl.J - 1].clone(), prev_n=last_n, lru_in=prev.lru_out.clone())
+        p.step()
+        ref.append(p.host())
+        prev = p
+    return ref
+
+
+def _same(h, ref, keys, msg):
+    assert h["err"] == 0, msg
+    for key in keys:
+        np.testing.assert_array_equal(np.asarray(h[key]), np.asarray(ref[key]), err_msg=f"{msg} {key}")
+
+
+def test_three_stream_chunk_pipeline_equals_serial():
+    # ChunkStream3 runs count+admit of chunk s, place+route+partition of chunk s-1 and the
+    # replay of chunk s-2 at once on three streams over three buffer sets; seven chunks
+    # enqueued without host synchronisation, then drained, must equal the chunks run one
+    # after another (the last three buffer sets' contents are compared)
+    wl = wl_mod.small_random(44, num_keys=1800, n=130_000, R=30, Ws=[48], J=5, hot=2, hot_share=0.3)
+    say(f"[case] three-stream chunks n={wl.n} J={wl.J}")
+    cs = ChunkStream3(wl)
+    for _ in range(7):
+        cs.step()
+    cs.drain()
+    torch.cuda.synchronize()
+    ref = _chunk_chain(wl, list(range(7)))
+    for k in (4, 5, 6):
+        pk = cs.pipe(k)
+        h = pk.host()
+        _same(h, ref[k], ("counts", "load", "dest", "stats", "lru"), f"chunk {k}")
+        for g in range(pk.NG):
+            for c in range(pk.P):
+                compare_plan(pk.plan_of(h, g, c), pk.plan_of(ref[k], g, c), f"chunk {k} plan {g}/{c}")
+
+
+def test_three_stream_chunk_graphs_equal_eager_chunks():
+    # the three-stream steady state captured as three HIP graphs (steps 4, 5, 6), replayed
+    # in turn six times with eager reads in between; after replay r (step 4 + r) chunk
+    # 3 + r is planned, routed and partitioned and chunk 2 + r replayed, each equal to the
+    # serial chain. Routing is the only stage that reads the global indices, and each graph
+    # keeps those of the chunk it routed when it was recorded (chunks 3, 4, 5 in turn)
+    wl = wl_mod.small_random(45, num_keys=1500, n=120_000, R=30, Ws=[32], J=4, hot=2, hot_share=0.3)
+    say(f"[case] three-stream chunk graphs n={wl.n} J={wl.J}")
+    cs = ChunkStream3(wl)
+    steps = cs.capture()
+    assert steps == [4, 5, 6]
+    ref = _chunk_chain(wl, [0, 1, 2, 3, 4, 5, 3, 4, 5, 3])
+    for r in range(6):
+        cs.replay_graph()
+        torch.cuda.synchronize()
+        _same(cs.pipe(3 + r).host(), ref[3 + r], ("counts", "load", "dest"), f"replay {r} chunk {3 + r}")
+        _same(cs.pipe(2 + r).host(), ref[2 + r], ("stats", "lru"), f"replay {r} chunk {2 + r}")
 
 
 def test_two_stream_chunk_graphs_equal_eager_chunks():
