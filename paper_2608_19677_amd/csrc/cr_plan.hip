@@ -14,6 +14,8 @@
 // k_plan_churn compares pairs of built plans for the replanning study.
 #include <math.h>
 
+#include <utility>
+
 #include "cr_common.h"
 
 namespace cr {
@@ -857,6 +859,39 @@ __device__ __forceinline__ double ds_bpermute_f64(uint32_t src_lane, double v)
     return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
 }
 
+// (o, orv) < (a, r) as 0 or 1, without branches
+__device__ __forceinline__ uint32_t lt_pair(double o, uint32_t orv, double a, uint32_t r)
+{
+    return (uint32_t)((o < a) | ((o == a) & (orv < r)));
+}
+
+// Lane i of a 16-lane row receives lane (i - kK) mod 16 of the same row (DPP row_ror:kK).
+template <int kK>
+__device__ __forceinline__ uint32_t row_ror_u32(uint32_t v)
+{
+    return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x120 + kK, 0xF, 0xF, true);  // every source is in range
+}
+
+template <int kK>
+__device__ __forceinline__ double row_ror_f64(double v)
+{
+    const uint64_t u = (uint64_t)__double_as_longlong(v);
+    const uint32_t lo = row_ror_u32<kK>((uint32_t)u), hi = row_ror_u32<kK>((uint32_t)(u >> 32));
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+// How many of the row rotations kKs of (ov, orv) are smaller than this lane's (a, r). One
+// rotation at a time (a scheduling barrier after each): unrolled together, their compare
+// masks outgrow the scalar registers.
+template <int... kKs>
+__device__ __forceinline__ uint32_t count_rotations(double a, uint32_t r, double ov, uint32_t orv,
+                                                    std::integer_sequence<int, kKs...>)
+{
+    uint32_t c = 0;
+    ((c += lt_pair(row_ror_f64<kKs>(ov), row_ror_u32<kKs>(orv), a, r), __builtin_amdgcn_sched_barrier(0)), ...);
+    return c;
+}
+
 // DPP move of a double; lanes whose source is outside the pattern (or whose row is masked
 // off) receive `fill`.
 template <int kCtrl, int kRowMask>
@@ -1013,29 +1048,17 @@ __global__ __launch_bounds__(64) void k_lpt_small(uint32_t KW, uint32_t R, uint3
                         const double av = charged ? a : Lv;
                         uint32_t np = 0;
                         if (4u * M > P2) {
-                            // All pairs: lane i counts the lanes with a smaller (L, r) by meeting
-                            // lane i ^ s for s = 1 .. P2-1 (every lane of the power-of-two block
-                            // that holds the R destinations, once). The exchanges are independent
-                            // of one another; lanes >= R hold +inf and count for no one.
-                            // (o, orv) < (av, rv), without branches
-                            auto less = [&](double o, uint32_t orv) {
-                                return (uint32_t)((o < av) | ((o == av) & (orv < rv)));
-                            };
-                            // P2 >= 2 here (M >= 2): s = 1, then 2 .. 3, then four at a time with
-                            // the four exchanges issued before any compare
-                            np = less(ds_bpermute_f64(lane ^ 1u, av), ds_bpermute_u32(lane ^ 1u, rv));
-                            if (P2 >= 4) {
-                                const double o2 = ds_bpermute_f64(lane ^ 2u, av), o3 = ds_bpermute_f64(lane ^ 3u, av);
-                                const uint32_t r2 = ds_bpermute_u32(lane ^ 2u, rv), r3 = ds_bpermute_u32(lane ^ 3u, rv);
-                                np += less(o2, r2) + less(o3, r3);
-                            }
-                            for (uint32_t s = 4; s < P2; s += 4) {
-                                const uint32_t i0 = lane ^ s, i1 = lane ^ (s + 1u), i2 = lane ^ (s + 2u), i3 = lane ^ (s + 3u);
-                                const double o0 = ds_bpermute_f64(i0, av), o1 = ds_bpermute_f64(i1, av);
-                                const double o2 = ds_bpermute_f64(i2, av), o3 = ds_bpermute_f64(i3, av);
-                                const uint32_t r0 = ds_bpermute_u32(i0, rv), r1 = ds_bpermute_u32(i1, rv);
-                                const uint32_t r2 = ds_bpermute_u32(i2, rv), r3 = ds_bpermute_u32(i3, rv);
-                                np += less(o0, r0) + less(o1, r1) + less(o2, r2) + less(o3, r3);
+                            // All pairs: lane i counts the lanes with a smaller (L, r). The 15
+                            // other lanes of its 16-lane row come by DPP row rotations; each other
+                            // row of the power-of-two block that holds the R destinations is
+                            // brought over once (lane i ^ x) and rotated the same way. Lanes >= R
+                            // hold +inf and count for no one.
+                            using Rot = std::integer_sequence<int, 1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15>;
+                            np = count_rotations(av, rv, av, rv, Rot{});
+                            for (uint32_t x = 16; x < P2; x += 16) {
+                                const double sw = ds_bpermute_f64(lane ^ x, av);
+                                const uint32_t sr = ds_bpermute_u32(lane ^ x, rv);
+                                np += lt_pair(sw, sr, av, rv) + count_rotations(av, rv, sw, sr, Rot{});
                             }
                             np = lane < R ? np : lane;
                         } else {
