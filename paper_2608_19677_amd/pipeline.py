@@ -384,19 +384,22 @@ class ChunkStream:
 class ChunkStream3:
     """Consecutive chunks of one request stream, three HIP streams deep.
 
-    A chunk goes through three phases: A (count and admission), B (placement, routing and
-    partition) and C (LRU replay). Step s runs A of chunk s, B of chunk s-1 and C of chunk
-    s-2 at the same time, one HIP stream each. Chunks 1, 2, ... take three buffer sets in
-    turn (chunk 0 has its own), so the three phases of a step touch disjoint buffers: A
-    writes its set's counts and plans, B its set's destinations, records and cleared
-    statistics, C its set's statistics and final cache state (it reads the cache state the
-    chunk before left in another set). Across steps, eager enqueues order each phase after
-    the phases it reads (A of chunk s-1 before B of chunk s-1, B before C) and after the
-    phases that last used its buffers (B of chunk s-3 before A of chunk s, C of chunk s-4
-    before B of chunk s-1); captured steps run one after another, which gives the same
-    order. Chunk k >= 1 plans its first interval from chunk k-1's last window and starts
-    its replay from chunk k-1's final cache state, as if the chunks ran one by one.
+    A chunk goes through four stages: count, admission (with the window sort), B (placement,
+    routing and partition) and the LRU replay. Step s runs, at the same time, the admission
+    of chunk s on one stream, B of chunk s-1 on a second, and on the third the replay of chunk
+    s-2 followed by the count of chunk s+1 (the count is bandwidth-bound and the replay
+    vector-bound, and the admission, which waits on the chip's largest blocks, then has a
+    stream to itself). A chunk's buffers are in use from its count (step k-1) to its replay
+    (step k+2), so chunks 1, 2, ... take four buffer sets in turn (chunk 0 has its own) and
+    the work of a step touches four disjoint sets. Eager enqueues order each stage after
+    the stages it reads (count(k) before admit(k) before B(k) before replay(k)) and after the
+    last users of its set (B of chunk k-4 before count(k) and admit(k), the replay of chunk
+    k-4 before B(k)); captured steps run one after another, which gives the same order.
+    Chunk k >= 1 plans its first interval from chunk k-1's last window and starts its
+    replay from chunk k-1's final cache state, as if the chunks ran one by one.
     """
+
+    NSETS = 4
 
     def __init__(self, wl, device="cuda"):
         self.wl = wl
@@ -405,32 +408,34 @@ class ChunkStream3:
         self.first = Pipeline(wl, device, self.inp)
         last_n = int(self.first.window_sizes[-1])
         self.slots = [Pipeline(wl, device, self.inp, prev_counts=self.first.counts[wl.J - 1], prev_n=last_n,
-                               lru_in=self.first.lru_out) for _ in range(3)]
+                               lru_in=self.first.lru_out) for _ in range(self.NSETS)]
         self.streams = [torch.cuda.Stream(device=device) for _ in range(3)]
-        self.ev = {}  # (phase, chunk) -> event recorded after that phase
+        self.ev = {}  # (stage, chunk) -> event recorded after that stage
         self.s = 0    # next step
+        self.limit = 1 << 62  # chunks from this one on are not started (set by drain)
 
     def pipe(self, k: int) -> Pipeline:
-        return self.first if k == 0 else self.slots[(k - 1) % 3]
+        return self.first if k == 0 else self.slots[(k - 1) % self.NSETS]
 
-    PHASES = {"A": ("count", "admit"), "B": ("place", "route", "partition"), "C": ("lru",)}
+    STAGES = {"count": ("count",), "admit": ("admit",), "B": ("place", "route", "partition"), "lru": ("lru",)}
 
-    def _phase(self, ph, k, stream, waits, timers, capturing=False):
+    def _stage(self, name, k, stream, waits, timers, capturing=False):
         if k < 0 or k >= self.limit:
             return
         p = self.pipe(k)
         with torch.cuda.stream(stream):
-            for key in waits:
-                e = self.ev.get(key)
-                if e is not None:
-                    stream.wait_event(e)
-            if ph == "A":
+            if not capturing:
+                for key in waits:
+                    e = self.ev.get(key)
+                    if e is not None:
+                        stream.wait_event(e)
+            if name == "count":
                 p.first_index = self.wl.first_index + k * self.n
                 if k:
                     prev = self.pipe(k - 1)
                     p.prev_counts = prev.counts[self.wl.J - 1]
                     p.lru_in = prev.lru_out
-            for stage in self.PHASES[ph]:
+            for stage in self.STAGES[name]:
                 if timers is None:
                     getattr(p, stage)()
                 else:
@@ -443,51 +448,52 @@ class ChunkStream3:
             if not capturing:
                 e = torch.cuda.Event()
                 e.record(stream)
-                self.ev[(ph, k)] = e
+                self.ev[(name, k)] = e
 
-    limit = 1 << 62  # chunks from this one on are not started (set by drain)
+    def _enqueue_step(self, s, timers, capturing=False):
+        sa, sb, sc = self.streams
+        if s == 0:  # chunk 0's count has no step before it
+            self._stage("count", 0, sc, [], timers, capturing)
+        self._stage("admit", s, sa, [("count", s), ("B", s - 4)], timers, capturing)
+        self._stage("B", s - 1, sb, [("admit", s - 1), ("lru", s - 5)], timers, capturing)
+        self._stage("lru", s - 2, sc, [("B", s - 2)], timers, capturing)
+        self._stage("count", s + 1, sc, [("B", s - 3)], timers, capturing)
 
     def step(self, timers=None):
-        """Enqueue step s: A of chunk s, B of chunk s-1, C of chunk s-2. Returns the chunk
-        whose replay this step enqueued (None before step 2)."""
+        """Enqueue step s. Returns the chunk whose replay this step enqueued (None if none)."""
         s = self.s
-        sa, sb, sc = self.streams
-        self._phase("A", s, sa, [("B", s - 3)], timers)
-        self._phase("B", s - 1, sb, [("A", s - 1), ("C", s - 4)], timers)
-        self._phase("C", s - 2, sc, [("B", s - 2)], timers)
-        # events no later enqueue waits for: A(k) is read by B(k) (step k+1), B(k) by C(k)
-        # and A(k+3) (steps k+2, k+3), C(k) by B(k+3) (step k+4)
-        for key in (("A", s - 1), ("B", s - 3), ("C", s - 4)):
+        self._enqueue_step(s, timers)
+        # events no later enqueue waits for: count(k) is read at step k, admit(k) at k+1,
+        # B(k) at steps k+2 .. k+4, lru(k) at step k+5
+        for key in (("count", s), ("admit", s - 1), ("B", s - 4), ("lru", s - 5)):
             self.ev.pop(key, None)
         self.s += 1
         return self.pipe(s - 2) if 0 <= s - 2 < self.limit else None
 
     def drain(self, timers=None):
-        """Finish the chunks already started (no new chunk is counted)."""
+        """Finish the chunks already admitted (no new chunk is admitted)."""
         self.limit = self.s
         while self.s < self.limit + 2:
             self.step(timers)
 
     def capture(self):
-        """Record the steady state as three HIP graphs (one per step modulo 3), each with the
-        three phases forked onto their streams and joined at the end. Returns the step
+        """Record the steady state as four HIP graphs (one per step modulo 4), each with the
+        three streams forked from the capture stream and joined at the end. Returns the step
         numbers the graphs were recorded for."""
-        while self.s < 4:
+        while self.s < 5:
             self.step()
         torch.cuda.synchronize()
         self.ev.clear()
         self.graphs = []
         recorded = []
-        for _ in range(3):
+        for _ in range(self.NSETS):
             s = self.s
             g = torch.cuda.CUDAGraph()
             with torch.cuda.graph(g):
                 cap = torch.cuda.current_stream()
                 for st in self.streams:
                     st.wait_stream(cap)
-                self._phase("A", s, self.streams[0], [], None, capturing=True)
-                self._phase("B", s - 1, self.streams[1], [], None, capturing=True)
-                self._phase("C", s - 2, self.streams[2], [], None, capturing=True)
+                self._enqueue_step(s, None, capturing=True)
                 for st in self.streams:
                     cap.wait_stream(st)
             self.graphs.append(g)
@@ -499,4 +505,4 @@ class ChunkStream3:
     def replay_graph(self):
         """One step of the captured steady state: the next graph in turn."""
         self.graphs[self.turn].replay()
-        self.turn = (self.turn + 1) % 3
+        self.turn = (self.turn + 1) % self.NSETS

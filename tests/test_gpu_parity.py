@@ -190,10 +190,11 @@ def _same(h, ref, keys, msg):
 
 
 def test_three_stream_chunk_pipeline_equals_serial():
-    # ChunkStream3 runs count+admit of chunk s, place+route+partition of chunk s-1 and the
-    # replay of chunk s-2 at once on three streams over three buffer sets; seven chunks
-    # enqueued without host synchronisation, then drained, must equal the chunks run one
-    # after another (the last three buffer sets' contents are compared)
+    # ChunkStream3 runs, per step, the admission of chunk s, placement + routing + partition
+    # of chunk s-1, and the replay of chunk s-2 followed by the count of chunk s+1, on three
+    # streams over four buffer sets; seven chunks enqueued without host synchronisation,
+    # then drained, must equal the chunks run one after another (the last three chunks'
+    # buffer sets are compared)
     wl = wl_mod.small_random(44, num_keys=1800, n=130_000, R=30, Ws=[48], J=5, hot=2, hot_share=0.3)
     say(f"[case] three-stream chunks n={wl.n} J={wl.J}")
     cs = ChunkStream3(wl)
@@ -212,22 +213,22 @@ def test_three_stream_chunk_pipeline_equals_serial():
 
 
 def test_three_stream_chunk_graphs_equal_eager_chunks():
-    # the three-stream steady state captured as three HIP graphs (steps 4, 5, 6), replayed
-    # in turn six times with eager reads in between; after replay r (step 4 + r) chunk
-    # 3 + r is planned, routed and partitioned and chunk 2 + r replayed, each equal to the
-    # serial chain. Routing is the only stage that reads the global indices, and each graph
-    # keeps those of the chunk it routed when it was recorded (chunks 3, 4, 5 in turn)
+    # the steady state captured as four HIP graphs (steps 5 .. 8), replayed in turn eight
+    # times with eager reads in between; after replay r (step 5 + r) chunk 4 + r is planned,
+    # routed and partitioned and chunk 3 + r replayed, each equal to the serial chain.
+    # Routing is the only stage that reads the global indices, and each graph keeps those
+    # of the chunk it routed when it was recorded (chunks 4 .. 7 in turn)
     wl = wl_mod.small_random(45, num_keys=1500, n=120_000, R=30, Ws=[32], J=4, hot=2, hot_share=0.3)
     say(f"[case] three-stream chunk graphs n={wl.n} J={wl.J}")
     cs = ChunkStream3(wl)
     steps = cs.capture()
-    assert steps == [4, 5, 6]
-    ref = _chunk_chain(wl, [0, 1, 2, 3, 4, 5, 3, 4, 5, 3])
-    for r in range(6):
+    assert steps == [5, 6, 7, 8]
+    ref = _chunk_chain(wl, [0, 1, 2, 3, 4, 5, 6, 7, 4, 5, 6, 7])
+    for r in range(8):
         cs.replay_graph()
         torch.cuda.synchronize()
-        _same(cs.pipe(3 + r).host(), ref[3 + r], ("counts", "load", "dest"), f"replay {r} chunk {3 + r}")
-        _same(cs.pipe(2 + r).host(), ref[2 + r], ("stats", "lru"), f"replay {r} chunk {2 + r}")
+        _same(cs.pipe(4 + r).host(), ref[4 + r], ("counts", "load", "dest"), f"replay {r} chunk {4 + r}")
+        _same(cs.pipe(3 + r).host(), ref[3 + r], ("stats", "lru"), f"replay {r} chunk {3 + r}")
 
 
 def test_two_stream_chunk_graphs_equal_eager_chunks():
