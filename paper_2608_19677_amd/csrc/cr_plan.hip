@@ -1238,6 +1238,9 @@ __global__ __launch_bounds__(64) void k_lpt(uint32_t KW, uint32_t R, uint32_t Cm
 // load sums are ordered, and one wavefront per plan adds them in admission order with
 // the destinations spread over its lanes (k_hash_loads).
 constexpr uint32_t kHashThreads = 256;
+constexpr uint32_t kHashStage = 4096;  // largest Cmax whose lists k_hash_loads keeps in LDS
+
+inline size_t hash_loads_lds_bytes(uint32_t Cmax) { return (size_t)Cmax * 14u + 2u + 512u; }
 
 __device__ __forceinline__ uint32_t place_key_hash(uint32_t seed, uint32_t b)
 {
@@ -1285,7 +1288,7 @@ __global__ void __launch_bounds__(64)
     k_hash_loads(uint32_t R, uint32_t Cmax, uint32_t NW, const cr_plan_spec* __restrict__ specs,
                  const uint32_t* __restrict__ order_count, const uint32_t* __restrict__ num_admitted,
                  const uint64_t* __restrict__ cold, const uint32_t* __restrict__ member_off,
-                 const uint16_t* __restrict__ members, double* __restrict__ load)
+                 const uint16_t* __restrict__ members, double* __restrict__ load, bool lds_ok)
 {
     const uint32_t p = blockIdx.x, lane = lane_id();
     const cr_plan_spec spec = specs[p];
@@ -1299,6 +1302,73 @@ __global__ void __launch_bounds__(64)
     double Lr[kS];
 #pragma unroll
     for (int s = 0; s < kS; ++s) Lr[s] = init;
+    // R <= 64 with the plan's lists in LDS (the host gives kS == 1 launches Cmax-sized
+    // dynamic LDS when Cmax <= kHashStage): a destination's load needs only its own jobs, in
+    // job order. The member copies (job order, each job's members distinct) are sorted
+    // stably by destination in LDS, 64 at a time (a copy's rank is its destination's count
+    // in earlier chunks plus the earlier lanes of its chunk with the same destination, by
+    // ballots over the destination bits); lane r then adds the charges of its own list in
+    // order -- the same additions, in the same order per destination, as the job loop below.
+    if (kS == 1 && lds_ok) {
+        extern __shared__ double s_dyn[];
+        double* s_x = s_dyn;                                                  // [Cmax] job charges
+        uint16_t* s_mem = reinterpret_cast<uint16_t*>(s_x + Cmax);           // [Cmax] members
+        uint16_t* s_job = s_mem + Cmax;                                       // [Cmax] job of a copy
+        uint16_t* s_ord = s_job + Cmax;                                       // [Cmax] sorted copies
+        uint32_t* s_cnt = reinterpret_cast<uint32_t*>(s_ord + Cmax + (Cmax & 1u));  // [64]
+        uint32_t* s_run = s_cnt + 64;                                         // [64]
+        const uint32_t total = A ? (uint32_t)__builtin_amdgcn_readfirstlane((int)moff[A]) : 0u;  // <= Cmax
+        s_cnt[lane] = 0;
+        for (uint32_t a = lane; a < A; a += 64u) {
+            const uint32_t o = moff[a], k = moff[a + 1u] - o;
+            s_x[a] = (double)ocnt[a] / (double)k;
+            for (uint32_t t = 0; t < k; ++t) s_job[o + t] = (uint16_t)a;
+        }
+        for (uint32_t i0 = 0; i0 < total; i0 += 16u * 64u) {  // all loads in flight
+            uint32_t v[16];
+#pragma unroll
+            for (uint32_t u = 0; u < 16; ++u) {
+                const uint32_t i = i0 + u * 64u + lane;
+                v[u] = i < total ? (uint32_t)mem[i] : 0xFFFFu;
+            }
+#pragma unroll
+            for (uint32_t u = 0; u < 16; ++u) {
+                const uint32_t i = i0 + u * 64u + lane;
+                if (i < total) {
+                    s_mem[i] = (uint16_t)v[u];
+                    if (v[u] < R) atomicAdd(&s_cnt[v[u]], 1u);
+                }
+            }
+        }
+        __syncthreads();
+        const uint32_t cnt = lane < R ? s_cnt[lane] : 0u;
+        const uint32_t off = wave_incl_scan_u32(cnt) - cnt;
+        s_run[lane] = off;
+        __syncthreads();
+        uint32_t nbits = 0;
+        while ((1u << nbits) < R) ++nbits;
+        for (uint32_t i0 = 0; i0 < total; i0 += 64u) {
+            const uint32_t i = i0 + lane;
+            const uint32_t m = i < total ? (uint32_t)s_mem[i] : 0xFFFFu;
+            const bool valid = m < R;
+            uint64_t peers = ballot(valid);
+            for (uint32_t bit = 0; bit < nbits; ++bit) {
+                const bool on = (m >> bit) & 1u;
+                const uint64_t bb = ballot(on);
+                peers &= on ? bb : ~bb;
+            }
+            const uint32_t rk = (uint32_t)__popcll(peers & lanemask_lt());
+            const uint32_t at = valid ? s_run[m] + rk : 0u;
+            if (valid) s_ord[at] = s_job[i];
+            __syncthreads();
+            if (valid && rk == 0) s_run[m] = at + (uint32_t)__popcll(peers);
+            __syncthreads();
+        }
+        double L = Lr[0];
+        for (uint32_t q = 0; q < cnt; ++q) L = L + s_x[s_ord[off + q]];
+        if (lane < R) load[(uint64_t)p * R + lane] = L;
+        return;
+    }
     for (uint32_t base = 0; base < A; base += 64u) {
         // lane j holds job base + j: its charge, copy count, first member and offset
         const uint32_t a = base + lane;
@@ -1529,16 +1599,17 @@ extern "C" cr_status cr_place_hash(const uint32_t* counts, const cr_plan_set* pl
                        dim3(kHashThreads), 0, st, plans->R, cmax, plans->num_windows, key_words(plans->num_keys),
                        plans->specs, plans->order, plans->num_admitted, plans->member_off, plans->key_index,
                        plans->members, plans->route);
-#define CR_HASH_LOADS(S)                                                                                            \
-    hipLaunchKernelGGL(k_hash_loads<S>, dim3(plans->num_plans), dim3(64), 0, st, plans->R, cmax, plans->num_windows, \
-                       plans->specs, plans->order_count, plans->num_admitted, plans->cold, plans->member_off,       \
-                       plans->members, plans->load)
+#define CR_HASH_LOADS(S, LDS, OK)                                                                                   \
+    hipLaunchKernelGGL(k_hash_loads<S>, dim3(plans->num_plans), dim3(64), (LDS), st, plans->R, cmax,                  \
+                       plans->num_windows, plans->specs, plans->order_count, plans->num_admitted, plans->cold,        \
+                       plans->member_off, plans->members, plans->load, (OK))
     const uint32_t s = (plans->R + 63) / 64;
-    if (s <= 1) CR_HASH_LOADS(1);
-    else if (s <= 2) CR_HASH_LOADS(2);
-    else if (s <= 4) CR_HASH_LOADS(4);
-    else if (s <= 8) CR_HASH_LOADS(8);
-    else CR_HASH_LOADS(16);
+    const bool lds_ok = s <= 1 && cmax <= kHashStage;  // R <= 64: the plan's lists fit in LDS
+    if (s <= 1) CR_HASH_LOADS(1, lds_ok ? hash_loads_lds_bytes(cmax) : 0, lds_ok);
+    else if (s <= 2) CR_HASH_LOADS(2, 0, false);
+    else if (s <= 4) CR_HASH_LOADS(4, 0, false);
+    else if (s <= 8) CR_HASH_LOADS(8, 0, false);
+    else CR_HASH_LOADS(16, 0, false);
 #undef CR_HASH_LOADS
     return hipGetLastError() == hipSuccess ? CR_OK : CR_EHIP;
 }
