@@ -487,7 +487,7 @@ __device__ __forceinline__ uint32_t mtf_core(uint32_t& sk, uint64_t m)
         "v_cndmask_b32_dpp %0, %2, %2, vcc wave_shr:1 row_mask:0xf bank_mask:0xf"
         : "=v"(out), "=&s"(p)
         : "v"(sk), "s"(m)
-        : "vcc");
+        : "vcc", "scc");  // s_lshl_b64 sets SCC
     sk = out;
     return p;
 }
@@ -550,7 +550,7 @@ __device__ __forceinline__ uint32_t il_core(uint32_t first, uint32_t last, uint6
         "v_cndmask_b32_dpp %0, %4, %3, vcc wave_shr:1 row_mask:0xf bank_mask:0xf"
         : "=v"(out), "=&s"(l), "=&s"(keep)
         : "v"(first), "v"(last), "s"(m)
-        : "vcc");
+        : "vcc", "scc");  // s_lshl_b64 sets SCC
     return out;
 }
 
