@@ -520,6 +520,20 @@ __device__ __forceinline__ uint32_t rebuild_batch(uint32_t (&sk)[SL], const uint
         uint32_t key[8];
 #pragma unroll
         for (uint32_t t = 0; t < 8; ++t) key[t] = (uint32_t)rk[7u - t];  // newest first
+        if (SL == 1 && q + 8u <= W) {
+            // Positions q and up are free while the list is rebuilt, so every key is written
+            // into lane q and q advances only past a new one; a repeated key left in lane q
+            // duplicates an entry at a smaller position, which every later lookup finds
+            // first, and the next new key overwrites it. Lanes past the final q are cleared
+            // once the rebuild ends. q + 8 <= W <= 64 keeps every write inside the wave.
+#pragma unroll
+            for (uint32_t t = 0; t < 8; ++t) {
+                const uint64_t m = ballot(sk[0] == key[t]);
+                sk[0] = wrlane(sk[0], key[t], q);
+                asm("s_cmp_eq_u64 %1, 0\n\ts_addc_u32 %0, %0, 0" : "+s"(q) : "s"(m) : "scc");  // q += (m == 0)
+            }
+            continue;
+        }
 #pragma unroll
         for (uint32_t t = 0; t < 8; ++t) {
             uint64_t m = 0;
@@ -726,6 +740,10 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
                 }
             }
         }
+    }
+
+    if constexpr (SL == 1) {
+        if (q < W) skey[0] = lane >= q ? CR_EMPTY_SLOT : skey[0];  // drop what the rebuild left past q
     }
 
     // Per-lane sums for the current interval; flushed (one atomic per statistic) when the
