@@ -41,13 +41,17 @@ struct WArg {
 // longer segments only save the backward rebuild of the initial state.
 constexpr uint64_t kSegTarget = 16384;
 
-// Records per segment: at least 16 W (the rebuild scans back to W distinct keys) and at
-// least the share that keeps the number of segments near kSegTarget.
+// Shortest segment; the launch sizes its grid for segments of this length.
+constexpr uint32_t kSegFloor = 1024;
+constexpr uint32_t kSegPerSlot = 16;
+
+// Records per segment: at least kSegPerSlot W (the rebuild scans back to W distinct keys)
+// and at least the share that keeps the number of segments near kSegTarget.
 __host__ __device__ __forceinline__ uint32_t seg_len(uint32_t W, uint32_t seg_min)
 {
-    uint32_t s = 16u * W;
+    uint32_t s = kSegPerSlot * W;
     s = s > seg_min ? s : seg_min;
-    return s < 1024u ? 1024u : (s > 65536u ? 65536u : s);
+    return s < kSegFloor ? kSegFloor : (s > 65536u ? 65536u : s);
 }
 
 __host__ __device__ __forceinline__ uint32_t slot_class(uint32_t W)
@@ -952,7 +956,7 @@ extern "C" cr_status cr_replay_lru(const uint32_t* prefix_len, uint32_t num_keys
     const ReplayWs w = replay_layout(ws_base(ws), n, P, R);
     const hipStream_t st = as_stream(stream);
     // Upper bound on work items: one per (c, d) plus one per full segment.
-    const uint64_t items = (uint64_t)P * R + (uint64_t)P * n / 1024u + 1u;
+    const uint64_t items = (uint64_t)P * R + (uint64_t)P * n / kSegFloor + 1u;
     const uint64_t blocks = (items + (kReplayThreads / 64) - 1) / (kReplayThreads / 64);
     if (blocks > 0x7FFFFFFFull) return CR_EINVAL;
     (void)hipGetLastError();
