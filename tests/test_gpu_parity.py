@@ -43,6 +43,10 @@ SMALL = [
     (10, 64, 4096, 128, [1, 63, 64], 2, 0, 0.0, [(1, 1)]),
     (11, 300, 20_000, 2, [8, 30], 3, 2, 0.5, [(1, 1)]),         # two destinations: one exchange per merge
     (12, 600, 40_000, 33, [6, 12], 4, 3, 0.4, [(1, 2)]),        # 31 idle lanes in the 64-lane merge
+    # 40 keys over two destinations, W = 64 and 48: every segment's rebuild runs through full
+    # 64-record batches to the start of the stream without filling the list, so repeated keys
+    # are written past q and must be cleared before the replay and the final state
+    (13, 40, 20_000, 2, [64, 48], 3, 0, 0.0, [(1, 1)]),
 ]
 
 
