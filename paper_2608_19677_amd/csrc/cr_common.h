@@ -17,6 +17,12 @@ __device__ __forceinline__ uint32_t lane_id()
 
 __device__ __forceinline__ uint64_t ballot(bool p) { return __ballot(p); }
 
+// Raises the calling wavefront's instruction-issue priority on its SIMD (s_setprio 3). The
+// placement, routing and partition kernels are chains of dependent latency-bound steps; when
+// they share SIMDs with the vector-bound replay launched on another stream, this keeps the
+// replay's wavefronts from taking every issue slot ahead of them. Results are unaffected.
+__device__ __forceinline__ void issue_priority_high() { __builtin_amdgcn_s_setprio(3); }
+
 __device__ __forceinline__ uint64_t lanemask_lt()
 {
     const uint32_t l = lane_id();

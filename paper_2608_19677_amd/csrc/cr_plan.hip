@@ -929,6 +929,7 @@ __global__ __launch_bounds__(64) void k_lpt_small(uint32_t KW, uint32_t R, uint3
                                                   uint16_t* __restrict__ members, double* __restrict__ load,
                                                   uint32_t* __restrict__ route)
 {
+    issue_priority_high();
     // member picked for single-copy job a in slot a mod 128; slots 128.. take the stores of
     // lanes >= R so that the round loop needs no divergent branch
     __shared__ uint32_t s_mem[192];
@@ -1162,6 +1163,7 @@ __global__ __launch_bounds__(64) void k_lpt(uint32_t KW, uint32_t R, uint32_t Cm
                                             const uint64_t* __restrict__ key_index, uint16_t* __restrict__ members,
                                             double* __restrict__ load, uint32_t* __restrict__ route)
 {
+    issue_priority_high();
     const uint32_t p = blockIdx.x, lane = lane_id();
     const cr_plan_spec spec = specs[p];
     if (hash_placed(spec.variant)) return;  // placed by cr_place_hash

@@ -82,6 +82,7 @@ __global__ __launch_bounds__(kHistThreads) void k_part_hist(const uint16_t* __re
                                                             uint64_t tile, uint64_t ntiles, uint32_t* __restrict__ tcnt,
                                                             uint32_t* __restrict__ err)
 {
+    issue_priority_high();
     extern __shared__ uint32_t h[];
     const uint32_t c = blockIdx.y;
     const uint64_t t = blockIdx.x;
@@ -118,6 +119,7 @@ constexpr uint32_t kScanThreads = 1024;
 __global__ __launch_bounds__(kScanThreads) void k_scan_dest(uint32_t* __restrict__ tcnt, uint64_t ntiles, uint32_t R,
                                                             uint32_t* __restrict__ dtot)
 {
+    issue_priority_high();
     __shared__ uint32_t s_scan[16];
     const uint32_t d = blockIdx.x, c = blockIdx.y;
     uint32_t* __restrict__ t = tcnt + ((uint64_t)c * R + d) * ntiles;
@@ -162,6 +164,7 @@ __global__ __launch_bounds__(64) void k_part_scatter(const uint32_t* __restrict_
                                                      const uint32_t* __restrict__ tcnt,
                                                      const uint32_t* __restrict__ grp_off, uint64_t* __restrict__ rec)
 {
+    issue_priority_high();
     extern __shared__ uint64_t lds[];
     uint64_t* srec = lds;                                        // [kSub] staged records
     uint32_t* spos = reinterpret_cast<uint32_t*>(srec + kSub);  // [kSub] their output positions
@@ -282,6 +285,7 @@ __global__ __launch_bounds__(64) void k_part_scatter64(const uint32_t* __restric
                                                        const uint32_t* __restrict__ grp_off,
                                                        uint64_t* __restrict__ rec)
 {
+    issue_priority_high();
     extern __shared__ uint64_t lds[];
     uint64_t* srec = lds;                                            // [kSub] staged records
     uint32_t* spos = reinterpret_cast<uint32_t*>(srec + kSub);      // [kSub] their output positions
@@ -419,6 +423,7 @@ __global__ __launch_bounds__(1024) void k_seg_items(const uint32_t* __restrict__
                                                     WArg wa, uint32_t* __restrict__ grp_off,
                                                     uint32_t* __restrict__ item_off)
 {
+    issue_priority_high();
     __shared__ uint32_t s_scan[16];
     __shared__ uint32_t s_cstart[CR_MAX_CANDS + 1];
     const uint32_t total = P * R;

@@ -31,6 +31,7 @@ __global__ __launch_bounds__(kRouteThreads) void k_route(
     const uint16_t* __restrict__ members, const double* __restrict__ load, uint16_t* __restrict__ dest,
     uint32_t* __restrict__ err)
 {
+    issue_priority_high();
     __shared__ uint32_t s_j0;
     __shared__ uint32_t s_rel[kBnd];     // next interval starts relative to the block (clamped)
     __shared__ uint32_t s_g[kBnd + 1];   // plan groups of intervals j0 .. j0 + kBnd
