@@ -8,9 +8,9 @@
 //                  count (descending), which yields (count desc, key asc) exactly;
 //   k_admit_plan   one block per plan: k by Eq. 1 in exact integers, block prefix sum of
 //                  k, and the longest prefix whose sum fits C = R * W.
-// LPT is a dependency chain of sum(k) steps per plan; one wavefront owns one plan and
-// keeps the R loads in registers (lane l holds destinations l, l+64, ...), so each pick
-// is a register scan plus a 6-step cross-lane (L, r) argmin.
+// LPT is a dependency chain of sum(k) steps per plan, cut into exact batches of
+// consecutive jobs: one wavefront per plan for R <= 64 (k_lpt_small), one block of up to
+// 1,024 threads per plan above that (k_lpt_block).
 // k_plan_churn compares pairs of built plans for the replanning study.
 #include <math.h>
 
@@ -1150,87 +1150,235 @@ __global__ __launch_bounds__(64) void k_lpt_small(uint32_t KW, uint32_t R, uint3
     if (lane < R) load[(uint64_t)p * R + rv] = Lv;
 }
 
-// R > 64: lane l holds destinations l, l+64, ... (kS registers); each pick is a register
-// scan plus a cross-lane (L, r) argmin.
-template <int kS>
-__global__ __launch_bounds__(64) void k_lpt(uint32_t KW, uint32_t R, uint32_t Cmax, uint32_t NW,
-                                            const cr_plan_spec* __restrict__ specs,
-                                            const uint32_t* __restrict__ order,
-                                            const uint32_t* __restrict__ order_count,
-                                            const uint32_t* __restrict__ num_admitted,
-                                            const uint64_t* __restrict__ cold,
-                                            const uint32_t* __restrict__ member_off,
-                                            const uint64_t* __restrict__ key_index, uint16_t* __restrict__ members,
-                                            double* __restrict__ load, uint32_t* __restrict__ route)
+// 64 < R <= 1024: one block of N threads (N = the power of two >= R) per plan; thread i
+// holds the i-th smallest (L, r) pair in registers, and the sorted state is mirrored in LDS.
+// Jobs are placed in batches, with the rule k_lpt_small uses: consecutive single-copy jobs
+// t, t+1, ... take sorted positions 0, 1, ... while position q's load is below every load
+// charged to the positions before it in the batch (position q is then the least (L, r) pair
+// when job t+q is placed), found by a block-wide exclusive prefix minimum; ties end the
+// batch. A job with k > 1 is a batch of its own that charges positions 0..k-1, its members in
+// that order. After a batch the charged positions are merged back into the sorted state:
+// when their new (L, r) pairs are still in order, by a merge path (each element's rank in the
+// other sorted list by binary search in LDS); otherwise by a bitonic sort of all N pairs.
+// On the large sweep (R = 1,024, up to 524,288 jobs per plan) a plan takes about 600
+// batches. Route words are written afterwards by k_route_words, in parallel.
+template <int N>
+struct LptBlockLds {
+    double v[2][N];        // sorted state (double-buffered for the merge)
+    uint32_t r[2][N];
+    double cv[N];          // the batch's charged pairs (positions 0..M-1)
+    uint32_t cr[N];
+    uint32_t jc[2 * N];    // job ring: counts, member offsets, k (0 past A)
+    uint32_t jo[2 * N];
+    uint16_t jk[2 * N];
+    double wmin[N / 64];   // per-wavefront minimum of the charged loads
+    double l0a[N / 64];    // per-wavefront lane 0: charged load, load, destination
+    double l0v[N / 64];
+    uint32_t l0r[N / 64];
+    uint32_t wfail[N / 64];  // per-wavefront first position that fails the batch rule
+    uint32_t wuns[N / 64];   // per-wavefront: the charged pairs are out of order
+};
+
+// Number of pairs among (v[lo .. lo+len)) smaller than (x, rx); the list is sorted.
+__device__ __forceinline__ uint32_t lower_bound_pair(const double* __restrict__ v, const uint32_t* __restrict__ r,
+                                                     uint32_t lo, uint32_t len, double x, uint32_t rx)
 {
+    uint32_t n = len, b = lo;
+    while (n > 0) {
+        const uint32_t h = n >> 1;
+        const uint32_t m = b + h;
+        if (lt_pair(v[m], r[m], x, rx)) {
+            b = m + 1;
+            n -= h + 1;
+        } else {
+            n = h;
+        }
+    }
+    return b - lo;
+}
+
+template <int N>
+__global__ __launch_bounds__(N) void k_lpt_block(uint32_t R, uint32_t Cmax, const cr_plan_spec* __restrict__ specs,
+                                                 const uint32_t* __restrict__ order_count,
+                                                 const uint32_t* __restrict__ num_admitted,
+                                                 const uint64_t* __restrict__ cold, uint32_t NW,
+                                                 const uint32_t* __restrict__ member_off,
+                                                 uint16_t* __restrict__ members, double* __restrict__ load)
+{
+    static_assert(N >= 128 && N <= 1024 && (N & (N - 1)) == 0, "block of 128..1024 threads");
+    constexpr uint32_t NWV = N / 64;
+    __shared__ LptBlockLds<N> sh;
     issue_priority_high();
-    const uint32_t p = blockIdx.x, lane = lane_id();
+    const uint32_t p = blockIdx.x, i = threadIdx.x, lane = lane_id(), wv = i >> 6;
     const cr_plan_spec spec = specs[p];
     if (hash_placed(spec.variant)) return;  // placed by cr_place_hash
     const uint32_t A = num_admitted[p];
     const uint32_t w = spec.window < NW ? spec.window : 0u;
-    const uint32_t* __restrict__ ord = order + (uint64_t)w * Cmax;
     const uint32_t* __restrict__ ocnt = order_count + (uint64_t)w * Cmax;
     const uint32_t* __restrict__ moff = member_off + (uint64_t)p * (Cmax + 1u);
     uint16_t* __restrict__ mem = members + (uint64_t)p * Cmax;
-    const uint64_t* __restrict__ kx = key_index + (uint64_t)p * 2u * KW;
-    uint32_t* __restrict__ rw = route + (uint64_t)p * Cmax;
-    const double init = (double)cold[p] / (double)R;
-    double Lr[kS];
-#pragma unroll
-    for (int s = 0; s < kS; ++s) Lr[s] = (s * 64u + lane < R) ? init : INFINITY;
-    uint32_t taken = 0;
-    LptBatch nxt = lpt_load(ord, ocnt, moff, lane, A);
-    for (uint32_t a0 = 0; a0 < A; a0 += 64) {
-        const LptBatch cur = nxt;
-        nxt = lpt_load(ord, ocnt, moff, a0 + 64 + lane, A);
-        const ulonglong2 kxc = kx_entry(kx, cur.key, a0 + lane < A);  // needed at the end of the batch
-        const uint32_t nb = A - a0 < 64u ? A - a0 : 64u;
-        const uint32_t k_l = cur.end - cur.off;
-        const double x_l = k_l == 1 ? (double)cur.cnt : (double)cur.cnt / (double)k_l;
-        uint32_t first = 0;
-        for (uint32_t t = 0; t < nb; ++t) {
-            const uint32_t off = rdlane(cur.off, t), k = rdlane(k_l, t);
-            const double x = rdlane_f64(x_l, t);
-            for (uint32_t m = 0; m < k; ++m) {
-                double bv = INFINITY;
-                uint32_t br = 0xFFFFFFFFu;
-#pragma unroll
-                for (int s = 0; s < kS; ++s) {
-                    const uint32_t r = s * 64u + lane;
-                    if (r < R && !((taken >> s) & 1u) && Lr[s] < bv) {
-                        bv = Lr[s];
-                        br = r;
-                    }
-                }
-#pragma unroll
-                for (int o = 32; o >= 1; o >>= 1) {
-                    const double ov = __shfl_xor(bv, o, 64);
-                    const uint32_t orr = __shfl_xor(br, o, 64);
-                    if (ov < bv || (ov == bv && orr < br)) {
-                        bv = ov;
-                        br = orr;
-                    }
-                }
-                if (k > 1 && lane == 0) mem[off + m] = (uint16_t)br;
-                if ((br & 63u) == lane) taken |= 1u << (br >> 6);
-                if (m == 0 && lane == t) first = br;
+    const double INF = INFINITY;
+    double v = i < R ? (double)cold[p] / (double)R : INF;
+    uint32_t r = i < R ? i : 0xFFFFFFFFu;
+    sh.v[0][i] = v;
+    sh.r[0][i] = r;
+    // job a: (count, member offset, k); k = 0 marks a >= A
+    auto job = [&](uint32_t a, uint32_t& c, uint32_t& o, uint32_t& k) {
+        const uint32_t aa = a < A ? a : 0u;
+        c = ocnt[aa];
+        o = moff[aa];
+        k = a < A ? moff[aa + 1] - o : 0u;
+    };
+    uint32_t pc, po, pk;  // job base + 2N + i, loaded one refill ahead
+    {
+        uint32_t c, o, k;
+        job(i, c, o, k);
+        sh.jc[i] = c, sh.jo[i] = o, sh.jk[i] = (uint16_t)k;
+        job(N + i, c, o, k);
+        sh.jc[N + i] = c, sh.jo[N + i] = o, sh.jk[N + i] = (uint16_t)k;
+        job(2 * N + i, pc, po, pk);
+    }
+    uint32_t cur = 0, base = 0, t = 0;
+    __syncthreads();
+    while (t < A) {
+        const uint32_t rj = (t + i) & (2u * N - 1u), r0 = t & (2u * N - 1u);
+        const uint32_t c = sh.jc[rj], o = sh.jo[rj], k = sh.jk[rj];
+        const uint32_t k0 = sh.jk[r0];
+        double a;
+        uint32_t M;
+        if (k0 > 1) {
+            // multi-copy job t: positions 0..k0-1, each charged count / k0
+            const double x0 = (double)sh.jc[r0] / (double)k0;
+            a = v + x0;
+            if (lane == 0) {
+                sh.l0a[wv] = a;
+                sh.l0v[wv] = v;
+                sh.l0r[wv] = r;
             }
-#pragma unroll
-            for (int s = 0; s < kS; ++s)
-                if ((taken >> s) & 1u) Lr[s] = Lr[s] + x;
-            taken = 0;
+            M = k0;
+            if (i < M) mem[sh.jo[r0] + i] = (uint16_t)r;
+            __syncthreads();
+        } else {
+            const bool single = k == 1 && i < R;
+            a = single ? v + (double)c : INF;  // position i's load once charged with job t+i
+            double pm = wave_exclusive_min_f64(a);
+            const double wtot = __shfl(fmin(pm, a), 63, 64);
+            if (lane == 0) {
+                sh.wmin[wv] = wtot;
+                sh.l0a[wv] = a;
+                sh.l0v[wv] = v;
+                sh.l0r[wv] = r;
+            }
+            __syncthreads();
+            for (uint32_t u = 0; u < wv; ++u) pm = fmin(pm, sh.wmin[u]);
+            const bool ok = single && (i == 0 || v < pm);
+            const uint64_t bad = ballot(!ok);
+            if (lane == 0) sh.wfail[wv] = bad ? wv * 64u + (uint32_t)__builtin_ctzll(bad) : N;
+            __syncthreads();
+            M = N;
+            for (uint32_t u = 0; u < NWV; ++u) M = min(M, sh.wfail[u]);
+            if (i < M) mem[o] = (uint16_t)r;
         }
-        if (lane < nb) {
-            if (k_l == 1) mem[cur.off] = (uint16_t)first;
-            rw[kx_rank(kxc, cur.key)] = k_l == 1 ? (CR_ROUTE_SINGLE | first) : (a0 + lane);
+        // charged pairs (positions < M) and whether they are still in (L, r) order
+        const bool charged = i < M;
+        const double wv_ = charged ? a : v;
+        double nx = __shfl_down(wv_, 1, 64);
+        uint32_t nr = __shfl_down(r, 1, 64);
+        if (lane == 63 && wv + 1 < NWV) {
+            nx = (wv + 1) * 64u < M ? sh.l0a[wv + 1] : sh.l0v[wv + 1];
+            nr = sh.l0r[wv + 1];
         }
+        const bool out_of_order = i + 1 < M && !lt_pair(wv_, r, nx, nr);
+        const uint64_t uns = ballot(out_of_order);
+        if (lane == 0) sh.wuns[wv] = uns != 0;
+        if (charged) {
+            sh.cv[i] = a;
+            sh.cr[i] = r;
+        }
+        __syncthreads();
+        uint32_t any_uns = 0;
+        for (uint32_t u = 0; u < NWV; ++u) any_uns |= sh.wuns[u];
+        const uint32_t nxt = cur ^ 1u;
+        if (!any_uns) {
+            // merge path: charged list cv[0..M) and the unchanged sorted positions M..R-1
+            if (i < R) {
+                const uint32_t pos = charged ? i + lower_bound_pair(sh.v[cur], sh.r[cur], M, R - M, a, r)
+                                             : (i - M) + lower_bound_pair(sh.cv, sh.cr, 0, M, v, r);
+                sh.v[nxt][pos] = charged ? a : v;
+                sh.r[nxt][pos] = r;
+            } else {
+                sh.v[nxt][i] = INF;
+                sh.r[nxt][i] = 0xFFFFFFFFu;
+            }
+            __syncthreads();
+            v = sh.v[nxt][i];
+            r = sh.r[nxt][i];
+        } else {
+            // bitonic sort of all N pairs (positions >= R hold (+inf, ~0) and stay last)
+            v = wv_;
+            for (uint32_t kk = 2; kk <= N; kk <<= 1) {
+                for (uint32_t j = kk >> 1; j > 0; j >>= 1) {
+                    double pv;
+                    uint32_t pr;
+                    if (j >= 64) {
+                        sh.v[nxt][i] = v;
+                        sh.r[nxt][i] = r;
+                        __syncthreads();
+                        pv = sh.v[nxt][i ^ j];
+                        pr = sh.r[nxt][i ^ j];
+                        __syncthreads();
+                    } else {
+                        pv = __shfl_xor(v, (int)j, 64);
+                        pr = __shfl_xor(r, (int)j, 64);
+                    }
+                    const bool up = (i & kk) == 0, lower = (i & j) == 0;
+                    const bool pless = lt_pair(pv, pr, v, r) != 0;
+                    if (pless == (lower == up)) {
+                        v = pv;
+                        r = pr;
+                    }
+                }
+            }
+            sh.v[nxt][i] = v;
+            sh.r[nxt][i] = r;
+        }
+        cur = nxt;
+        t += k0 > 1 ? 1u : (M ? M : 1u);  // M = 0 only for a job with k = 0, which admission never makes
+        if (t >= base + N) {  // the ring's older half is consumed: refill it one half ahead
+            const uint32_t slot = (base + i) & (2u * N - 1u);
+            sh.jc[slot] = pc, sh.jo[slot] = po, sh.jk[slot] = (uint16_t)pk;
+            base += N;
+            job(base + 2 * N + i, pc, po, pk);
+        }
+        __syncthreads();
     }
-#pragma unroll
-    for (int s = 0; s < kS; ++s) {
-        const uint32_t r = s * 64u + lane;
-        if (r < R) load[(uint64_t)p * R + r] = Lr[s];
-    }
+    if (i < R) load[(uint64_t)p * R + r] = v;
+}
+
+// Route words of plans placed by k_lpt_block: per admitted key a, CR_ROUTE_SINGLE | its
+// member when k = 1, else a, stored at the key's rank in the plan's key index.
+constexpr uint32_t kWordThreads = 256;
+
+__global__ __launch_bounds__(kWordThreads) void k_route_words(uint32_t Cmax, uint32_t NW, uint32_t KW,
+                                                              const cr_plan_spec* __restrict__ specs,
+                                                              const uint32_t* __restrict__ order,
+                                                              const uint32_t* __restrict__ num_admitted,
+                                                              const uint32_t* __restrict__ member_off,
+                                                              const uint16_t* __restrict__ members,
+                                                              const uint64_t* __restrict__ key_index,
+                                                              uint32_t* __restrict__ route)
+{
+    const uint32_t p = blockIdx.y;
+    const uint32_t a = blockIdx.x * kWordThreads + threadIdx.x;
+    const cr_plan_spec spec = specs[p];
+    if (hash_placed(spec.variant) || a >= num_admitted[p]) return;
+    const uint32_t w = spec.window < NW ? spec.window : 0u;
+    const uint32_t b = order[(uint64_t)w * Cmax + a];
+    const uint32_t* __restrict__ moff = member_off + (uint64_t)p * (Cmax + 1u);
+    const uint32_t o = moff[a], k = moff[a + 1] - o;
+    const uint32_t word = k == 1 ? (CR_ROUTE_SINGLE | members[(uint64_t)p * Cmax + o]) : a;
+    const ulonglong2 e = kx_entry(key_index + (uint64_t)p * 2u * KW, b, (b >> 6) < KW);
+    route[(uint64_t)p * Cmax + kx_rank(e, b)] = word;
 }
 
 // Hash placement of the ablation variants (Section 5.2, 8B component ablation table).
@@ -1560,17 +1708,19 @@ extern "C" cr_status cr_place_lpt(const uint32_t* counts, const cr_plan_set* pla
                            plans->load, plans->route);
         return hipGetLastError() == hipSuccess ? CR_OK : CR_EHIP;
     }
-#define CR_LPT(S)                                                                                                   \
-    hipLaunchKernelGGL(k_lpt<S>, dim3(plans->num_plans), dim3(64), 0, st, key_words(plans->num_keys), plans->R,   \
-                       cmax, plans->num_windows, plans->specs, plans->order, plans->order_count,                    \
-                       plans->num_admitted, plans->cold, plans->member_off, plans->key_index, plans->members,       \
-                       plans->load, plans->route)
-    const uint32_t s = (plans->R + 63) / 64;
-    if (s <= 2) CR_LPT(2);
-    else if (s <= 4) CR_LPT(4);
-    else if (s <= 8) CR_LPT(8);
-    else CR_LPT(16);
-#undef CR_LPT
+#define CR_LPT_BLOCK(NT)                                                                                          \
+    hipLaunchKernelGGL(k_lpt_block<NT>, dim3(plans->num_plans), dim3(NT), 0, st, plans->R, cmax, plans->specs,     \
+                       plans->order_count, plans->num_admitted, plans->cold, plans->num_windows, plans->member_off, \
+                       plans->members, plans->load)
+    if (plans->R <= 128) CR_LPT_BLOCK(128);
+    else if (plans->R <= 256) CR_LPT_BLOCK(256);
+    else if (plans->R <= 512) CR_LPT_BLOCK(512);
+    else CR_LPT_BLOCK(1024);
+#undef CR_LPT_BLOCK
+    hipLaunchKernelGGL(k_route_words, dim3((cmax + kWordThreads - 1) / kWordThreads, plans->num_plans),
+                       dim3(kWordThreads), 0, st, cmax, plans->num_windows, key_words(plans->num_keys), plans->specs,
+                       plans->order, plans->num_admitted, plans->member_off, plans->members, plans->key_index,
+                       plans->route);
     return hipGetLastError() == hipSuccess ? CR_OK : CR_EHIP;
 }
 

@@ -22,6 +22,8 @@ large stream can be generated without the others.
 """
 from __future__ import annotations
 
+import os
+from concurrent.futures import ThreadPoolExecutor
 from dataclasses import dataclass, field
 from typing import List, Optional, Sequence, Tuple
 
@@ -83,8 +85,8 @@ class Workload:
         return len(self.candidates)
 
 
-def _rng(seed: int, tag: int, stream: int, sub: int = 0) -> np.random.Generator:
-    return np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, tag, stream, sub])))
+def _rng(seed: int, tag: int, stream: int, sub: int = 0, *more: int) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, tag, stream, sub, *more])))
 
 
 def _tag(name: str) -> int:
@@ -330,22 +332,50 @@ def sweep_candidates() -> List[Candidate]:
     return [Candidate(W, 28 + 2 * m, 35) for W in SWEEP_W for m in range(8)]
 
 
+SWEEP_CHUNKS = 10          # 1e9 requests in ten 1e8-request chunks (= control intervals)
+SWEEP_SUBBLOCKS = 16       # each chunk is drawn as 16 independently seeded sub-blocks
+
+
+def _sweep_tables(seed: int, num_keys: int, _cache: dict = {}):
+    """The sweep's rank -> key permutation and Zipf(0.9) sampler (cached: 1e6 keys)."""
+    ck = (seed, num_keys)
+    if ck not in _cache:
+        perm = _rng(seed, _tag("sweep"), _S_PERM).permutation(num_keys).astype(np.uint32)
+        _cache.clear()
+        _cache[ck] = (perm, CategoricalSampler(zipf_probs(num_keys, 0.9)))
+    return _cache[ck]
+
+
 def sweep_chunk(chunk: int, seed: int = 2, chunk_n: int = 100_000_000, num_keys: int = 1_000_000,
                 R: int = 1024, candidates: Optional[List[Candidate]] = None,
-                _sampler_cache: dict = {}) -> Workload:
+                threads: Optional[int] = None) -> Workload:
     """One 1e8-request chunk (= one control interval) of the 1e9-request sweep:
-    1,000,000 keys, Zipf 0.9, 1,024 destinations, 64 candidate plans."""
+    1,000,000 keys, Zipf 0.9, 1,024 destinations, 64 candidate plans.
+
+    The chunk is cut into ``SWEEP_SUBBLOCKS`` equal sub-blocks, each with its own seed
+    (seed, tag, stream, chunk, sub-block), so the sub-blocks can be drawn by several
+    threads at once; the result does not depend on ``threads``."""
     name = "sweep"
     tag = _tag(name)
-    ck = (seed, num_keys)
-    if ck not in _sampler_cache:
-        perm = _rng(seed, tag, _S_PERM).permutation(num_keys)
-        _sampler_cache.clear()
-        _sampler_cache[ck] = (perm, CategoricalSampler(zipf_probs(num_keys, 0.9)))
-    perm, sampler = _sampler_cache[ck]
-    ranks = sampler.sample(_rng(seed, tag, _S_KEYS, chunk), chunk_n)
-    keys = perm[ranks].astype(np.uint32)
-    suffix = _suffixes(_rng(seed, tag, _S_SUFFIX, chunk), chunk_n)
+    perm, sampler = _sweep_tables(seed, num_keys)
+    keys = np.empty(chunk_n, dtype=np.uint32)
+    suffix = np.empty(chunk_n, dtype=np.uint16)
+    bounds = [b * chunk_n // SWEEP_SUBBLOCKS for b in range(SWEEP_SUBBLOCKS + 1)]
+
+    def fill(b: int) -> None:
+        s, e = bounds[b], bounds[b + 1]
+        ranks = sampler.sample(_rng(seed, tag, _S_KEYS, chunk, b), e - s)
+        keys[s:e] = perm[ranks]
+        suffix[s:e] = _rng(seed, tag, _S_SUFFIX, chunk, b).integers(SUFFIX_LO, SUFFIX_HI + 1, size=e - s,
+                                                                    dtype=np.uint16)
+
+    nt = threads if threads is not None else min(16, os.cpu_count() or 1)
+    if nt <= 1:
+        for b in range(SWEEP_SUBBLOCKS):
+            fill(b)
+    else:
+        with ThreadPoolExecutor(nt) as ex:
+            list(ex.map(fill, range(SWEEP_SUBBLOCKS)))
     plen = _prefix_lengths(seed, tag, num_keys, 2000.0, 0.5)
     return Workload(name=name, num_keys=num_keys, R=R,
                     candidates=candidates if candidates is not None else sweep_candidates(),
