@@ -102,7 +102,24 @@ typedef struct {
  *   key_index  u64 [NP][KW][2]          {admitted-key bits of keys 64w..64w+63,
  *                                        key rank of the first admitted key among them}
  *   route      u32 [NP][C_max]           by key rank: CR_ROUTE_SINGLE | dest (k = 1)
- *                                        or the admission index a (k > 1) */
+ *                                        or the admission index a (k > 1)
+ *
+ * Optional group dispatch tables (all three NULL = per-plan tables only). When every
+ * candidate of a group is built from the same counting window, a candidate admits a prefix
+ * of that window's order, so cr_route can serve all candidates of a request from one row:
+ * with these buffers present, cr_route first rebuilds them from the built plans and then
+ * reads, per request, one position, one row of CS destinations and one P2C bit word
+ * (CS = cands rounded up to a multiple of 8, PW = ceil(cands / 64)):
+ *   window_rank u32 [num_windows][num_keys]  position of each key in its window's order
+ *                                             (0xFFFFFFFF when absent)
+ *   group_dest  u16 [NG][C_max][CS]          by position a: the member of candidate c when it
+ *                                             admits the key with k = 1, CR_GROUP_MULTI when
+ *                                             k > 1, CR_GROUP_COLD when it does not admit it
+ *   group_p2c   u64 [NG][R][R][PW]           bit c of pair (d1, d2): L_c[d2] < L_c[d1]
+ * A group whose candidates name different windows sets CR_ERR_SPEC, and its destinations
+ * are then unspecified. group_dest must be 16-byte aligned. Sizes: cr_plan_sizes. */
+#define CR_GROUP_MULTI 0xFFFEu
+#define CR_GROUP_COLD 0xFFFFu
 typedef struct {
     uint32_t num_plans;   /* NP = NG * cands                                       */
     uint32_t cands;       /* candidates per group, 1..CR_MAX_CANDS                 */
@@ -122,6 +139,9 @@ typedef struct {
     double* load;
     uint64_t* key_index;
     uint32_t* route;
+    uint32_t* window_rank;  /* optional group dispatch tables (see above), or NULL      */
+    uint16_t* group_dest;
+    uint64_t* group_p2c;
 } cr_plan_set;
 
 /* Rates per key per control interval (Algorithm 1 input "rates"; Appendix A.2: the

@@ -45,7 +45,8 @@ class CrPlanSet(ctypes.Structure):
     _fields_ = [("num_plans", _u32), ("cands", _u32), ("R", _u32), ("max_W", _u32), ("num_keys", _u32),
                 ("num_windows", _u32), ("specs", _P), ("order", _P), ("order_count", _P), ("n_order", _P),
                 ("num_admitted", _P), ("cold", _P), ("clamped", _P), ("member_off", _P), ("members", _P),
-                ("load", _P), ("key_index", _P), ("route", _P)]
+                ("load", _P), ("key_index", _P), ("route", _P), ("window_rank", _P), ("group_dest", _P),
+                ("group_p2c", _P)]
 
 
 class CrError(RuntimeError):
@@ -225,9 +226,13 @@ def cr_replay_lru(prefix_len, num_keys: int, n: int, J: int, P: int, R: int, W: 
 
 
 class PlanSet:
-    """Device buffers of a cr_plan_set (NP = NG * cands plans over num_windows rows)."""
+    """Device buffers of a cr_plan_set (NP = NG * cands plans over num_windows rows).
+    ``group_tables`` also allocates the optional group dispatch tables that let cr_route
+    serve every candidate of a request from one row (candidates of a group must share
+    their counting window)."""
 
-    def __init__(self, specs, cands: int, R: int, max_W: int, num_keys: int, num_windows: int, device):
+    def __init__(self, specs, cands: int, R: int, max_W: int, num_keys: int, num_windows: int, device,
+                 group_tables: bool = False):
         self.num_plans = len(specs)
         self.cands, self.R, self.max_W, self.num_keys, self.num_windows = cands, R, max_W, num_keys, num_windows
         cmax = R * max_W
@@ -248,7 +253,25 @@ class PlanSet:
         self.load = torch.empty((NP, R), dtype=torch.float64, device=device)
         self.key_index = torch.empty((NP, (num_keys + 63) // 64, 2), dtype=torch.int64, device=device)
         self.route = torch.empty((NP, cmax), **i32)
+        self.window_rank = self.group_dest = self.group_p2c = None
+        if group_tables:
+            NG = NP // cands
+            self.window_rank = torch.empty((NW, num_keys), **i32)
+            self.group_dest = torch.empty((NG, cmax, group_row(cands)), dtype=torch.int16, device=device)
+            self.group_p2c = torch.empty((NG, R, R, (cands + 63) // 64), dtype=torch.int64, device=device)
         self.c = CrPlanSet(NP, cands, R, max_W, num_keys, NW, _ptr(self.specs), _ptr(self.order),
                            _ptr(self.order_count), _ptr(self.n_order),
                            _ptr(self.num_admitted), _ptr(self.cold), _ptr(self.clamped), _ptr(self.member_off),
-                           _ptr(self.members), _ptr(self.load), _ptr(self.key_index), _ptr(self.route))
+                           _ptr(self.members), _ptr(self.load), _ptr(self.key_index), _ptr(self.route),
+                           _ptr(self.window_rank), _ptr(self.group_dest), _ptr(self.group_p2c))
+
+
+def group_row(cands: int) -> int:
+    """Entries per group_dest row: cands rounded up to a multiple of 8."""
+    return (cands + 7) // 8 * 8
+
+
+def group_table_bytes(NG: int, cands: int, R: int, max_W: int, num_keys: int, num_windows: int) -> int:
+    """Bytes of the three group dispatch tables."""
+    return (num_windows * num_keys * 4 + NG * R * max_W * group_row(cands) * 2
+            + NG * R * R * ((cands + 63) // 64) * 8)

@@ -147,6 +147,224 @@ __global__ __launch_bounds__(kRouteThreads) void k_route(
     if (bad) atomicOr(err, CR_ERR_KEY_RANGE);
 }
 
+// ---------------------------------------------------------------------------------------
+// Group dispatch tables. Candidates of one group built from the same window admit prefixes
+// of that window's order, so one row per order position holds every candidate's dispatch of
+// a key, and one bit word per destination pair holds every candidate's power-of-two-choices
+// outcome. A request then reads its key's position, one row of CS u16 entries and one P2C
+// word instead of a handful of gathers per candidate into per-plan tables.
+// ---------------------------------------------------------------------------------------
+constexpr uint32_t kGrpRows = 64;      // order positions per k_group_dest block
+constexpr uint32_t kGrpThreads = 256;
+
+__global__ void k_fill_u32(uint32_t* __restrict__ p, uint64_t n, uint32_t v)
+{
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = v;
+}
+
+// window_rank[w][order[w][a]] = a for a < n_order[w]
+__global__ __launch_bounds__(256) void k_win_rank_set(const uint32_t* __restrict__ order,
+                                                      const uint32_t* __restrict__ n_order, uint32_t cmax, uint32_t K,
+                                                      uint32_t* __restrict__ wr)
+{
+    const uint32_t w = blockIdx.y, a = blockIdx.x * 256u + threadIdx.x;
+    const uint32_t no = n_order[w] < cmax ? n_order[w] : cmax;
+    if (a >= no) return;
+    const uint32_t b = order[(uint64_t)w * cmax + a];
+    if (b < K) wr[(uint64_t)w * K + b] = a;
+}
+
+// Rows a0 .. a0+63 of group g: entry c = candidate c's dispatch of the key at order position a.
+__global__ __launch_bounds__(kGrpThreads) void k_group_dest(uint32_t cands, uint32_t CS, uint32_t cmax,
+                                                            const cr_plan_spec* __restrict__ specs,
+                                                            const uint32_t* __restrict__ num_admitted,
+                                                            const uint32_t* __restrict__ member_off,
+                                                            const uint16_t* __restrict__ members,
+                                                            uint16_t* __restrict__ gdest, uint32_t* __restrict__ err)
+{
+    __shared__ uint16_t tile[kGrpRows * (CR_MAX_CANDS + 8)];
+    const uint32_t g = blockIdx.y, a0 = blockIdx.x * kGrpRows;
+    const uint32_t row = threadIdx.x % kGrpRows, a = a0 + row;
+    const uint32_t w0 = specs[(uint64_t)g * cands].window;
+    bool mismatch = false;
+    for (uint32_t c = threadIdx.x / kGrpRows; c < CS; c += kGrpThreads / kGrpRows) {
+        uint16_t e = (uint16_t)CR_GROUP_COLD;
+        if (c < cands) {
+            const uint64_t p = (uint64_t)g * cands + c;
+            mismatch |= specs[p].window != w0;
+            if (a < num_admitted[p] && a < cmax) {
+                const uint32_t* __restrict__ mo = member_off + p * (cmax + 1u);
+                const uint32_t o = mo[a], k = mo[a + 1] - o;
+                e = k == 1 ? members[p * cmax + o] : (uint16_t)CR_GROUP_MULTI;
+            }
+        }
+        tile[row * CS + c] = e;
+    }
+    if (mismatch && row == 0) atomicOr(err, CR_ERR_SPEC);
+    __syncthreads();
+    const uint32_t per = CS / 8u;  // 16-byte pieces per row
+    for (uint32_t q = threadIdx.x; q < kGrpRows * per; q += kGrpThreads) {
+        const uint32_t r = q / per, part = q % per;
+        if (a0 + r >= cmax) continue;
+        const uint16_t* src = tile + r * CS + part * 8u;
+        uint4 v;
+        v.x = (uint32_t)src[0] | ((uint32_t)src[1] << 16);
+        v.y = (uint32_t)src[2] | ((uint32_t)src[3] << 16);
+        v.z = (uint32_t)src[4] | ((uint32_t)src[5] << 16);
+        v.w = (uint32_t)src[6] | ((uint32_t)src[7] << 16);
+        *reinterpret_cast<uint4*>(gdest + ((uint64_t)g * cmax + a0 + r) * CS + part * 8u) = v;
+    }
+}
+
+// Pair words of group g, first draw d1: bit c of word (d1, d2) = L_c[d2] < L_c[d1].
+__global__ __launch_bounds__(256) void k_group_p2c(uint32_t R, uint32_t cands, uint32_t PW,
+                                                   const double* __restrict__ load, uint64_t* __restrict__ gp2c)
+{
+    __shared__ double s_l1[CR_MAX_CANDS];
+    const uint32_t d1 = blockIdx.x, g = blockIdx.y;
+    for (uint32_t c = threadIdx.x; c < cands; c += blockDim.x) s_l1[c] = load[((uint64_t)g * cands + c) * R + d1];
+    __syncthreads();
+    for (uint32_t d2 = threadIdx.x; d2 < R; d2 += blockDim.x) {
+        for (uint32_t wd = 0; wd < PW; ++wd) {
+            uint64_t word = 0;
+            const uint32_t ce = cands - wd * 64u < 64u ? cands - wd * 64u : 64u;
+            for (uint32_t u = 0; u < ce; ++u) {
+                const uint32_t c = wd * 64u + u;
+                word |= (uint64_t)(load[((uint64_t)g * cands + c) * R + d2] < s_l1[c]) << u;
+            }
+            gp2c[(((uint64_t)g * R + d1) * R + d2) * PW + wd] = word;
+        }
+    }
+}
+
+// Dispatch of every candidate of the request's plan group from the group tables; results
+// equal k_route's. Each thread owns 4 consecutive requests; per 8 candidates it reads one
+// 16-byte piece of each request's row and writes one 8-byte store per candidate.
+template <bool kVec, int kPW>
+__global__ __launch_bounds__(kRouteThreads) void k_route_group(
+    const uint32_t* __restrict__ keys, uint64_t n, uint64_t first_index, uint32_t smix,
+    const uint64_t* __restrict__ off, const uint32_t* __restrict__ gmap, uint32_t J, uint32_t K, uint32_t R,
+    uint32_t cands, uint32_t CS, uint32_t PW, uint32_t NG, uint32_t NW, uint32_t cmax,
+    const cr_plan_spec* __restrict__ specs, const uint32_t* __restrict__ wrank, const uint16_t* __restrict__ gdest,
+    const uint64_t* __restrict__ gp2c, const uint32_t* __restrict__ member_off, const uint16_t* __restrict__ members,
+    uint16_t* __restrict__ dest, uint32_t* __restrict__ err)
+{
+    __shared__ uint32_t s_j0;
+    __shared__ uint32_t s_rel[kBnd];
+    __shared__ uint32_t s_g[kBnd + 1];
+    __shared__ uint32_t s_w[kBnd + 1];
+    const uint64_t bstart = (uint64_t)xcd_tile(blockIdx.x, gridDim.x) * kBlockReq;
+    if (bstart >= n) return;
+    if (threadIdx.x < 64) {
+        const uint32_t j0 = find_interval(off, J, bstart);
+        if (threadIdx.x == 0) s_j0 = j0;
+        if (threadIdx.x < kBnd) {
+            const uint32_t jb = j0 + 1 + threadIdx.x;
+            const uint64_t e = jb < J ? off[jb] : ~0ull;
+            s_rel[threadIdx.x] = e - bstart < kBlockReq ? (uint32_t)(e - bstart) : kBlockReq;
+        }
+        if (threadIdx.x <= kBnd) {
+            const uint32_t jj = j0 + threadIdx.x < J ? j0 + threadIdx.x : J - 1;
+            const uint32_t gg = gmap[jj] < NG ? gmap[jj] : NG - 1;
+            const uint32_t ww = specs[(uint64_t)gg * cands].window;
+            s_g[threadIdx.x] = gg;
+            s_w[threadIdx.x] = ww < NW ? ww : 0u;
+        }
+    }
+    __syncthreads();
+    const uint32_t rel0 = threadIdx.x * kPer;
+    const uint64_t base = bstart + rel0;
+    if (base >= n) return;
+    const bool full = kVec && base + kPer <= n;
+    uint32_t b[kPer];
+    if (full) {
+        const uint4 q = *reinterpret_cast<const uint4*>(keys + base);
+        b[0] = q.x, b[1] = q.y, b[2] = q.z, b[3] = q.w;
+    } else {
+#pragma unroll
+        for (int t = 0; t < kPer; ++t) b[t] = base + t < n ? keys[base + t] : 0u;
+    }
+    const uint32_t j0 = s_j0;
+    const uint32_t r0 = s_rel[0], r1 = s_rel[1], r2 = s_rel[2], r3 = s_rel[3];
+    const uint64_t gi0 = first_index + base;
+    const uint32_t inner0 = fmix32((uint32_t)(gi0 >> 32) ^ smix);
+    uint32_t g[kPer], h[kPer], d1[kPer], d2[kPer], a[kPer];
+    uint64_t pw[kPer][kPW];
+    bool bad = false;
+#pragma unroll
+    for (int t = 0; t < kPer; ++t) {
+        const uint32_t rel = rel0 + t;
+        const uint32_t q = (rel >= r0) + (rel >= r1) + (rel >= r2) + (rel >= r3);
+        uint32_t w;
+        if (rel >= r3 && r3 < kBlockReq) {  // more than kBnd boundaries in this block
+            uint32_t j = j0 + kBnd;
+            while (j + 1 < J && off[j + 1] <= base + t) ++j;
+            g[t] = gmap[j] < NG ? gmap[j] : NG - 1;
+            w = specs[(uint64_t)g[t] * cands].window;
+            w = w < NW ? w : 0u;
+        } else {
+            g[t] = s_g[q];
+            w = s_w[q];
+        }
+        const uint64_t gi = gi0 + t;
+        const uint32_t inner = (uint32_t)(gi >> 32) == (uint32_t)(gi0 >> 32) ? inner0 : fmix32((uint32_t)(gi >> 32) ^ smix);
+        h[t] = fmix32((uint32_t)gi ^ inner);
+        d1[t] = ((h[t] & 0xFFFFu) * R) >> 16;
+        d2[t] = ((h[t] >> 16) * R) >> 16;
+        const bool in = base + t < n;
+        bad |= in && b[t] >= K;
+        const uint32_t ar = b[t] < K ? wrank[(uint64_t)w * K + b[t]] : 0xFFFFFFFFu;
+        a[t] = ar < cmax ? ar : 0xFFFFFFFFu;
+        const uint64_t* __restrict__ pp = gp2c + (((uint64_t)g[t] * R + d1[t]) * R + d2[t]) * PW;
+#pragma unroll
+        for (uint32_t wd = 0; wd < (uint32_t)kPW; ++wd) pw[t][wd] = wd < PW ? pp[wd] : 0ull;
+    }
+    for (uint32_t cg = 0; cg < CS; cg += 8) {
+        uint4 row[kPer];
+#pragma unroll
+        for (int t = 0; t < kPer; ++t) {
+            row[t] = a[t] != 0xFFFFFFFFu
+                         ? *reinterpret_cast<const uint4*>(gdest + ((uint64_t)g[t] * cmax + a[t]) * CS + cg)
+                         : make_uint4(0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu);
+        }
+        const uint32_t nc = cands - cg < 8u ? cands - cg : 8u;
+        for (uint32_t u = 0; u < nc; ++u) {
+            const uint32_t c = cg + u;
+            uint32_t d[kPer];
+            bool multi = false;
+#pragma unroll
+            for (int t = 0; t < kPer; ++t) {
+                const uint32_t wv = u < 2 ? row[t].x : (u < 4 ? row[t].y : (u < 6 ? row[t].z : row[t].w));
+                const uint32_t e = (u & 1u) ? (wv >> 16) : (wv & 0xFFFFu);
+                const uint32_t bit = (uint32_t)(pw[t][kPW == 1 ? 0u : (c >> 6)] >> (c & 63u)) & 1u;
+                const uint32_t cold = bit ? d2[t] : d1[t];
+                d[t] = e == CR_GROUP_COLD ? cold : e;
+                multi |= e == CR_GROUP_MULTI;
+            }
+            if (ballot(multi)) {  // k > 1 for some request of this wave: pick by the hash
+#pragma unroll
+                for (int t = 0; t < kPer; ++t) {
+                    if (d[t] != CR_GROUP_MULTI) continue;
+                    const uint64_t p = (uint64_t)g[t] * cands + c;
+                    const uint32_t* __restrict__ mo = member_off + p * (cmax + 1u);
+                    const uint32_t o = mo[a[t]], k = mo[a[t] + 1] - o;
+                    d[t] = members[p * cmax + o + (((h[t] >> 16) * k) >> 16)];
+                }
+            }
+            uint16_t* __restrict__ dc = dest + (uint64_t)c * n + base;
+            if (full) {
+                *reinterpret_cast<uint2*>(dc) = make_uint2(d[0] | (d[1] << 16), d[2] | (d[3] << 16));
+            } else {
+#pragma unroll
+                for (int t = 0; t < kPer; ++t)
+                    if (base + t < n) dc[t] = (uint16_t)d[t];
+            }
+        }
+    }
+    if (bad) atomicOr(err, CR_ERR_KEY_RANGE);
+}
+
 // Live-load dispatch (Section 3.1 "Placement and dispatch"; Fig. 1): during an interval,
 // admitted keys take the least-loaded member of T(b) and the rest power of two choices,
 // on the running count of requests each destination has received in the interval. Every
@@ -310,7 +528,40 @@ extern "C" cr_status cr_route(const uint32_t* keys, uint64_t n, uint64_t first_i
     if (blocks > 0x7FFFFFF0ull) return CR_EINVAL;
     // 16-byte key loads and 8-byte destination stores need aligned rows.
     const bool vec = ((uintptr_t)keys & 15u) == 0 && ((uintptr_t)dest & 7u) == 0 && (n & 3u) == 0;
+    const bool grouped = plans->window_rank || plans->group_dest || plans->group_p2c;
+    if (grouped) {
+        if (!plans->window_rank || !plans->group_dest || !plans->group_p2c || ((uintptr_t)plans->group_dest & 15u) ||
+            ((uintptr_t)plans->group_p2c & 7u) || ((uintptr_t)plans->window_rank & 3u) || !plans->specs ||
+            !plans->order || !plans->n_order || !plans->num_admitted)
+            return CR_EINVAL;
+        if (plans->num_windows > 65535u || plans->num_plans / plans->cands > 65535u) return CR_EINVAL;  // grid y
+    }
     (void)hipGetLastError();
+    if (grouped) {
+        const hipStream_t st = as_stream(stream);
+        const uint32_t NG = plans->num_plans / plans->cands, cands = plans->cands;
+        const uint32_t CS = (cands + 7u) & ~7u, PW = (cands + 63u) / 64u;
+        const uint64_t wr_n = (uint64_t)plans->num_windows * plans->num_keys;
+        hipLaunchKernelGGL(k_fill_u32, dim3(2048), dim3(256), 0, st, plans->window_rank, wr_n, 0xFFFFFFFFu);
+        hipLaunchKernelGGL(k_win_rank_set, dim3((cmax + 255u) / 256u, plans->num_windows), dim3(256), 0, st,
+                           plans->order, plans->n_order, cmax, plans->num_keys, plans->window_rank);
+        hipLaunchKernelGGL(k_group_dest, dim3((cmax + kGrpRows - 1u) / kGrpRows, NG), dim3(kGrpThreads), 0, st, cands,
+                           CS, cmax, plans->specs, plans->num_admitted, plans->member_off, plans->members,
+                           plans->group_dest, err);
+        hipLaunchKernelGGL(k_group_p2c, dim3(plans->R, NG), dim3(256), 0, st, plans->R, cands, PW, plans->load,
+                           plans->group_p2c);
+#define CR_ROUTE_GROUP(V, W)                                                                                       \
+    hipLaunchKernelGGL((k_route_group<V, W>), dim3(xcd_grid((uint32_t)blocks)), dim3(kRouteThreads), 0, st, keys, n,      \
+                       first_index, seed_mix(seed), off, gmap, J, plans->num_keys, plans->R, cands, CS, PW, NG,       \
+                       plans->num_windows, cmax, plans->specs, plans->window_rank, plans->group_dest,                \
+                       plans->group_p2c, plans->member_off, plans->members, dest, err)
+        if (vec && PW == 1) CR_ROUTE_GROUP(true, 1);
+        else if (vec) CR_ROUTE_GROUP(true, 4);
+        else if (PW == 1) CR_ROUTE_GROUP(false, 1);
+        else CR_ROUTE_GROUP(false, 4);
+#undef CR_ROUTE_GROUP
+        return hipGetLastError() == hipSuccess ? CR_OK : CR_EHIP;
+    }
 #define CR_ROUTE_LAUNCH(V)                                                                                         \
     hipLaunchKernelGGL(k_route<V>, dim3(xcd_grid((uint32_t)blocks)), dim3(kRouteThreads), 0, as_stream(stream), keys, n, \
                        first_index, seed_mix(seed), off, gmap, J, plans->num_keys, plans->R, plans->cands,        \

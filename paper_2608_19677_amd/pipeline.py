@@ -49,9 +49,12 @@ def upload(wl, device="cuda") -> DeviceInputs:
 class Pipeline:
     """All device buffers for one workload (or one chunk of a chunked stream)."""
 
+    GROUP_TABLE_BUDGET = 4 << 30  # bytes the optional group dispatch tables may take
+
     def __init__(self, wl, device="cuda", dev_in: Optional[DeviceInputs] = None,
                  prev_counts: Optional[torch.Tensor] = None, prev_n: int = 0,
-                 lru_in: Optional[torch.Tensor] = None, dispatch: str = "static"):
+                 lru_in: Optional[torch.Tensor] = None, dispatch: str = "static",
+                 group_tables: Optional[bool] = None):
         if dispatch not in ("static", "live"):
             raise ValueError(f"unknown dispatch {dispatch!r}")
         self.dispatch = dispatch
@@ -114,7 +117,17 @@ class Pipeline:
         # hash-placed ablation stages need cr_place_hash after cr_place_lpt
         self.hash_placed = any(getattr(c, "variant", "full") in ("affinity", "replicated") for c in wl.candidates)
         self.NW = self.win_src.shape[0]  # counts rows the plans are built from
-        self.plans = B.PlanSet(specs, P, R, self.max_W, K, self.NW, device)
+        # Group dispatch tables (one row per request for all candidates) need every
+        # candidate of a group to plan from the same window; by default they are used for
+        # several candidates when they fit the budget.
+        shared = all(len(set(window[g])) == 1 for g in range(NG))
+        if group_tables is None:
+            group_tables = (P > 1 and shared and dispatch == "static" and
+                            B.group_table_bytes(NG, P, R, self.max_W, K, self.NW) <= self.GROUP_TABLE_BUDGET)
+        elif group_tables and not shared:
+            raise ValueError("group dispatch tables need every candidate of a group to share its window")
+        self.group_tables = bool(group_tables)
+        self.plans = B.PlanSet(specs, P, R, self.max_W, K, self.NW, device, group_tables=self.group_tables)
         self.ws_admit = torch.empty(B.cr_admit_workspace_bytes(self.NW, R, self.max_W), dtype=torch.uint8,
                                     device=device)
         self.ws_replay = torch.empty(B.cr_replay_workspace_bytes(wl.n, P, R), dtype=torch.uint8, device=device)

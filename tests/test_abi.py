@@ -56,4 +56,4 @@ def test_host_only_queries(lib_path):
 def test_struct_layouts_match_header(lib_path):
     from paper_2608_19677_amd import binding
     assert ctypes.sizeof(binding.CrPlanSpec) == 40
-    assert ctypes.sizeof(binding.CrPlanSet) == 6 * 4 + 12 * 8
+    assert ctypes.sizeof(binding.CrPlanSet) == 6 * 4 + 15 * 8

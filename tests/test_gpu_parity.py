@@ -18,10 +18,12 @@ from cr_check import compare_all, compare_plan, say
 pytestmark = pytest.mark.gpu
 
 
-def _run(wl):
+def _run(wl, group_tables=None):
     say(f"[case] {wl.name} n={wl.n} J={wl.J} K={wl.num_keys} R={wl.R} P={wl.P} "
-        f"W={[c.W for c in wl.candidates]}")
-    gp = Pipeline(wl)
+        f"W={[c.W for c in wl.candidates]} group_tables={group_tables}")
+    gp = Pipeline(wl, group_tables=group_tables)
+    if group_tables is not None:
+        assert gp.group_tables == group_tables
     gp.step()
     h = gp.host()
     orc = opipe.run(wl)
@@ -55,6 +57,27 @@ def test_small_random_parity(case):
     seed, K, n, R, Ws, J, hot, share, qs = case
     wl = wl_mod.small_random(seed, num_keys=K, n=n, R=R, Ws=Ws, J=J, hot=hot, hot_share=share, qs=qs)
     _run(wl)
+
+
+MULTI = [c for c in SMALL if len(c[4]) * len(c[8]) > 1]
+
+
+@pytest.mark.parametrize("case", MULTI, ids=[f"s{c[0]}" for c in MULTI])
+@pytest.mark.parametrize("group_tables", [False, True])
+def test_multi_candidate_route_paths(case, group_tables):
+    # several candidates per plan group: cr_route with the group dispatch tables (one row
+    # per request for all candidates) and with the per-plan tables only
+    seed, K, n, R, Ws, J, hot, share, qs = case
+    wl = wl_mod.small_random(seed, num_keys=K, n=n, R=R, Ws=Ws, J=J, hot=hot, hot_share=share, qs=qs)
+    _run(wl, group_tables=group_tables)
+
+
+def test_group_tables_many_candidates():
+    # 100 candidates: two P2C words per destination pair and a padded row (CS = 104)
+    Ws = [3, 9, 17, 33, 60]
+    qs = [(a, 10) for a in range(5, 25)]
+    wl = wl_mod.small_random(15, num_keys=2000, n=30_000, R=70, Ws=Ws, J=3, qs=qs, hot=3, hot_share=0.4)
+    _run(wl, group_tables=True)
 
 
 def test_tiny_intervals_parity():
