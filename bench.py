@@ -1,29 +1,28 @@
 """Benchmark: count -> plan -> route -> LRU replay on one MI355X, plus the CPU oracle baseline.
 
-A step is one pass of the whole path over one batch of the 70B-like workload (20,000 keys,
-Zipf 1.0 capped at a 0.3 % share, 1e7 requests at 176 QPS in 60-s control intervals = 948
-intervals, 30 destinations x 64 LRU slots). By default (--schedule overlap) consecutive
-batches run as chunks of one stream, three HIP streams deep: step s counts and admits chunk
-s, places, routes and partitions chunk s-1 and replays chunk s-2 (cache state and last
-window carried, three buffer sets), and the timed steps replay that steady state captured
-as three HIP graphs, one chunk per step. --schedule overlap2 is the two-stream form (chunk k
-placed, routed and partitioned while chunk k-1 replays; two graphs); --schedule serial runs
-every step from scratch on one stream (one HIP graph). --eager times plain launches. The
-per-stage times and the roofline come from an eager pass of the same schedule with HIP
-events around each library call.
-Inputs are resident in HBM before timing starts. Prints ONE JSON line.
+Default (--workload sweep): the large sweep, 1e9 requests streamed as ten 1e8-request
+chunks (one control interval each) over 1,000,000 keys with Zipf(0.9) popularity and 1,024
+destinations, with 64 candidate plans (8 warm-slot budgets x 8 load targets) replayed in
+parallel. A step is one chunk: counting, one window sort shared by the 64 admissions, LPT
+for all 64 plans, routing of every request under every plan, the partition and the replay,
+with the plan taken from the previous chunk's window and every cache state carried. The
+default 10 timed steps are one pass over the 1e9-request stream. The chunks are generated
+and uploaded before timing; per-stage times are HIP events on the stream the library uses.
 
-  python bench.py [--gpus 1] [--steps K] [--warmup W] [--eager] [--schedule serial|overlap]
-                  [--workload llama70b|tiny|replication|burst|drift|ablation|llama70b_gamma]
-                  [--dispatch static|live] [--opaque]
+Other workloads (--workload llama70b|tiny|replication|burst|drift|ablation|llama70b_gamma)
+keep their schedules: by default (--schedule overlap) consecutive batches run as chunks of
+one stream, three HIP streams deep (step s counts and admits chunk s, places, routes and
+partitions chunk s-1 and replays chunk s-2), timed as replays of that steady state captured
+as HIP graphs; --schedule overlap2 is two streams deep; --schedule serial runs every step
+from scratch on one stream; --eager times plain launches. --workload drift times the
+replanning study, --workload ablation the component ablation; --dispatch live routes by
+running loads within each interval; --opaque remaps salted 32-bit ids on the device.
 
---workload drift times the replanning study instead (six drift intervals of 1e6 requests,
-fresh and held plans as six candidates, 600 statistics bins, churn between consecutive
-fresh plans) and adds its per-transition report under "study". --workload ablation times
-the component ablation (the injected-whale stream under the flat, affinity, replicated
-and full plans as four candidates) and adds the hit and imbalance of each under "study".
---dispatch live routes by running loads within each interval; --opaque remaps salted
-32-bit ids to dense keys on the device inside every step.
+The oracle baseline runs the C oracle with its units fanned out over every host thread
+this process may use, on a bounded sample (stated in the line). Prints ONE JSON line.
+
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--schedule ...]
+                  [--dispatch static|live] [--opaque] [--no-cpu-baseline] [--cpu-threads N]
 """
 from __future__ import annotations
 
@@ -49,9 +48,12 @@ ALU_PEAK_GOPS = 256 * 4 * 16 * 2.4
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="llama70b")
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed steps (default: 10 for the sweep, one pass over its 1e9 requests; 20 otherwise)")
+    ap.add_argument("--warmup", type=int, default=None, help="untimed steps first (default: 2 sweep, 3 otherwise)")
+    ap.add_argument("--workload", default="sweep")
+    ap.add_argument("--cpu-threads", type=int, default=0,
+                    help="host threads for the oracle baseline (default: every core this process may use)")
     ap.add_argument("--schedule", default="overlap", choices=("overlap", "overlap2", "serial"),
                     help="overlap: consecutive chunks of one stream three HIP streams deep, step s counting and "
                          "admitting chunk s, placing, routing and partitioning chunk s-1 and replaying chunk s-2 "
@@ -150,12 +152,151 @@ def describe(name, wl):
     }
 
 
+def run_sweep(args):
+    """The large sweep: ten 1e8-request chunks (1,000,000 keys, Zipf 0.9, R = 1,024, 64
+    candidate plans), one chunk per step through ChunkChain: count, admission for all 64
+    candidates from one window sort, LPT, routing of every candidate through the group
+    tables, partition and replay, with the plan taken from the previous chunk's window and
+    the cache state carried. Step s runs the inputs of chunk s mod 10 at global indices
+    s * 1e8 onwards. The chunks are generated and uploaded before timing."""
+    import numpy as np
+    import torch
+
+    from paper_2608_19677_amd import workload
+    from paper_2608_19677_amd.pipeline import ChunkChain, Pipeline
+
+    steps = 10 if args.steps is None else args.steps
+    warmup = 2 if args.warmup is None else args.warmup
+    chunks = [workload.sweep_chunk(k) for k in range(workload.SWEEP_CHUNKS)]
+    w0 = chunks[0]
+    torch.cuda.set_device(0)
+    chain = ChunkChain(chunks, device="cuda:0")
+    for _ in range(warmup):
+        chain.step()
+    torch.cuda.synchronize()
+    ev = {}
+    t0 = time.perf_counter()
+    last = None
+    for _ in range(steps):
+        last = chain.step(timers=ev)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_step = (t1 - t0) * 1e3 / steps
+    stage_ms = {s: float(np.mean([a.elapsed_time(b) for a, b in ev[s]])) for s in Pipeline.STAGES}
+    err = int(last.err.cpu().numpy().view(np.uint32)[0])
+    assert err == 0, f"device error word {err:#x}"
+    n, P, R = w0.n, w0.P, w0.R
+    st = last.stats.cpu().numpy().view(np.uint64).sum(axis=(0, 2)).astype(np.float64)  # [P][4]
+    hit = st[:, 1] / st[:, 0]
+    Ws = np.array([c.W for c in w0.candidates], dtype=np.float64)
+    # replay: per record a W-slot compare, and on a miss a W-wide reduction for the victim
+    lru_work = float(np.sum(n * Ws * (2.0 - hit)))
+    kern = {
+        "count": dict(kernel="k_count_*", bound="hbm", unit="GB/s", work=4.0 * n, peak=HBM_PEAK_GBS),
+        "route": dict(kernel="k_route_group<true,1> + group tables", bound="hbm", unit="GB/s",
+                      work=(4.0 + 2.0 * P) * n, peak=HBM_PEAK_GBS),
+        "lru": dict(kernel="k_replay<1,2,4,8> (one cr_replay_lru call)", bound="alu", unit="Glane-op/s",
+                    work=lru_work, peak=ALU_PEAK_GOPS),
+    }
+    for k, v in kern.items():
+        v["ms"] = stage_ms[k]
+        v["achieved"] = v["work"] / (stage_ms[k] * 1e-3) / 1e9
+        v["frac"] = v["achieved"] / v["peak"]
+    d = kern["lru"]
+    out = {
+        "metric": "requests/sec through count+route+LRU replay",
+        "value": n / (ms_step * 1e-3),
+        "unit": "requests/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u32",
+        "data": "synthetic",
+        "config": {
+            "workload": "Large sweep: 1,000,000 keys Zipf(0.9); 1e9 requests streamed in ten 1e8-request chunks "
+                        "(one control interval each); 1,024 destinations; 64 candidate plans = 8 warm-slot budgets "
+                        "(8..512 per destination) x 8 load targets (0.8..1.2 x mean), replayed in parallel",
+            "requests_per_step": n, "chunks": workload.SWEEP_CHUNKS, "keys": w0.num_keys, "destinations": R,
+            "slots": sorted({c.W for c in w0.candidates}), "candidates": P, "plan_builds_per_step": P,
+            "schedule": "chunk chain, one stream", "dispatch": "static", "launch": "eager",
+        },
+        "roofline": {"bound": d["bound"], "achieved": d["achieved"], "peak": d["peak"], "unit": d["unit"],
+                     "frac": d["frac"], "traffic": sweep_traffic(), "kernel": d["kernel"]},
+        "request_plans_per_s": n * P / (ms_step * 1e-3),
+        "us_per_plan_build": (stage_ms["admit"] + stage_ms["place"]) * 1e3 / P,
+        "stage_ms": stage_ms,
+        "kernels": {k: {kk: vv for kk, vv in v.items() if kk != "work"} for k, v in kern.items()},
+        "hbm_frac": {"count": kern["count"]["frac"], "route": kern["route"]["frac"]},
+        "hit_rate": {"min": float(hit.min()), "max": float(hit.max())},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = sweep_cpu_baseline(args, chunks[0])
+    return out
+
+
+def sweep_traffic():
+    """HBM bytes per replay stage from the committed counter summary of the sweep, or None
+    when the replay's sources changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "sweep_hbm_traffic.md")
+    if not os.path.exists(path):
+        return None
+    rec = None
+    with open(path) as f:
+        for line in f:
+            if line.startswith("traffic-json: "):
+                rec = json.loads(line[len("traffic-json: "):])
+    if rec is None or "lru" not in rec.get("bytes_per_step", {}):
+        return None
+    for rel, sha in rec["sources_sha256"].items():
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            if hashlib.sha256(f.read()).hexdigest() != sha:
+                return None
+    return rec["bytes_per_step"]["lru"]
+
+
+def sweep_cpu_baseline(args, w0):
+    """The oracle, fanned out over this host's threads, on a bounded sample of the sweep:
+    the first 4e6 requests of chunk 0 as one window (count, 64 plans, routing and replay of
+    every candidate), timed end to end."""
+    import dataclasses
+
+    import numpy as np
+
+    from oracle import pipeline as opipe
+    S = 4_000_000
+    ws = dataclasses.replace(w0, keys=w0.keys[:S], suffix=w0.suffix[:S], offsets=np.array([0, S], dtype=np.uint64))
+    threads = args.cpu_threads or opipe.host_threads()
+    tm = {}
+    t = time.perf_counter()
+    opipe.run(ws, threads=threads, timings=tm)
+    sec = time.perf_counter() - t
+    return {"value": S / sec, "unit": "requests/s", "cores": threads, "kind": "oracle",
+            "sample": f"the first {S:.0e} requests of sweep chunk 0 as one window, all 64 candidates "
+                      f"(count, plans, route, replay), {sec:.1f} s on {threads} host threads; stages (s) "
+                      + ", ".join(f"{k} {v:.2f}" for k, v in tm.items() if k in ("count", "plan", "route", "replay"))}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
         print(json.dumps({"error": "one GPU only: the path runs on a single MI355X and has no multi-GPU "
                                    "sharding", "n_gpus": args.gpus}), flush=True)
         sys.exit(2)
+    if args.workload == "sweep":
+        from paper_2608_19677_amd import build as hip_build
+        if not os.path.exists(hip_build.LIB):
+            hip_build.build()
+        print(json.dumps(run_sweep(args)), flush=True)
+        return
+    if args.steps is None:
+        args.steps = 20
+    if args.warmup is None:
+        args.warmup = 3
     import numpy as np
     import torch
 
@@ -302,9 +443,8 @@ def main():
     # Algorithmic work per launch of the single-kernel calls (the statistics are cleared in
     # the partition stage; count, place, route and lru each launch exactly one kernel here).
     kern = {
-        # counting reads every key and writes the dense [J][K] counts matrix it defines
-        "count": dict(kernel="k_count_*", bound="hbm", unit="GB/s", work=4.0 * n + 4.0 * wl.J * wl.num_keys,
-                      peak=HBM_PEAK_GBS),
+        # counting reads every key once: 4 B per request
+        "count": dict(kernel="k_count_*", bound="hbm", unit="GB/s", work=4.0 * n, peak=HBM_PEAK_GBS),
         "route": dict(kernel="k_route<true>" if args.dispatch == "static" else "k_route_live<%s>" % (
             "false" if R <= 64 else "true"), bound="hbm", unit="GB/s", work=(4.0 + 2.0 * P) * n, peak=HBM_PEAK_GBS),
         # LPT: every job copy is compared against the R destination loads.
@@ -379,20 +519,21 @@ def main():
         out["calib_copy_bytes"] = nb
 
     if not args.no_cpu_baseline:
-        import oracle
         from oracle import pipeline as opipe
+        threads = args.cpu_threads or opipe.host_threads()
         times = []
         t_start = time.perf_counter()
         while True:
             s = time.perf_counter()
-            opipe.run(wl, dispatch=args.dispatch)
+            opipe.run(wl, dispatch=args.dispatch, threads=threads)
             times.append(time.perf_counter() - s)
             if time.perf_counter() - t_start > args.cpu_seconds or len(times) >= 10:
                 break
         med = float(np.median(times))
-        out["cpu_baseline"] = {"value": n / med, "unit": "requests/s", "cores": 1, "kind": "oracle",
+        out["cpu_baseline"] = {"value": n / med, "unit": "requests/s", "cores": threads, "kind": "oracle",
                                "sample": f"the full workload, {len(times)} passes, median "
-                                         f"{med:.3f} s per pass (single-threaded C oracle)"}
+                                         f"{med:.3f} s per pass (C oracle, units fanned out over {threads} "
+                                         f"host threads)"}
     print(json.dumps(out), flush=True)
 
 

@@ -71,12 +71,16 @@ typedef int32_t cr_status;
 
 /* One plan problem (Algorithm 1 inputs: rates, R, q_cap, C). Arrays of these live in
  * DEVICE memory. q_cap = q_num / q_den requests per window, so Eq. 1 is evaluated as
- * k = max(1, ceil(c * q_den / q_num)) in exact integers; k is clamped to R. */
+ * k = max(1, ceil(c * q_den / q_num)) in exact integers; k is clamped to R.
+ * With n_window = CR_WINDOW_SUM the device takes N_w = the counts row's sum and the target
+ * is relative to the mean per-destination load: q_cap = (q_num / q_den) * N_w / R, i.e. the
+ * rule above with q_num * N_w and q_den * R (q_num * N_w < 2^63, q_den * R < 2^31). */
+#define CR_WINDOW_SUM 0xFFFFFFFFFFFFFFFFull
 typedef struct {
     uint32_t window;     /* row of counts the plan is built from (< num_windows)      */
     uint32_t W;          /* warm slots per destination, 1..max_W; C = R * W           */
-    uint64_t n_window;   /* requests in that row (its sum)                            */
-    uint64_t q_num;      /* > 0 unless n_window == 0 (unused by AFFINITY and FLAT)   */
+    uint64_t n_window;   /* requests in that row (its sum), or CR_WINDOW_SUM          */
+    uint64_t q_num;      /* > 0 unless the window is empty (unused by AFFINITY, FLAT) */
     uint64_t q_den;      /* 1 .. 2^31 - 1 (likewise)                                  */
     uint32_t variant;    /* CR_PLAN_*                                                 */
     uint32_t place_seed; /* hash placement seed (AFFINITY, REPLICATED)                */
@@ -144,6 +148,18 @@ typedef struct {
     uint64_t* group_p2c;
 } cr_plan_set;
 
+/* Rates of one slice of the log, accumulated (Algorithm 1 input "rates"; Appendix A.2):
+ *   counts[b] += #{ i < n : keys[i] == b }
+ * keys u32 [n] (n < 2^32 - 1); counts u32 [num_keys] (accumulated: clear it for a fresh
+ * window). Meant for key spaces beyond LDS (e.g. 10^6 keys): the slice is bucket-sorted by
+ * key range in tiles and each bucket counted in LDS, with no global atomics, in a workspace
+ * of cr_count_slice_workspace_bytes(n, num_keys) bytes (CR_ESIZE if smaller; buckets of up
+ * to 32,768 keys and at most 256 buckets, CR_EINVAL beyond). A key >= num_keys is not
+ * counted and sets CR_ERR_KEY_RANGE. */
+size_t cr_count_slice_workspace_bytes(uint64_t n, uint32_t num_keys);
+cr_status cr_count_slice(const uint32_t* keys, uint64_t n, uint32_t num_keys, uint32_t* counts, uint32_t* err,
+                         void* ws, size_t ws_bytes, void* stream);
+
 /* Rates per key per control interval (Algorithm 1 input "rates"; Appendix A.2: the
  * planner needs only {(b, lambda_b)}). Rates are kept in requests per window.
  *   counts[j * num_keys + b] = #{ i in [off[j], off[j+1]) : keys[i] == b }
@@ -154,6 +170,19 @@ cr_status cr_count_rates(const uint32_t* keys, uint64_t n, const uint64_t* off, 
 
 /* Workspace for cr_admit, in bytes. */
 size_t cr_admit_workspace_bytes(uint32_t num_windows, uint32_t R, uint32_t max_W);
+
+/* Byte sizes of the buffers of a cr_plan_set with these fields, in struct order: specs, order,
+ * order_count, n_order, num_admitted, cold, clamped, member_off, members, load, key_index,
+ * route, window_rank, group_dest, group_p2c (the last three: the optional group tables).
+ * out_bytes has CR_PLAN_BUFFERS entries. */
+#define CR_PLAN_BUFFERS 15
+void cr_plan_sizes(uint32_t num_plans, uint32_t cands, uint32_t R, uint32_t max_W, uint32_t num_keys,
+                   uint32_t num_windows, size_t out_bytes[CR_PLAN_BUFFERS]);
+
+/* One workspace size that serves cr_count_slice for slices of up to max_n requests and
+ * cr_replay / cr_replay_partition / cr_replay_lru for up to max_n requests, P candidates and
+ * R destinations (cr_admit's depends on the windows and has its own query). */
+size_t cr_workspace_bytes(uint32_t num_keys, uint32_t R, uint32_t P, uint64_t max_n);
 
 /* Top-rate admission (Eq. 1; Section 3.1 "Warm-set admission"; Algorithm 1 sort/admit).
  * For every window: order its nonzero keys by (count desc, key asc), cut at C_max.
@@ -228,6 +257,12 @@ cr_status cr_plan_churn(const cr_plan_set* plans, const uint32_t* pairs, uint32_
 
 /* Workspace for cr_replay (and for its two phases), in bytes. */
 size_t cr_replay_workspace_bytes(uint64_t n, uint32_t P, uint32_t R);
+
+/* Carried LRU state of the replay, u32 [P][R][max_W] (most recent first, CR_EMPTY_SLOT after
+ * the used entries): its size in bytes, and a reset of all of it to empty caches (a fill
+ * kernel on `stream`; it records no memset, so it can be captured in a HIP graph). */
+size_t cr_lru_state_bytes(uint32_t P, uint32_t R, uint32_t max_W);
+cr_status cr_lru_reset(uint32_t* lru_state, uint32_t P, uint32_t R, uint32_t max_W, void* stream);
 
 /* Shadow replay (Section 3.2: admitted and cold prefixes share each destination's
  * cache) against an LRU of W_c whole-prefix slots per destination (the equal-slot model

@@ -23,10 +23,14 @@ CR_EMPTY_SLOT = 0xFFFFFFFF
 CR_ROUTE_SINGLE = 0x80000000
 CR_MAX_R, CR_MAX_W, CR_MAX_CANDS, CR_MAX_J = 1024, 512, 256, 65535
 
-EXPORTS = ("cr_count_rates", "cr_admit_workspace_bytes", "cr_admit", "cr_place_lpt", "cr_place_hash", "cr_route",
+EXPORTS = ("cr_count_rates", "cr_count_slice_workspace_bytes", "cr_count_slice", "cr_admit_workspace_bytes",
+           "cr_admit", "cr_plan_sizes", "cr_workspace_bytes", "cr_place_lpt", "cr_place_hash", "cr_route",
            "cr_route_live", "cr_plan_churn", "cr_keymap_bytes", "cr_keymap_workspace_bytes", "cr_keymap_build",
-           "cr_keymap_lookup", "cr_keymap_scatter",
-           "cr_replay_workspace_bytes", "cr_replay", "cr_replay_partition", "cr_replay_lru", "cr_version")
+           "cr_keymap_lookup", "cr_keymap_scatter", "cr_replay_workspace_bytes", "cr_lru_state_bytes",
+           "cr_lru_reset", "cr_replay", "cr_replay_partition", "cr_replay_lru", "cr_version")
+CR_WINDOW_SUM = 0xFFFFFFFFFFFFFFFF
+CR_PLAN_BUFFERS = 15
+CR_GROUP_MULTI, CR_GROUP_COLD = 0xFFFE, 0xFFFF
 
 _u32, _u64, _P = ctypes.c_uint32, ctypes.c_uint64, ctypes.c_void_p
 
@@ -66,6 +70,16 @@ def load(path: Optional[str] = None):
         raise CrError(f"{p} is missing: build it with paper_2608_19677_amd/build.py (no fallback exists)")
     L = ctypes.CDLL(p)
     L.cr_count_rates.argtypes = [_P, _u64, _P, _u32, _u32, _P, _P, _P]
+    L.cr_count_slice_workspace_bytes.argtypes = [_u64, _u32]
+    L.cr_count_slice_workspace_bytes.restype = ctypes.c_size_t
+    L.cr_count_slice.argtypes = [_P, _u64, _u32, _P, _P, _P, ctypes.c_size_t, _P]
+    L.cr_plan_sizes.argtypes = [_u32, _u32, _u32, _u32, _u32, _u32, ctypes.POINTER(ctypes.c_size_t)]
+    L.cr_plan_sizes.restype = None
+    L.cr_workspace_bytes.argtypes = [_u32, _u32, _u32, _u64]
+    L.cr_workspace_bytes.restype = ctypes.c_size_t
+    L.cr_lru_state_bytes.argtypes = [_u32, _u32, _u32]
+    L.cr_lru_state_bytes.restype = ctypes.c_size_t
+    L.cr_lru_reset.argtypes = [_P, _u32, _u32, _u32, _P]
     L.cr_admit_workspace_bytes.argtypes = [_u32, _u32, _u32]
     L.cr_admit_workspace_bytes.restype = ctypes.c_size_t
     L.cr_admit.argtypes = [_P, ctypes.POINTER(CrPlanSet), _P, ctypes.c_size_t, _P, _P]
@@ -90,7 +104,7 @@ def load(path: Optional[str] = None):
     L.cr_replay_lru.argtypes = [_P, _u32, _u64, _u32, _u32, _u32, ctypes.POINTER(_u32), _u32, _P, _P, _P, _P,
                                 ctypes.c_size_t, _P, _P]
     L.cr_version.restype = ctypes.c_char_p
-    for f in ("cr_count_rates", "cr_admit", "cr_place_lpt", "cr_place_hash", "cr_route", "cr_route_live", "cr_plan_churn",
+    for f in ("cr_count_rates", "cr_count_slice", "cr_lru_reset", "cr_admit", "cr_place_lpt", "cr_place_hash", "cr_route", "cr_route_live", "cr_plan_churn",
               "cr_keymap_build", "cr_keymap_lookup", "cr_keymap_scatter", "cr_replay",
               "cr_replay_partition", "cr_replay_lru"):
         getattr(L, f).restype = ctypes.c_int32
@@ -126,6 +140,34 @@ def cr_count_rates(keys, off, J: int, num_keys: int, counts, err, stream=None, n
     n = keys.numel() if n is None else n
     _check(load().cr_count_rates(_ptr(keys), n, _ptr(off), J, num_keys, _ptr(counts), _ptr(err), _stream(stream)),
            "cr_count_rates")
+
+
+def cr_count_slice_workspace_bytes(n: int, num_keys: int) -> int:
+    return int(load().cr_count_slice_workspace_bytes(n, num_keys))
+
+
+def cr_count_slice(keys, num_keys: int, counts, err, ws, stream=None, n: Optional[int] = None):
+    n = keys.numel() if n is None else n
+    _check(load().cr_count_slice(_ptr(keys), n, num_keys, _ptr(counts), _ptr(err), _ptr(ws), _nbytes(ws),
+                                 _stream(stream)), "cr_count_slice")
+
+
+def cr_plan_sizes(num_plans: int, cands: int, R: int, max_W: int, num_keys: int, num_windows: int):
+    out = (ctypes.c_size_t * CR_PLAN_BUFFERS)()
+    load().cr_plan_sizes(num_plans, cands, R, max_W, num_keys, num_windows, out)
+    return [int(x) for x in out]
+
+
+def cr_workspace_bytes(num_keys: int, R: int, P: int, max_n: int) -> int:
+    return int(load().cr_workspace_bytes(num_keys, R, P, max_n))
+
+
+def cr_lru_state_bytes(P: int, R: int, max_W: int) -> int:
+    return int(load().cr_lru_state_bytes(P, R, max_W))
+
+
+def cr_lru_reset(lru_state, P: int, R: int, max_W: int, stream=None):
+    _check(load().cr_lru_reset(_ptr(lru_state), P, R, max_W, _stream(stream)), "cr_lru_reset")
 
 
 def cr_admit_workspace_bytes(num_windows: int, R: int, max_W: int) -> int:

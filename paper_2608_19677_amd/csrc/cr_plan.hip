@@ -675,8 +675,19 @@ __global__ __launch_bounds__(kAdmitThreads) void k_admit_plan(
     bool ok = spec.window < NW && spec.W >= 1 && (uint64_t)R * spec.W <= Cmax && spec.variant <= CR_PLAN_FLAT;
     // the flat variant admits nothing: its whole window is cold
     const uint32_t M = ok && spec.variant != CR_PLAN_FLAT ? n_order[spec.window] : 0u;
-    if (ok && spec.n_window != row_sum[spec.window]) ok = false;
-    if (ok && eq1 && M > 0 && (spec.q_num == 0 || spec.q_den == 0 || spec.q_den >= (1ull << 31))) ok = false;
+    // N_w: given, or (CR_WINDOW_SUM) the row's sum with the target relative to the mean load,
+    // q_cap = (q_num / q_den) N_w / R, i.e. Eq. 1 with q_num N_w and q_den R
+    const uint64_t nw = ok ? row_sum[spec.window] : 0ull;
+    const bool rel = spec.n_window == CR_WINDOW_SUM;
+    if (ok && !rel && spec.n_window != nw) ok = false;
+    uint64_t q_num = spec.q_num, q_den = spec.q_den;
+    if (ok && rel) {
+        if (nw && q_num > 0x7FFFFFFFFFFFFFFFull / nw) ok = false;
+        q_num *= nw;
+        q_den *= R;
+    }
+    const uint64_t n_window = nw;
+    if (ok && eq1 && M > 0 && (q_num == 0 || q_den == 0 || q_den >= (1ull << 31))) ok = false;
     if (!ok) {
         if (tid == 0) {
             num_admitted[p] = 0;
@@ -702,8 +713,8 @@ __global__ __launch_bounds__(kAdmitThreads) void k_admit_plan(
         if (valid && !eq1) {
             k = 1;  // affinity: one copy per admitted key
         } else if (valid) {
-            const uint64_t num = (uint64_t)c * spec.q_den;
-            uint64_t kk = num / spec.q_num + (num % spec.q_num != 0);
+            const uint64_t num = (uint64_t)c * q_den;
+            uint64_t kk = num / q_num + (num % q_num != 0);
             if (kk < 1) kk = 1;
             if (kk > R) {
                 kk = R;
@@ -732,7 +743,7 @@ __global__ __launch_bounds__(kAdmitThreads) void k_admit_plan(
         moff[A] = (uint32_t)used;
         num_admitted[p] = A;
         const uint64_t carried = s_carried;
-        cold[p] = spec.n_window >= carried ? spec.n_window - carried : 0ull;
+        cold[p] = n_window >= carried ? n_window - carried : 0ull;
         clamped[p] = ncl;
     }
     build_key_index(order + (uint64_t)spec.window * Cmax, A, KW, kx, s_bits, s_scan);
@@ -1651,6 +1662,20 @@ extern "C" size_t cr_admit_workspace_bytes(uint32_t num_windows, uint32_t R, uin
 {
     const uint64_t cmax = (uint64_t)R * max_W;
     return (size_t)(num_windows * (2u * cmax * sizeof(uint2) + sizeof(uint64_t)) + 256u);
+}
+
+extern "C" void cr_plan_sizes(uint32_t num_plans, uint32_t cands, uint32_t R, uint32_t max_W, uint32_t num_keys,
+                              uint32_t num_windows, size_t out_bytes[CR_PLAN_BUFFERS])
+{
+    if (!out_bytes) return;
+    const uint64_t NP = num_plans, NW = num_windows, cmax = (uint64_t)R * max_W;
+    const uint64_t NG = cands ? NP / cands : 0, CS = ((uint64_t)cands + 7) / 8 * 8, PW = ((uint64_t)cands + 63) / 64;
+    const uint64_t KW = ((uint64_t)num_keys + 63) / 64;
+    const uint64_t b[CR_PLAN_BUFFERS] = {
+        NP * sizeof(cr_plan_spec), NW * cmax * 4, NW * cmax * 4, NW * 4, NP * 4, NP * 8, NP * 4,
+        NP * (cmax + 1) * 4, NP * cmax * 2, NP * R * 8, NP * KW * 16, NP * cmax * 4,
+        NW * num_keys * 4, NG * cmax * CS * 2, NG * R * R * PW * 8};
+    for (int i = 0; i < CR_PLAN_BUFFERS; ++i) out_bytes[i] = (size_t)b[i];
 }
 
 extern "C" cr_status cr_admit(const uint32_t* counts, const cr_plan_set* plans, void* ws, size_t ws_bytes,

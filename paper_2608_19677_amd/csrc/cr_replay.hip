@@ -904,6 +904,39 @@ extern "C" size_t cr_replay_workspace_bytes(uint64_t n, uint32_t P, uint32_t R)
     return cr::replay_layout(nullptr, n, P, R).bytes;
 }
 
+extern "C" size_t cr_workspace_bytes(uint32_t num_keys, uint32_t R, uint32_t P, uint64_t max_n)
+{
+    const size_t a = cr_count_slice_workspace_bytes(max_n, num_keys), b = cr_replay_workspace_bytes(max_n, P, R);
+    return a > b ? a : b;
+}
+
+extern "C" size_t cr_lru_state_bytes(uint32_t P, uint32_t R, uint32_t max_W)
+{
+    return (size_t)P * R * max_W * sizeof(uint32_t);
+}
+
+namespace cr {
+namespace {
+__global__ void k_lru_fill(uint32_t* __restrict__ p, uint64_t n)
+{
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = CR_EMPTY_SLOT;
+}
+}  // namespace
+}  // namespace cr
+
+extern "C" cr_status cr_lru_reset(uint32_t* lru_state, uint32_t P, uint32_t R, uint32_t max_W, void* stream)
+{
+    using namespace cr;
+    if (!lru_state || P == 0 || P > CR_MAX_CANDS || R == 0 || R > CR_MAX_R || max_W == 0 || max_W > CR_MAX_W)
+        return CR_EINVAL;
+    const uint64_t n = (uint64_t)P * R * max_W;
+    (void)hipGetLastError();
+    hipLaunchKernelGGL(k_lru_fill, dim3((uint32_t)((n + 255) / 256 < 4096 ? (n + 255) / 256 : 4096)), dim3(256), 0,
+                       as_stream(stream), lru_state, n);
+    return hipGetLastError() == hipSuccess ? CR_OK : CR_EHIP;
+}
+
 extern "C" cr_status cr_replay_partition(const uint32_t* keys, const uint16_t* suffix, const uint16_t* dest,
                                          uint64_t n, const uint64_t* off, uint32_t J, uint32_t P, uint32_t R,
                                          const uint32_t* W, void* ws, size_t ws_bytes, uint32_t* err, void* stream)

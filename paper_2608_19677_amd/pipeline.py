@@ -50,9 +50,10 @@ class Pipeline:
     """All device buffers for one workload (or one chunk of a chunked stream)."""
 
     GROUP_TABLE_BUDGET = 4 << 30  # bytes the optional group dispatch tables may take
+    SLICE_MIN_KEYS = 100_000      # one-interval streams with this many keys use cr_count_slice
 
     def __init__(self, wl, device="cuda", dev_in: Optional[DeviceInputs] = None,
-                 prev_counts: Optional[torch.Tensor] = None, prev_n: int = 0,
+                 prev_counts: Optional[torch.Tensor] = None,
                  lru_in: Optional[torch.Tensor] = None, dispatch: str = "static",
                  group_tables: Optional[bool] = None):
         if dispatch not in ("static", "live"):
@@ -65,11 +66,6 @@ class Pipeline:
         self.J, self.K, self.R, self.P, self.n = J, K, R, P, wl.n
         self.Ws = [c.W for c in wl.candidates]
         self.max_W = max(self.Ws)
-        # requests per window that count (keys < num_keys): a window's N_w is its row sum
-        off = self.inp.off_host.astype(np.int64)
-        csum = np.concatenate([[0], np.cumsum(np.asarray(wl.keys) < K, dtype=np.int64)])
-        sizes = csum[off[1:]] - csum[off[:-1]]
-        self.window_sizes = sizes
         i32 = dict(dtype=torch.int32, device=device)
         self.err = torch.zeros(1, **i32)
         # plan groups g = 0..NG-1 (interval j -> group gmap[j]); window[g][c] = counts row
@@ -82,7 +78,6 @@ class Pipeline:
             self.win_src = self.counts[:NG]
             gmap = [max(j - 1, 0) for j in range(J)]
             window = [[g] * P for g in range(NG)]
-            n_win = [int(sizes[g]) for g in range(NG)]
         elif prev_counts is None:
             self.counts = torch.empty((J, K), **i32)
             NG = J
@@ -91,7 +86,6 @@ class Pipeline:
             window = [[int(pw[j][c]) for c in range(P)] for j in range(J)]
             if any(not 0 <= w < J for row in window for w in row):
                 raise ValueError("plan_windows names a window outside the stream")
-            n_win = [int(x) for x in sizes]
         else:
             if pw is not None:
                 raise ValueError("a stream processed in chunks plans every interval from the window before it")
@@ -103,17 +97,18 @@ class Pipeline:
             self.win_src = self.cbuf[:J]
             gmap = list(range(J))
             window = [[g] * P for g in range(NG)]
-            n_win = [int(prev_n)] + [int(sizes[g]) for g in range(J - 1)]
         self.NG = NG
         self.gmap_host = gmap
         self.gmap = torch.tensor(gmap, dtype=torch.int32, device=device)
         self.plan_window = [window[g][c] for g in range(NG) for c in range(P)]  # by plan p = g * P + c
+        # N_w of every window is its counts row's sum, taken on the device (CR_WINDOW_SUM), and
+        # q_cap = (a / b) N_w / R is given relative to the mean per-destination load
         specs = []
         for g in range(NG):
             for c, cand in enumerate(wl.candidates):
                 w = window[g][c]
                 v = B.PLAN_VARIANTS[getattr(cand, "variant", "full")]
-                specs.append((w, cand.W, n_win[w], cand.a * n_win[w], cand.b * R, v, getattr(cand, "place_seed", 0)))
+                specs.append((w, cand.W, B.CR_WINDOW_SUM, cand.a, cand.b, v, getattr(cand, "place_seed", 0)))
         # hash-placed ablation stages need cr_place_hash after cr_place_lpt
         self.hash_placed = any(getattr(c, "variant", "full") in ("affinity", "replicated") for c in wl.candidates)
         self.NW = self.win_src.shape[0]  # counts rows the plans are built from
@@ -131,6 +126,10 @@ class Pipeline:
         self.ws_admit = torch.empty(B.cr_admit_workspace_bytes(self.NW, R, self.max_W), dtype=torch.uint8,
                                     device=device)
         self.ws_replay = torch.empty(B.cr_replay_workspace_bytes(wl.n, P, R), dtype=torch.uint8, device=device)
+        # one interval over a key space beyond LDS: counted as one slice (no global atomics)
+        self.slice_count = J == 1 and K >= self.SLICE_MIN_KEYS and wl.n > 0
+        self.ws_count = (torch.empty(B.cr_count_slice_workspace_bytes(wl.n, K), dtype=torch.uint8, device=device)
+                         if self.slice_count else None)
         self.dest = torch.empty((P, max(wl.n, 1)), dtype=torch.int16, device=device)
         soff = getattr(wl, "stat_offsets", None)
         if soff is None:
@@ -148,9 +147,21 @@ class Pipeline:
         self.lru_out = torch.empty((P, R, self.max_W), **i32)
         self.first_index = wl.first_index  # global index of the chunk's first request
 
+    def set_inputs(self, dev_in: DeviceInputs):
+        """Point the pipeline at another chunk's device inputs (same sizes and intervals)."""
+        if dev_in.keys.numel() != self.inp.keys.numel() or not np.array_equal(dev_in.off_host, self.inp.off_host):
+            raise ValueError("a chunk must have the same length and interval offsets as the pipeline's")
+        if self.stat_off is self.inp.off:
+            self.stat_off = dev_in.off
+        self.inp = dev_in
+
     # -- the five calls ----------------------------------------------------------------
     def count(self, stream=None):
-        B.cr_count_rates(self.inp.keys, self.inp.off, self.J, self.K, self.counts, self.err, stream, n=self.n)
+        if self.slice_count:
+            self.counts.zero_()
+            B.cr_count_slice(self.inp.keys, self.K, self.counts, self.err, self.ws_count, stream, n=self.n)
+        else:
+            B.cr_count_rates(self.inp.keys, self.inp.off, self.J, self.K, self.counts, self.err, stream, n=self.n)
         if self.prev_counts is not None:
             self.cbuf[0].copy_(self.prev_counts)
 
@@ -264,8 +275,7 @@ class ChunkStream:
         self.n = wl.n
         self.inp = upload(wl, device)
         self.first = Pipeline(wl, device, self.inp)
-        last_n = int(self.first.window_sizes[-1])
-        self.slots = [Pipeline(wl, device, self.inp, prev_counts=self.first.counts[wl.J - 1], prev_n=last_n,
+        self.slots = [Pipeline(wl, device, self.inp, prev_counts=self.first.counts[wl.J - 1],
                                lru_in=self.first.lru_out) for _ in range(2)]
         self.s_plan = torch.cuda.Stream(device=device)
         self.s_rep = torch.cuda.Stream(device=device)
@@ -419,8 +429,7 @@ class ChunkStream3:
         self.n = wl.n
         self.inp = upload(wl, device)
         self.first = Pipeline(wl, device, self.inp)
-        last_n = int(self.first.window_sizes[-1])
-        self.slots = [Pipeline(wl, device, self.inp, prev_counts=self.first.counts[wl.J - 1], prev_n=last_n,
+        self.slots = [Pipeline(wl, device, self.inp, prev_counts=self.first.counts[wl.J - 1],
                                lru_in=self.first.lru_out) for _ in range(self.NSETS)]
         self.streams = [torch.cuda.Stream(device=device) for _ in range(3)]
         self.ev = {}  # (stage, chunk) -> event recorded after that stage
@@ -519,3 +528,63 @@ class ChunkStream3:
         """One step of the captured steady state: the next graph in turn."""
         self.graphs[self.turn].replay()
         self.turn = (self.turn + 1) % self.NSETS
+
+
+class ChunkChain:
+    """Consecutive chunks of one request stream, each with its own inputs, through two
+    buffer sets on one stream. Step s runs chunk s: the inputs of ``chunks[s % len]`` at
+    global indices s * n .. s * n + n - 1, every interval planned from the window before
+    it (chunk s's first interval from chunk s-1's last window; chunk 0's from its own
+    first window) and the replay started from chunk s-1's final cache state (empty for
+    chunk 0). Every chunk must have the same length and intervals (every window's N_w is
+    taken on the device, so the plan specs of the two buffer sets fit every chunk). This is
+    how the large sweep streams 1e9 requests as ten 1e8-request chunks."""
+
+    def __init__(self, chunks, device="cuda"):
+        self.chunks = list(chunks)
+        w0 = self.chunks[0]
+        for w in self.chunks[1:]:
+            if (w.n, w.num_keys, w.R, w.P) != (w0.n, w0.num_keys, w0.R, w0.P) or \
+                    not np.array_equal(np.asarray(w.offsets), np.asarray(w0.offsets)):
+                raise ValueError("chunks of a chain must have the same shape and intervals")
+        if w0.plan_windows is not None or getattr(w0, "stat_offsets", None) is not None:
+            raise ValueError("a chain plans every interval from the window before it")
+        self.n = w0.n
+        self.inputs = [upload(w, device) for w in self.chunks]
+        self.sets = [Pipeline(w0, device, self.inputs[0], prev_counts=torch.empty(0), lru_in=None) for _ in range(2)]
+        self.s = 0
+
+    def pipe(self, s: int) -> Pipeline:
+        return self.sets[s % 2]
+
+    def prepare(self, s: int) -> Pipeline:
+        """Set up buffer set s % 2 for chunk s (no launches)."""
+        p = self.pipe(s)
+        p.set_inputs(self.inputs[s % len(self.inputs)])
+        p.first_index = s * self.n
+        if s == 0:
+            p.prev_counts = p.counts[0]  # plan chunk 0's first interval from its own window
+            p.lru_in = None
+        else:
+            prev = self.pipe(s - 1)
+            p.prev_counts = prev.counts[prev.J - 1]
+            p.lru_in = prev.lru_out
+        return p
+
+    def step(self, timers=None, stream=None) -> Pipeline:
+        """Enqueue chunk s on the current stream; returns its buffer set. ``timers`` maps
+        stage -> list of (start, end) events."""
+        p = self.prepare(self.s)
+        st = stream if stream is not None else torch.cuda.current_stream()
+        for stage in Pipeline.STAGES:
+            if timers is None:
+                getattr(p, stage)()
+            else:
+                a = torch.cuda.Event(enable_timing=True)
+                b = torch.cuda.Event(enable_timing=True)
+                a.record(st)
+                getattr(p, stage)()
+                b.record(st)
+                timers.setdefault(stage, []).append((a, b))
+        self.s += 1
+        return p

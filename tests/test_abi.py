@@ -57,3 +57,27 @@ def test_struct_layouts_match_header(lib_path):
     from paper_2608_19677_amd import binding
     assert ctypes.sizeof(binding.CrPlanSpec) == 40
     assert ctypes.sizeof(binding.CrPlanSet) == 6 * 4 + 15 * 8
+
+
+def test_plan_sizes_follow_the_header_layouts(lib_path):
+    # restated from the layouts documented in cr.h: C_max = R max_W, KW = ceil(K / 64),
+    # NG = NP / cands, CS = cands rounded up to 8, PW = ceil(cands / 64)
+    from paper_2608_19677_amd import binding
+    for NP, cands, R, W, K, NW in [(1, 1, 30, 64, 20_000, 1), (948, 1, 30, 64, 20_000, 948),
+                                   (64, 64, 1024, 512, 10**6, 1), (300, 100, 70, 60, 2000, 3)]:
+        cm, KW, NG, CS, PW = R * W, (K + 63) // 64, NP // cands, (cands + 7) // 8 * 8, (cands + 63) // 64
+        want = [NP * 40, NW * cm * 4, NW * cm * 4, NW * 4, NP * 4, NP * 8, NP * 4, NP * (cm + 1) * 4, NP * cm * 2,
+                NP * R * 8, NP * KW * 16, NP * cm * 4, NW * K * 4, NG * cm * CS * 2, NG * R * R * PW * 8]
+        assert binding.cr_plan_sizes(NP, cands, R, W, K, NW) == want
+
+
+def test_workspace_and_state_sizes(lib_path):
+    from paper_2608_19677_amd import binding
+    for K, R, P, n in [(1000, 30, 1, 10**5), (10**6, 1024, 64, 10**8), (5, 1, 1, 0)]:
+        ws = binding.cr_workspace_bytes(K, R, P, n)
+        assert ws >= binding.cr_replay_workspace_bytes(n, P, R)
+        assert ws >= binding.cr_count_slice_workspace_bytes(n, K)
+    # the slice workspace holds the bucket-sorted keys: at least 4 B per request
+    assert binding.cr_count_slice_workspace_bytes(10**8, 10**6) >= 4 * 10**8
+    assert binding.cr_lru_state_bytes(64, 1024, 512) == 64 * 1024 * 512 * 4
+    assert binding.cr_lru_state_bytes(1, 30, 16) == 30 * 16 * 4

@@ -163,8 +163,7 @@ def test_chunked_stream_equals_whole_stream():
     b = part(cut, wl.n, cut_j, wl.J, cut)
     pa = Pipeline(a)
     pa.step()
-    pb = Pipeline(b, prev_counts=pa.counts[a.J - 1].clone(), prev_n=int(a.offsets[-1] - a.offsets[-2]),
-                  lru_in=pa.lru_out.clone())
+    pb = Pipeline(b, prev_counts=pa.counts[a.J - 1].clone(), lru_in=pa.lru_out.clone())
     pb.step()
     ha, hb = pa.host(), pb.host()
     np.testing.assert_array_equal(np.concatenate([ha["dest"], hb["dest"]], axis=1), hw["dest"])
@@ -196,14 +195,13 @@ def _chunk_chain(wl, firsts):
     """Host results of chunks run one by one, chunk i with the global indices of chunk
     firsts[i], each planned from the previous chunk's last window with its cache state."""
     import dataclasses
-    last_n = int(wl.offsets[-1] - wl.offsets[-2])
     ref, prev = [], None
     for f in firsts:
         wk = dataclasses.replace(wl, first_index=wl.first_index + f * wl.n)
         if prev is None:
             p = Pipeline(wk)
         else:
-            p = Pipeline(wk, prev_counts=prev.counts[wl.J - 1].clone(), prev_n=last_n, lru_in=prev.lru_out.clone())
+            p = Pipeline(wk, prev_counts=prev.counts[wl.J - 1].clone(), lru_in=prev.lru_out.clone())
         p.step()
         ref.append(p.host())
         prev = p
@@ -270,14 +268,13 @@ def test_two_stream_chunk_graphs_equal_eager_chunks():
     cs = ChunkStream(wl)
     k0, k1 = cs.capture()
     firsts = [0, 1, 2, k0, k1, k0, k1]  # chunk index whose global indices each chunk uses
-    last_n = int(wl.offsets[-1] - wl.offsets[-2])
     ref, prev = [], None
     for f in firsts:
         wk = dataclasses.replace(wl, first_index=wl.first_index + f * wl.n)
         if prev is None:
             p = Pipeline(wk)
         else:
-            p = Pipeline(wk, prev_counts=prev.counts[wl.J - 1].clone(), prev_n=last_n, lru_in=prev.lru_out.clone())
+            p = Pipeline(wk, prev_counts=prev.counts[wl.J - 1].clone(), lru_in=prev.lru_out.clone())
         p.step()
         ref.append(p.host())
         prev = p
@@ -316,14 +313,13 @@ def test_two_stream_chunk_schedule_equals_serial():
         cs.enqueue()
     cs.flush()
     torch.cuda.synchronize()
-    last_n = int(wl.offsets[-1] - wl.offsets[-2])
     prev, ref = None, []
     for k in range(n_chunks):
         wk = dataclasses.replace(wl, first_index=wl.first_index + k * wl.n)
         if prev is None:
             p = Pipeline(wk)
         else:
-            p = Pipeline(wk, prev_counts=prev.counts[wl.J - 1].clone(), prev_n=last_n, lru_in=prev.lru_out.clone())
+            p = Pipeline(wk, prev_counts=prev.counts[wl.J - 1].clone(), lru_in=prev.lru_out.clone())
         p.step()
         ref.append(p.host())
         prev = p
