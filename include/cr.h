@@ -197,6 +197,16 @@ size_t cr_workspace_bytes(uint32_t num_keys, uint32_t R, uint32_t P, uint64_t ma
 cr_status cr_admit(const uint32_t* counts, const cr_plan_set* plans, void* ws, size_t ws_bytes,
                    uint32_t* err, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): cr_admit with its workspace in a
+ * library-owned device array of CR_ADMIT_SCRATCH_BYTES per GPU (held until the process
+ * ends) instead of a caller workspace. The caller still owns counts, the plan set and err.
+ * CR_ESIZE when cr_admit_workspace_bytes(num_windows, R, max_W) exceeds the array. The
+ * call allocates nothing; every call on one GPU uses that GPU's array, so calls that
+ * overlap on one GPU race (serialise them on one stream). Otherwise as cr_admit. */
+#define CR_ADMIT_SCRATCH_BYTES (64u << 20)
+cr_status cr_admit_noalloc(const uint32_t* counts, const cr_plan_set* plans, uint32_t* err, void* stream);
+
 /* LPT placement (Section 3.1 "Placement and dispatch"; Algorithm 1 placement loop).
  * Per plan: L[r] = cold / R; admitted keys in admission order take the k smallest
  * (L[r], r) destinations, listed in that order, each charged count / k (IEEE double,

@@ -22,9 +22,10 @@ CR_NO_KEY = 0xFFFFFFFF
 CR_EMPTY_SLOT = 0xFFFFFFFF
 CR_ROUTE_SINGLE = 0x80000000
 CR_MAX_R, CR_MAX_W, CR_MAX_CANDS, CR_MAX_J = 1024, 512, 256, 65535
+CR_ADMIT_SCRATCH_BYTES = 64 << 20
 
 EXPORTS = ("cr_count_rates", "cr_count_slice_workspace_bytes", "cr_count_slice", "cr_admit_workspace_bytes",
-           "cr_admit", "cr_plan_sizes", "cr_workspace_bytes", "cr_place_lpt", "cr_place_hash", "cr_route",
+           "cr_admit", "cr_admit_noalloc", "cr_plan_sizes", "cr_workspace_bytes", "cr_place_lpt", "cr_place_hash", "cr_route",
            "cr_route_live", "cr_plan_churn", "cr_keymap_bytes", "cr_keymap_workspace_bytes", "cr_keymap_build",
            "cr_keymap_lookup", "cr_keymap_scatter", "cr_replay_workspace_bytes", "cr_lru_state_bytes",
            "cr_lru_reset", "cr_replay", "cr_replay_partition", "cr_replay_lru", "cr_version")
@@ -83,6 +84,7 @@ def load(path: Optional[str] = None):
     L.cr_admit_workspace_bytes.argtypes = [_u32, _u32, _u32]
     L.cr_admit_workspace_bytes.restype = ctypes.c_size_t
     L.cr_admit.argtypes = [_P, ctypes.POINTER(CrPlanSet), _P, ctypes.c_size_t, _P, _P]
+    L.cr_admit_noalloc.argtypes = [_P, ctypes.POINTER(CrPlanSet), _P, _P]
     L.cr_place_lpt.argtypes = [_P, ctypes.POINTER(CrPlanSet), _P]
     L.cr_place_hash.argtypes = [_P, ctypes.POINTER(CrPlanSet), _P]
     L.cr_route.argtypes = [_P, _u64, _u64, _u64, _P, _P, _u32, ctypes.POINTER(CrPlanSet), _P, _P, _P]
@@ -104,7 +106,7 @@ def load(path: Optional[str] = None):
     L.cr_replay_lru.argtypes = [_P, _u32, _u64, _u32, _u32, _u32, ctypes.POINTER(_u32), _u32, _P, _P, _P, _P,
                                 ctypes.c_size_t, _P, _P]
     L.cr_version.restype = ctypes.c_char_p
-    for f in ("cr_count_rates", "cr_count_slice", "cr_lru_reset", "cr_admit", "cr_place_lpt", "cr_place_hash", "cr_route", "cr_route_live", "cr_plan_churn",
+    for f in ("cr_count_rates", "cr_count_slice", "cr_lru_reset", "cr_admit", "cr_admit_noalloc", "cr_place_lpt", "cr_place_hash", "cr_route", "cr_route_live", "cr_plan_churn",
               "cr_keymap_build", "cr_keymap_lookup", "cr_keymap_scatter", "cr_replay",
               "cr_replay_partition", "cr_replay_lru"):
         getattr(L, f).restype = ctypes.c_int32
@@ -177,6 +179,10 @@ def cr_admit_workspace_bytes(num_windows: int, R: int, max_W: int) -> int:
 def cr_admit(counts, plans: CrPlanSet, ws, err, stream=None):
     _check(load().cr_admit(_ptr(counts), ctypes.byref(plans), _ptr(ws), ws.numel() * ws.element_size(), _ptr(err),
                            _stream(stream)), "cr_admit")
+
+
+def cr_admit_noalloc(counts, plans: CrPlanSet, err, stream=None):
+    _check(load().cr_admit_noalloc(_ptr(counts), ctypes.byref(plans), _ptr(err), _stream(stream)), "cr_admit_noalloc")
 
 
 def cr_place_lpt(counts, plans: CrPlanSet, stream=None):

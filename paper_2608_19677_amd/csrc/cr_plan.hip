@@ -14,6 +14,7 @@
 // k_plan_churn compares pairs of built plans for the replanning study.
 #include <math.h>
 
+#include <mutex>
 #include <utility>
 
 #include "cr_common.h"
@@ -1789,4 +1790,49 @@ extern "C" cr_status cr_place_hash(const uint32_t* counts, const cr_plan_set* pl
     else CR_HASH_LOADS(16, 0, false);
 #undef CR_HASH_LOADS
     return hipGetLastError() == hipSuccess ? CR_OK : CR_EHIP;
+}
+
+// ---------------------------------------------------------------------------------------
+// cr_admit_noalloc: cr_admit with its workspace in a library-owned device array instead of
+// the caller's. The array is a file-scope __device__ variable; its name in host code is a
+// stand-in, so its device address is taken once per device with hipGetSymbolAddress (with
+// that device current) and kept. Every call on a device shares that device's array.
+// ---------------------------------------------------------------------------------------
+namespace cr {
+namespace {
+
+constexpr size_t kAdmitScratchBytes = (size_t)CR_ADMIT_SCRATCH_BYTES;
+constexpr int kMaxDevices = 64;
+
+static __device__ __align__(256) uint8_t scratch[kAdmitScratchBytes];
+
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];
+
+cr_status admit_scratch(void** out)
+{
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return CR_EHIP;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return CR_EHIP;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return CR_OK;
+}
+
+}  // namespace
+}  // namespace cr
+
+extern "C" cr_status cr_admit_noalloc(const uint32_t* counts, const cr_plan_set* plans, uint32_t* err, void* stream)
+{
+    using namespace cr;
+    if (!counts || !valid_set(plans) || !err) return CR_EINVAL;
+    if (cr_admit_workspace_bytes(plans->num_windows, plans->R, plans->max_W) > kAdmitScratchBytes) return CR_ESIZE;
+    void* ws = nullptr;
+    const cr_status st = admit_scratch(&ws);
+    if (st != CR_OK) return st;
+    return cr_admit(counts, plans, ws, kAdmitScratchBytes, err, stream);
 }
