@@ -49,6 +49,12 @@ SMALL = [
     # 64-record batches to the start of the stream without filling the list, so repeated keys
     # are written past q and must be cleared before the replay and the final state
     (13, 40, 20_000, 2, [64, 48], 3, 0, 0.0, [(1, 1)]),
+    # 100 keys over two destinations with 130 to 512 slots: the blocked lists never fill,
+    # every rebuild reaches the start of the stream with several registers in use
+    (14, 100, 30_000, 2, [130, 300, 512], 3, 0, 0.0, [(1, 1)]),
+    # 2,000 keys spread thin over 5 destinations, 65 to 257 slots: deep hits and misses in
+    # every register, lists filled past one register
+    (15, 2000, 60_000, 5, [65, 129, 257], 4, 0, 0.0, [(1, 1)]),
 ]
 
 
