@@ -414,6 +414,144 @@ __global__ __launch_bounds__(64) void k_part_scatter64(const uint32_t* __restric
     }
 }
 
+// R > 64, several wavefronts per block: sub-tiles of kWideSub requests, wavefront w taking
+// the sub-tile's requests 1024 w .. 1024 w + 1023 as 16 chunks of 64 in order. A chunk ranks
+// each request among its chunk's requests to the same destination by ballots over the
+// destination bits; the chunk's leader adds the chunk's count to the wavefront's counter of
+// that destination in LDS and hands the old value to its peers, which ranks the request
+// within the wavefront's requests. Per destination, a block scan over the totals gives the
+// destination's run in the sub-tile and each wavefront's base in it; the records are staged
+// in LDS in destination order and written out run by run (about kWideSub / R consecutive
+// records per destination, against one in k_part_scatter's 1,024-request sub-tiles). The
+// grid takes candidates fastest, so the candidates of one tile read its keys together.
+constexpr uint32_t kWideWaves = 4;
+constexpr uint32_t kWideThreads = 64 * kWideWaves;
+constexpr uint32_t kWideSub = 1024 * kWideWaves;
+constexpr uint32_t kWideChunks = 16;  // chunks of 64 per wavefront and sub-tile
+
+inline size_t scatter_wide_lds_bytes(uint32_t R)
+{
+    return (size_t)kWideSub * 12u + (size_t)R * 4u * (kWideWaves + 3u);
+}
+
+__global__ __launch_bounds__(kWideThreads) void k_part_scatter_wide(
+    const uint32_t* __restrict__ keys, const uint16_t* __restrict__ suffix, const uint16_t* __restrict__ dest,
+    uint64_t n, const uint64_t* __restrict__ off, uint32_t J, uint32_t R, uint32_t nbits, uint64_t tile,
+    uint64_t ntiles, const uint32_t* __restrict__ tcnt, const uint32_t* __restrict__ grp_off,
+    uint64_t* __restrict__ rec)
+{
+    issue_priority_high();
+    extern __shared__ uint64_t lds[];
+    uint64_t* srec = lds;                                        // [kWideSub] staged records
+    uint32_t* spos = reinterpret_cast<uint32_t*>(srec + kWideSub);  // [kWideSub] their output positions
+    uint32_t* cnt = spos + kWideSub;                             // [kWideWaves][R] counts, then bases
+    uint32_t* run = cnt + kWideWaves * R;                        // [R] next output position
+    uint32_t* loff = run + R;                                    // [R] run start in the sub-tile
+    uint32_t* tot = loff + R;                                    // [R] run length
+    __shared__ uint32_t s_scan[16];
+    const uint32_t c = blockIdx.x, lane = lane_id(), wv = wave_in_block(), tid = threadIdx.x;
+    const uint64_t t = blockIdx.y;
+    if (t >= ntiles) return;
+    const uint64_t t0 = t * tile, t1 = t0 + tile < n ? t0 + tile : n;
+    for (uint32_t d = tid; d < R; d += kWideThreads)
+        run[d] = grp_off[(uint64_t)c * (R + 1u) + d] + tcnt[((uint64_t)c * R + d) * ntiles + t];
+    const uint16_t* __restrict__ dc = dest + (uint64_t)c * n;
+    uint64_t* __restrict__ rc = rec + (uint64_t)c * n;
+    uint32_t* __restrict__ wc = cnt + wv * R;
+    const uint32_t per = (R + kWideThreads - 1u) / kWideThreads;  // destinations per thread in the scan
+    for (uint64_t sb = t0; sb < t1; sb += kWideSub) {
+        const uint64_t se = sb + kWideSub < t1 ? sb + kWideSub : t1;
+        for (uint32_t x = tid; x < kWideWaves * R; x += kWideThreads) cnt[x] = 0;
+        __syncthreads();
+        // this wavefront's requests: ws .. ws + 1023 of the sub-tile
+        const uint64_t ws = sb + 1024u * wv;
+        uint32_t jl = ws < se ? find_interval(off, J, ws) : 0u;
+        uint64_t jend = jl + 1 < J ? off[jl + 1] : ~0ull;
+        uint32_t dk[kWideChunks], kv[kWideChunks], mv[kWideChunks];
+#pragma unroll
+        for (uint32_t m = 0; m < kWideChunks; ++m) {
+            const uint64_t i = ws + 64u * m + lane;
+            const bool in = i < se;
+            dk[m] = in ? dc[i] : 0xFFFFu;
+            kv[m] = in ? keys[i] : 0u;
+            mv[m] = in ? suffix[i] : 0u;
+        }
+#pragma unroll
+        for (uint32_t m = 0; m < kWideChunks; ++m) {
+            const uint64_t base = ws + 64u * m;
+            if (base >= se) {
+                dk[m] = 0xFFFFFFFFu;
+                continue;
+            }
+            const uint64_t i = base + lane;
+            const uint32_t d = dk[m];
+            const bool valid = i < se && d < R;
+            uint32_t j = jl;
+            if (base + 63 >= jend) {  // an interval boundary falls inside these 64 requests
+                while (j + 1 < J && off[j + 1] <= i) ++j;
+                jl = rdlane(j, 63);
+                jend = jl + 1 < J ? off[jl + 1] : ~0ull;
+            }
+            uint64_t peers = ballot(valid);
+            for (uint32_t bit = 0; bit < nbits; ++bit) {
+                const bool on = (d >> bit) & 1u;
+                const uint64_t bb = ballot(on);
+                peers &= on ? bb : ~bb;
+            }
+            const uint32_t rk = (uint32_t)__popcll(peers & lanemask_lt());
+            const uint32_t leader = valid ? (uint32_t)__builtin_ctzll(peers) : lane;
+            uint32_t old = 0;
+            if (valid && rk == 0) old = atomicAdd(&wc[d], (uint32_t)__popcll(peers));
+            old = (uint32_t)__builtin_amdgcn_ds_bpermute((int)(leader << 2), (int)old);
+            dk[m] = valid ? (d << 16) | (old + rk) : 0xFFFFFFFFu;  // destination, rank in the wavefront
+            mv[m] |= j << 16;
+        }
+        __syncthreads();
+        // destination runs in the sub-tile and each wavefront's base within its run
+        uint32_t own = 0;
+        for (uint32_t q = 0; q < per; ++q) {
+            const uint32_t d = tid * per + q;
+            if (d < R) {
+                uint32_t sum = 0;
+#pragma unroll
+                for (uint32_t w = 0; w < kWideWaves; ++w) sum += cnt[w * R + d];
+                tot[d] = sum;
+                own += sum;
+            }
+        }
+        uint32_t total;
+        uint32_t acc = block_exscan_u32(own, s_scan, &total);
+        for (uint32_t q = 0; q < per; ++q) {
+            const uint32_t d = tid * per + q;
+            if (d < R) {
+                loff[d] = acc;
+                uint32_t b = acc;
+#pragma unroll
+                for (uint32_t w = 0; w < kWideWaves; ++w) {
+                    const uint32_t x = cnt[w * R + d];
+                    cnt[w * R + d] = b;
+                    b += x;
+                }
+                acc += tot[d];
+            }
+        }
+        __syncthreads();
+#pragma unroll
+        for (uint32_t m = 0; m < kWideChunks; ++m) {
+            if (dk[m] != 0xFFFFFFFFu) {
+                const uint32_t d = dk[m] >> 16, lr = dk[m] & 0xFFFFu;
+                const uint32_t slot = wc[d] + lr;
+                srec[slot] = (uint64_t)kv[m] | ((uint64_t)mv[m] << 32);
+                spos[slot] = run[d] + (slot - loff[d]);
+            }
+        }
+        __syncthreads();
+        for (uint32_t q = tid; q < total; q += kWideThreads) rc[spos[q]] = srec[q];
+        for (uint32_t d = tid; d < R; d += kWideThreads) run[d] += tot[d];
+        __syncthreads();
+    }
+}
+
 // Destination bases and work items, from the destination totals dtot[c][d]:
 //   grp_off[c][d] = records of candidate c routed to destinations < d (grp_off[c][R] = all),
 //   item_off[e]   = first work item of stream e = c * R + d, one item per segment of S
@@ -973,7 +1111,14 @@ extern "C" cr_status cr_replay_partition(const uint32_t* keys, const uint16_t* s
         hipLaunchKernelGGL(k_part_scatter64<false>, dim3(xcd_grid((uint32_t)g.ntiles), P), dim3(64),
                            scatter64_lds_bytes(R), st, keys, suffix, dest, n, off, J, R, g.tile, g.ntiles, w.tcnt,
                            w.grp_off, w.rec);
-    else if (g.ntiles)
+    else if (g.ntiles && g.ntiles <= 65535u) {
+        const size_t lds = scatter_wide_lds_bytes(R);
+        if (hipFuncSetAttribute((const void*)k_part_scatter_wide, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                (int)lds) != hipSuccess)
+            return CR_EHIP;
+        hipLaunchKernelGGL(k_part_scatter_wide, dim3(P, (uint32_t)g.ntiles), dim3(kWideThreads), lds, st, keys, suffix,
+                           dest, n, off, J, R, nbits, g.tile, g.ntiles, w.tcnt, w.grp_off, w.rec);
+    } else if (g.ntiles)
         hipLaunchKernelGGL(k_part_scatter, dim3(xcd_grid((uint32_t)g.ntiles), P), dim3(64), scatter_lds_bytes(R), st, keys,
                            suffix, dest, n, off, J, R, nbits, g.tile, g.ntiles, w.tcnt, w.grp_off, w.rec);
     return hipGetLastError() == hipSuccess ? CR_OK : CR_EHIP;
