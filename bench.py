@@ -52,6 +52,9 @@ def parse():
                     help="timed steps (default: 10 for the sweep, one pass over its 1e9 requests; 20 otherwise)")
     ap.add_argument("--warmup", type=int, default=None, help="untimed steps first (default: 2 sweep, 3 otherwise)")
     ap.add_argument("--workload", default="sweep")
+    ap.add_argument("--sweep-chunks", type=int, default=0,
+                    help="sweep: distinct 1e8-request chunks generated and cycled through (default all ten; fewer "
+                         "only shortens set-up, for example under a profiler)")
     ap.add_argument("--cpu-threads", type=int, default=0,
                     help="host threads for the oracle baseline (default: every core this process may use)")
     ap.add_argument("--schedule", default="overlap", choices=("overlap", "overlap2", "serial"),
@@ -167,7 +170,8 @@ def run_sweep(args):
 
     steps = 10 if args.steps is None else args.steps
     warmup = 2 if args.warmup is None else args.warmup
-    chunks = [workload.sweep_chunk(k) for k in range(workload.SWEEP_CHUNKS)]
+    nchunks = args.sweep_chunks or workload.SWEEP_CHUNKS
+    chunks = [workload.sweep_chunk(k) for k in range(nchunks)]
     w0 = chunks[0]
     torch.cuda.set_device(0)
     chain = ChunkChain(chunks, device="cuda:0")
@@ -233,6 +237,15 @@ def run_sweep(args):
         "hbm_frac": {"count": kern["count"]["frac"], "route": kern["route"]["frac"]},
         "hit_rate": {"min": float(hit.min()), "max": float(hit.max())},
     }
+    if args.calib_copy_mb:
+        nb = args.calib_copy_mb << 20
+        src = torch.empty(nb, dtype=torch.uint8, device="cuda:0")
+        dst = torch.empty_like(src)
+        src.fill_(1)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        out["calib_copy_bytes"] = nb
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = sweep_cpu_baseline(args, chunks[0])
     return out
