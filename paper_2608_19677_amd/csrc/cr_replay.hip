@@ -429,9 +429,11 @@ constexpr uint32_t kWideThreads = 64 * kWideWaves;
 constexpr uint32_t kWideSub = 1024 * kWideWaves;
 constexpr uint32_t kWideChunks = 16;  // chunks of 64 per wavefront and sub-tile
 
+__host__ __device__ __forceinline__ uint32_t wide_row(uint32_t R) { return (R + 3u) & ~3u; }  // padded to 4 per thread
+
 inline size_t scatter_wide_lds_bytes(uint32_t R)
 {
-    return (size_t)kWideSub * 12u + (size_t)R * 4u * (kWideWaves + 3u);
+    return (size_t)kWideSub * 12u + (size_t)wide_row(R) * 4u * (kWideWaves + 1u);
 }
 
 __global__ __launch_bounds__(kWideThreads) void k_part_scatter_wide(
@@ -442,26 +444,33 @@ __global__ __launch_bounds__(kWideThreads) void k_part_scatter_wide(
 {
     issue_priority_high();
     extern __shared__ uint64_t lds[];
-    uint64_t* srec = lds;                                        // [kWideSub] staged records
+    const uint32_t R4 = wide_row(R);
+    uint64_t* srec = lds;                                           // [kWideSub] staged records
     uint32_t* spos = reinterpret_cast<uint32_t*>(srec + kWideSub);  // [kWideSub] their output positions
-    uint32_t* cnt = spos + kWideSub;                             // [kWideWaves][R] counts, then bases
-    uint32_t* run = cnt + kWideWaves * R;                        // [R] next output position
-    uint32_t* loff = run + R;                                    // [R] run start in the sub-tile
-    uint32_t* tot = loff + R;                                    // [R] run length
+    uint32_t* cnt = spos + kWideSub;  // [kWideWaves][R4] counts per wavefront, then its slot bases
+    uint32_t* gbase = cnt + kWideWaves * R4;  // [R4] output position of the destination's run minus its start
     __shared__ uint32_t s_scan[16];
     const uint32_t c = blockIdx.x, lane = lane_id(), wv = wave_in_block(), tid = threadIdx.x;
     const uint64_t t = blockIdx.y;
     if (t >= ntiles) return;
     const uint64_t t0 = t * tile, t1 = t0 + tile < n ? t0 + tile : n;
-    for (uint32_t d = tid; d < R; d += kWideThreads)
-        run[d] = grp_off[(uint64_t)c * (R + 1u) + d] + tcnt[((uint64_t)c * R + d) * ntiles + t];
+    // thread tid owns destinations 4 tid .. 4 tid + 3 in the scans: their next output positions
+    const bool owner = 4u * tid < R4;
+    uint32_t run[4];
+#pragma unroll
+    for (uint32_t q = 0; q < 4; ++q) {
+        const uint32_t d = 4u * tid + q;
+        run[q] = d < R ? grp_off[(uint64_t)c * (R + 1u) + d] + tcnt[((uint64_t)c * R + d) * ntiles + t] : 0u;
+    }
     const uint16_t* __restrict__ dc = dest + (uint64_t)c * n;
     uint64_t* __restrict__ rc = rec + (uint64_t)c * n;
-    uint32_t* __restrict__ wc = cnt + wv * R;
-    const uint32_t per = (R + kWideThreads - 1u) / kWideThreads;  // destinations per thread in the scan
+    uint32_t* __restrict__ wc = cnt + wv * R4;
     for (uint64_t sb = t0; sb < t1; sb += kWideSub) {
         const uint64_t se = sb + kWideSub < t1 ? sb + kWideSub : t1;
-        for (uint32_t x = tid; x < kWideWaves * R; x += kWideThreads) cnt[x] = 0;
+        if (owner)
+#pragma unroll
+            for (uint32_t w = 0; w < kWideWaves; ++w)
+                *reinterpret_cast<uint4*>(cnt + w * R4 + 4u * tid) = make_uint4(0u, 0u, 0u, 0u);
         __syncthreads();
         // this wavefront's requests: ws .. ws + 1023 of the sub-tile
         const uint64_t ws = sb + 1024u * wv;
@@ -507,33 +516,38 @@ __global__ __launch_bounds__(kWideThreads) void k_part_scatter_wide(
             mv[m] |= j << 16;
         }
         __syncthreads();
-        // destination runs in the sub-tile and each wavefront's base within its run
-        uint32_t own = 0;
-        for (uint32_t q = 0; q < per; ++q) {
-            const uint32_t d = tid * per + q;
-            if (d < R) {
-                uint32_t sum = 0;
+        // destination runs in the sub-tile: each wavefront's slot base within its destination's
+        // run, and the run's output position minus its start (16-byte accesses, one thread per
+        // four destinations)
+        uint4 cw[kWideWaves];
+        uint32_t tq[4] = {0u, 0u, 0u, 0u};
+        if (owner) {
 #pragma unroll
-                for (uint32_t w = 0; w < kWideWaves; ++w) sum += cnt[w * R + d];
-                tot[d] = sum;
-                own += sum;
+            for (uint32_t w = 0; w < kWideWaves; ++w) {
+                cw[w] = *reinterpret_cast<const uint4*>(cnt + w * R4 + 4u * tid);
+                tq[0] += cw[w].x, tq[1] += cw[w].y, tq[2] += cw[w].z, tq[3] += cw[w].w;
             }
         }
         uint32_t total;
-        uint32_t acc = block_exscan_u32(own, s_scan, &total);
-        for (uint32_t q = 0; q < per; ++q) {
-            const uint32_t d = tid * per + q;
-            if (d < R) {
-                loff[d] = acc;
-                uint32_t b = acc;
+        uint32_t acc = block_exscan_u32(tq[0] + tq[1] + tq[2] + tq[3], s_scan, &total);
+        if (owner) {
+            uint32_t st[4];
 #pragma unroll
-                for (uint32_t w = 0; w < kWideWaves; ++w) {
-                    const uint32_t x = cnt[w * R + d];
-                    cnt[w * R + d] = b;
-                    b += x;
-                }
-                acc += tot[d];
+            for (uint32_t q = 0; q < 4; ++q) {
+                st[q] = acc;
+                acc += tq[q];
             }
+            uint32_t b[4] = {st[0], st[1], st[2], st[3]};
+#pragma unroll
+            for (uint32_t w = 0; w < kWideWaves; ++w) {
+                const uint4 x = cw[w];
+                *reinterpret_cast<uint4*>(cnt + w * R4 + 4u * tid) = make_uint4(b[0], b[1], b[2], b[3]);
+                b[0] += x.x, b[1] += x.y, b[2] += x.z, b[3] += x.w;
+            }
+            *reinterpret_cast<uint4*>(gbase + 4u * tid) =
+                make_uint4(run[0] - st[0], run[1] - st[1], run[2] - st[2], run[3] - st[3]);
+#pragma unroll
+            for (uint32_t q = 0; q < 4; ++q) run[q] += tq[q];
         }
         __syncthreads();
 #pragma unroll
@@ -542,12 +556,11 @@ __global__ __launch_bounds__(kWideThreads) void k_part_scatter_wide(
                 const uint32_t d = dk[m] >> 16, lr = dk[m] & 0xFFFFu;
                 const uint32_t slot = wc[d] + lr;
                 srec[slot] = (uint64_t)kv[m] | ((uint64_t)mv[m] << 32);
-                spos[slot] = run[d] + (slot - loff[d]);
+                spos[slot] = gbase[d] + slot;
             }
         }
         __syncthreads();
         for (uint32_t q = tid; q < total; q += kWideThreads) rc[spos[q]] = srec[q];
-        for (uint32_t d = tid; d < R; d += kWideThreads) run[d] += tot[d];
         __syncthreads();
     }
 }
