@@ -621,14 +621,32 @@ __device__ __forceinline__ bool lru_contains(const uint32_t (&skey)[SL], uint32_
     return m != 0;
 }
 
-// Position q of the list is lane q / SL of register q % SL.
-template <int SL>
+// List positions in registers. Interleaved (kTwo false): position SL lane + s in register s.
+// Two-level (kTwo, SL >= 2): register 0 is the front, position lane (the 64 most recent
+// keys), and registers 1..SL-1 the back, position 64 + (SL-1) lane + (s-1) in register s.
+template <int SL, bool kTwo>
+__device__ __forceinline__ uint32_t list_pos(uint32_t s, uint32_t lane)
+{
+    if (kTwo) return s == 0 ? lane : 64u + (uint32_t)(SL - 1) * lane + (s - 1u);
+    return (uint32_t)SL * lane + s;
+}
+
+template <int SL, bool kTwo>
 __device__ __forceinline__ void lru_put_slot(uint32_t (&skey)[SL], uint32_t q, uint32_t kk, uint32_t lane)
 {
     (void)lane;
+    uint32_t rs, rl;  // register and lane of position q
+    if (kTwo) {
+        const uint32_t b = q - 64u;
+        rs = q < 64u ? 0u : 1u + b % (uint32_t)(SL - 1);
+        rl = q < 64u ? q : b / (uint32_t)(SL - 1);
+    } else {
+        rs = q % (uint32_t)SL;
+        rl = q / (uint32_t)SL;
+    }
 #pragma unroll
     for (int s = 0; s < SL; ++s)
-        if ((uint32_t)s == q % (uint32_t)SL) skey[s] = wrlane(skey[s], kk, q / (uint32_t)SL);
+        if ((uint32_t)s == rs) skey[s] = wrlane(skey[s], kk, rl);
 }
 
 // Move-to-front update after a lookup whose hit mask is m: p = first set bit of m
@@ -668,7 +686,7 @@ __device__ __forceinline__ uint32_t mtf_step(uint32_t& sk, uint32_t kk, uint64_t
 // for a new key and no position otherwise. q is compared with W once per 8 records, so up
 // to 7 keys may land past W; positions >= W are ignored everywhere (and positions past
 // the registers are never written). Returns the new q.
-template <int SL>
+template <int SL, bool kTwo>
 __device__ __forceinline__ uint32_t rebuild_batch(uint32_t (&sk)[SL], const uint64_t* __restrict__ rb, uint32_t q,
                                                   uint32_t W, uint32_t lane)
 {
@@ -702,7 +720,7 @@ __device__ __forceinline__ uint32_t rebuild_batch(uint32_t (&sk)[SL], const uint
             const bool fresh = m == 0;
             const uint32_t target = fresh ? q : 0xFFFFFFFFu;
 #pragma unroll
-            for (int s = 0; s < SL; ++s) sk[s] = lane * (uint32_t)SL + (uint32_t)s == target ? key[t] : sk[s];
+            for (int s = 0; s < SL; ++s) sk[s] = list_pos<SL, kTwo>((uint32_t)s, lane) == target ? key[t] : sk[s];
             q += fresh ? 1u : 0u;
         }
     }
@@ -779,6 +797,81 @@ __device__ __forceinline__ uint32_t mtf_batch_il(uint32_t (&sk)[SL], const uint6
     return depth;
 }
 
+// Two-level list, back operation for an access that missed the front: kk is the accessed
+// key and ins the key the front pushed out (its old position 63). If kk is in the back, the
+// back positions before it move back by one; otherwise every back position does, dropping
+// the least recent key of a full list. ins takes back position 0. The interleaved move-to-
+// front of mtf_step_il over registers 1..SL-1, inserting ins instead of kk. Returns whether
+// kk was in the back.
+template <int SL, bool kMasked>
+__device__ __forceinline__ bool back_step(uint32_t (&sk)[SL], uint32_t kk, uint32_t ins, const uint64_t (&vm)[SL])
+{
+    uint64_t mh[SL];
+    uint64_t m = 0;
+#pragma unroll
+    for (int s = 1; s < SL; ++s) {
+        mh[s] = ballot(sk[s] == kk);
+        if (kMasked) mh[s] &= vm[s];
+        m |= mh[s];
+    }
+    if constexpr (SL == 2) {
+        mtf_core(sk[1], m);
+        sk[1] = wrlane(sk[1], ins, 0u);
+    } else {
+        uint64_t keep;
+        uint32_t l;
+        const uint32_t r1 = il_core(sk[1], sk[SL - 1], m, keep, l);
+        uint64_t before[SL];  // hit bits of back registers before s
+        before[1] = 0;
+#pragma unroll
+        for (int s = 2; s < SL; ++s) before[s] = before[s - 1] | mh[s - 1];
+#pragma unroll
+        for (int s = SL - 1; s >= 2; --s)
+            sk[s] = __builtin_amdgcn_inverse_ballot_w64(keep | before[s]) ? sk[s] : sk[s - 1];
+        sk[1] = wrlane(r1, ins, 0u);
+    }
+    return m != 0;
+}
+
+// Two-level list, 64 records (all valid). Every access changes the front alone until it
+// misses there, and the back changes only on those misses, so the batch runs in two
+// phases: the 64 front accesses, branch-free and unrolled like the one-register list, each
+// writing its key and the front's position-63 key into lane j of evk / evv and advancing j
+// on a front miss; then one back operation per logged miss, in order. Returns lane t = 1
+// if record t hit (in the front or the back).
+template <int SL, bool kMasked>
+__device__ __forceinline__ uint32_t mtf_batch_two(uint32_t (&sk)[SL], const uint64_t* __restrict__ rb,
+                                                  const uint64_t (&vm)[SL], uint32_t lane)
+{
+    uint32_t depth = 0xFFFFFFFFu, evk = 0u, evv = 0u;
+    uint32_t j = 0;
+#pragma unroll
+    for (uint32_t g = 0; g < 8; ++g) {
+        uint64_t rk[8];
+#pragma unroll
+        for (uint32_t t = 0; t < 8; ++t) rk[t] = rb[8u * g + t];
+#pragma unroll
+        for (uint32_t t = 0; t < 8; ++t) {
+            const uint32_t key = (uint32_t)rk[t];
+            const uint64_t m = ballot(sk[0] == key);
+            const uint32_t ev = rdlane(sk[0], 63u);
+            const uint32_t p = mtf_core(sk[0], m);
+            sk[0] = wrlane(sk[0], key, 0u);
+            depth = wrlane(depth, p, 8u * g + t);
+            evk = wrlane(evk, key, j);
+            evv = wrlane(evv, ev, j);
+            asm("s_cmp_eq_u64 %1, 0\n\ts_addc_u32 %0, %0, 0" : "+s"(j) : "s"(m) : "scc");  // j += front miss
+        }
+    }
+    uint64_t rem = ballot(depth == 0xFFFFFFFFu), bh = 0;
+    for (uint32_t e = 0; rem; ++e) {
+        const uint32_t t = (uint32_t)__builtin_ctzll(rem);
+        rem &= rem - 1ull;
+        if (back_step<SL, kMasked>(sk, rdlane(evk, e), rdlane(evv, e), vm)) bh |= 1ull << t;
+    }
+    return (depth != 0xFFFFFFFFu || ((bh >> lane) & 1ull)) ? 1u : 0u;
+}
+
 // 64 records (lane t of kl = key of record t, all valid) through the move-to-front list;
 // returns lane t = hit depth of record t. Keys are read 16 at a time ahead of their use.
 template <bool kMasked>
@@ -813,7 +906,7 @@ __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v)
     return v;
 }
 
-template <int SL>
+template <int SL, bool kTwo>
 __global__ __launch_bounds__(kReplayThreads) void k_replay(
     const uint64_t* __restrict__ rec, uint64_t n, const uint32_t* __restrict__ grp_off,
     const uint32_t* __restrict__ item_off, uint32_t P, uint32_t R, uint32_t K, uint32_t J,
@@ -846,11 +939,14 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
     // Slot q of the rebuilt state (q = 64 s + lane) is the q-th most recent key, which is
     // already the move-to-front order.
     uint32_t skey[SL];
-    uint64_t vm[SL];  // lanes of register s whose position SL lane + s is < W
+    uint64_t vm[SL];  // lanes of register s whose position is < W
 #pragma unroll
     for (int s = 0; s < SL; ++s) {
         skey[s] = CR_EMPTY_SLOT;
-        const uint32_t nl = W > (uint32_t)s ? (W - (uint32_t)s + SL - 1u) / (uint32_t)SL : 0u;
+        uint32_t nl;  // lanes l with list_pos(s, l) < W
+        if (kTwo && s == 0) nl = W < 64u ? W : 64u;
+        else if (kTwo) nl = W > 63u + (uint32_t)s ? (W - 63u - (uint32_t)s + SL - 2u) / (uint32_t)(SL - 1) : 0u;
+        else nl = W > (uint32_t)s ? (W - (uint32_t)s + SL - 1u) / (uint32_t)SL : 0u;
         vm[s] = nl >= 64u ? ~0ull : (1ull << nl) - 1ull;
     }
     const uint64_t wmask = vm[0];
@@ -868,14 +964,14 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
             nb = pos < 64u ? pos : 64u;
             kl_next = lane < nb ? (uint32_t)rl[pos - nb + lane] : CR_EMPTY_SLOT;
             if (cnb == 64u && ballot(kl < K) == ~0ull) {
-                q = rebuild_batch<SL>(skey, rl + pos, q, W, lane);
+                q = rebuild_batch<SL, kTwo>(skey, rl + pos, q, W, lane);
                 continue;
             }
             for (int t = (int)cnb - 1; t >= 0 && q < W; --t) {
                 const uint32_t kk = rdlane(kl, (uint32_t)t);
                 if (kk >= K) continue;
                 if (!lru_contains<SL>(skey, kk)) {
-                    lru_put_slot<SL>(skey, q, kk, lane);
+                    lru_put_slot<SL, kTwo>(skey, q, kk, lane);
                     ++q;
                 }
             }
@@ -895,7 +991,7 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
                 }
                 if (kk >= K) continue;
                 if (!lru_contains<SL>(skey, kk)) {
-                    lru_put_slot<SL>(skey, q, kk, lane);
+                    lru_put_slot<SL, kTwo>(skey, q, kk, lane);
                     ++q;
                 }
             }
@@ -947,6 +1043,23 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
                 }
             }
             hl = depth != 0xFFFFFFFFu;
+        } else if constexpr (kTwo) {
+            uint32_t hit = 0;  // lane t: 1 if record t hit
+            if (ballot(vl) == ~0ull) {
+                hit = W == 64u * SL ? mtf_batch_two<SL, false>(skey, rl + b0, vm, lane)
+                                    : mtf_batch_two<SL, true>(skey, rl + b0, vm, lane);
+            } else {
+                for (uint32_t t = 0; t < nb; ++t) {
+                    const uint32_t kk = rdlane(kl, t);
+                    if (kk >= K) continue;
+                    const uint64_t m = ballot(skey[0] == kk);
+                    const uint32_t ev = rdlane(skey[0], 63u);
+                    mtf_core(skey[0], m);
+                    skey[0] = wrlane(skey[0], kk, 0u);
+                    if (m || back_step<SL, true>(skey, kk, ev, vm)) hit = wrlane(hit, 1u, t);
+                }
+            }
+            hl = hit != 0u;
         } else {
             uint32_t depth = 0xFFFFFFFFu;  // lane t: hit lane of record t
             if (ballot(vl) == ~0ull) {
@@ -985,7 +1098,7 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
         uint32_t* __restrict__ lo_ = lru_out + ((uint64_t)c * R + d) * max_W;
 #pragma unroll
         for (int s = 0; s < SL; ++s) {
-            const uint32_t idx = lane * (uint32_t)SL + (uint32_t)s;
+            const uint32_t idx = list_pos<SL, kTwo>((uint32_t)s, lane);
             if (idx < W) lo_[idx] = skey[s];
         }
         for (uint32_t idx = W + lane; idx < max_W; idx += 64) lo_[idx] = CR_EMPTY_SLOT;
@@ -1156,13 +1269,13 @@ extern "C" cr_status cr_replay_lru(const uint32_t* prefix_len, uint32_t num_keys
     const uint64_t blocks = (items + (kReplayThreads / 64) - 1) / (kReplayThreads / 64);
     if (blocks > 0x7FFFFFFFull) return CR_EINVAL;
     (void)hipGetLastError();
-#define CR_REPLAY(SL)                                                                                               \
-    hipLaunchKernelGGL(k_replay<SL>, dim3((uint32_t)blocks), dim3(kReplayThreads), 0, st, w.rec, n, w.grp_off,       \
+#define CR_REPLAY(SL, TWO)                                                                                          \
+    hipLaunchKernelGGL((k_replay<SL, TWO>), dim3((uint32_t)blocks), dim3(kReplayThreads), 0, st, w.rec, n, w.grp_off, \
                        w.item_off, P, R, num_keys, J, prefix_len, ra.wa, max_W, lru_in, lru_out, stats, err)
-    if (ra.classes & 1u) CR_REPLAY(1);
-    if (ra.classes & 2u) CR_REPLAY(2);
-    if (ra.classes & 4u) CR_REPLAY(4);
-    if (ra.classes & 8u) CR_REPLAY(8);
+    if (ra.classes & 1u) CR_REPLAY(1, false);
+    if (ra.classes & 2u) CR_REPLAY(2, false);
+    if (ra.classes & 4u) CR_REPLAY(4, false);  // two-level measured slower with three back registers
+    if (ra.classes & 8u) CR_REPLAY(8, true);
 #undef CR_REPLAY
     return hipGetLastError() == hipSuccess ? CR_OK : CR_EHIP;
 }
