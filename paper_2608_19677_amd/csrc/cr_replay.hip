@@ -906,38 +906,64 @@ __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v)
     return v;
 }
 
-template <int SL, bool kTwo>
+// One work item per segment (kSeq false) or per (candidate, destination) stream whose
+// segments could not all rebuild their state within the budget (kSeq true).
+//
+// A segment rebuilds its initial state by scanning back for W distinct keys; a stream with
+// fewer distinct keys than W would make every segment scan to the stream's start, which is
+// quadratic in its length. The scan therefore stops after kRebuildBudget segment lengths:
+// a segment that has neither found W keys nor reached the start writes nothing and marks
+// itself in `aborted` and its stream in `sflag`. The kSeq launch that follows replays each
+// marked stream from its start in one wavefront, segment after segment, keeping the
+// statistics of the marked segments only (the others were counted by their own work
+// items) and writing the stream's final state. Every record is then replayed at most twice
+// and scanned at most kRebuildBudget + 1 times, whatever the keys.
+constexpr uint32_t kRebuildBudget = 2;
+
+template <int SL, bool kTwo, bool kSeq>
 __global__ __launch_bounds__(kReplayThreads) void k_replay(
     const uint64_t* __restrict__ rec, uint64_t n, const uint32_t* __restrict__ grp_off,
     const uint32_t* __restrict__ item_off, uint32_t P, uint32_t R, uint32_t K, uint32_t J,
     const uint32_t* __restrict__ prefix_len, WArg wa, uint32_t max_W, const uint32_t* __restrict__ lru_in,
-    uint32_t* __restrict__ lru_out, uint64_t* __restrict__ stats, uint32_t* __restrict__ err)
+    uint32_t* __restrict__ lru_out, uint64_t* __restrict__ stats, uint32_t* __restrict__ aborted,
+    uint32_t* __restrict__ sflag, uint32_t* __restrict__ err)
 {
     const uint32_t lane = lane_id();
-    const uint64_t item = (uint64_t)blockIdx.x * (kReplayThreads / 64) + wave_in_block();
+    const uint64_t wid = (uint64_t)blockIdx.x * (kReplayThreads / 64) + wave_in_block();
     const uint32_t ncd = P * R;
-    if (item >= item_off[ncd]) return;
-    uint32_t lo = 0, hi = ncd;
-    while (hi - lo > 1) {
-        const uint32_t mid = (lo + hi) >> 1;
-        if (item_off[mid] <= item) lo = mid;
-        else hi = mid;
+    uint32_t lo = 0;
+    uint64_t item = 0;
+    if constexpr (kSeq) {
+        if (wid >= ncd) return;
+        lo = (uint32_t)wid;
+        if (sflag[lo] == 0) return;
+    } else {
+        item = wid;
+        if (item >= item_off[ncd]) return;
+        uint32_t hi = ncd;
+        while (hi - lo > 1) {
+            const uint32_t mid = (lo + hi) >> 1;
+            if (item_off[mid] <= item) lo = mid;
+            else hi = mid;
+        }
     }
     const uint32_t c = lo / R, d = lo % R;
     const uint32_t W = wa.W[c];
     if (slot_class(W) != (uint32_t)SL) return;
-    const uint32_t seg = (uint32_t)(item - item_off[lo]);
     const uint32_t* go = grp_off + (uint64_t)c * (R + 1u);
     const uint32_t gs = go[d], cnt = go[d + 1] - gs;
     const uint32_t S = seg_len(W, wa.seg_min);
-    const uint64_t s0w = (uint64_t)seg * S;
-    if (s0w > cnt) return;  // only if the partition used other slot counts
-    const uint32_t s0 = (uint32_t)s0w;
-    const uint32_t s1 = cnt - s0 < S ? cnt : s0 + S;
+    uint32_t s0 = 0, s1 = cnt;
+    if constexpr (!kSeq) {
+        const uint64_t s0w = (item - item_off[lo]) * (uint64_t)S;
+        if (s0w > cnt) return;  // only if the partition used other slot counts
+        s0 = (uint32_t)s0w;
+        s1 = cnt - s0 < S ? cnt : s0 + S;
+    }
     const uint64_t* __restrict__ rl = rec + (uint64_t)c * n + gs;
 
-    // Slot q of the rebuilt state (q = 64 s + lane) is the q-th most recent key, which is
-    // already the move-to-front order.
+    // Slot q of the rebuilt state is the q-th most recent key, which is already the
+    // move-to-front order.
     uint32_t skey[SL];
     uint64_t vm[SL];  // lanes of register s whose position is < W
 #pragma unroll
@@ -950,17 +976,27 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
         vm[s] = nl >= 64u ? ~0ull : (1ull << nl) - 1ull;
     }
     const uint64_t wmask = vm[0];
-    // State before the segment: the most recent W distinct keys, newest first. Records are
-    // read backwards 64 at a time, the next (older) batch in flight while one is scanned.
     uint32_t q = 0;
-    {
-        uint32_t pos = s0;
+    if constexpr (!kSeq) {
+        // State before the segment: the most recent W distinct keys, newest first. Records
+        // are read backwards 64 at a time, the next (older) batch in flight while one is
+        // scanned.
+        uint32_t pos = s0, scanned = 0;
+        const uint32_t budget = kRebuildBudget * S;
         uint32_t nb = pos < 64u ? pos : 64u;
         uint32_t kl_next = lane < nb ? (uint32_t)rl[pos - nb + lane] : CR_EMPTY_SLOT;
         while (q < W && pos > 0) {
+            if (scanned >= budget) {  // too few distinct keys: left to the stream's kSeq pass
+                if (lane == 0) {
+                    atomicOr(&aborted[item >> 5], 1u << (item & 31u));
+                    atomicOr(&sflag[lo], 1u);
+                }
+                return;
+            }
             const uint32_t kl = kl_next;
             const uint32_t cnb = nb;
             pos -= cnb;
+            scanned += cnb;
             nb = pos < 64u ? pos : 64u;
             kl_next = lane < nb ? (uint32_t)rl[pos - nb + lane] : CR_EMPTY_SLOT;
             if (cnb == 64u && ballot(kl < K) == ~0ull) {
@@ -1003,7 +1039,7 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
     }
 
     // Per-lane sums for the current interval; flushed (one atomic per statistic) when the
-    // interval changes and at the end of the segment.
+    // interval changes and at the end of a range.
     uint64_t a_req = 0, a_hit = 0, a_pre = 0, a_hp = 0;
     uint32_t cur = 0xFFFFFFFFu;
     bool bad = false;
@@ -1020,79 +1056,94 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
         }
         a_req = a_hit = a_pre = a_hp = 0;
     };
-    // Forward replay; the next batch of records is in flight while one is replayed. Lane t
-    // of `hitf` records whether record t of the batch hit.
-    uint64_t rv_next = s0 + lane < s1 ? rl[s0 + lane] : 0ull;
-    for (uint32_t b0 = s0; b0 < s1; b0 += 64) {
-        const uint32_t nb = s1 - b0 < 64u ? s1 - b0 : 64u;
-        const uint64_t rv = rv_next;
-        rv_next = b0 + 64u + lane < s1 ? rl[b0 + 64u + lane] : 0ull;
-        const uint32_t kl = lane < nb ? (uint32_t)rv : CR_EMPTY_SLOT;
-        const bool vl = lane < nb && kl < K;
-        bad |= lane < nb && kl >= K;
-        const uint32_t pl = vl ? prefix_len[kl] : 0u;  // consumed after the batch
-        bool hl;
-        if constexpr (SL == 1) {
-            uint32_t depth = 0xFFFFFFFFu;  // lane t: hit depth of record t
-            if (ballot(vl) == ~0ull) {
-                depth = W == 64u ? mtf_batch<false>(skey[0], rl + b0, wmask) : mtf_batch<true>(skey[0], rl + b0, wmask);
-            } else {
-                for (uint32_t t = 0; t < nb; ++t) {
-                    const uint32_t kk = rdlane(kl, t);
-                    if (kk < K) depth = wrlane(depth, mtf_step(skey[0], kk, wmask), t);
+    // Forward replay of records [r0, r1); the next batch of records is in flight while one
+    // is replayed. With `on` false the list advances but nothing is counted.
+    auto run = [&](uint32_t r0, uint32_t r1, bool on) {
+        uint64_t rv_next = r0 + lane < r1 ? rl[r0 + lane] : 0ull;
+        for (uint32_t b0 = r0; b0 < r1; b0 += 64) {
+            const uint32_t nb = r1 - b0 < 64u ? r1 - b0 : 64u;
+            const uint64_t rv = rv_next;
+            rv_next = b0 + 64u + lane < r1 ? rl[b0 + 64u + lane] : 0ull;
+            const uint32_t kl = lane < nb ? (uint32_t)rv : CR_EMPTY_SLOT;
+            const bool vl = lane < nb && kl < K;
+            bad |= lane < nb && kl >= K;
+            const uint32_t pl = vl && on ? prefix_len[kl] : 0u;  // consumed after the batch
+            bool hl;
+            if constexpr (SL == 1) {
+                uint32_t depth = 0xFFFFFFFFu;  // lane t: hit depth of record t
+                if (ballot(vl) == ~0ull) {
+                    depth = W == 64u ? mtf_batch<false>(skey[0], rl + b0, wmask)
+                                     : mtf_batch<true>(skey[0], rl + b0, wmask);
+                } else {
+                    for (uint32_t t = 0; t < nb; ++t) {
+                        const uint32_t kk = rdlane(kl, t);
+                        if (kk < K) depth = wrlane(depth, mtf_step(skey[0], kk, wmask), t);
+                    }
                 }
-            }
-            hl = depth != 0xFFFFFFFFu;
-        } else if constexpr (kTwo) {
-            uint32_t hit = 0;  // lane t: 1 if record t hit
-            if (ballot(vl) == ~0ull) {
-                hit = W == 64u * SL ? mtf_batch_two<SL, false>(skey, rl + b0, vm, lane)
-                                    : mtf_batch_two<SL, true>(skey, rl + b0, vm, lane);
-            } else {
-                for (uint32_t t = 0; t < nb; ++t) {
-                    const uint32_t kk = rdlane(kl, t);
-                    if (kk >= K) continue;
-                    const uint64_t m = ballot(skey[0] == kk);
-                    const uint32_t ev = rdlane(skey[0], 63u);
-                    mtf_core(skey[0], m);
-                    skey[0] = wrlane(skey[0], kk, 0u);
-                    if (m || back_step<SL, true>(skey, kk, ev, vm)) hit = wrlane(hit, 1u, t);
+                hl = depth != 0xFFFFFFFFu;
+            } else if constexpr (kTwo) {
+                uint32_t hit = 0;  // lane t: 1 if record t hit
+                if (ballot(vl) == ~0ull) {
+                    hit = W == 64u * SL ? mtf_batch_two<SL, false>(skey, rl + b0, vm, lane)
+                                        : mtf_batch_two<SL, true>(skey, rl + b0, vm, lane);
+                } else {
+                    for (uint32_t t = 0; t < nb; ++t) {
+                        const uint32_t kk = rdlane(kl, t);
+                        if (kk >= K) continue;
+                        const uint64_t m = ballot(skey[0] == kk);
+                        const uint32_t ev = rdlane(skey[0], 63u);
+                        mtf_core(skey[0], m);
+                        skey[0] = wrlane(skey[0], kk, 0u);
+                        if (m || back_step<SL, true>(skey, kk, ev, vm)) hit = wrlane(hit, 1u, t);
+                    }
                 }
-            }
-            hl = hit != 0u;
-        } else {
-            uint32_t depth = 0xFFFFFFFFu;  // lane t: hit lane of record t
-            if (ballot(vl) == ~0ull) {
-                depth = W == 64u * SL ? mtf_batch_il<SL, false>(skey, rl + b0, vm)
-                                      : mtf_batch_il<SL, true>(skey, rl + b0, vm);
+                hl = hit != 0u;
             } else {
-                for (uint32_t t = 0; t < nb; ++t) {
-                    const uint32_t kk = rdlane(kl, t);
-                    if (kk < K) depth = wrlane(depth, mtf_step_il<SL, true>(skey, kk, vm), t);
+                uint32_t depth = 0xFFFFFFFFu;  // lane t: hit lane of record t
+                if (ballot(vl) == ~0ull) {
+                    depth = W == 64u * SL ? mtf_batch_il<SL, false>(skey, rl + b0, vm)
+                                          : mtf_batch_il<SL, true>(skey, rl + b0, vm);
+                } else {
+                    for (uint32_t t = 0; t < nb; ++t) {
+                        const uint32_t kk = rdlane(kl, t);
+                        if (kk < K) depth = wrlane(depth, mtf_step_il<SL, true>(skey, kk, vm), t);
+                    }
                 }
+                hl = depth != 0xFFFFFFFFu;
             }
-            hl = depth != 0xFFFFFFFFu;
+            if (!on) continue;
+            const uint32_t sfx = (uint32_t)(rv >> 32) & 0xFFFFu;
+            const uint32_t ivl = (uint32_t)(rv >> 48);
+            uint64_t rem = ballot(vl);
+            while (rem) {
+                const uint32_t iv = rdlane(ivl, first_lane(rem));
+                if (iv != cur) {
+                    flush();
+                    cur = iv;
+                }
+                const uint64_t sel = rem & ballot(ivl == iv);
+                if ((sel >> lane) & 1ull) {
+                    a_req += 1;
+                    a_hit += hl ? 1u : 0u;
+                    a_pre += sfx + (hl ? 0u : pl);
+                    a_hp += hl ? pl : 0u;
+                }
+                rem &= ~sel;
+            }
         }
-        const uint32_t sfx = (uint32_t)(rv >> 32) & 0xFFFFu;
-        const uint32_t ivl = (uint32_t)(rv >> 48);
-        uint64_t rem = ballot(vl);
-        while (rem) {
-            const uint32_t iv = rdlane(ivl, first_lane(rem));
-            if (iv != cur) {
-                flush();
-                cur = iv;
-            }
-            const uint64_t sel = rem & ballot(ivl == iv);
-            if ((sel >> lane) & 1ull) {
-                a_req += 1;
-                a_hit += hl ? 1u : 0u;
-                a_pre += sfx + (hl ? 0u : pl);
-                a_hp += hl ? pl : 0u;
-            }
-            rem &= ~sel;
+        flush();
+    };
+    if constexpr (kSeq) {
+        // every segment of the stream in order, counting the ones their work items left
+        const uint64_t i0 = item_off[lo];
+        for (uint32_t a = 0, k = 0; a < cnt; a += S, ++k) {
+            const uint64_t it = i0 + k;
+            const bool on = (aborted[it >> 5] >> (it & 31u)) & 1u;
+            run(a, cnt - a < S ? cnt : a + S, on);
         }
+    } else {
+        run(s0, s1, true);
     }
-    flush();
     if (ballot(bad) && lane == 0) atomicOr(err, CR_ERR_KEY_RANGE);
     if (s1 == cnt) {
         uint32_t* __restrict__ lo_ = lru_out + ((uint64_t)c * R + d) * max_W;
@@ -1105,14 +1156,26 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
     }
 }
 
+__global__ void k_zero_u32(uint32_t* __restrict__ p, uint64_t n)
+{
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = 0u;
+}
+
 struct ReplayWs {
     uint64_t* rec;
     uint32_t* tcnt;
     uint32_t* dtot;
     uint32_t* grp_off;
     uint32_t* item_off;
+    uint32_t* aborted;  // bit per work item: its rebuild ran out of budget
+    uint32_t* sflag;    // per (candidate, destination): some segment of the stream did
+    uint64_t flag_words;
     size_t bytes;
 };
+
+// Upper bound on replay work items: one per (c, d) plus one per full shortest segment.
+inline uint64_t max_items(uint64_t n, uint32_t P, uint32_t R) { return (uint64_t)P * R + (uint64_t)P * n / kSegFloor + 1u; }
 
 inline ReplayWs replay_layout(void* base, uint64_t n, uint32_t P, uint32_t R)
 {
@@ -1131,6 +1194,10 @@ inline ReplayWs replay_layout(void* base, uint64_t n, uint32_t P, uint32_t R)
     o = up(o + (uint64_t)P * (R + 1u) * 4u);
     w.item_off = reinterpret_cast<uint32_t*>(b + o);
     o = up(o + ((uint64_t)P * R + 1u) * 4u);
+    w.aborted = reinterpret_cast<uint32_t*>(b + o);
+    w.flag_words = (max_items(n, P, R) + 31u) / 32u + (uint64_t)P * R;  // aborted bits, then sflag
+    w.sflag = w.aborted + (max_items(n, P, R) + 31u) / 32u;
+    o = up(o + w.flag_words * 4u);
     w.bytes = (size_t)o + 256u;
     return w;
 }
@@ -1264,18 +1331,25 @@ extern "C" cr_status cr_replay_lru(const uint32_t* prefix_len, uint32_t num_keys
         return CR_EINVAL;
     const ReplayWs w = replay_layout(ws_base(ws), n, P, R);
     const hipStream_t st = as_stream(stream);
-    // Upper bound on work items: one per (c, d) plus one per full segment.
-    const uint64_t items = (uint64_t)P * R + (uint64_t)P * n / kSegFloor + 1u;
+    const uint64_t items = max_items(n, P, R);
     const uint64_t blocks = (items + (kReplayThreads / 64) - 1) / (kReplayThreads / 64);
+    const uint64_t sblocks = ((uint64_t)P * R + (kReplayThreads / 64) - 1) / (kReplayThreads / 64);
     if (blocks > 0x7FFFFFFFull) return CR_EINVAL;
     (void)hipGetLastError();
-#define CR_REPLAY(SL, TWO)                                                                                          \
-    hipLaunchKernelGGL((k_replay<SL, TWO>), dim3((uint32_t)blocks), dim3(kReplayThreads), 0, st, w.rec, n, w.grp_off, \
-                       w.item_off, P, R, num_keys, J, prefix_len, ra.wa, max_W, lru_in, lru_out, stats, err)
-    if (ra.classes & 1u) CR_REPLAY(1, false);
-    if (ra.classes & 2u) CR_REPLAY(2, false);
-    if (ra.classes & 4u) CR_REPLAY(4, false);  // two-level measured slower with three back registers
-    if (ra.classes & 8u) CR_REPLAY(8, true);
+    hipLaunchKernelGGL(k_zero_u32, dim3(256), dim3(256), 0, st, w.aborted, w.flag_words);
+#define CR_REPLAY(SL, TWO, SEQ, NB)                                                                                 \
+    hipLaunchKernelGGL((k_replay<SL, TWO, SEQ>), dim3((uint32_t)(NB)), dim3(kReplayThreads), 0, st, w.rec, n,        \
+                       w.grp_off, w.item_off, P, R, num_keys, J, prefix_len, ra.wa, max_W, lru_in, lru_out, stats,    \
+                       w.aborted, w.sflag, err)
+    // two-level lists only for the largest class: measured slower with three back registers
+    if (ra.classes & 1u) CR_REPLAY(1, false, false, blocks);
+    if (ra.classes & 2u) CR_REPLAY(2, false, false, blocks);
+    if (ra.classes & 4u) CR_REPLAY(4, false, false, blocks);
+    if (ra.classes & 8u) CR_REPLAY(8, true, false, blocks);
+    if (ra.classes & 1u) CR_REPLAY(1, false, true, sblocks);
+    if (ra.classes & 2u) CR_REPLAY(2, false, true, sblocks);
+    if (ra.classes & 4u) CR_REPLAY(4, false, true, sblocks);
+    if (ra.classes & 8u) CR_REPLAY(8, true, true, sblocks);
 #undef CR_REPLAY
     return hipGetLastError() == hipSuccess ? CR_OK : CR_EHIP;
 }
