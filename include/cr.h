@@ -108,20 +108,28 @@ typedef struct {
  *   route      u32 [NP][C_max]           by key rank: CR_ROUTE_SINGLE | dest (k = 1)
  *                                        or the admission index a (k > 1)
  *
- * Optional group dispatch tables (all three NULL = per-plan tables only). When every
+ * Optional group dispatch tables (all four NULL = per-plan tables only). When every
  * candidate of a group is built from the same counting window, a candidate admits a prefix
  * of that window's order, so cr_route can serve all candidates of a request from one row:
  * with these buffers present, cr_route first rebuilds them from the built plans and then
- * reads, per request, one position, one row of CS destinations and one P2C bit word
- * (CS = cands rounded up to a multiple of 8, PW = ceil(cands / 64)):
+ * reads, per request, one position, one row of CS destinations and the load-rank rows of
+ * the request's two fallback draws (CS = cands rounded up to a multiple of 8):
  *   window_rank u32 [num_windows][num_keys]  position of each key in its window's order
  *                                             (0xFFFFFFFF when absent)
  *   group_dest  u16 [NG][C_max][CS]          by position a: the member of candidate c when it
  *                                             admits the key with k = 1, CR_GROUP_MULTI when
  *                                             k > 1, CR_GROUP_COLD when it does not admit it
- *   group_p2c   u64 [NG][R][R][PW]           bit c of pair (d1, d2): L_c[d2] < L_c[d1]
+ *   group_rank  u16 [NG][R][CS]              by destination d: entry c = number of
+ *                                             destinations whose L_c is strictly below L_c[d]
+ *                                             (so L_c[d2] < L_c[d1] iff rank c of d2 < rank
+ *                                             c of d1)
+ *   group_multi u32 [NG][C_max][CS]          where group_dest holds CR_GROUP_MULTI:
+ *                                             o | k << 20 with members[o .. o+k) the key's
+ *                                             member list in candidate c (else unspecified)
  * A group whose candidates name different windows sets CR_ERR_SPEC, and its destinations
- * are then unspecified. group_dest must be 16-byte aligned. Sizes: cr_plan_sizes. */
+ * are then unspecified. group_dest, group_rank and group_multi must be 16-byte aligned, and
+ * window_rank, group_multi and the members of all plans must each stay below 4 GiB
+ * (CR_EINVAL otherwise). Sizes: cr_plan_sizes. */
 #define CR_GROUP_MULTI 0xFFFEu
 #define CR_GROUP_COLD 0xFFFFu
 typedef struct {
@@ -145,7 +153,8 @@ typedef struct {
     uint32_t* route;
     uint32_t* window_rank;  /* optional group dispatch tables (see above), or NULL      */
     uint16_t* group_dest;
-    uint64_t* group_p2c;
+    uint16_t* group_rank;
+    uint32_t* group_multi;
 } cr_plan_set;
 
 /* Rates of one slice of the log, accumulated (Algorithm 1 input "rates"; Appendix A.2):
@@ -173,9 +182,10 @@ size_t cr_admit_workspace_bytes(uint32_t num_windows, uint32_t R, uint32_t max_W
 
 /* Byte sizes of the buffers of a cr_plan_set with these fields, in struct order: specs, order,
  * order_count, n_order, num_admitted, cold, clamped, member_off, members, load, key_index,
- * route, window_rank, group_dest, group_p2c (the last three: the optional group tables).
+ * route, window_rank, group_dest, group_rank, group_multi (the last four: the optional group
+ * tables).
  * out_bytes has CR_PLAN_BUFFERS entries. */
-#define CR_PLAN_BUFFERS 15
+#define CR_PLAN_BUFFERS 16
 void cr_plan_sizes(uint32_t num_plans, uint32_t cands, uint32_t R, uint32_t max_W, uint32_t num_keys,
                    uint32_t num_windows, size_t out_bytes[CR_PLAN_BUFFERS]);
 

@@ -30,7 +30,7 @@ EXPORTS = ("cr_count_rates", "cr_count_slice_workspace_bytes", "cr_count_slice",
            "cr_keymap_lookup", "cr_keymap_scatter", "cr_replay_workspace_bytes", "cr_lru_state_bytes",
            "cr_lru_reset", "cr_replay", "cr_replay_partition", "cr_replay_lru", "cr_version")
 CR_WINDOW_SUM = 0xFFFFFFFFFFFFFFFF
-CR_PLAN_BUFFERS = 15
+CR_PLAN_BUFFERS = 16
 CR_GROUP_MULTI, CR_GROUP_COLD = 0xFFFE, 0xFFFF
 
 _u32, _u64, _P = ctypes.c_uint32, ctypes.c_uint64, ctypes.c_void_p
@@ -51,7 +51,7 @@ class CrPlanSet(ctypes.Structure):
                 ("num_windows", _u32), ("specs", _P), ("order", _P), ("order_count", _P), ("n_order", _P),
                 ("num_admitted", _P), ("cold", _P), ("clamped", _P), ("member_off", _P), ("members", _P),
                 ("load", _P), ("key_index", _P), ("route", _P), ("window_rank", _P), ("group_dest", _P),
-                ("group_p2c", _P)]
+                ("group_rank", _P), ("group_multi", _P)]
 
 
 class CrError(RuntimeError):
@@ -301,17 +301,19 @@ class PlanSet:
         self.load = torch.empty((NP, R), dtype=torch.float64, device=device)
         self.key_index = torch.empty((NP, (num_keys + 63) // 64, 2), dtype=torch.int64, device=device)
         self.route = torch.empty((NP, cmax), **i32)
-        self.window_rank = self.group_dest = self.group_p2c = None
+        self.window_rank = self.group_dest = self.group_rank = self.group_multi = None
         if group_tables:
             NG = NP // cands
             self.window_rank = torch.empty((NW, num_keys), **i32)
             self.group_dest = torch.empty((NG, cmax, group_row(cands)), dtype=torch.int16, device=device)
-            self.group_p2c = torch.empty((NG, R, R, (cands + 63) // 64), dtype=torch.int64, device=device)
+            self.group_rank = torch.empty((NG, R, group_row(cands)), dtype=torch.int16, device=device)
+            self.group_multi = torch.empty((NG, cmax, group_row(cands)), **i32)
         self.c = CrPlanSet(NP, cands, R, max_W, num_keys, NW, _ptr(self.specs), _ptr(self.order),
                            _ptr(self.order_count), _ptr(self.n_order),
                            _ptr(self.num_admitted), _ptr(self.cold), _ptr(self.clamped), _ptr(self.member_off),
                            _ptr(self.members), _ptr(self.load), _ptr(self.key_index), _ptr(self.route),
-                           _ptr(self.window_rank), _ptr(self.group_dest), _ptr(self.group_p2c))
+                           _ptr(self.window_rank), _ptr(self.group_dest), _ptr(self.group_rank),
+                           _ptr(self.group_multi))
 
 
 def group_row(cands: int) -> int:
@@ -320,6 +322,6 @@ def group_row(cands: int) -> int:
 
 
 def group_table_bytes(NG: int, cands: int, R: int, max_W: int, num_keys: int, num_windows: int) -> int:
-    """Bytes of the three group dispatch tables."""
-    return (num_windows * num_keys * 4 + NG * R * max_W * group_row(cands) * 2
-            + NG * R * R * ((cands + 63) // 64) * 8)
+    """Bytes of the four group dispatch tables."""
+    return (num_windows * num_keys * 4 + NG * R * max_W * group_row(cands) * 6
+            + NG * R * group_row(cands) * 2)

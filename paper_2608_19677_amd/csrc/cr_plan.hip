@@ -1670,12 +1670,12 @@ extern "C" void cr_plan_sizes(uint32_t num_plans, uint32_t cands, uint32_t R, ui
 {
     if (!out_bytes) return;
     const uint64_t NP = num_plans, NW = num_windows, cmax = (uint64_t)R * max_W;
-    const uint64_t NG = cands ? NP / cands : 0, CS = ((uint64_t)cands + 7) / 8 * 8, PW = ((uint64_t)cands + 63) / 64;
+    const uint64_t NG = cands ? NP / cands : 0, CS = ((uint64_t)cands + 7) / 8 * 8;
     const uint64_t KW = ((uint64_t)num_keys + 63) / 64;
     const uint64_t b[CR_PLAN_BUFFERS] = {
         NP * sizeof(cr_plan_spec), NW * cmax * 4, NW * cmax * 4, NW * 4, NP * 4, NP * 8, NP * 4,
         NP * (cmax + 1) * 4, NP * cmax * 2, NP * R * 8, NP * KW * 16, NP * cmax * 4,
-        NW * num_keys * 4, NG * cmax * CS * 2, NG * R * R * PW * 8};
+        NW * num_keys * 4, NG * cmax * CS * 2, NG * R * CS * 2, NG * cmax * CS * 4};
     for (int i = 0; i < CR_PLAN_BUFFERS; ++i) out_bytes[i] = (size_t)b[i];
 }
 

@@ -150,9 +150,10 @@ __global__ __launch_bounds__(kRouteThreads) void k_route(
 // ---------------------------------------------------------------------------------------
 // Group dispatch tables. Candidates of one group built from the same window admit prefixes
 // of that window's order, so one row per order position holds every candidate's dispatch of
-// a key, and one bit word per destination pair holds every candidate's power-of-two-choices
-// outcome. A request then reads its key's position, one row of CS u16 entries and one P2C
-// word instead of a handful of gathers per candidate into per-plan tables.
+// a key, and one row per destination holds every candidate's load rank, which decides the
+// power-of-two-choices fallback. A request then reads its key's position, one row of CS
+// u16 entries and the rank rows of its two draws (a table of R x CS u16 that stays in
+// cache) instead of a handful of gathers per candidate into per-plan tables.
 // ---------------------------------------------------------------------------------------
 constexpr uint32_t kGrpRows = 64;      // order positions per k_group_dest block
 constexpr uint32_t kGrpThreads = 256;
@@ -181,7 +182,8 @@ __global__ __launch_bounds__(kGrpThreads) void k_group_dest(uint32_t cands, uint
                                                             const uint32_t* __restrict__ num_admitted,
                                                             const uint32_t* __restrict__ member_off,
                                                             const uint16_t* __restrict__ members,
-                                                            uint16_t* __restrict__ gdest, uint32_t* __restrict__ err)
+                                                            uint16_t* __restrict__ gdest, uint32_t* __restrict__ gmulti,
+                                                            uint32_t* __restrict__ err)
 {
     __shared__ uint16_t tile[kGrpRows * (CR_MAX_CANDS + 8)];
     const uint32_t g = blockIdx.y, a0 = blockIdx.x * kGrpRows;
@@ -197,6 +199,7 @@ __global__ __launch_bounds__(kGrpThreads) void k_group_dest(uint32_t cands, uint
                 const uint32_t* __restrict__ mo = member_off + p * (cmax + 1u);
                 const uint32_t o = mo[a], k = mo[a + 1] - o;
                 e = k == 1 ? members[p * cmax + o] : (uint16_t)CR_GROUP_MULTI;
+                if (k != 1) gmulti[((uint64_t)g * cmax + a) * CS + c] = o | (k << 20);
             }
         }
         tile[row * CS + c] = e;
@@ -217,52 +220,105 @@ __global__ __launch_bounds__(kGrpThreads) void k_group_dest(uint32_t cands, uint
     }
 }
 
-// Pair words of group g, first draw d1: bit c of word (d1, d2) = L_c[d2] < L_c[d1].
-__global__ __launch_bounds__(256) void k_group_p2c(uint32_t R, uint32_t cands, uint32_t PW,
-                                                   const double* __restrict__ load, uint64_t* __restrict__ gp2c)
+// Load ranks of group g: entry c of row d = #{d' : L_c[d'] < L_c[d]}, so that
+// L_c[d2] < L_c[d1] exactly when rank_c[d2] < rank_c[d1] (equal loads share a rank).
+// One block per (candidate slot, group); slots past cands get 0 and are never used.
+__global__ __launch_bounds__(256) void k_group_rank(uint32_t R, uint32_t cands, uint32_t CS,
+                                                    const double* __restrict__ load, uint16_t* __restrict__ grank)
 {
-    __shared__ double s_l1[CR_MAX_CANDS];
-    const uint32_t d1 = blockIdx.x, g = blockIdx.y;
-    for (uint32_t c = threadIdx.x; c < cands; c += blockDim.x) s_l1[c] = load[((uint64_t)g * cands + c) * R + d1];
+    __shared__ double s_l[CR_MAX_R];
+    const uint32_t c = blockIdx.x, g = blockIdx.y;
+    uint16_t* __restrict__ out = grank + (uint64_t)g * R * CS + c;
+    if (c >= cands) {
+        for (uint32_t d = threadIdx.x; d < R; d += blockDim.x) out[(uint64_t)d * CS] = 0;
+        return;
+    }
+    const double* __restrict__ l = load + ((uint64_t)g * cands + c) * R;
+    for (uint32_t d = threadIdx.x; d < R; d += blockDim.x) s_l[d] = l[d];
     __syncthreads();
-    for (uint32_t d2 = threadIdx.x; d2 < R; d2 += blockDim.x) {
-        for (uint32_t wd = 0; wd < PW; ++wd) {
-            uint64_t word = 0;
-            const uint32_t ce = cands - wd * 64u < 64u ? cands - wd * 64u : 64u;
-            for (uint32_t u = 0; u < ce; ++u) {
-                const uint32_t c = wd * 64u + u;
-                word |= (uint64_t)(load[((uint64_t)g * cands + c) * R + d2] < s_l1[c]) << u;
-            }
-            gp2c[(((uint64_t)g * R + d1) * R + d2) * PW + wd] = word;
-        }
+    for (uint32_t d = threadIdx.x; d < R; d += blockDim.x) {
+        const double x = s_l[d];
+        uint32_t r = 0;
+        for (uint32_t e = 0; e < R; ++e) r += s_l[e] < x ? 1u : 0u;  // same address across lanes: broadcast
+        out[(uint64_t)d * CS] = (uint16_t)r;
     }
 }
 
+// Requests per k_route_group block: the destination tile holds CS x T entries in LDS
+// (kGrpTileWords 32-bit words at most); T is a multiple of 64 in 64 .. 1024.
+constexpr uint32_t kGrpTileWords = 8192;
+
+__host__ __device__ __forceinline__ uint32_t group_tile(uint32_t CS)
+{
+    const uint32_t t = (2u * kGrpTileWords / CS) & ~63u;
+    return t > 1024u ? 1024u : (t < 64u ? 64u : t);
+}
+
+// Row stride of the LDS tile in 32-bit words: T/2 + 2 puts the eight candidate rows that a
+// wavefront's lanes write at once 16 banks apart.
+__host__ __device__ __forceinline__ uint32_t group_tile_stride(uint32_t T) { return T / 2u + 2u; }
+
+__host__ __device__ __forceinline__ size_t group_route_lds(uint32_t CS)
+{
+    const uint32_t T = group_tile(CS);
+    return ((size_t)CS * group_tile_stride(T) + (size_t)T * 4u) * 4u;
+}
+
+// Load of a T at a 32-bit byte offset from a kernel-argument base (every group table is
+// below 4 GiB), so the address is a scalar base plus one 32-bit register.
+template <typename V, typename B>
+__device__ __forceinline__ V ld_at(const B* base, uint32_t byte_off)
+{
+    return *reinterpret_cast<const V*>(reinterpret_cast<const char*>(base) + byte_off);
+}
+
+__device__ __forceinline__ uint32_t u4_at(const uint4& v, int i)
+{
+    return i == 0 ? v.x : (i == 1 ? v.y : (i == 2 ? v.z : v.w));
+}
+
 // Dispatch of every candidate of the request's plan group from the group tables; results
-// equal k_route's. Each thread owns 4 consecutive requests; per 8 candidates it reads one
-// 16-byte piece of each request's row and writes one 8-byte store per candidate.
-template <bool kVec, int kPW>
+// equal k_route's. A block takes T consecutive requests in three phases:
+//  1. per request: key, plan group, window position a, hash and both fallback draws into LDS;
+//  2. one task per (4 consecutive requests, 8-candidate piece): the requests' 16-byte row
+//     pieces (consecutive lanes read consecutive pieces of a row, so a row is one 128-byte
+//     line per 8 lanes) and the 16-byte load-rank pieces of their draws, resolved to
+//     destinations (a key with k > 1: its member list from the multi table, then the member
+//     the request hash picks) and written to an LDS tile [candidate][request pair];
+//  3. each candidate's T destinations leave as one contiguous run of 32-bit stores, marked
+//     non-temporal so that they do not push the tables out of the L2.
+// Gathers are issued unconditionally (clamped indices, results selected afterwards) so that
+// a lane keeps all of them in flight together.
+template <bool kVec>
 __global__ __launch_bounds__(kRouteThreads) void k_route_group(
     const uint32_t* __restrict__ keys, uint64_t n, uint64_t first_index, uint32_t smix,
     const uint64_t* __restrict__ off, const uint32_t* __restrict__ gmap, uint32_t J, uint32_t K, uint32_t R,
-    uint32_t cands, uint32_t CS, uint32_t PW, uint32_t NG, uint32_t NW, uint32_t cmax,
-    const cr_plan_spec* __restrict__ specs, const uint32_t* __restrict__ wrank, const uint16_t* __restrict__ gdest,
-    const uint64_t* __restrict__ gp2c, const uint32_t* __restrict__ member_off, const uint16_t* __restrict__ members,
-    uint16_t* __restrict__ dest, uint32_t* __restrict__ err)
+    uint32_t cands, uint32_t CS, uint32_t NG, uint32_t NW, uint32_t cmax, const cr_plan_spec* __restrict__ specs,
+    const uint32_t* __restrict__ wrank, const uint16_t* __restrict__ gdest, const uint16_t* __restrict__ grank,
+    const uint32_t* __restrict__ gmulti, const uint16_t* __restrict__ members, uint16_t* __restrict__ dest,
+    uint32_t* __restrict__ err)
 {
+    extern __shared__ __align__(16) uint32_t s_dyn[];
     __shared__ uint32_t s_j0;
     __shared__ uint32_t s_rel[kBnd];
     __shared__ uint32_t s_g[kBnd + 1];
     __shared__ uint32_t s_w[kBnd + 1];
-    const uint64_t bstart = (uint64_t)xcd_tile(blockIdx.x, gridDim.x) * kBlockReq;
+    const uint32_t T = group_tile(CS), TS2 = group_tile_stride(T), NP = CS / 8u;
+    uint32_t* __restrict__ m_a = s_dyn;                 // window position, 0xFFFFFFFF = none
+    uint32_t* __restrict__ m_d = m_a + T;               // d1 | d2 << 16
+    uint32_t* __restrict__ m_g = m_d + T;               // plan group
+    uint32_t* __restrict__ m_h = m_g + T;               // request hash
+    uint32_t* __restrict__ tile = m_h + T;              // [CS][TS2]: destinations of requests 2i, 2i+1
+    const uint64_t bstart = (uint64_t)xcd_tile(blockIdx.x, gridDim.x) * T;
     if (bstart >= n) return;
+    const uint32_t nb = n - bstart < T ? (uint32_t)(n - bstart) : T;
     if (threadIdx.x < 64) {
         const uint32_t j0 = find_interval(off, J, bstart);
         if (threadIdx.x == 0) s_j0 = j0;
         if (threadIdx.x < kBnd) {
             const uint32_t jb = j0 + 1 + threadIdx.x;
             const uint64_t e = jb < J ? off[jb] : ~0ull;
-            s_rel[threadIdx.x] = e - bstart < kBlockReq ? (uint32_t)(e - bstart) : kBlockReq;
+            s_rel[threadIdx.x] = e - bstart < T ? (uint32_t)(e - bstart) : T;
         }
         if (threadIdx.x <= kBnd) {
             const uint32_t jj = j0 + threadIdx.x < J ? j0 + threadIdx.x : J - 1;
@@ -273,92 +329,129 @@ __global__ __launch_bounds__(kRouteThreads) void k_route_group(
         }
     }
     __syncthreads();
-    const uint32_t rel0 = threadIdx.x * kPer;
-    const uint64_t base = bstart + rel0;
-    if (base >= n) return;
-    const bool full = kVec && base + kPer <= n;
-    uint32_t b[kPer];
-    if (full) {
-        const uint4 q = *reinterpret_cast<const uint4*>(keys + base);
-        b[0] = q.x, b[1] = q.y, b[2] = q.z, b[3] = q.w;
-    } else {
-#pragma unroll
-        for (int t = 0; t < kPer; ++t) b[t] = base + t < n ? keys[base + t] : 0u;
-    }
+    // phase 1: up to four requests per thread, keys first, then positions
     const uint32_t j0 = s_j0;
     const uint32_t r0 = s_rel[0], r1 = s_rel[1], r2 = s_rel[2], r3 = s_rel[3];
-    const uint64_t gi0 = first_index + base;
-    const uint32_t inner0 = fmix32((uint32_t)(gi0 >> 32) ^ smix);
-    uint32_t g[kPer], h[kPer], d1[kPer], d2[kPer], a[kPer];
-    uint64_t pw[kPer][kPW];
     bool bad = false;
+    {
+        constexpr int kP1 = 1024 / kRouteThreads;
+        uint32_t b[kP1], w[kP1], g[kP1];
 #pragma unroll
-    for (int t = 0; t < kPer; ++t) {
-        const uint32_t rel = rel0 + t;
-        const uint32_t q = (rel >= r0) + (rel >= r1) + (rel >= r2) + (rel >= r3);
-        uint32_t w;
-        if (rel >= r3 && r3 < kBlockReq) {  // more than kBnd boundaries in this block
-            uint32_t j = j0 + kBnd;
-            while (j + 1 < J && off[j + 1] <= base + t) ++j;
-            g[t] = gmap[j] < NG ? gmap[j] : NG - 1;
-            w = specs[(uint64_t)g[t] * cands].window;
-            w = w < NW ? w : 0u;
-        } else {
-            g[t] = s_g[q];
-            w = s_w[q];
+        for (int t = 0; t < kP1; ++t) {
+            const uint32_t r = threadIdx.x + (uint32_t)t * kRouteThreads;
+            b[t] = r < nb ? keys[bstart + r] : 0u;
         }
-        const uint64_t gi = gi0 + t;
-        const uint32_t inner = (uint32_t)(gi >> 32) == (uint32_t)(gi0 >> 32) ? inner0 : fmix32((uint32_t)(gi >> 32) ^ smix);
-        h[t] = fmix32((uint32_t)gi ^ inner);
-        d1[t] = ((h[t] & 0xFFFFu) * R) >> 16;
-        d2[t] = ((h[t] >> 16) * R) >> 16;
-        const bool in = base + t < n;
-        bad |= in && b[t] >= K;
-        const uint32_t ar = b[t] < K ? wrank[(uint64_t)w * K + b[t]] : 0xFFFFFFFFu;
-        a[t] = ar < cmax ? ar : 0xFFFFFFFFu;
-        const uint64_t* __restrict__ pp = gp2c + (((uint64_t)g[t] * R + d1[t]) * R + d2[t]) * PW;
 #pragma unroll
-        for (uint32_t wd = 0; wd < (uint32_t)kPW; ++wd) pw[t][wd] = wd < PW ? pp[wd] : 0ull;
-    }
-    for (uint32_t cg = 0; cg < CS; cg += 8) {
-        uint4 row[kPer];
-#pragma unroll
-        for (int t = 0; t < kPer; ++t) {
-            row[t] = a[t] != 0xFFFFFFFFu
-                         ? *reinterpret_cast<const uint4*>(gdest + ((uint64_t)g[t] * cmax + a[t]) * CS + cg)
-                         : make_uint4(0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu);
-        }
-        const uint32_t nc = cands - cg < 8u ? cands - cg : 8u;
-        for (uint32_t u = 0; u < nc; ++u) {
-            const uint32_t c = cg + u;
-            uint32_t d[kPer];
-            bool multi = false;
-#pragma unroll
-            for (int t = 0; t < kPer; ++t) {
-                const uint32_t wv = u < 2 ? row[t].x : (u < 4 ? row[t].y : (u < 6 ? row[t].z : row[t].w));
-                const uint32_t e = (u & 1u) ? (wv >> 16) : (wv & 0xFFFFu);
-                const uint32_t bit = (uint32_t)(pw[t][kPW == 1 ? 0u : (c >> 6)] >> (c & 63u)) & 1u;
-                const uint32_t cold = bit ? d2[t] : d1[t];
-                d[t] = e == CR_GROUP_COLD ? cold : e;
-                multi |= e == CR_GROUP_MULTI;
+        for (int t = 0; t < kP1; ++t) {
+            const uint32_t r = threadIdx.x + (uint32_t)t * kRouteThreads;
+            const uint32_t q = (r >= r0) + (r >= r1) + (r >= r2) + (r >= r3);
+            g[t] = s_g[q < kBnd ? q : kBnd];
+            w[t] = s_w[q < kBnd ? q : kBnd];
+            if (r < nb && r >= r3 && r3 < T) {  // more than kBnd boundaries in this block
+                uint32_t j = j0 + kBnd;
+                while (j + 1 < J && off[j + 1] <= bstart + r) ++j;
+                g[t] = gmap[j] < NG ? gmap[j] : NG - 1;
+                const uint32_t ww = specs[(uint64_t)g[t] * cands].window;
+                w[t] = ww < NW ? ww : 0u;
             }
-            if (ballot(multi)) {  // k > 1 for some request of this wave: pick by the hash
+        }
+        uint32_t ar[kP1];
 #pragma unroll
-                for (int t = 0; t < kPer; ++t) {
-                    if (d[t] != CR_GROUP_MULTI) continue;
-                    const uint64_t p = (uint64_t)g[t] * cands + c;
-                    const uint32_t* __restrict__ mo = member_off + p * (cmax + 1u);
-                    const uint32_t o = mo[a[t]], k = mo[a[t] + 1] - o;
-                    d[t] = members[p * cmax + o + (((h[t] >> 16) * k) >> 16)];
+        for (int t = 0; t < kP1; ++t) {
+            const uint32_t r = threadIdx.x + (uint32_t)t * kRouteThreads;
+            const bool ok = r < nb && b[t] < K;
+            bad |= r < nb && b[t] >= K;
+            ar[t] = ld_at<uint32_t>(wrank, (w[t] * K + (ok ? b[t] : 0u)) * 4u);
+            ar[t] = ok && ar[t] < cmax ? ar[t] : 0xFFFFFFFFu;
+        }
+#pragma unroll
+        for (int t = 0; t < kP1; ++t) {
+            const uint32_t r = threadIdx.x + (uint32_t)t * kRouteThreads;
+            if (r >= T) break;
+            const uint64_t gi = first_index + bstart + r;
+            const uint32_t h = fmix32((uint32_t)gi ^ fmix32((uint32_t)(gi >> 32) ^ smix));
+            m_a[r] = ar[t];
+            m_d[r] = (((h & 0xFFFFu) * R) >> 16) | ((((h >> 16) * R) >> 16) << 16);
+            m_g[r] = g[t];
+            m_h[r] = h;
+        }
+    }
+    __syncthreads();
+    // phase 2
+    const uint32_t tasks = (T / 4u) * NP;
+    for (uint32_t q = threadIdx.x; q < tasks; q += kRouteThreads) {
+        const uint32_t rq = q / NP, pc = q % NP, ra = 4u * rq;
+        const uint4 va = *reinterpret_cast<const uint4*>(m_a + ra);
+        const uint4 vd = *reinterpret_cast<const uint4*>(m_d + ra);
+        const uint4 vg = *reinterpret_cast<const uint4*>(m_g + ra);
+        uint32_t roff[4];  // element index of the 8-entry piece in group_dest and group_multi
+        uint4 row[4], x1[4], x2[4];
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            const uint32_t A = u4_at(va, s), D = u4_at(vd, s), G = u4_at(vg, s);
+            roff[s] = (G * cmax + (A != 0xFFFFFFFFu ? A : 0u)) * CS + 8u * pc;
+            row[s] = ld_at<uint4>(gdest, roff[s] * 2u);
+            const uint32_t rb = G * R * CS + 8u * pc;
+            x1[s] = ld_at<uint4>(grank, (rb + (D & 0xFFFFu) * CS) * 2u);
+            x2[s] = ld_at<uint4>(grank, (rb + (D >> 16) * CS) * 2u);
+        }
+        uint32_t ent[4][8];
+        bool multi = false;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            const uint32_t A = u4_at(va, s), D = u4_at(vd, s);
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const uint32_t sh = (u & 1) * 16;
+                const uint32_t ev = A == 0xFFFFFFFFu ? CR_GROUP_COLD : (u4_at(row[s], u >> 1) >> sh) & 0xFFFFu;
+                const uint32_t q1 = (u4_at(x1[s], u >> 1) >> sh) & 0xFFFFu, q2 = (u4_at(x2[s], u >> 1) >> sh) & 0xFFFFu;
+                const uint32_t cold = q2 < q1 ? (D >> 16) : (D & 0xFFFFu);
+                ent[s][u] = ev == CR_GROUP_COLD ? cold : ev;
+                multi |= ev == CR_GROUP_MULTI;
+            }
+        }
+        if (multi) {  // k > 1: the member picked by the request hash
+            uint4 mv[4][2];
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                mv[s][0] = ld_at<uint4>(gmulti, roff[s] * 4u);
+                mv[s][1] = ld_at<uint4>(gmulti, roff[s] * 4u + 16u);
+            }
+            const uint4 vh = *reinterpret_cast<const uint4*>(m_h + ra);
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                const uint32_t G = u4_at(vg, s), H = u4_at(vh, s);
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    const bool m = ent[s][u] == CR_GROUP_MULTI;
+                    const uint32_t ok = u4_at(mv[s][u >> 2], u & 3);
+                    const uint32_t pick = (ok & 0xFFFFFu) + (((H >> 16) * (ok >> 20)) >> 16);
+                    const uint32_t idx = m ? (G * cands + 8u * pc + (uint32_t)u) * cmax + pick : 0u;
+                    const uint32_t dm = ld_at<uint16_t>(members, idx * 2u);
+                    ent[s][u] = m ? dm : ent[s][u];
                 }
             }
-            uint16_t* __restrict__ dc = dest + (uint64_t)c * n + base;
-            if (full) {
-                *reinterpret_cast<uint2*>(dc) = make_uint2(d[0] | (d[1] << 16), d[2] | (d[3] << 16));
-            } else {
+        }
 #pragma unroll
-                for (int t = 0; t < kPer; ++t)
-                    if (base + t < n) dc[t] = (uint16_t)d[t];
+        for (int u = 0; u < 8; ++u) {
+            uint32_t* __restrict__ tr = tile + (8u * pc + u) * TS2 + 2u * rq;
+            tr[0] = ent[0][u] | (ent[1][u] << 16);
+            tr[1] = ent[2][u] | (ent[3][u] << 16);
+        }
+    }
+    __syncthreads();
+    // phase 3
+    const uint32_t nw = (nb + 1u) / 2u;  // words holding at least one request of the block
+    for (uint32_t c = 0; c < cands; ++c) {
+        const uint32_t* __restrict__ tr = tile + c * TS2;
+        uint16_t* __restrict__ dc = dest + (uint64_t)c * n + bstart;
+        for (uint32_t wdx = threadIdx.x; wdx < nw; wdx += kRouteThreads) {
+            const uint32_t v = tr[wdx];
+            if (kVec) {
+                __builtin_nontemporal_store(v, reinterpret_cast<uint32_t*>(dc) + wdx);  // n even: both halves used
+            } else {
+                dc[2u * wdx] = (uint16_t)v;
+                if (2u * wdx + 1u < nb) dc[2u * wdx + 1u] = (uint16_t)(v >> 16);
             }
         }
     }
@@ -528,37 +621,52 @@ extern "C" cr_status cr_route(const uint32_t* keys, uint64_t n, uint64_t first_i
     if (blocks > 0x7FFFFFF0ull) return CR_EINVAL;
     // 16-byte key loads and 8-byte destination stores need aligned rows.
     const bool vec = ((uintptr_t)keys & 15u) == 0 && ((uintptr_t)dest & 7u) == 0 && (n & 3u) == 0;
-    const bool grouped = plans->window_rank || plans->group_dest || plans->group_p2c;
+    const bool grouped = plans->window_rank || plans->group_dest || plans->group_rank || plans->group_multi;
     if (grouped) {
-        if (!plans->window_rank || !plans->group_dest || !plans->group_p2c || ((uintptr_t)plans->group_dest & 15u) ||
-            ((uintptr_t)plans->group_p2c & 7u) || ((uintptr_t)plans->window_rank & 3u) || !plans->specs ||
+        if (!plans->window_rank || !plans->group_dest || !plans->group_rank || !plans->group_multi ||
+            ((uintptr_t)plans->group_dest & 15u) || ((uintptr_t)plans->group_rank & 15u) ||
+            ((uintptr_t)plans->group_multi & 15u) || ((uintptr_t)plans->window_rank & 3u) || !plans->specs ||
             !plans->order || !plans->n_order || !plans->num_admitted)
             return CR_EINVAL;
         if (plans->num_windows > 65535u || plans->num_plans / plans->cands > 65535u) return CR_EINVAL;  // grid y
+        // the kernels address every table with 32-bit byte offsets
+        const uint64_t NG = plans->num_plans / plans->cands, CS = (plans->cands + 7u) & ~7u;
+        if ((uint64_t)plans->num_windows * plans->num_keys * 4u > 0xFFFFFFFFull ||
+            NG * cmax * CS * 4u > 0xFFFFFFFFull || (uint64_t)plans->num_plans * cmax * 2u > 0xFFFFFFFFull)
+            return CR_EINVAL;
     }
     (void)hipGetLastError();
     if (grouped) {
         const hipStream_t st = as_stream(stream);
         const uint32_t NG = plans->num_plans / plans->cands, cands = plans->cands;
-        const uint32_t CS = (cands + 7u) & ~7u, PW = (cands + 63u) / 64u;
+        const uint32_t CS = (cands + 7u) & ~7u;
         const uint64_t wr_n = (uint64_t)plans->num_windows * plans->num_keys;
+        const uint32_t T = group_tile(CS);
+        const uint64_t gblocks = (n + T - 1) / T;
+        if (gblocks > 0x7FFFFFF0ull) return CR_EINVAL;
+        const size_t lds = group_route_lds(CS);
         hipLaunchKernelGGL(k_fill_u32, dim3(2048), dim3(256), 0, st, plans->window_rank, wr_n, 0xFFFFFFFFu);
         hipLaunchKernelGGL(k_win_rank_set, dim3((cmax + 255u) / 256u, plans->num_windows), dim3(256), 0, st,
                            plans->order, plans->n_order, cmax, plans->num_keys, plans->window_rank);
         hipLaunchKernelGGL(k_group_dest, dim3((cmax + kGrpRows - 1u) / kGrpRows, NG), dim3(kGrpThreads), 0, st, cands,
                            CS, cmax, plans->specs, plans->num_admitted, plans->member_off, plans->members,
-                           plans->group_dest, err);
-        hipLaunchKernelGGL(k_group_p2c, dim3(plans->R, NG), dim3(256), 0, st, plans->R, cands, PW, plans->load,
-                           plans->group_p2c);
-#define CR_ROUTE_GROUP(V, W)                                                                                       \
-    hipLaunchKernelGGL((k_route_group<V, W>), dim3(xcd_grid((uint32_t)blocks)), dim3(kRouteThreads), 0, st, keys, n,      \
-                       first_index, seed_mix(seed), off, gmap, J, plans->num_keys, plans->R, cands, CS, PW, NG,       \
-                       plans->num_windows, cmax, plans->specs, plans->window_rank, plans->group_dest,                \
-                       plans->group_p2c, plans->member_off, plans->members, dest, err)
-        if (vec && PW == 1) CR_ROUTE_GROUP(true, 1);
-        else if (vec) CR_ROUTE_GROUP(true, 4);
-        else if (PW == 1) CR_ROUTE_GROUP(false, 1);
-        else CR_ROUTE_GROUP(false, 4);
+                           plans->group_dest, plans->group_multi, err);
+        hipLaunchKernelGGL(k_group_rank, dim3(CS, NG), dim3(256), 0, st, plans->R, cands, CS, plans->load,
+                           plans->group_rank);
+        // 32-bit destination stores need an even n and a 4-byte aligned dest
+        const bool v32 = ((uintptr_t)dest & 3u) == 0 && (n & 1u) == 0;
+#define CR_ROUTE_GROUP(V)                                                                                          \
+    do {                                                                                                           \
+        if (hipFuncSetAttribute((const void*)k_route_group<V>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) \
+            != hipSuccess)                                                                                         \
+            return CR_EHIP;                                                                                        \
+        hipLaunchKernelGGL((k_route_group<V>), dim3(xcd_grid((uint32_t)gblocks)), dim3(kRouteThreads), lds, st, keys, \
+                           n, first_index, seed_mix(seed), off, gmap, J, plans->num_keys, plans->R, cands, CS, NG,   \
+                           plans->num_windows, cmax, plans->specs, plans->window_rank, plans->group_dest,            \
+                           plans->group_rank, plans->group_multi, plans->members, dest, err);                       \
+    } while (0)
+        if (v32) CR_ROUTE_GROUP(true);
+        else CR_ROUTE_GROUP(false);
 #undef CR_ROUTE_GROUP
         return hipGetLastError() == hipSuccess ? CR_OK : CR_EHIP;
     }

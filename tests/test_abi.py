@@ -56,18 +56,18 @@ def test_host_only_queries(lib_path):
 def test_struct_layouts_match_header(lib_path):
     from paper_2608_19677_amd import binding
     assert ctypes.sizeof(binding.CrPlanSpec) == 40
-    assert ctypes.sizeof(binding.CrPlanSet) == 6 * 4 + 15 * 8
+    assert ctypes.sizeof(binding.CrPlanSet) == 6 * 4 + 16 * 8
 
 
 def test_plan_sizes_follow_the_header_layouts(lib_path):
     # restated from the layouts documented in cr.h: C_max = R max_W, KW = ceil(K / 64),
-    # NG = NP / cands, CS = cands rounded up to 8, PW = ceil(cands / 64)
+    # NG = NP / cands, CS = cands rounded up to 8
     from paper_2608_19677_amd import binding
     for NP, cands, R, W, K, NW in [(1, 1, 30, 64, 20_000, 1), (948, 1, 30, 64, 20_000, 948),
                                    (64, 64, 1024, 512, 10**6, 1), (300, 100, 70, 60, 2000, 3)]:
-        cm, KW, NG, CS, PW = R * W, (K + 63) // 64, NP // cands, (cands + 7) // 8 * 8, (cands + 63) // 64
+        cm, KW, NG, CS = R * W, (K + 63) // 64, NP // cands, (cands + 7) // 8 * 8
         want = [NP * 40, NW * cm * 4, NW * cm * 4, NW * 4, NP * 4, NP * 8, NP * 4, NP * (cm + 1) * 4, NP * cm * 2,
-                NP * R * 8, NP * KW * 16, NP * cm * 4, NW * K * 4, NG * cm * CS * 2, NG * R * R * PW * 8]
+                NP * R * 8, NP * KW * 16, NP * cm * 4, NW * K * 4, NG * cm * CS * 2, NG * R * CS * 2, NG * cm * CS * 4]
         assert binding.cr_plan_sizes(NP, cands, R, W, K, NW) == want
 
 

@@ -192,10 +192,11 @@ def test_lru_reset_rejects(L):
 
 
 def test_route_rejects_partial_group_tables(L):
-    # the three group tables come together, group_dest 16-byte aligned
+    # the four group tables come together, group_dest, group_rank and group_multi 16-byte aligned
     keys = FAKE
-    for wr, gd, gp in [(FAKE, None, None), (FAKE, FAKE, None), (None, FAKE, FAKE), (FAKE, FAKE + 8, FAKE),
-                       (FAKE, FAKE, FAKE + 4)]:
+    for wr, gd, gp, gm in [(FAKE, None, None, None), (FAKE, FAKE, None, FAKE), (None, FAKE, FAKE, FAKE),
+                           (FAKE, FAKE, FAKE, None), (FAKE, FAKE + 8, FAKE, FAKE), (FAKE, FAKE, FAKE + 8, FAKE),
+                           (FAKE, FAKE, FAKE, FAKE + 4)]:
         ps = _set(cands=2, num_plans=2)
-        ps.window_rank, ps.group_dest, ps.group_p2c = wr, gd, gp
+        ps.window_rank, ps.group_dest, ps.group_rank, ps.group_multi = wr, gd, gp, gm
         assert L.cr_route(keys, 16, 0, 1, FAKE, FAKE, 1, ctypes.byref(ps), FAKE, FAKE, None) == B.CR_EINVAL
