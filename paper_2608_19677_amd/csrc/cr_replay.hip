@@ -670,6 +670,22 @@ __device__ __forceinline__ uint32_t mtf_core(uint32_t& sk, uint64_t m)
     return p;
 }
 
+// mtf_core with the lane mask made by the vector unit (VCC = lanes above p, one compare of
+// the lane id with p) instead of s_lshl: for lists whose scalar unit is the busier one. A
+// miss (p = 0xFFFFFFFF) leaves VCC empty, so every lane shifts, as in mtf_core.
+__device__ __forceinline__ uint32_t mtf_core_v(uint32_t& sk, uint64_t m, uint32_t lane)
+{
+    uint32_t p, out;
+    asm("s_ff1_i32_b64 %1, %3\n\t"
+        "v_cmp_lt_u32 vcc, %1, %4\n\t"
+        "v_cndmask_b32_dpp %0, %2, %2, vcc wave_shr:1 row_mask:0xf bank_mask:0xf"
+        : "=v"(out), "=&s"(p)
+        : "v"(sk), "s"(m), "v"(lane)
+        : "vcc");
+    sk = out;
+    return p;
+}
+
 // Move-to-front access of key kk (lane i = i-th most recent key; lanes outside `wmask`
 // are ignored). Returns the hit depth, or 0xFFFFFFFF on a miss. On a miss the shift runs
 // over every lane, which drops the least recent key of a full list.
@@ -836,15 +852,15 @@ __device__ __forceinline__ bool back_step(uint32_t (&sk)[SL], uint32_t kk, uint3
 // Two-level list, 64 records (all valid). Every access changes the front alone until it
 // misses there, and the back changes only on those misses, so the batch runs in two
 // phases: the 64 front accesses, branch-free and unrolled like the one-register list, each
-// writing its key and the front's position-63 key into lane j of evk / evv and advancing j
-// on a front miss; then one back operation per logged miss, in order. Returns lane t = 1
-// if record t hit (in the front or the back).
+// writing its key and the front's position-63 key into lane t of evk / evv (t = record);
+// then one back operation per front miss, in record order. The front's lane mask comes
+// from the vector unit (mtf_core_v): this list's scalar unit is the busier one. Returns
+// lane t = 1 if record t hit (in the front or the back).
 template <int SL, bool kMasked>
 __device__ __forceinline__ uint32_t mtf_batch_two(uint32_t (&sk)[SL], const uint64_t* __restrict__ rb,
                                                   const uint64_t (&vm)[SL], uint32_t lane)
 {
     uint32_t depth = 0xFFFFFFFFu, evk = 0u, evv = 0u;
-    uint32_t j = 0;
 #pragma unroll
     for (uint32_t g = 0; g < 8; ++g) {
         uint64_t rk[8];
@@ -855,19 +871,18 @@ __device__ __forceinline__ uint32_t mtf_batch_two(uint32_t (&sk)[SL], const uint
             const uint32_t key = (uint32_t)rk[t];
             const uint64_t m = ballot(sk[0] == key);
             const uint32_t ev = rdlane(sk[0], 63u);
-            const uint32_t p = mtf_core(sk[0], m);
+            const uint32_t p = mtf_core_v(sk[0], m, lane);
             sk[0] = wrlane(sk[0], key, 0u);
             depth = wrlane(depth, p, 8u * g + t);
-            evk = wrlane(evk, key, j);
-            evv = wrlane(evv, ev, j);
-            asm("s_cmp_eq_u64 %1, 0\n\ts_addc_u32 %0, %0, 0" : "+s"(j) : "s"(m) : "scc");  // j += front miss
+            evk = wrlane(evk, key, 8u * g + t);
+            evv = wrlane(evv, ev, 8u * g + t);
         }
     }
     uint64_t rem = ballot(depth == 0xFFFFFFFFu), bh = 0;
-    for (uint32_t e = 0; rem; ++e) {
+    while (rem) {
         const uint32_t t = (uint32_t)__builtin_ctzll(rem);
         rem &= rem - 1ull;
-        if (back_step<SL, kMasked>(sk, rdlane(evk, e), rdlane(evv, e), vm)) bh |= 1ull << t;
+        if (back_step<SL, kMasked>(sk, rdlane(evk, t), rdlane(evv, t), vm)) bh |= 1ull << t;
     }
     return (depth != 0xFFFFFFFFu || ((bh >> lane) & 1ull)) ? 1u : 0u;
 }
