@@ -255,7 +255,7 @@ def sweep_traffic():
     """HBM bytes per replay stage from the committed counter summary of the sweep, or None
     when the replay's sources changed since the counters were taken."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", "sweep_hbm_traffic.md")
+    path = os.path.join(ROOT, "profiles", "sweep_counters.md")
     if not os.path.exists(path):
         return None
     rec = None
@@ -274,14 +274,14 @@ def sweep_traffic():
 
 def sweep_cpu_baseline(args, w0):
     """The oracle, fanned out over this host's threads, on a bounded sample of the sweep:
-    the first 4e6 requests of chunk 0 as one window (count, 64 plans, routing and replay of
+    the first 2.4e7 requests of chunk 0 as one window (count, 64 plans, routing and replay of
     every candidate), timed end to end."""
     import dataclasses
 
     import numpy as np
 
     from oracle import pipeline as opipe
-    S = 4_000_000
+    S = 24_000_000
     ws = dataclasses.replace(w0, keys=w0.keys[:S], suffix=w0.suffix[:S], offsets=np.array([0, S], dtype=np.uint64))
     threads = args.cpu_threads or opipe.host_threads()
     tm = {}
