@@ -317,10 +317,11 @@ cr_status cr_replay_partition(const uint32_t* keys, const uint16_t* suffix, cons
 /* Second phase of cr_replay: replays the partitioned workspace (same n, J, P, R, W)
  * through the per-destination LRU caches and accumulates stats. Each segment rebuilds the
  * cache state it starts from by scanning its stream backwards for W distinct keys, at most
- * two segment lengths; a segment whose scan runs out before that (a stream with fewer than
- * W distinct keys) is left to a second launch that replays its whole stream in order in
- * one wavefront. Each request is thus replayed at most twice and scanned at most three
- * times, whatever the key mix; the results do not depend on which launch counts them. */
+ * two segment lengths; a segment whose scan runs out before that (a stretch with fewer than
+ * W distinct keys) is left to a second launch, in which one wavefront per run of such
+ * segments replays the segment before the run (without counting it) and then the run, in
+ * order. Each request is thus replayed at most twice and scanned at most three times,
+ * whatever the key mix; the results do not depend on which launch counts them. */
 cr_status cr_replay_lru(const uint32_t* prefix_len, uint32_t num_keys, uint64_t n, uint32_t J,
                         uint32_t P, uint32_t R, const uint32_t* W, uint32_t max_W,
                         const uint32_t* lru_in, uint32_t* lru_out, uint64_t* stats, void* ws,

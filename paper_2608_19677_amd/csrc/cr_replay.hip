@@ -921,19 +921,26 @@ __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v)
     return v;
 }
 
-// One work item per segment (kSeq false) or per (candidate, destination) stream whose
-// segments could not all rebuild their state within the budget (kSeq true).
+// One work item per segment (kSeq false), or per run of consecutive segments whose
+// rebuild ran out of budget (kSeq true).
 //
 // A segment rebuilds its initial state by scanning back for W distinct keys; a stream with
 // fewer distinct keys than W would make every segment scan to the stream's start, which is
 // quadratic in its length. The scan therefore stops after kRebuildBudget segment lengths:
 // a segment that has neither found W keys nor reached the start writes nothing and marks
-// itself in `aborted` and its stream in `sflag`. The kSeq launch that follows replays each
-// marked stream from its start in one wavefront, segment after segment, keeping the
-// statistics of the marked segments only (the others were counted by their own work
-// items) and writing the stream's final state. Every record is then replayed at most twice
-// and scanned at most kRebuildBudget + 1 times, whatever the keys.
+// itself in `aborted`. In the kSeq launch that follows, the wavefront of the first segment
+// of each run of marked segments starts at the run's predecessor (which is never marked:
+// the first segment of a stream has nothing to rebuild), rebuilds the predecessor's state
+// as that segment did, replays it without counting, and then replays the run in order,
+// counting it and writing the final state if the run ends the stream. Each marked record
+// is thus replayed once more, and every record is scanned at most kRebuildBudget + 1 times,
+// whatever the keys.
 constexpr uint32_t kRebuildBudget = 2;
+
+__device__ __forceinline__ bool item_marked(const uint32_t* __restrict__ aborted, uint64_t it)
+{
+    return (aborted[it >> 5] >> (it & 31u)) & 1u;
+}
 
 template <int SL, bool kTwo, bool kSeq>
 __global__ __launch_bounds__(kReplayThreads) void k_replay(
@@ -941,20 +948,15 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
     const uint32_t* __restrict__ item_off, uint32_t P, uint32_t R, uint32_t K, uint32_t J,
     const uint32_t* __restrict__ prefix_len, WArg wa, uint32_t max_W, const uint32_t* __restrict__ lru_in,
     uint32_t* __restrict__ lru_out, uint64_t* __restrict__ stats, uint32_t* __restrict__ aborted,
-    uint32_t* __restrict__ sflag, uint32_t* __restrict__ err)
+    uint32_t* __restrict__ err)
 {
     const uint32_t lane = lane_id();
-    const uint64_t wid = (uint64_t)blockIdx.x * (kReplayThreads / 64) + wave_in_block();
+    const uint64_t item = (uint64_t)blockIdx.x * (kReplayThreads / 64) + wave_in_block();
     const uint32_t ncd = P * R;
+    if (item >= item_off[ncd]) return;
+    if (kSeq && !item_marked(aborted, item)) return;
     uint32_t lo = 0;
-    uint64_t item = 0;
-    if constexpr (kSeq) {
-        if (wid >= ncd) return;
-        lo = (uint32_t)wid;
-        if (sflag[lo] == 0) return;
-    } else {
-        item = wid;
-        if (item >= item_off[ncd]) return;
+    {
         uint32_t hi = ncd;
         while (hi - lo > 1) {
             const uint32_t mid = (lo + hi) >> 1;
@@ -962,19 +964,27 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
             else hi = mid;
         }
     }
+    // kSeq: only the first marked segment of a run, which is never a stream's first item
+    if (kSeq && (item == item_off[lo] || item_marked(aborted, item - 1))) return;
     const uint32_t c = lo / R, d = lo % R;
     const uint32_t W = wa.W[c];
     if (slot_class(W) != (uint32_t)SL) return;
     const uint32_t* go = grp_off + (uint64_t)c * (R + 1u);
     const uint32_t gs = go[d], cnt = go[d + 1] - gs;
     const uint32_t S = seg_len(W, wa.seg_min);
-    uint32_t s0 = 0, s1 = cnt;
-    if constexpr (!kSeq) {
-        const uint64_t s0w = (item - item_off[lo]) * (uint64_t)S;
-        if (s0w > cnt) return;  // only if the partition used other slot counts
-        s0 = (uint32_t)s0w;
-        s1 = cnt - s0 < S ? cnt : s0 + S;
+    // [s0, s1): the records this wavefront replays; [s0, sc) of them are replayed only to
+    // reach the state at sc (the run's predecessor in the kSeq pass)
+    uint64_t i0 = item, i1 = item + 1;
+    if (kSeq) {
+        i0 = item - 1;
+        while (i1 < item_off[lo + 1] && item_marked(aborted, i1)) ++i1;
     }
+    const uint64_t s0w = (i0 - item_off[lo]) * (uint64_t)S;
+    if (s0w > cnt) return;  // only if the partition used other slot counts
+    const uint32_t s0 = (uint32_t)s0w;
+    const uint32_t sc = kSeq ? s0 + S : s0;
+    const uint64_t s1w = (i1 - item_off[lo]) * (uint64_t)S;
+    const uint32_t s1 = s1w < cnt ? (uint32_t)s1w : cnt;
     const uint64_t* __restrict__ rl = rec + (uint64_t)c * n + gs;
 
     // Slot q of the rebuilt state is the q-th most recent key, which is already the
@@ -992,20 +1002,17 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
     }
     const uint64_t wmask = vm[0];
     uint32_t q = 0;
-    if constexpr (!kSeq) {
-        // State before the segment: the most recent W distinct keys, newest first. Records
+    {
+        // State before record s0: the most recent W distinct keys, newest first. Records
         // are read backwards 64 at a time, the next (older) batch in flight while one is
-        // scanned.
+        // scanned. (A kSeq wavefront rebuilds an unmarked segment, which stays in budget.)
         uint32_t pos = s0, scanned = 0;
         const uint32_t budget = kRebuildBudget * S;
         uint32_t nb = pos < 64u ? pos : 64u;
         uint32_t kl_next = lane < nb ? (uint32_t)rl[pos - nb + lane] : CR_EMPTY_SLOT;
         while (q < W && pos > 0) {
-            if (scanned >= budget) {  // too few distinct keys: left to the stream's kSeq pass
-                if (lane == 0) {
-                    atomicOr(&aborted[item >> 5], 1u << (item & 31u));
-                    atomicOr(&sflag[lo], 1u);
-                }
+            if (!kSeq && scanned >= budget) {  // too few distinct keys: left to the kSeq pass
+                if (lane == 0) atomicOr(&aborted[item >> 5], 1u << (item & 31u));
                 return;
             }
             const uint32_t kl = kl_next;
@@ -1148,17 +1155,8 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
         }
         flush();
     };
-    if constexpr (kSeq) {
-        // every segment of the stream in order, counting the ones their work items left
-        const uint64_t i0 = item_off[lo];
-        for (uint32_t a = 0, k = 0; a < cnt; a += S, ++k) {
-            const uint64_t it = i0 + k;
-            const bool on = (aborted[it >> 5] >> (it & 31u)) & 1u;
-            run(a, cnt - a < S ? cnt : a + S, on);
-        }
-    } else {
-        run(s0, s1, true);
-    }
+    if (sc > s0) run(s0, sc < s1 ? sc : s1, false);
+    run(sc, s1, true);
     if (ballot(bad) && lane == 0) atomicOr(err, CR_ERR_KEY_RANGE);
     if (s1 == cnt) {
         uint32_t* __restrict__ lo_ = lru_out + ((uint64_t)c * R + d) * max_W;
@@ -1184,7 +1182,6 @@ struct ReplayWs {
     uint32_t* grp_off;
     uint32_t* item_off;
     uint32_t* aborted;  // bit per work item: its rebuild ran out of budget
-    uint32_t* sflag;    // per (candidate, destination): some segment of the stream did
     uint64_t flag_words;
     size_t bytes;
 };
@@ -1210,8 +1207,7 @@ inline ReplayWs replay_layout(void* base, uint64_t n, uint32_t P, uint32_t R)
     w.item_off = reinterpret_cast<uint32_t*>(b + o);
     o = up(o + ((uint64_t)P * R + 1u) * 4u);
     w.aborted = reinterpret_cast<uint32_t*>(b + o);
-    w.flag_words = (max_items(n, P, R) + 31u) / 32u + (uint64_t)P * R;  // aborted bits, then sflag
-    w.sflag = w.aborted + (max_items(n, P, R) + 31u) / 32u;
+    w.flag_words = (max_items(n, P, R) + 31u) / 32u;
     o = up(o + w.flag_words * 4u);
     w.bytes = (size_t)o + 256u;
     return w;
@@ -1348,23 +1344,22 @@ extern "C" cr_status cr_replay_lru(const uint32_t* prefix_len, uint32_t num_keys
     const hipStream_t st = as_stream(stream);
     const uint64_t items = max_items(n, P, R);
     const uint64_t blocks = (items + (kReplayThreads / 64) - 1) / (kReplayThreads / 64);
-    const uint64_t sblocks = ((uint64_t)P * R + (kReplayThreads / 64) - 1) / (kReplayThreads / 64);
     if (blocks > 0x7FFFFFFFull) return CR_EINVAL;
     (void)hipGetLastError();
     hipLaunchKernelGGL(k_zero_u32, dim3(256), dim3(256), 0, st, w.aborted, w.flag_words);
 #define CR_REPLAY(SL, TWO, SEQ, NB)                                                                                 \
     hipLaunchKernelGGL((k_replay<SL, TWO, SEQ>), dim3((uint32_t)(NB)), dim3(kReplayThreads), 0, st, w.rec, n,        \
                        w.grp_off, w.item_off, P, R, num_keys, J, prefix_len, ra.wa, max_W, lru_in, lru_out, stats,    \
-                       w.aborted, w.sflag, err)
+                       w.aborted, err)
     // two-level lists only for the largest class: measured slower with three back registers
     if (ra.classes & 1u) CR_REPLAY(1, false, false, blocks);
     if (ra.classes & 2u) CR_REPLAY(2, false, false, blocks);
     if (ra.classes & 4u) CR_REPLAY(4, false, false, blocks);
     if (ra.classes & 8u) CR_REPLAY(8, true, false, blocks);
-    if (ra.classes & 1u) CR_REPLAY(1, false, true, sblocks);
-    if (ra.classes & 2u) CR_REPLAY(2, false, true, sblocks);
-    if (ra.classes & 4u) CR_REPLAY(4, false, true, sblocks);
-    if (ra.classes & 8u) CR_REPLAY(8, true, true, sblocks);
+    if (ra.classes & 1u) CR_REPLAY(1, false, true, blocks);
+    if (ra.classes & 2u) CR_REPLAY(2, false, true, blocks);
+    if (ra.classes & 4u) CR_REPLAY(4, false, true, blocks);
+    if (ra.classes & 8u) CR_REPLAY(8, true, true, blocks);
 #undef CR_REPLAY
     return hipGetLastError() == hipSuccess ? CR_OK : CR_EHIP;
 }
