@@ -431,9 +431,12 @@ constexpr uint32_t kWideChunks = 16;  // chunks of 64 per wavefront and sub-tile
 
 __host__ __device__ __forceinline__ uint32_t wide_row(uint32_t R) { return (R + 3u) & ~3u; }  // padded to 4 per thread
 
+// LDS: staged records and positions, per-wavefront counters and the runs' bases, and per
+// wavefront the matching scratch (64 peer masks, then one byte per destination).
 inline size_t scatter_wide_lds_bytes(uint32_t R)
 {
-    return (size_t)kWideSub * 12u + (size_t)wide_row(R) * 4u * (kWideWaves + 1u);
+    return (size_t)kWideSub * 12u + (size_t)wide_row(R) * 4u * (kWideWaves + 1u) +
+           (size_t)kWideWaves * (512u + ((wide_row(R) + 7u) & ~7u));
 }
 
 __global__ __launch_bounds__(kWideThreads) void k_part_scatter_wide(
@@ -451,6 +454,10 @@ __global__ __launch_bounds__(kWideThreads) void k_part_scatter_wide(
     uint32_t* gbase = cnt + kWideWaves * R4;  // [R4] output position of the destination's run minus its start
     __shared__ uint32_t s_scan[16];
     const uint32_t c = blockIdx.x, lane = lane_id(), wv = wave_in_block(), tid = threadIdx.x;
+    // this wavefront's matching scratch: peer masks by representative lane, and a tag byte per
+    // destination naming the representative
+    unsigned long long* pm = reinterpret_cast<unsigned long long*>(gbase + R4) + wv * (64u + (R4 + 7u) / 8u);
+    uint8_t* tag = reinterpret_cast<uint8_t*>(pm + 64);
     const uint64_t t = blockIdx.y;
     if (t >= ntiles) return;
     const uint64_t t0 = t * tile, t1 = t0 + tile < n ? t0 + tile : n;
@@ -501,12 +508,16 @@ __global__ __launch_bounds__(kWideThreads) void k_part_scatter_wide(
                 jl = rdlane(j, 63);
                 jend = jl + 1 < J ? off[jl + 1] : ~0ull;
             }
-            uint64_t peers = ballot(valid);
-            for (uint32_t bit = 0; bit < nbits; ++bit) {
-                const bool on = (d >> bit) & 1u;
-                const uint64_t bb = ballot(on);
-                peers &= on ? bb : ~bb;
-            }
+            // Lanes with the same destination: every lane writes its id into the destination's
+            // tag byte and reads it back, so the lanes of one destination read one common
+            // representative (whichever write landed last); each lane then sets its bit in
+            // the representative's peer mask and reads the mask. LDS operations of a
+            // wavefront complete in order, so no barrier is needed.
+            pm[lane] = 0ull;
+            if (valid) tag[d] = (uint8_t)lane;
+            const uint32_t rep = valid ? (uint32_t)tag[d] : lane;
+            if (valid) atomicOr(&pm[rep], 1ull << lane);
+            const uint64_t peers = valid ? (uint64_t)pm[rep] : 0ull;
             const uint32_t rk = (uint32_t)__popcll(peers & lanemask_lt());
             const uint32_t leader = valid ? (uint32_t)__builtin_ctzll(peers) : lane;
             uint32_t old = 0;
