@@ -431,12 +431,13 @@ constexpr uint32_t kWideChunks = 16;  // chunks of 64 per wavefront and sub-tile
 
 __host__ __device__ __forceinline__ uint32_t wide_row(uint32_t R) { return (R + 3u) & ~3u; }  // padded to 4 per thread
 
-// LDS: staged records and positions, per-wavefront counters and the runs' bases, and per
-// wavefront the matching scratch (64 peer masks, then one byte per destination).
+// LDS: staged records and their destinations, per-wavefront counters and the runs' bases,
+// and per wavefront two matching scratch areas (64 peer masks, then one byte per
+// destination), one for even and one for odd chunks.
 inline size_t scatter_wide_lds_bytes(uint32_t R)
 {
-    return (size_t)kWideSub * 12u + (size_t)wide_row(R) * 4u * (kWideWaves + 1u) +
-           (size_t)kWideWaves * (512u + ((wide_row(R) + 7u) & ~7u));
+    return (size_t)kWideSub * 10u + (size_t)wide_row(R) * 4u * (kWideWaves + 1u) +
+           (size_t)kWideWaves * 2u * (512u + ((wide_row(R) + 7u) & ~7u));
 }
 
 __global__ __launch_bounds__(kWideThreads) void k_part_scatter_wide(
@@ -449,15 +450,18 @@ __global__ __launch_bounds__(kWideThreads) void k_part_scatter_wide(
     extern __shared__ uint64_t lds[];
     const uint32_t R4 = wide_row(R);
     uint64_t* srec = lds;                                           // [kWideSub] staged records
-    uint32_t* spos = reinterpret_cast<uint32_t*>(srec + kWideSub);  // [kWideSub] their output positions
-    uint32_t* cnt = spos + kWideSub;  // [kWideWaves][R4] counts per wavefront, then its slot bases
+    uint16_t* sdst = reinterpret_cast<uint16_t*>(srec + kWideSub);  // [kWideSub] their destinations
+    uint32_t* cnt = reinterpret_cast<uint32_t*>(sdst + kWideSub);  // [kWideWaves][R4] counts per wavefront, then its slot bases
     uint32_t* gbase = cnt + kWideWaves * R4;  // [R4] output position of the destination's run minus its start
     __shared__ uint32_t s_scan[16];
     const uint32_t c = blockIdx.x, lane = lane_id(), wv = wave_in_block(), tid = threadIdx.x;
-    // this wavefront's matching scratch: peer masks by representative lane, and a tag byte per
-    // destination naming the representative
-    unsigned long long* pm = reinterpret_cast<unsigned long long*>(gbase + R4) + wv * (64u + (R4 + 7u) / 8u);
-    uint8_t* tag = reinterpret_cast<uint8_t*>(pm + 64);
+    // this wavefront's matching scratch, two areas (even and odd chunks): peer masks by
+    // representative lane, and a tag byte per destination naming the representative
+    const uint32_t area = 64u + (R4 + 7u) / 8u;  // 8-byte words
+    unsigned long long* pm0 = reinterpret_cast<unsigned long long*>(gbase + R4) + wv * 2u * area;
+    unsigned long long* pm1 = pm0 + area;
+    uint8_t* tag0 = reinterpret_cast<uint8_t*>(pm0 + 64);
+    uint8_t* tag1 = reinterpret_cast<uint8_t*>(pm1 + 64);
     const uint64_t t = blockIdx.y;
     if (t >= ntiles) return;
     const uint64_t t0 = t * tile, t1 = t0 + tile < n ? t0 + tile : n;
@@ -492,39 +496,54 @@ __global__ __launch_bounds__(kWideThreads) void k_part_scatter_wide(
             kv[m] = in ? keys[i] : 0u;
             mv[m] = in ? suffix[i] : 0u;
         }
+        // Chunks in pairs, each with its own matching area, so that the LDS round trips of
+        // the two chunks overlap. Lanes with the same destination: every lane writes its id
+        // into the destination's tag byte and reads it back, so the lanes of one destination
+        // read one common representative (whichever write landed last); each lane then sets
+        // its bit in the representative's peer mask and reads the mask. LDS operations of a
+        // wavefront complete in order, so no barrier is needed, and the counter updates of
+        // chunk m precede those of chunk m + 1.
 #pragma unroll
-        for (uint32_t m = 0; m < kWideChunks; ++m) {
-            const uint64_t base = ws + 64u * m;
-            if (base >= se) {
-                dk[m] = 0xFFFFFFFFu;
-                continue;
+        for (uint32_t m = 0; m < kWideChunks; m += 2) {
+            uint32_t dd[2], jj[2];
+            bool vv[2];
+#pragma unroll
+            for (uint32_t h = 0; h < 2; ++h) {
+                const uint64_t base = ws + 64u * (m + h);
+                const uint64_t i = base + lane;
+                dd[h] = dk[m + h];
+                vv[h] = i < se && dd[h] < R;
+                uint32_t j = jl;
+                if (base < se && base + 63 >= jend) {  // an interval boundary falls inside these 64
+                    while (j + 1 < J && off[j + 1] <= i) ++j;
+                    jl = rdlane(j, 63);
+                    jend = jl + 1 < J ? off[jl + 1] : ~0ull;
+                }
+                jj[h] = j;
             }
-            const uint64_t i = base + lane;
-            const uint32_t d = dk[m];
-            const bool valid = i < se && d < R;
-            uint32_t j = jl;
-            if (base + 63 >= jend) {  // an interval boundary falls inside these 64 requests
-                while (j + 1 < J && off[j + 1] <= i) ++j;
-                jl = rdlane(j, 63);
-                jend = jl + 1 < J ? off[jl + 1] : ~0ull;
-            }
-            // Lanes with the same destination: every lane writes its id into the destination's
-            // tag byte and reads it back, so the lanes of one destination read one common
-            // representative (whichever write landed last); each lane then sets its bit in
-            // the representative's peer mask and reads the mask. LDS operations of a
-            // wavefront complete in order, so no barrier is needed.
-            pm[lane] = 0ull;
-            if (valid) tag[d] = (uint8_t)lane;
-            const uint32_t rep = valid ? (uint32_t)tag[d] : lane;
-            if (valid) atomicOr(&pm[rep], 1ull << lane);
-            const uint64_t peers = valid ? (uint64_t)pm[rep] : 0ull;
-            const uint32_t rk = (uint32_t)__popcll(peers & lanemask_lt());
-            const uint32_t leader = valid ? (uint32_t)__builtin_ctzll(peers) : lane;
-            uint32_t old = 0;
-            if (valid && rk == 0) old = atomicAdd(&wc[d], (uint32_t)__popcll(peers));
-            old = (uint32_t)__builtin_amdgcn_ds_bpermute((int)(leader << 2), (int)old);
-            dk[m] = valid ? (d << 16) | (old + rk) : 0xFFFFFFFFu;  // destination, rank in the wavefront
-            mv[m] |= j << 16;
+            pm0[lane] = 0ull;
+            pm1[lane] = 0ull;
+            if (vv[0]) tag0[dd[0]] = (uint8_t)lane;
+            if (vv[1]) tag1[dd[1]] = (uint8_t)lane;
+            const uint32_t rep0 = vv[0] ? (uint32_t)tag0[dd[0]] : lane;
+            const uint32_t rep1 = vv[1] ? (uint32_t)tag1[dd[1]] : lane;
+            if (vv[0]) atomicOr(&pm0[rep0], 1ull << lane);
+            if (vv[1]) atomicOr(&pm1[rep1], 1ull << lane);
+            const uint64_t peers0 = vv[0] ? (uint64_t)pm0[rep0] : 0ull;
+            const uint64_t peers1 = vv[1] ? (uint64_t)pm1[rep1] : 0ull;
+            const uint32_t rk0 = (uint32_t)__popcll(peers0 & lanemask_lt());
+            const uint32_t rk1 = (uint32_t)__popcll(peers1 & lanemask_lt());
+            const uint32_t ld0 = vv[0] ? (uint32_t)__builtin_ctzll(peers0) : lane;
+            const uint32_t ld1 = vv[1] ? (uint32_t)__builtin_ctzll(peers1) : lane;
+            uint32_t old0 = 0, old1 = 0;
+            if (vv[0] && rk0 == 0) old0 = atomicAdd(&wc[dd[0]], (uint32_t)__popcll(peers0));
+            if (vv[1] && rk1 == 0) old1 = atomicAdd(&wc[dd[1]], (uint32_t)__popcll(peers1));
+            old0 = (uint32_t)__builtin_amdgcn_ds_bpermute((int)(ld0 << 2), (int)old0);
+            old1 = (uint32_t)__builtin_amdgcn_ds_bpermute((int)(ld1 << 2), (int)old1);
+            dk[m] = vv[0] ? (dd[0] << 16) | (old0 + rk0) : 0xFFFFFFFFu;  // destination, rank in the wavefront
+            dk[m + 1] = vv[1] ? (dd[1] << 16) | (old1 + rk1) : 0xFFFFFFFFu;
+            mv[m] |= jj[0] << 16;
+            mv[m + 1] |= jj[1] << 16;
         }
         __syncthreads();
         // destination runs in the sub-tile: each wavefront's slot base within its destination's
@@ -567,11 +586,11 @@ __global__ __launch_bounds__(kWideThreads) void k_part_scatter_wide(
                 const uint32_t d = dk[m] >> 16, lr = dk[m] & 0xFFFFu;
                 const uint32_t slot = wc[d] + lr;
                 srec[slot] = (uint64_t)kv[m] | ((uint64_t)mv[m] << 32);
-                spos[slot] = gbase[d] + slot;
+                sdst[slot] = (uint16_t)d;
             }
         }
         __syncthreads();
-        for (uint32_t q = tid; q < total; q += kWideThreads) rc[spos[q]] = srec[q];
+        for (uint32_t q = tid; q < total; q += kWideThreads) rc[gbase[sdst[q]] + q] = srec[q];
         __syncthreads();
     }
 }
