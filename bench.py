@@ -251,6 +251,15 @@ def run_sweep(args):
     return out
 
 
+def check_graph_errors(gs):
+    """The device error words of every buffer set a captured schedule used (they accumulate
+    over the replays): zero, or the bench stops."""
+    import numpy as np
+    for p in [gs.first] + list(gs.slots):
+        e = int(p.err.cpu().numpy().view(np.uint32)[0])
+        assert e == 0, f"device error word {e:#x} after the graph replays"
+
+
 def sweep_traffic():
     """HBM bytes per replay stage from the committed counter summary of the sweep, or None
     when the replay's sources changed since the counters were taken."""
@@ -414,6 +423,7 @@ def main():
                 gs.replay_graph()
             torch.cuda.synchronize()
             t1 = time.perf_counter()
+            check_graph_errors(gs)
     else:
         cs = ChunkStream(wl, device="cuda:0")
         for _ in range(args.warmup):
@@ -439,6 +449,7 @@ def main():
                 gs.replay_graph()
             torch.cuda.synchronize()
             t1 = time.perf_counter()
+            check_graph_errors(gs)
     n_plans = last.plans.num_plans
     ms_step = (t1 - t0) * 1e3 / args.steps
     one_build_us = None if args.no_unbatched else one_plan_build_us(wl, last, torch)

@@ -1246,6 +1246,7 @@ inline ReplayWs replay_layout(void* base, uint64_t n, uint32_t P, uint32_t R)
 struct ReplayArgs {
     WArg wa;
     uint32_t classes;
+    uint32_t seg_short;  // the shortest segment of this call's candidates
 };
 
 inline cr_status replay_args(uint64_t n, uint32_t J, uint32_t P, uint32_t R, const uint32_t* W, uint32_t max_W,
@@ -1257,10 +1258,13 @@ inline cr_status replay_args(uint64_t n, uint32_t J, uint32_t P, uint32_t R, con
     ra->wa = WArg{};
     ra->wa.seg_min = (uint32_t)(((uint64_t)n * P + kSegTarget - 1) / kSegTarget);
     ra->classes = 0;
+    ra->seg_short = 0xFFFFFFFFu;
     for (uint32_t c = 0; c < P; ++c) {
         if (W[c] == 0 || W[c] > max_W) return CR_EINVAL;
         ra->wa.W[c] = (uint16_t)W[c];
         ra->classes |= slot_class(W[c]);
+        const uint32_t S = seg_len(W[c], ra->wa.seg_min);
+        ra->seg_short = S < ra->seg_short ? S : ra->seg_short;
     }
     if (ws_bytes < replay_layout(nullptr, n, P, R).bytes) return CR_ESIZE;
     return CR_OK;
@@ -1372,7 +1376,10 @@ extern "C" cr_status cr_replay_lru(const uint32_t* prefix_len, uint32_t num_keys
         return CR_EINVAL;
     const ReplayWs w = replay_layout(ws_base(ws), n, P, R);
     const hipStream_t st = as_stream(stream);
-    const uint64_t items = max_items(n, P, R);
+    // Work items: at most one per stream plus one per full segment, and no segment is shorter
+    // than seg_short, so P R + P n / seg_short bounds them (at most P R + 16,384 + 1, since
+    // seg_short >= n P / 16,384); the bitmap is sized by the looser max_items.
+    const uint64_t items = (uint64_t)P * R + (uint64_t)P * n / ra.seg_short + 1u;
     const uint64_t blocks = (items + (kReplayThreads / 64) - 1) / (kReplayThreads / 64);
     if (blocks > 0x7FFFFFFFull) return CR_EINVAL;
     (void)hipGetLastError();
