@@ -199,7 +199,7 @@ def run_sweep(args):
         "count": dict(kernel="k_count_*", bound="hbm", unit="GB/s", work=4.0 * n, peak=HBM_PEAK_GBS),
         "route": dict(kernel="k_route_group<true,1> + group tables", bound="hbm", unit="GB/s",
                       work=(4.0 + 2.0 * P) * n, peak=HBM_PEAK_GBS),
-        "lru": dict(kernel="k_replay<1,2,4,8> (one cr_replay_lru call)", bound="alu", unit="Glane-op/s",
+        "lru": dict(kernel="k_replay<1..8> (one cr_replay_lru call)", bound="alu", unit="Glane-op/s",
                     work=lru_work, peak=ALU_PEAK_GOPS),
     }
     for k, v in kern.items():
@@ -472,8 +472,7 @@ def main():
                       peak=ALU_PEAK_GOPS),
         # LRU: every request compares its key with the W slots and moves up to W of them one
         # place (a move-to-front list: one compare and one shift per slot).
-        "lru": dict(kernel="k_replay<%d>" % max({1 if c.W <= 64 else 2 if c.W <= 128 else 4 if c.W <= 256 else 8
-                                                 for c in wl.candidates}), bound="alu", unit="Glane-op/s",
+        "lru": dict(kernel="k_replay<%d>" % max((c.W + 63) // 64 for c in wl.candidates), bound="alu", unit="Glane-op/s",
                     work=float(sum(2.0 * c.W for c in wl.candidates)) * n, peak=ALU_PEAK_GOPS),
     }
     for k, v in kern.items():

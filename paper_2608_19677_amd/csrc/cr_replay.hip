@@ -18,12 +18,14 @@
 // lane i holds the i-th most recent key. A lookup is one compare and a ballot; the first
 // set bit p is the hit depth, and the update shifts lanes 0..p (all lanes on a miss) up
 // by one and writes the key into lane 0, a single select between a lane and its left
-// neighbour under a scalar mask. Above 64 slots the list is interleaved over SL registers
-// (position SL * lane + s in register s), so that moving a position back by one is a copy
-// from register s-1 in the same lane, and only the last register wraps into register 0 of
-// the next lane through a one-lane DPP shift; an access is SL compares and SL selects
-// under scalar masks, without branches. Neither form needs a per-request search or
-// reduction.
+// neighbour under a scalar mask. Above 64 slots the list takes SL = ceil(W / 64)
+// registers. Up to 256 slots it is interleaved over them (position SL * lane + s in
+// register s), so that moving a position back by one is a copy from register s-1 in the
+// same lane, and only the last register wraps into register 0 of the next lane through a
+// one-lane DPP shift; an access is SL compares and SL selects under scalar masks, without
+// branches. Above 256 slots it is two-level: the 64 most recent keys in a front register
+// that every access updates like the one-register list, the rest interleaved behind it and
+// touched only when the front misses. No form needs a per-request search or reduction.
 #include "cr_common.h"
 
 namespace cr {
@@ -54,10 +56,17 @@ __host__ __device__ __forceinline__ uint32_t seg_len(uint32_t W, uint32_t seg_mi
     return s < kSegFloor ? kSegFloor : (s > 65536u ? 65536u : s);
 }
 
+// Registers per lane of a W-slot list: ceil(W / 64), 1 .. 8. An access costs about one
+// compare and one select per register, so each W gets the fewest that hold it.
 __host__ __device__ __forceinline__ uint32_t slot_class(uint32_t W)
 {
-    return W <= 64 ? 1u : (W <= 128 ? 2u : (W <= 256 ? 4u : 8u));
+    const uint32_t sl = (W + 63u) / 64u;
+    return sl < 1u ? 1u : (sl > 8u ? 8u : sl);
 }
+
+// Lists of 5 registers and more are two-level (a 64-key front and the rest behind it):
+// measured faster there than interleaved, and slower than interleaved with 3 back registers.
+constexpr uint32_t kTwoLevelFrom = 5;
 
 struct PartGeom {
     uint64_t tile;
@@ -1245,7 +1254,7 @@ inline ReplayWs replay_layout(void* base, uint64_t n, uint32_t P, uint32_t R)
 
 struct ReplayArgs {
     WArg wa;
-    uint32_t classes;
+    uint32_t classes;    // bit SL - 1: some candidate's list has SL registers
     uint32_t seg_short;  // the shortest segment of this call's candidates
 };
 
@@ -1262,7 +1271,7 @@ inline cr_status replay_args(uint64_t n, uint32_t J, uint32_t P, uint32_t R, con
     for (uint32_t c = 0; c < P; ++c) {
         if (W[c] == 0 || W[c] > max_W) return CR_EINVAL;
         ra->wa.W[c] = (uint16_t)W[c];
-        ra->classes |= slot_class(W[c]);
+        ra->classes |= 1u << (slot_class(W[c]) - 1u);
         const uint32_t S = seg_len(W[c], ra->wa.seg_min);
         ra->seg_short = S < ra->seg_short ? S : ra->seg_short;
     }
@@ -1388,15 +1397,13 @@ extern "C" cr_status cr_replay_lru(const uint32_t* prefix_len, uint32_t num_keys
     hipLaunchKernelGGL((k_replay<SL, TWO, SEQ>), dim3((uint32_t)(NB)), dim3(kReplayThreads), 0, st, w.rec, n,        \
                        w.grp_off, w.item_off, P, R, num_keys, J, prefix_len, ra.wa, max_W, lru_in, lru_out, stats,    \
                        w.aborted, err)
-    // two-level lists only for the largest class: measured slower with three back registers
-    if (ra.classes & 1u) CR_REPLAY(1, false, false, blocks);
-    if (ra.classes & 2u) CR_REPLAY(2, false, false, blocks);
-    if (ra.classes & 4u) CR_REPLAY(4, false, false, blocks);
-    if (ra.classes & 8u) CR_REPLAY(8, true, false, blocks);
-    if (ra.classes & 1u) CR_REPLAY(1, false, true, blocks);
-    if (ra.classes & 2u) CR_REPLAY(2, false, true, blocks);
-    if (ra.classes & 4u) CR_REPLAY(4, false, true, blocks);
-    if (ra.classes & 8u) CR_REPLAY(8, true, true, blocks);
+#define CR_CLASS(SL, SEQ) \
+    if (ra.classes & (1u << ((SL) - 1))) CR_REPLAY(SL, (SL) >= kTwoLevelFrom, SEQ, blocks)
+    CR_CLASS(1, false); CR_CLASS(2, false); CR_CLASS(3, false); CR_CLASS(4, false);
+    CR_CLASS(5, false); CR_CLASS(6, false); CR_CLASS(7, false); CR_CLASS(8, false);
+    CR_CLASS(1, true); CR_CLASS(2, true); CR_CLASS(3, true); CR_CLASS(4, true);
+    CR_CLASS(5, true); CR_CLASS(6, true); CR_CLASS(7, true); CR_CLASS(8, true);
+#undef CR_CLASS
 #undef CR_REPLAY
     return hipGetLastError() == hipSuccess ? CR_OK : CR_EHIP;
 }

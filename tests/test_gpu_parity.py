@@ -61,6 +61,12 @@ SMALL = [
     (16, 50, 1_000_000, 1, [60, 100, 200, 512], 5, 0, 0.0, [(1, 1)]),
     # 60 keys over three destinations: long streams, budget exhausted in most segments
     (17, 60, 300_000, 3, [64, 300], 7, 2, 0.5, [(1, 1), (1, 2)]),
+    # every list size from 2 to 8 registers, full ones (W = 64 SL) among them: 3,000 keys
+    # over six destinations fill every list
+    (18, 3000, 120_000, 6, [192, 193, 320, 321, 384, 385, 448, 449], 3, 2, 0.3, [(1, 1)]),
+    # 80 keys over two destinations with 150 to 420 slots: no rebuild of the 3- to 7-register
+    # lists finds W keys, so their streams go through the sequential pass
+    (19, 80, 400_000, 2, [150, 310, 350, 420], 3, 0, 0.0, [(1, 1)]),
 ]
 
 
