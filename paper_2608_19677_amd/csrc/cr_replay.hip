@@ -13,7 +13,10 @@
 //        recent W distinct keys seen at that destination (carried state appended), so a
 //        wavefront rebuilds it by scanning backwards, then replays its segment. This
 //        turns R*P sequential streams into thousands of independent wavefronts with
-//        results identical to one sequential pass.
+//        results identical to one sequential pass;
+//   k_replay_grp<G>
+//        lists of at most 16 slots in calls with one interval: G = 4 or 8 segments per
+//        wavefront, one per lane group (below).
 // The LRU lives in registers. Up to 64 slots it is a move-to-front list across the lanes:
 // lane i holds the i-th most recent key. A lookup is one compare and a ballot; the first
 // set bit p is the hit depth, and the update shifts lanes 0..p (all lanes on a miss) up
@@ -35,6 +38,7 @@ constexpr int kReplayThreads = 256;
 
 struct WArg {
     uint16_t W[CR_MAX_CANDS];
+    uint8_t grp[CR_MAX_CANDS];  // lists per wavefront: G > 1 for k_replay_grp<G>, else 1
     uint32_t seg_min;  // shortest segment for this call's record count
 };
 
@@ -48,12 +52,26 @@ constexpr uint32_t kSegFloor = 1024;
 constexpr uint32_t kSegPerSlot = 16;
 
 // Records per segment: at least kSegPerSlot W (the rebuild scans back to W distinct keys)
-// and at least the share that keeps the number of segments near kSegTarget.
-__host__ __device__ __forceinline__ uint32_t seg_len(uint32_t W, uint32_t seg_min)
+// and at least the share that keeps the number of segments near kSegTarget. A candidate
+// whose wavefronts hold G lists (k_replay_grp) takes segments G times shorter, so that it
+// still has as many wavefronts.
+__host__ __device__ __forceinline__ uint32_t seg_len(uint32_t W, uint32_t seg_min, uint32_t G)
 {
     uint32_t s = kSegPerSlot * W;
     s = s > seg_min ? s : seg_min;
-    return s < kSegFloor ? kSegFloor : (s > 65536u ? 65536u : s);
+    s = s < kSegFloor ? kSegFloor : (s > 65536u ? 65536u : s);
+    if (G > 1u) s = s / G < kSegFloor ? kSegFloor : s / G;
+    return s;
+}
+
+// Lists per wavefront of a W-slot list in k_replay_grp (lane groups of 64 / G lanes), or 1
+// for the one-wavefront-per-list kernels. Only calls with one interval: the grouped kernel
+// keeps one set of statistics per segment. Two lists per wavefront (W <= 32) measured
+// slower than one on the 1e8-request sweep (10.2 against 7.2 ms for its W = 26 plans).
+__host__ __device__ __forceinline__ uint32_t grp_of(uint32_t W, uint32_t J)
+{
+    if (J != 1u || W > 16u) return 1u;
+    return W <= 8u ? 8u : 4u;
 }
 
 // Registers per lane of a W-slot list: ceil(W / 64), 1 .. 8. An access costs about one
@@ -611,7 +629,7 @@ __global__ __launch_bounds__(kWideThreads) void k_part_scatter_wide(
 // Pass one scans over all (c, d) in one block; pass two rebases grp_off per candidate.
 __global__ __launch_bounds__(1024) void k_seg_items(const uint32_t* __restrict__ dtot, uint32_t P, uint32_t R,
                                                     WArg wa, uint32_t* __restrict__ grp_off,
-                                                    uint32_t* __restrict__ item_off)
+                                                    uint32_t* __restrict__ item_off, uint32_t* __restrict__ gwave_off)
 {
     issue_priority_high();
     __shared__ uint32_t s_scan[16];
@@ -623,7 +641,7 @@ __global__ __launch_bounds__(1024) void k_seg_items(const uint32_t* __restrict__
         uint32_t cnt = 0, nseg = 0;
         if (e < total) {
             cnt = dtot[e];
-            const uint32_t S = seg_len(wa.W[e / R], wa.seg_min);
+            const uint32_t S = seg_len(wa.W[e / R], wa.seg_min, wa.grp[e / R]);
             nseg = cnt ? (cnt + S - 1) / S : 1u;
         }
         uint32_t tot, itot;
@@ -649,6 +667,16 @@ __global__ __launch_bounds__(1024) void k_seg_items(const uint32_t* __restrict__
     }
     for (uint32_t c = threadIdx.x; c < P; c += blockDim.x)
         grp_off[(uint64_t)c * (R + 1u) + R] = s_cstart[c + 1] - s_cstart[c];
+    // gwave_off[c]: first k_replay_grp wavefront of candidate c (G work items per wavefront;
+    // none for candidates replayed one list per wavefront)
+    __syncthreads();
+    const uint32_t c = threadIdx.x;
+    const uint32_t G = c < P ? wa.grp[c] : 1u;
+    const uint32_t nw = G > 1u ? (item_off[(c + 1u) * R] - item_off[c * R] + G - 1u) / G : 0u;
+    uint32_t wtot;
+    const uint32_t wex = block_exscan_u32(nw, s_scan, &wtot);  // P <= CR_MAX_CANDS <= blockDim.x
+    if (c < P) gwave_off[c] = wex;
+    if (c == 0) gwave_off[P] = wtot;
 }
 
 template <int SL>
@@ -1008,9 +1036,10 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
     const uint32_t c = lo / R, d = lo % R;
     const uint32_t W = wa.W[c];
     if (slot_class(W) != (uint32_t)SL) return;
+    if (!kSeq && wa.grp[c] > 1u) return;  // k_replay_grp's segments (its marked ones come here in kSeq)
     const uint32_t* go = grp_off + (uint64_t)c * (R + 1u);
     const uint32_t gs = go[d], cnt = go[d + 1] - gs;
-    const uint32_t S = seg_len(W, wa.seg_min);
+    const uint32_t S = seg_len(W, wa.seg_min, wa.grp[c]);
     // [s0, s1): the records this wavefront replays; [s0, sc) of them are replayed only to
     // reach the state at sc (the run's predecessor in the kSeq pass)
     uint64_t i0 = item, i1 = item + 1;
@@ -1208,6 +1237,265 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
     }
 }
 
+// ---------------------------------------------------------------------------------------
+// Small lists, several segments per wavefront (calls with one interval). A list of
+// W <= 64 / G slots needs W lanes, so a wavefront keeps G lists side by side in lane groups
+// of w = 64 / G lanes (group g: lanes g w .. g w + w - 1, position j in lane g w + j), each
+// replaying its own segment, and one instruction advances all G of them. Per step, group g
+// reads its record's key from LDS into all of its lanes; one compare gives the hit mask m
+// (at most one lane per group). With END the lanes of position W - 1 and START those of
+// position 0, M = m | END has a set bit in every group and its lowest one at or above the
+// group's START is the hit (or position W - 1 on a miss), so the borrow of M - START runs
+// exactly over positions 0 .. hit of each group: M ^ (M - START) is the set of lanes that
+// move back by one, in every group at once. The move is one select with a wave_shr:1 DPP
+// source, and the key goes into each group's position 0 by a second select. Groups without
+// a record at a step (segment ended, key out of range) read a marker key that matches no
+// slot and are masked out of both selects.
+//
+// The state before a segment is rebuilt forward: the D records before it are replayed from
+// an empty list (from the carried state where the window reaches the stream start). When
+// the window holds W distinct keys the list is exactly the W most recent ones, so it is full
+// when it is right; otherwise D grows, up to the budget of the backward rebuild
+// (kRebuildBudget S rounded up to whole 64-record batches). A segment whose window still
+// holds fewer than W distinct keys there is marked in `aborted` under the same condition as
+// the backward rebuild's, and the kSeq pass of k_replay<1> replays it from its predecessor.
+//
+// Statistics: a step's hit is the bit of the lane that held its key; each lane shifts its
+// bits into a register, and after a round of 64 steps the group's registers, OR-ed, give the
+// round's hits. Every lane then adds the count, suffix + prefix lengths and the prefix
+// lengths of the hits over the records it staged; the group's lanes are summed at the end.
+constexpr uint32_t kGrpSent = 0xFFFFFFFEu;  // staged key of a skipped step: never a key (K <= 0xFFFFFFFE), never empty
+
+// Positions 0 .. hit of every group move back by one: lanes with `keep` set hold their key,
+// the others take their left neighbour's (a wave_shr:1 DPP source). The destination is the
+// source, so lane 0, which has no left neighbour, keeps its key.
+__device__ __forceinline__ void grp_move(uint32_t& sk, uint64_t movebits, uint64_t act)
+{
+    asm("s_nand_b64 vcc, %1, %2\n\t"
+        "v_cndmask_b32_dpp %0, %0, %0, vcc wave_shr:1 row_mask:0xf bank_mask:0xf"
+        : "+v"(sk)
+        : "s"(movebits), "s"(act)
+        : "vcc");
+}
+
+// h = 2 h + (this lane's bit of m): one add with carry-in
+__device__ __forceinline__ void shift_in_lane_bit(uint32_t& h, uint64_t m)
+{
+    uint64_t dummy;
+    asm("v_addc_co_u32 %0, %1, %0, %0, %2" : "+v"(h), "=s"(dummy) : "s"(m));
+}
+
+template <int G>
+__global__ __launch_bounds__(kReplayThreads) void k_replay_grp(
+    const uint64_t* __restrict__ rec, uint64_t n, const uint32_t* __restrict__ grp_off,
+    const uint32_t* __restrict__ item_off, const uint32_t* __restrict__ gwave_off, uint32_t P, uint32_t R, uint32_t K,
+    const uint32_t* __restrict__ prefix_len, WArg wa, uint32_t max_W, const uint32_t* __restrict__ lru_in,
+    uint32_t* __restrict__ lru_out, uint64_t* __restrict__ stats, uint32_t* __restrict__ aborted,
+    uint32_t* __restrict__ err)
+{
+    constexpr uint32_t w = 64u / G;
+    constexpr uint32_t kStride = 65u;  // keys per group in the stage (padded: groups on other banks)
+    __shared__ uint32_t s_stage[kReplayThreads / 64][G * kStride];
+    const uint32_t lane = lane_id(), wv = wave_in_block();
+    const uint32_t g = lane / w, j = lane % w;
+    const uint32_t wid = blockIdx.x * (kReplayThreads / 64u) + wv;
+    if (wid >= gwave_off[P]) return;
+    uint32_t c = 0;  // the candidate: the last c with gwave_off[c] <= wid
+    {
+        uint32_t hi = P;
+        while (hi - c > 1) {
+            const uint32_t mid = (c + hi) >> 1;
+            if (gwave_off[mid] <= wid) c = mid;
+            else hi = mid;
+        }
+    }
+    if (wa.grp[c] != (uint32_t)G) return;
+    const uint32_t W = wa.W[c];
+    const uint64_t it1 = item_off[(uint64_t)(c + 1) * R];
+    const uint64_t item = item_off[(uint64_t)c * R] + (uint64_t)G * (wid - gwave_off[c]) + g;
+    bool live = item < it1;
+    uint32_t lo = c * R;  // the item's stream
+    if (live) {
+        uint32_t hi = (c + 1) * R;
+        while (hi - lo > 1) {
+            const uint32_t mid = (lo + hi) >> 1;
+            if (item_off[mid] <= item) lo = mid;
+            else hi = mid;
+        }
+    }
+    const uint32_t d = lo - c * R;
+    const uint32_t S = seg_len(W, wa.seg_min, G);
+    const uint32_t* go = grp_off + (uint64_t)c * (R + 1u);
+    const uint32_t gs = live ? go[d] : 0u, cnt = live ? go[d + 1] - gs : 0u;
+    const uint64_t s0w = live ? (item - item_off[lo]) * (uint64_t)S : 0u;
+    live = live && s0w <= cnt;
+    const uint32_t s0 = live ? (uint32_t)s0w : 0u;
+    const uint64_t s1w = s0w + S;
+    const uint32_t s1 = live ? (s1w < cnt ? (uint32_t)s1w : cnt) : 0u;
+    const uint64_t* __restrict__ rl = rec + (uint64_t)c * n + gs;
+    uint32_t* __restrict__ stage = s_stage[wv] + g * kStride;
+
+    uint64_t START = 0, END = 0;
+#pragma unroll
+    for (uint32_t q = 0; q < G; ++q) {
+        START |= 1ull << (q * w);
+        END |= 1ull << (q * w + W - 1u);
+    }
+    uint32_t sk = CR_EMPTY_SLOT;
+    bool bad = false;
+    uint32_t a_hit = 0, a_req = 0;
+    uint64_t a_hp = 0, a_all = 0;
+
+    // One step of every group: key kv (kGrpSent: none). With hb, each lane shifts its hit
+    // bit of the step into hb (hb = 2 hb + hit: after 32 steps, step t is bit 31 - t).
+    auto step = [&](uint32_t kv, uint32_t* hb) {
+        const uint64_t m = ballot(sk == kv);
+        const uint64_t act = ballot(kv != kGrpSent);
+        const uint64_t M = m | END;
+        grp_move(sk, M ^ (M - START), act);
+        sk = __builtin_amdgcn_inverse_ballot_w64(START & act) ? kv : sk;
+        if (hb) shift_in_lane_bit(*hb, m);
+    };
+    // Records [a, a + len) of each group's stream through its list, in rounds of 64 steps:
+    // lane j of a group stages the keys of steps j, j + w, ... of its group in LDS. The next
+    // round's records are loaded while a round runs. With statistics, the prefix lengths of
+    // a round's records are gathered as it starts and used once it has run: every round is
+    // 64 steps (idle ones at the end of a group's range), and the hit bits of the group's
+    // lanes, OR-ed together, say which of its steps hit.
+    auto run = [&](uint32_t a, uint32_t len, bool with_stats) {
+        uint32_t most = len;
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) {
+            const uint32_t x = __shfl_xor(most, o, 64);
+            most = x > most ? x : most;
+        }
+        most = __builtin_amdgcn_readfirstlane(most);
+        uint64_t rv[G];
+#pragma unroll
+        for (uint32_t i = 0; i < G; ++i) {
+            const uint32_t t = j + w * i;
+            rv[i] = t < len ? rl[a + t] : 0ull;
+        }
+        for (uint32_t t0 = 0; t0 < most; t0 += 64u) {
+            uint32_t key[G], sfx[G];
+            bool ok[G];
+#pragma unroll
+            for (uint32_t i = 0; i < G; ++i) {
+                const uint32_t t = t0 + j + w * i;
+                key[i] = (uint32_t)rv[i];
+                sfx[i] = (uint32_t)(rv[i] >> 32) & 0xFFFFu;
+                ok[i] = t < len && key[i] < K;
+                bad |= t < len && key[i] >= K;
+                stage[j + w * i] = ok[i] ? key[i] : kGrpSent;
+            }
+            uint32_t pl[G];
+            if (with_stats) {
+#pragma unroll
+                for (uint32_t i = 0; i < G; ++i) pl[i] = prefix_len[ok[i] ? key[i] : 0u];
+            }
+#pragma unroll
+            for (uint32_t i = 0; i < G; ++i) {  // the next round's records
+                const uint32_t t = t0 + 64u + j + w * i;
+                rv[i] = t < len ? rl[a + t] : 0ull;
+            }
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            if (with_stats) {
+                uint32_t h0 = 0, h1 = 0;
+#pragma unroll
+                for (uint32_t t = 0; t < 32u; ++t) step(stage[t], &h0);
+#pragma unroll
+                for (uint32_t t = 32; t < 64u; ++t) step(stage[t], &h1);
+#pragma unroll
+                for (uint32_t o = w / 2; o >= 1; o >>= 1) {
+                    h0 |= __shfl_xor(h0, o, 64);
+                    h1 |= __shfl_xor(h1, o, 64);
+                }
+                if (j == 0) a_hit += __builtin_popcount(h0) + __builtin_popcount(h1);
+#pragma unroll
+                for (uint32_t i = 0; i < G; ++i) {
+                    const uint32_t t = j + w * i;
+                    const bool hit = ((t < 32u ? h0 >> (31u - t) : h1 >> (63u - t)) & 1u) != 0u;
+                    a_req += ok[i] ? 1u : 0u;
+                    a_all += ok[i] ? (uint64_t)sfx[i] + pl[i] : 0ull;
+                    a_hp += ok[i] && hit ? (uint64_t)pl[i] : 0ull;
+                }
+            } else {
+                const uint32_t nt = most - t0 < 64u ? most - t0 : 64u;
+                if (nt == 64u) {
+#pragma unroll 16
+                    for (uint32_t t = 0; t < 64u; ++t) step(stage[t], nullptr);
+                } else {
+                    for (uint32_t t = 0; t < nt; ++t) step(stage[t], nullptr);
+                }
+            }
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        }
+    };
+    // The carried state of the groups in `on`, oldest entry first, through their lists: the
+    // entries before the row's first empty slot, keys >= K skipped, as the backward rebuild
+    // appends them.
+    auto carried = [&](bool on) {
+        const uint32_t* __restrict__ li = lru_in + ((uint64_t)c * R + d) * max_W;
+        const uint32_t v = on && j < W ? li[j] : CR_EMPTY_SLOT;
+        uint32_t fe = W;  // the row's first empty slot
+        for (uint32_t i = 0; i < W; ++i) {
+            const uint32_t x = __shfl(v, g * w + i, 64);
+            fe = x == CR_EMPTY_SLOT && fe == W ? i : fe;
+        }
+        for (uint32_t i = W; i-- > 0;) {
+            const uint32_t x = __shfl(v, g * w + i, 64);
+            step(on && i < fe && x < K ? x : kGrpSent, nullptr);
+        }
+    };
+
+    // rebuild the state at s0
+    const uint32_t budget = (kRebuildBudget * S + 63u) & ~63u;
+    const uint32_t dmax = s0 < budget ? s0 : budget;
+    bool ready = !live || s0 == 0;
+    if (lru_in && ballot(live && s0 == 0)) carried(live && s0 == 0);
+    for (uint32_t D = 4u * W; ballot(!ready) != 0; D *= 8u) {
+        const bool part = !ready;
+        const uint32_t dg = D < dmax ? D : dmax;
+        sk = part ? CR_EMPTY_SLOT : sk;
+        if (lru_in && ballot(part && dg == s0)) carried(part && dg == s0);
+        run(s0 - dg, part ? dg : 0u, false);
+        const uint64_t F = ballot(j == W - 1u && sk != CR_EMPTY_SLOT);
+        const bool full = (F >> (g * w + W - 1u)) & 1ull;
+        const bool ok = part && (full || dg == s0);
+        if (part && !ok && dg == dmax) {  // too few distinct keys in reach: left to the kSeq pass
+            if (j == 0) atomicOr(&aborted[item >> 5], 1u << (item & 31u));
+            live = false;
+        }
+        ready = ready || ok || (part && dg == dmax);
+    }
+    run(s0, live ? s1 - s0 : 0u, true);
+    if (ballot(bad) && lane == 0) atomicOr(err, CR_ERR_KEY_RANGE);
+    // the group's sums in its lane 0
+#pragma unroll
+    for (uint32_t o = w / 2; o >= 1; o >>= 1) {
+        a_hit += __shfl_xor(a_hit, o, 64);
+        a_req += __shfl_xor(a_req, o, 64);
+        a_hp += (uint64_t)__shfl_xor((unsigned long long)a_hp, o, 64);
+        a_all += (uint64_t)__shfl_xor((unsigned long long)a_all, o, 64);
+    }
+    if (live && j == 0) {
+        unsigned long long* st = (unsigned long long*)(stats + ((uint64_t)c * R + d) * 4u);  // interval 0
+        atomicAdd(st + 0, (unsigned long long)a_req);
+        if (a_hit) atomicAdd(st + 1, (unsigned long long)a_hit);
+        atomicAdd(st + 2, (unsigned long long)(a_all - a_hp));
+        if (a_hp) atomicAdd(st + 3, (unsigned long long)a_hp);
+    }
+    if (live && s1 == cnt) {
+        uint32_t* __restrict__ lo_ = lru_out + ((uint64_t)c * R + d) * max_W;
+        if (j < W) lo_[j] = sk;
+        for (uint32_t idx = W + j; idx < max_W; idx += w) lo_[idx] = CR_EMPTY_SLOT;
+    }
+}
+
 __global__ void k_zero_u32(uint32_t* __restrict__ p, uint64_t n)
 {
     const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
@@ -1220,6 +1508,7 @@ struct ReplayWs {
     uint32_t* dtot;
     uint32_t* grp_off;
     uint32_t* item_off;
+    uint32_t* gwave_off;  // [P + 1] first k_replay_grp wavefront of each candidate
     uint32_t* aborted;  // bit per work item: its rebuild ran out of budget
     uint64_t flag_words;
     size_t bytes;
@@ -1245,6 +1534,8 @@ inline ReplayWs replay_layout(void* base, uint64_t n, uint32_t P, uint32_t R)
     o = up(o + (uint64_t)P * (R + 1u) * 4u);
     w.item_off = reinterpret_cast<uint32_t*>(b + o);
     o = up(o + ((uint64_t)P * R + 1u) * 4u);
+    w.gwave_off = reinterpret_cast<uint32_t*>(b + o);
+    o = up(o + ((uint64_t)P + 1u) * 4u);
     w.aborted = reinterpret_cast<uint32_t*>(b + o);
     w.flag_words = (max_items(n, P, R) + 31u) / 32u;
     o = up(o + w.flag_words * 4u);
@@ -1255,7 +1546,10 @@ inline ReplayWs replay_layout(void* base, uint64_t n, uint32_t P, uint32_t R)
 struct ReplayArgs {
     WArg wa;
     uint32_t classes;    // bit SL - 1: some candidate's list has SL registers
+    uint32_t wclasses;   // the same, candidates replayed one list per wavefront only
     uint32_t seg_short;  // the shortest segment of this call's candidates
+    uint32_t groups;     // bit G: some candidate is replayed by k_replay_grp<G>
+    uint64_t grp_waves;  // bound on k_replay_grp wavefronts
 };
 
 inline cr_status replay_args(uint64_t n, uint32_t J, uint32_t P, uint32_t R, const uint32_t* W, uint32_t max_W,
@@ -1267,13 +1561,23 @@ inline cr_status replay_args(uint64_t n, uint32_t J, uint32_t P, uint32_t R, con
     ra->wa = WArg{};
     ra->wa.seg_min = (uint32_t)(((uint64_t)n * P + kSegTarget - 1) / kSegTarget);
     ra->classes = 0;
+    ra->wclasses = 0;
     ra->seg_short = 0xFFFFFFFFu;
+    ra->groups = 0;
+    ra->grp_waves = 0;
     for (uint32_t c = 0; c < P; ++c) {
         if (W[c] == 0 || W[c] > max_W) return CR_EINVAL;
         ra->wa.W[c] = (uint16_t)W[c];
+        const uint32_t G = grp_of(W[c], J);
+        ra->wa.grp[c] = (uint8_t)G;
         ra->classes |= 1u << (slot_class(W[c]) - 1u);
-        const uint32_t S = seg_len(W[c], ra->wa.seg_min);
+        if (G == 1u) ra->wclasses |= 1u << (slot_class(W[c]) - 1u);
+        const uint32_t S = seg_len(W[c], ra->wa.seg_min, G);
         ra->seg_short = S < ra->seg_short ? S : ra->seg_short;
+        if (G > 1u) {  // at most R + n / S work items, G per wavefront
+            ra->groups |= 1u << G;
+            ra->grp_waves += ((uint64_t)R + n / S) / G + 1u;
+        }
     }
     if (ws_bytes < replay_layout(nullptr, n, P, R).bytes) return CR_ESIZE;
     return CR_OK;
@@ -1349,7 +1653,8 @@ extern "C" cr_status cr_replay_partition(const uint32_t* keys, const uint16_t* s
         hipLaunchKernelGGL(k_part_hist<false>, dim3((uint32_t)g.ntiles, P), dim3(kHistThreads), (size_t)R * 4u, st, dest,
                            n, R, g.tile, g.ntiles, w.tcnt, err);
     hipLaunchKernelGGL(k_scan_dest, dim3(R, P), dim3(kScanThreads), 0, st, w.tcnt, g.ntiles, R, w.dtot);
-    hipLaunchKernelGGL(k_seg_items, dim3(1), dim3(1024), 0, st, w.dtot, P, R, ra.wa, w.grp_off, w.item_off);
+    hipLaunchKernelGGL(k_seg_items, dim3(1), dim3(1024), 0, st, w.dtot, P, R, ra.wa, w.grp_off, w.item_off,
+                       w.gwave_off);
     if (g.ntiles && R <= 64 && vec)
         hipLaunchKernelGGL(k_part_scatter64<true>, dim3(xcd_grid((uint32_t)g.ntiles), P), dim3(64),
                            scatter64_lds_bytes(R), st, keys, suffix, dest, n, off, J, R, g.tile, g.ntiles, w.tcnt,
@@ -1390,7 +1695,8 @@ extern "C" cr_status cr_replay_lru(const uint32_t* prefix_len, uint32_t num_keys
     // seg_short >= n P / 16,384); the bitmap is sized by the looser max_items.
     const uint64_t items = (uint64_t)P * R + (uint64_t)P * n / ra.seg_short + 1u;
     const uint64_t blocks = (items + (kReplayThreads / 64) - 1) / (kReplayThreads / 64);
-    if (blocks > 0x7FFFFFFFull) return CR_EINVAL;
+    const uint64_t gblocks = (ra.grp_waves + (kReplayThreads / 64) - 1) / (kReplayThreads / 64);
+    if (blocks > 0x7FFFFFFFull || gblocks > 0x7FFFFFFFull) return CR_EINVAL;
     (void)hipGetLastError();
     hipLaunchKernelGGL(k_zero_u32, dim3(256), dim3(256), 0, st, w.aborted, w.flag_words);
 #define CR_REPLAY(SL, TWO, SEQ, NB)                                                                                 \
@@ -1398,9 +1704,17 @@ extern "C" cr_status cr_replay_lru(const uint32_t* prefix_len, uint32_t num_keys
                        w.grp_off, w.item_off, P, R, num_keys, J, prefix_len, ra.wa, max_W, lru_in, lru_out, stats,    \
                        w.aborted, err)
 #define CR_CLASS(SL, SEQ) \
-    if (ra.classes & (1u << ((SL) - 1))) CR_REPLAY(SL, (SL) >= kTwoLevelFrom, SEQ, blocks)
+    if ((SEQ ? ra.classes : ra.wclasses) & (1u << ((SL) - 1))) CR_REPLAY(SL, (SL) >= kTwoLevelFrom, SEQ, blocks)
     CR_CLASS(1, false); CR_CLASS(2, false); CR_CLASS(3, false); CR_CLASS(4, false);
     CR_CLASS(5, false); CR_CLASS(6, false); CR_CLASS(7, false); CR_CLASS(8, false);
+    // several lists per wavefront; their marked segments join the kSeq pass of k_replay<1>
+#define CR_GRP(G)                                                                                                   \
+    if (ra.groups & (1u << (G)))                                                                                     \
+    hipLaunchKernelGGL((k_replay_grp<G>), dim3((uint32_t)gblocks), dim3(kReplayThreads), 0, st, w.rec, n, w.grp_off, \
+                       w.item_off, w.gwave_off, P, R, num_keys, prefix_len, ra.wa, max_W, lru_in, lru_out, stats,     \
+                       w.aborted, err)
+    CR_GRP(4); CR_GRP(8);
+#undef CR_GRP
     CR_CLASS(1, true); CR_CLASS(2, true); CR_CLASS(3, true); CR_CLASS(4, true);
     CR_CLASS(5, true); CR_CLASS(6, true); CR_CLASS(7, true); CR_CLASS(8, true);
 #undef CR_CLASS
