@@ -472,7 +472,8 @@ def main():
                       peak=ALU_PEAK_GOPS),
         # LRU: every request compares its key with the W slots and moves up to W of them one
         # place (a move-to-front list: one compare and one shift per slot).
-        "lru": dict(kernel="k_replay<%d>" % max((c.W + 63) // 64 for c in wl.candidates), bound="alu", unit="Glane-op/s",
+        "lru": dict(kernel="k_replay<%d, %s, false>" % (lambda sl: (sl, "true" if sl >= 5 else "false"))(
+                        max((c.W + 63) // 64 for c in wl.candidates)), bound="alu", unit="Glane-op/s",
                     work=float(sum(2.0 * c.W for c in wl.candidates)) * n, peak=ALU_PEAK_GOPS),
     }
     for k, v in kern.items():

@@ -317,15 +317,24 @@ cr_status cr_replay_partition(const uint32_t* keys, const uint16_t* suffix, cons
 /* Second phase of cr_replay: replays the partitioned workspace (same n, J, P, R, W)
  * through the per-destination LRU caches and accumulates stats. Each segment rebuilds the
  * cache state it starts from by scanning its stream backwards for W distinct keys, at most
- * two segment lengths; a segment whose scan runs out before that (a stretch with fewer than
+ * eight segment lengths; a segment whose scan runs out before that (a stretch with fewer than
  * W distinct keys) is left to a second launch, in which one wavefront per run of such
  * segments replays the segment before the run (without counting it) and then the run, in
- * order. Each request is thus replayed at most twice and scanned at most three times,
+ * order. Each request is thus replayed at most twice and scanned at most nine times,
  * whatever the key mix; the results do not depend on which launch counts them. */
 cr_status cr_replay_lru(const uint32_t* prefix_len, uint32_t num_keys, uint64_t n, uint32_t J,
                         uint32_t P, uint32_t R, const uint32_t* W, uint32_t max_W,
                         const uint32_t* lru_in, uint32_t* lru_out, uint64_t* stats, void* ws,
                         size_t ws_bytes, uint32_t* err, void* stream);
+
+/* Size rule of the replay of small caches (process-wide, not a result): in a call with one
+ * interval (J == 1), the candidates with W <= 16 are replayed several per wavefront (4 or 8
+ * caches side by side) when n times their number is at least min_records (default 2^25);
+ * below that there are too few segments for the grouped form to fill the GPU. The results
+ * are the same either way; 0 makes every such call use the grouped form (for tests). Takes
+ * effect for calls issued after it returns; calls that overlap it in other threads may see
+ * either value. */
+void cr_replay_set_group_min_records(uint64_t min_records);
 
 /* Opaque-key directory (Appendix A.2 "Data handling": the planner needs only the pairs
  * (b, lambda_b), and b may be salted or ephemeral; Section 2.1: the workload summaries

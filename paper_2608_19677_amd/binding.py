@@ -28,7 +28,8 @@ EXPORTS = ("cr_count_rates", "cr_count_slice_workspace_bytes", "cr_count_slice",
            "cr_admit", "cr_admit_noalloc", "cr_plan_sizes", "cr_workspace_bytes", "cr_place_lpt", "cr_place_hash", "cr_route",
            "cr_route_live", "cr_plan_churn", "cr_keymap_bytes", "cr_keymap_workspace_bytes", "cr_keymap_build",
            "cr_keymap_lookup", "cr_keymap_scatter", "cr_replay_workspace_bytes", "cr_lru_state_bytes",
-           "cr_lru_reset", "cr_replay", "cr_replay_partition", "cr_replay_lru", "cr_version")
+           "cr_lru_reset", "cr_replay", "cr_replay_partition", "cr_replay_lru", "cr_replay_set_group_min_records",
+           "cr_version")
 CR_WINDOW_SUM = 0xFFFFFFFFFFFFFFFF
 CR_PLAN_BUFFERS = 16
 CR_GROUP_MULTI, CR_GROUP_COLD = 0xFFFE, 0xFFFF
@@ -71,6 +72,8 @@ def load(path: Optional[str] = None):
         raise CrError(f"{p} is missing: build it with paper_2608_19677_amd/build.py (no fallback exists)")
     L = ctypes.CDLL(p)
     L.cr_count_rates.argtypes = [_P, _u64, _P, _u32, _u32, _P, _P, _P]
+    L.cr_replay_set_group_min_records.argtypes = [_u64]
+    L.cr_replay_set_group_min_records.restype = None
     L.cr_count_slice_workspace_bytes.argtypes = [_u64, _u32]
     L.cr_count_slice_workspace_bytes.restype = ctypes.c_size_t
     L.cr_count_slice.argtypes = [_P, _u64, _u32, _P, _P, _P, ctypes.c_size_t, _P]
@@ -245,6 +248,13 @@ def cr_plan_churn(plans: CrPlanSet, pairs, out, err, stream=None):
 
 def cr_replay_workspace_bytes(n: int, P: int, R: int) -> int:
     return int(load().cr_replay_workspace_bytes(n, P, R))
+
+
+GROUP_MIN_RECORDS_DEFAULT = 1 << 25
+
+
+def cr_replay_set_group_min_records(min_records: int) -> None:
+    load().cr_replay_set_group_min_records(min_records)
 
 
 def cr_replay(keys, suffix, prefix_len, num_keys: int, dest, off, J: int, P: int, R: int, W: Sequence[int],

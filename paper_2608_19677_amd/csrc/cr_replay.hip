@@ -1001,8 +1001,17 @@ __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v)
 // as that segment did, replays it without counting, and then replays the run in order,
 // counting it and writing the final state if the run ends the stream. Each marked record
 // is thus replayed once more, and every record is scanned at most kRebuildBudget + 1 times,
-// whatever the keys.
-constexpr uint32_t kRebuildBudget = 2;
+// whatever the keys. The kSeq launch rebuilds without a budget: a run's predecessor is an
+// unmarked segment, whose rebuild ended within its budget. Eight segment lengths: with two,
+// the whale-dominated destinations of the component ablation (8 keys at 6 % each) sent most
+// of their segments to the serial kSeq pass (1.8 ms per step against 0.01 ms with eight).
+constexpr uint32_t kRebuildBudget = 8;
+
+// Budget of k_replay_grp's forward rebuild, in its own (G times shorter) segment lengths.
+// Its rebuild windows run in lockstep with the other lists of the wavefront, so a deep one
+// holds up G - 1 others: with eight, the 1e8-request sweep's W = 8 and 14 plans took 15.6 ms
+// against 12.7 ms with two (kSeq pass included).
+constexpr uint32_t kGrpRebuildBudget = 2;
 
 __device__ __forceinline__ bool item_marked(const uint32_t* __restrict__ aborted, uint64_t it)
 {
@@ -1255,10 +1264,9 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
 // The state before a segment is rebuilt forward: the D records before it are replayed from
 // an empty list (from the carried state where the window reaches the stream start). When
 // the window holds W distinct keys the list is exactly the W most recent ones, so it is full
-// when it is right; otherwise D grows, up to the budget of the backward rebuild
-// (kRebuildBudget S rounded up to whole 64-record batches). A segment whose window still
-// holds fewer than W distinct keys there is marked in `aborted` under the same condition as
-// the backward rebuild's, and the kSeq pass of k_replay<1> replays it from its predecessor.
+// when it is right; otherwise D grows, up to kGrpRebuildBudget S rounded up to whole
+// 64-record batches. A segment whose window still holds fewer than W distinct keys there is
+// marked in `aborted`, and the kSeq pass of k_replay<1> replays it from its predecessor.
 //
 // Statistics: a step's hit is the bit of the lane that held its key; each lane shifts its
 // bits into a register, and after a round of 64 steps the group's registers, OR-ed, give the
@@ -1453,7 +1461,7 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay_grp(
     };
 
     // rebuild the state at s0
-    const uint32_t budget = (kRebuildBudget * S + 63u) & ~63u;
+    const uint32_t budget = (kGrpRebuildBudget * S + 63u) & ~63u;
     const uint32_t dmax = s0 < budget ? s0 : budget;
     bool ready = !live || s0 == 0;
     if (lru_in && ballot(live && s0 == 0)) carried(live && s0 == 0);
@@ -1552,6 +1560,11 @@ struct ReplayArgs {
     uint64_t grp_waves;  // bound on k_replay_grp wavefronts
 };
 
+// Records (n times the number of candidates with W <= 16) from which a one-interval call
+// replays those candidates by k_replay_grp; below it there are too few segments to fill the
+// chip with a G-th of the wavefronts.
+uint64_t g_grp_min_records = 1ull << 25;
+
 inline cr_status replay_args(uint64_t n, uint32_t J, uint32_t P, uint32_t R, const uint32_t* W, uint32_t max_W,
                              size_t ws_bytes, void* ws, ReplayArgs* ra)
 {
@@ -1565,10 +1578,13 @@ inline cr_status replay_args(uint64_t n, uint32_t J, uint32_t P, uint32_t R, con
     ra->seg_short = 0xFFFFFFFFu;
     ra->groups = 0;
     ra->grp_waves = 0;
+    uint64_t small = 0;  // candidates k_replay_grp could take
+    for (uint32_t c = 0; c < P; ++c) small += grp_of(W[c], J) > 1u ? 1u : 0u;
+    const bool grouped = small > 0 && n * small >= g_grp_min_records;
     for (uint32_t c = 0; c < P; ++c) {
         if (W[c] == 0 || W[c] > max_W) return CR_EINVAL;
         ra->wa.W[c] = (uint16_t)W[c];
-        const uint32_t G = grp_of(W[c], J);
+        const uint32_t G = grouped ? grp_of(W[c], J) : 1u;
         ra->wa.grp[c] = (uint8_t)G;
         ra->classes |= 1u << (slot_class(W[c]) - 1u);
         if (G == 1u) ra->wclasses |= 1u << (slot_class(W[c]) - 1u);
@@ -1587,6 +1603,8 @@ inline void* ws_base(void* ws) { return reinterpret_cast<void*>(((uintptr_t)ws +
 
 }  // namespace
 }  // namespace cr
+
+extern "C" void cr_replay_set_group_min_records(uint64_t min_records) { cr::g_grp_min_records = min_records; }
 
 extern "C" size_t cr_replay_workspace_bytes(uint64_t n, uint32_t P, uint32_t R)
 {

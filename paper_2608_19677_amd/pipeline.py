@@ -114,10 +114,11 @@ class Pipeline:
         self.NW = self.win_src.shape[0]  # counts rows the plans are built from
         # Group dispatch tables (one row per request for all candidates) need every
         # candidate of a group to plan from the same window; by default they are used for
-        # several candidates when they fit the budget.
+        # groups of at least 8 candidates (rows are padded to a multiple of 8) when they fit
+        # the budget.
         shared = all(len(set(window[g])) == 1 for g in range(NG))
         if group_tables is None:
-            group_tables = (P > 1 and shared and dispatch == "static" and
+            group_tables = (P >= 8 and shared and dispatch == "static" and
                             B.group_table_bytes(NG, P, R, self.max_W, K, self.NW) <= self.GROUP_TABLE_BUDGET)
         elif group_tables and not shared:
             raise ValueError("group dispatch tables need every candidate of a group to share its window")

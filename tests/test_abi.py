@@ -51,6 +51,9 @@ def test_host_only_queries(lib_path):
     r = binding.cr_replay_workspace_bytes(10**6, 2, 30)
     assert r >= 2 * 10**6 * 8
     assert binding.cr_replay_workspace_bytes(0, 1, 1) > 0
+    # the grouped-replay size rule is host state only: setting and restoring it launches nothing
+    binding.cr_replay_set_group_min_records(0)
+    binding.cr_replay_set_group_min_records(binding.GROUP_MIN_RECORDS_DEFAULT)
 
 
 def test_struct_layouts_match_header(lib_path):

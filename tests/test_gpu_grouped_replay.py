@@ -1,8 +1,9 @@
 """GPU parity of the replay that keeps several small lists per wavefront (k_replay_grp).
 
-Calls with one interval replay every candidate with W <= 16 slots by k_replay_grp: lane
-groups of 8 lanes (W <= 8) or 16 lanes (W <= 16), one segment each, with the initial state
-rebuilt forward. The cases cover W from 1 to 16 next to larger lists in the same call, one
+Calls with one interval replay their candidates with W <= 16 slots by k_replay_grp (lane
+groups of 8 lanes for W <= 8, 16 lanes for W <= 16, one segment each, initial state rebuilt
+forward) once n times their number reaches a size threshold; these cases lower the
+threshold to 0 so that they take that path, and restore it afterwards. The cases cover W from 1 to 16 next to larger lists in the same call, one
 key and one destination, streams of many segments, streams with fewer distinct keys than W
 (segments out of rebuild budget, replayed by the sequential pass), carried cache state
 between chunks, out-of-range keys, and 1,024 destinations."""
@@ -18,6 +19,13 @@ from paper_2608_19677_amd import binding as B
 from cr_check import compare_all, say
 
 pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def grouped_everywhere():
+    B.cr_replay_set_group_min_records(0)
+    yield
+    B.cr_replay_set_group_min_records(B.GROUP_MIN_RECORDS_DEFAULT)
 
 CASES = [
     # seed, K, n, R, Ws, hot, hot_share, qs

@@ -56,7 +56,7 @@ SMALL = [
     # every register, lists filled past one register
     (15, 2000, 60_000, 5, [65, 129, 257], 4, 0, 0.0, [(1, 1)]),
     # 50 keys, one destination, 1e6 requests, every list class: no rebuild ever finds W
-    # distinct keys, so every segment from the third on runs out of its rebuild budget and
+    # distinct keys, so every segment from the ninth on runs out of its rebuild budget and
     # is replayed by its stream's sequential pass
     (16, 50, 1_000_000, 1, [60, 100, 200, 512], 5, 0, 0.0, [(1, 1)]),
     # 60 keys over three destinations: long streams, budget exhausted in most segments
