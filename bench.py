@@ -52,6 +52,8 @@ def parse():
                     help="timed steps (default: 10 for the sweep, one pass over its 1e9 requests; 20 otherwise)")
     ap.add_argument("--warmup", type=int, default=None, help="untimed steps first (default: 2 sweep, 3 otherwise)")
     ap.add_argument("--workload", default="sweep")
+    ap.add_argument("--sweep-serial", action="store_true",
+                    help="sweep: every call on one stream in order (kernels alone on the chip, for profiles)")
     ap.add_argument("--sweep-chunks", type=int, default=0,
                     help="sweep: distinct 1e8-request chunks generated and cycled through (default all ten; fewer "
                          "only shortens set-up, for example under a profiler)")
@@ -160,8 +162,10 @@ def run_sweep(args):
     candidate plans), one chunk per step through ChunkChain: count, admission for all 64
     candidates from one window sort, LPT, routing of every candidate through the group
     tables, partition and replay, with the plan taken from the previous chunk's window and
-    the cache state carried. Step s runs the inputs of chunk s mod 10 at global indices
-    s * 1e8 onwards. The chunks are generated and uploaded before timing."""
+    the cache state carried; chunk s+1's front half runs on a second HIP stream while chunk s
+    is replayed. Step s runs the inputs of chunk s mod 10 at global indices s * 1e8 onwards.
+    The chunks are generated and uploaded before timing; the timed region starts and ends
+    with the device idle, so its K steps are K whole chunks."""
     import numpy as np
     import torch
 
@@ -174,7 +178,7 @@ def run_sweep(args):
     chunks = [workload.sweep_chunk(k) for k in range(nchunks)]
     w0 = chunks[0]
     torch.cuda.set_device(0)
-    chain = ChunkChain(chunks, device="cuda:0")
+    chain = ChunkChain(chunks, device="cuda:0", overlap=not args.sweep_serial)
     for _ in range(warmup):
         chain.step()
     torch.cuda.synchronize()
@@ -226,7 +230,9 @@ def run_sweep(args):
                         "(8..512 per destination) x 8 load targets (0.8..1.2 x mean), replayed in parallel",
             "requests_per_step": n, "chunks": workload.SWEEP_CHUNKS, "keys": w0.num_keys, "destinations": R,
             "slots": sorted({c.W for c in w0.candidates}), "candidates": P, "plan_builds_per_step": P,
-            "schedule": "chunk chain, one stream", "dispatch": "static", "launch": "eager",
+            "schedule": "chunk chain, one stream" if args.sweep_serial else
+                        "chunk chain, two HIP streams (count, plans, routing, partition of chunk s+1 "
+                        "under the replay of chunk s)", "dispatch": "static", "launch": "eager",
         },
         "roofline": {"bound": d["bound"], "achieved": d["achieved"], "peak": d["peak"], "unit": d["unit"],
                      "frac": d["frac"], "traffic": sweep_traffic(), "kernel": d["kernel"]},

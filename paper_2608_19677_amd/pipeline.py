@@ -539,9 +539,17 @@ class ChunkChain:
     first window) and the replay started from chunk s-1's final cache state (empty for
     chunk 0). Every chunk must have the same length and intervals (every window's N_w is
     taken on the device, so the plan specs of the two buffer sets fit every chunk). This is
-    how the large sweep streams 1e9 requests as ten 1e8-request chunks."""
+    how the large sweep streams 1e9 requests as ten 1e8-request chunks.
 
-    def __init__(self, chunks, device="cuda"):
+    With ``overlap`` (the default) a chunk's count, plans, routing and partition run on one
+    HIP stream and its replay on a second, so that chunk s+1's front half runs while chunk s
+    is replayed. Only two orders cross the streams: the replay of chunk s waits for its
+    partition, and the partition of chunk s (which rewrites the buffer set's records and
+    clears its statistics) waits for the replay of chunk s-2 on the same set; everything
+    else a chunk reads was written earlier on its own stream. Without ``overlap`` every
+    call goes to the caller's stream in order."""
+
+    def __init__(self, chunks, device="cuda", overlap: bool = True):
         self.chunks = list(chunks)
         w0 = self.chunks[0]
         for w in self.chunks[1:]:
@@ -554,6 +562,11 @@ class ChunkChain:
         self.inputs = [upload(w, device) for w in self.chunks]
         self.sets = [Pipeline(w0, device, self.inputs[0], prev_counts=torch.empty(0), lru_in=None) for _ in range(2)]
         self.s = 0
+        self.overlap = overlap
+        if overlap:  # both at the default priority
+            self.front = torch.cuda.Stream(device=device)
+            self.back = torch.cuda.Stream(device=device)
+            self.replayed = [None, None]  # per buffer set: event after its last replay
 
     def pipe(self, s: int) -> Pipeline:
         return self.sets[s % 2]
@@ -572,20 +585,60 @@ class ChunkChain:
             p.lru_in = prev.lru_out
         return p
 
-    def step(self, timers=None, stream=None) -> Pipeline:
-        """Enqueue chunk s on the current stream; returns its buffer set. ``timers`` maps
-        stage -> list of (start, end) events."""
+    def step(self, timers=None, stream=None, on_done=None) -> Pipeline:
+        """Enqueue chunk s; returns its buffer set. ``timers`` maps stage -> list of (start,
+        end) events. ``on_done(p)`` is called with the set after its replay has been
+        enqueued, on the stream that replays it and before the set can be reused, so that
+        it may enqueue copies of the chunk's results there. With ``overlap`` the work goes
+        to the chain's own streams, after what the caller's stream has enqueued so far;
+        synchronize the device (or ``join``) before reading results on the host."""
         p = self.prepare(self.s)
-        st = stream if stream is not None else torch.cuda.current_stream()
-        for stage in Pipeline.STAGES:
+
+        def run(stage, st):
             if timers is None:
                 getattr(p, stage)()
-            else:
-                a = torch.cuda.Event(enable_timing=True)
-                b = torch.cuda.Event(enable_timing=True)
-                a.record(st)
-                getattr(p, stage)()
-                b.record(st)
-                timers.setdefault(stage, []).append((a, b))
+                return
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record(st)
+            getattr(p, stage)()
+            b.record(st)
+            timers.setdefault(stage, []).append((a, b))
+
+        if not self.overlap:
+            st = stream if stream is not None else torch.cuda.current_stream()
+            for stage in Pipeline.STAGES:
+                run(stage, st)
+            if on_done is not None:
+                on_done(p)
+        else:
+            cur = stream if stream is not None else torch.cuda.current_stream()
+            F, L = self.front, self.back
+            F.wait_stream(cur)
+            L.wait_stream(cur)
+            k = self.s % 2
+            with torch.cuda.stream(F):
+                for stage in Pipeline.STAGES[:-2]:
+                    run(stage, F)
+                if self.replayed[k] is not None:
+                    F.wait_event(self.replayed[k])  # the replay of chunk s-2 is done with the set
+                run("partition", F)
+                parted = torch.cuda.Event()
+                parted.record(F)
+            with torch.cuda.stream(L):
+                L.wait_event(parted)
+                run("lru", L)
+                if on_done is not None:
+                    on_done(p)
+                ev = torch.cuda.Event()
+                ev.record(L)
+                self.replayed[k] = ev
         self.s += 1
         return p
+
+    def join(self, stream=None):
+        """Make ``stream`` (default: the current one) wait for everything enqueued so far."""
+        if self.overlap:
+            st = stream if stream is not None else torch.cuda.current_stream()
+            st.wait_stream(self.front)
+            st.wait_stream(self.back)
