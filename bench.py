@@ -108,11 +108,12 @@ def measured_traffic(kernel: str, workload: str):
     return rec["bytes_per_launch"][kernel]
 
 
-def one_plan_build_us(wl, pipe, torch, reps=20):
+def one_plan_build_us(wl, pipe, torch, reps=20, cand=None):
     """One unbatched plan build: cr_admit + cr_place_lpt for a single plan (the first
-    interval's window, first candidate), timed with events on the current stream."""
+    interval's window; the first candidate unless `cand` is given), timed with events on the
+    current stream."""
     from paper_2608_19677_amd import binding as B
-    cand = wl.candidates[0]
+    cand = wl.candidates[0] if cand is None else cand
     n_win = int(wl.offsets[1] - wl.offsets[0])
     ps = B.PlanSet([(0, cand.W, n_win, cand.a * n_win, cand.b * wl.R)], 1, wl.R, cand.W, wl.num_keys, 1,
                    pipe.device)
@@ -252,6 +253,11 @@ def run_sweep(args):
         dst.copy_(src)
         torch.cuda.synchronize()
         out["calib_copy_bytes"] = nb
+    if not args.no_unbatched:
+        # one plan alone: the largest budget (W = 512, C = 524,288) at the mean load target
+        big = max(w0.candidates, key=lambda c: (c.W, -abs(c.a - c.b)))
+        out["us_one_plan_build"] = one_plan_build_us(w0, last, torch, cand=big)
+        out["one_plan_build"] = f"W = {big.W}, q_cap = {big.a}/{big.b} x mean, window of {w0.n:,} requests"
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = sweep_cpu_baseline(args, chunks[0])
     return out

@@ -917,18 +917,19 @@ __device__ __forceinline__ bool back_step(uint32_t (&sk)[SL], uint32_t kk, uint3
 }
 
 // Two-level list, 64 records (all valid). Every access changes the front alone until it
-// misses there, and the back changes only on those misses, so the batch runs in two
-// phases: the 64 front accesses, branch-free and unrolled like the one-register list, each
-// writing its key and the front's position-63 key into lane t of evk / evv (t = record);
-// then one back operation per front miss, in record order. The front's lane mask comes
-// from the vector unit (mtf_core_v): this list's scalar unit is the busier one. Returns
-// lane t = 1 if record t hit (in the front or the back).
+// misses there, and the back changes only on those misses (its operation takes the key and
+// the key the front pushed out of position 63). Each record's front access is branch-free;
+// a front miss then runs its back operation at once, behind a branch the whole wavefront
+// takes together, so nothing is logged per record. The keys come by scalar loads, 8 records
+// per load, and the 8 records of a load are unrolled with one copy of the back operation
+// each. The front's lane mask comes from the vector unit (mtf_core_v): this list's scalar
+// unit is the busier one. Returns lane t = 1 if record t hit (in the front or the back).
 template <int SL, bool kMasked>
 __device__ __forceinline__ uint32_t mtf_batch_two(uint32_t (&sk)[SL], const uint64_t* __restrict__ rb,
                                                   const uint64_t (&vm)[SL], uint32_t lane)
 {
-    uint32_t depth = 0xFFFFFFFFu, evk = 0u, evv = 0u;
-#pragma unroll
+    uint64_t fm = 0, bh = 0;  // records that missed the front; of those, the ones the back held
+#pragma unroll 1
     for (uint32_t g = 0; g < 8; ++g) {
         uint64_t rk[8];
 #pragma unroll
@@ -938,20 +939,16 @@ __device__ __forceinline__ uint32_t mtf_batch_two(uint32_t (&sk)[SL], const uint
             const uint32_t key = (uint32_t)rk[t];
             const uint64_t m = ballot(sk[0] == key);
             const uint32_t ev = rdlane(sk[0], 63u);
-            const uint32_t p = mtf_core_v(sk[0], m, lane);
+            mtf_core_v(sk[0], m, lane);
             sk[0] = wrlane(sk[0], key, 0u);
-            depth = wrlane(depth, p, 8u * g + t);
-            evk = wrlane(evk, key, 8u * g + t);
-            evv = wrlane(evv, ev, 8u * g + t);
+            if (m == 0) {
+                const uint64_t bit = 1ull << (8u * g + t);
+                fm |= bit;
+                if (back_step<SL, kMasked>(sk, key, ev, vm)) bh |= bit;
+            }
         }
     }
-    uint64_t rem = ballot(depth == 0xFFFFFFFFu), bh = 0;
-    while (rem) {
-        const uint32_t t = (uint32_t)__builtin_ctzll(rem);
-        rem &= rem - 1ull;
-        if (back_step<SL, kMasked>(sk, rdlane(evk, t), rdlane(evv, t), vm)) bh |= 1ull << t;
-    }
-    return (depth != 0xFFFFFFFFu || ((bh >> lane) & 1ull)) ? 1u : 0u;
+    return ((~fm | bh) >> lane) & 1ull ? 1u : 0u;
 }
 
 // 64 records (lane t of kl = key of record t, all valid) through the move-to-front list;
