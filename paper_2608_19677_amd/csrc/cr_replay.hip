@@ -22,11 +22,11 @@
 // set bit p is the hit depth, and the update shifts lanes 0..p (all lanes on a miss) up
 // by one and writes the key into lane 0, a single select between a lane and its left
 // neighbour under a scalar mask. Above 64 slots the list takes SL = ceil(W / 64)
-// registers. Up to 256 slots it is interleaved over them (position SL * lane + s in
+// registers. Up to 128 slots it is interleaved over them (position SL * lane + s in
 // register s), so that moving a position back by one is a copy from register s-1 in the
 // same lane, and only the last register wraps into register 0 of the next lane through a
 // one-lane DPP shift; an access is SL compares and SL selects under scalar masks, without
-// branches. Above 256 slots it is two-level: the 64 most recent keys in a front register
+// branches. Above 128 slots it is two-level: the 64 most recent keys in a front register
 // that every access updates like the one-register list, the rest interleaved behind it and
 // touched only when the front misses. No form needs a per-request search or reduction.
 #include "cr_common.h"
@@ -82,9 +82,10 @@ __host__ __device__ __forceinline__ uint32_t slot_class(uint32_t W)
     return sl < 1u ? 1u : (sl > 8u ? 8u : sl);
 }
 
-// Lists of 5 registers and more are two-level (a 64-key front and the rest behind it):
-// measured faster there than interleaved, and slower than interleaved with 3 back registers.
-constexpr uint32_t kTwoLevelFrom = 5;
+// Lists of 3 registers and more are two-level (a 64-key front and the rest behind it). On
+// the 1e8-request sweep: W = 156 19.8 ms two-level against 21.6 interleaved, W = 283 26.6
+// against 32.7; at W = 86 (two registers) interleaved was faster, 16.1 against 16.5 ms.
+constexpr uint32_t kTwoLevelFrom = 3;
 
 struct PartGeom {
     uint64_t tile;
@@ -449,8 +450,12 @@ __global__ __launch_bounds__(64) void k_part_scatter64(const uint32_t* __restric
 // within the wavefront's requests. Per destination, a block scan over the totals gives the
 // destination's run in the sub-tile and each wavefront's base in it; the records are staged
 // in LDS in destination order and written out run by run (about kWideSub / R consecutive
-// records per destination, against one in k_part_scatter's 1,024-request sub-tiles). The
-// grid takes candidates fastest, so the candidates of one tile read its keys together.
+// records per destination, against one in k_part_scatter's 1,024-request sub-tiles).
+// Blocks are dealt to the XCDs round-robin; block b takes candidate (b / 8) mod P of tile
+// ((b / 8) / P) * 8 + b mod 8, so that an XCD runs the P candidates of one tile together
+// and fetches the tile's keys and suffixes into its L2 once for all of them (with the
+// candidates fastest over the whole grid, each XCD held eight tiles' keys at a time, more
+// than its L2, and read them about once per candidate).
 constexpr uint32_t kWideWaves = 4;
 constexpr uint32_t kWideThreads = 64 * kWideWaves;
 constexpr uint32_t kWideSub = 1024 * kWideWaves;
@@ -469,8 +474,8 @@ inline size_t scatter_wide_lds_bytes(uint32_t R)
 
 __global__ __launch_bounds__(kWideThreads) void k_part_scatter_wide(
     const uint32_t* __restrict__ keys, const uint16_t* __restrict__ suffix, const uint16_t* __restrict__ dest,
-    uint64_t n, const uint64_t* __restrict__ off, uint32_t J, uint32_t R, uint32_t nbits, uint64_t tile,
-    uint64_t ntiles, const uint32_t* __restrict__ tcnt, const uint32_t* __restrict__ grp_off,
+    uint64_t n, const uint64_t* __restrict__ off, uint32_t J, uint32_t P, uint32_t R, uint32_t nbits,
+    uint64_t tile, uint64_t ntiles, const uint32_t* __restrict__ tcnt, const uint32_t* __restrict__ grp_off,
     uint64_t* __restrict__ rec)
 {
     issue_priority_high();
@@ -481,7 +486,8 @@ __global__ __launch_bounds__(kWideThreads) void k_part_scatter_wide(
     uint32_t* cnt = reinterpret_cast<uint32_t*>(sdst + kWideSub);  // [kWideWaves][R4] counts per wavefront, then its slot bases
     uint32_t* gbase = cnt + kWideWaves * R4;  // [R4] output position of the destination's run minus its start
     __shared__ uint32_t s_scan[16];
-    const uint32_t c = blockIdx.x, lane = lane_id(), wv = wave_in_block(), tid = threadIdx.x;
+    const uint32_t bi = blockIdx.x / kXcds;
+    const uint32_t c = bi % P, lane = lane_id(), wv = wave_in_block(), tid = threadIdx.x;
     // this wavefront's matching scratch, two areas (even and odd chunks): peer masks by
     // representative lane, and a tag byte per destination naming the representative
     const uint32_t area = 64u + (R4 + 7u) / 8u;  // 8-byte words
@@ -489,7 +495,7 @@ __global__ __launch_bounds__(kWideThreads) void k_part_scatter_wide(
     unsigned long long* pm1 = pm0 + area;
     uint8_t* tag0 = reinterpret_cast<uint8_t*>(pm0 + 64);
     uint8_t* tag1 = reinterpret_cast<uint8_t*>(pm1 + 64);
-    const uint64_t t = blockIdx.y;
+    const uint64_t t = (uint64_t)(bi / P) * kXcds + blockIdx.x % kXcds;
     if (t >= ntiles) return;
     const uint64_t t0 = t * tile, t1 = t0 + tile < n ? t0 + tile : n;
     // thread tid owns destinations 4 tid .. 4 tid + 3 in the scans: their next output positions
@@ -1683,8 +1689,8 @@ extern "C" cr_status cr_replay_partition(const uint32_t* keys, const uint16_t* s
         if (hipFuncSetAttribute((const void*)k_part_scatter_wide, hipFuncAttributeMaxDynamicSharedMemorySize,
                                 (int)lds) != hipSuccess)
             return CR_EHIP;
-        hipLaunchKernelGGL(k_part_scatter_wide, dim3(P, (uint32_t)g.ntiles), dim3(kWideThreads), lds, st, keys, suffix,
-                           dest, n, off, J, R, nbits, g.tile, g.ntiles, w.tcnt, w.grp_off, w.rec);
+        hipLaunchKernelGGL(k_part_scatter_wide, dim3(P * xcd_grid((uint32_t)g.ntiles)), dim3(kWideThreads), lds, st,
+                           keys, suffix, dest, n, off, J, P, R, nbits, g.tile, g.ntiles, w.tcnt, w.grp_off, w.rec);
     } else if (g.ntiles)
         hipLaunchKernelGGL(k_part_scatter, dim3(xcd_grid((uint32_t)g.ntiles), P), dim3(64), scatter_lds_bytes(R), st, keys,
                            suffix, dest, n, off, J, R, nbits, g.tile, g.ntiles, w.tcnt, w.grp_off, w.rec);
