@@ -42,6 +42,26 @@ struct WArg {
     uint32_t seg_min;  // shortest segment for this call's record count
 };
 
+// The candidates one k_replay launch serves and the first wavefront of each: wavefront v
+// takes work item v - wv0[i] of candidate cand[i] for wv0[i] <= v < wv0[i + 1]. Each
+// candidate gets as many wavefronts as it can have work items (one per stream plus one per
+// full segment), so a launch runs no wavefront for another list size's candidates.
+struct CandMap {
+    uint32_t n;
+    uint16_t cand[CR_MAX_CANDS];
+    uint32_t wv0[CR_MAX_CANDS + 1];
+};
+
+// Segment i of a stream of cnt records cut into nseg = ceil(cnt / S) segments (at least one):
+// records [seg_start(i), seg_start(i + 1)). Lengths differ by at most one and none exceeds
+// S, so the wavefronts of a launch run for about as long as each other (with segments of
+// exactly S, a stream's last one was its remainder, and those short wavefronts left the
+// chip part empty near each launch's end).
+__host__ __device__ __forceinline__ uint32_t seg_start(uint64_t i, uint64_t nseg, uint64_t cnt)
+{
+    return (uint32_t)(i * cnt / nseg);
+}
+
 // Segments the whole replay is cut into, a few rounds of wavefronts over the chip: a
 // wavefront's LRU chain is serial, so several per SIMD hide its latency, and beyond that
 // longer segments only save the backward rebuild of the initial state.
@@ -944,14 +964,13 @@ __device__ __forceinline__ uint32_t mtf_batch_two(uint32_t (&sk)[SL], const uint
         for (uint32_t t = 0; t < 8; ++t) {
             const uint32_t key = (uint32_t)rk[t];
             const uint64_t m = ballot(sk[0] == key);
-            const uint32_t ev = rdlane(sk[0], 63u);
-            mtf_core_v(sk[0], m, lane);
-            sk[0] = wrlane(sk[0], key, 0u);
-            if (m == 0) {
+            if (m == 0) {  // the back operation first, while front position 63 still holds the key it pushes out
                 const uint64_t bit = 1ull << (8u * g + t);
                 fm |= bit;
-                if (back_step<SL, kMasked>(sk, key, ev, vm)) bh |= bit;
+                if (back_step<SL, kMasked>(sk, key, rdlane(sk[0], 63u), vm)) bh |= bit;
             }
+            mtf_core_v(sk[0], m, lane);
+            sk[0] = wrlane(sk[0], key, 0u);
         }
     }
     return ((~fm | bh) >> lane) & 1ull ? 1u : 0u;
@@ -1025,18 +1044,29 @@ template <int SL, bool kTwo, bool kSeq>
 __global__ __launch_bounds__(kReplayThreads) void k_replay(
     const uint64_t* __restrict__ rec, uint64_t n, const uint32_t* __restrict__ grp_off,
     const uint32_t* __restrict__ item_off, uint32_t P, uint32_t R, uint32_t K, uint32_t J,
-    const uint32_t* __restrict__ prefix_len, WArg wa, uint32_t max_W, const uint32_t* __restrict__ lru_in,
-    uint32_t* __restrict__ lru_out, uint64_t* __restrict__ stats, uint32_t* __restrict__ aborted,
-    uint32_t* __restrict__ err)
+    const uint32_t* __restrict__ prefix_len, WArg wa, CandMap cm, uint32_t max_W,
+    const uint32_t* __restrict__ lru_in, uint32_t* __restrict__ lru_out, uint64_t* __restrict__ stats,
+    uint32_t* __restrict__ aborted, uint32_t* __restrict__ err)
 {
     const uint32_t lane = lane_id();
-    const uint64_t item = (uint64_t)blockIdx.x * (kReplayThreads / 64) + wave_in_block();
-    const uint32_t ncd = P * R;
-    if (item >= item_off[ncd]) return;
-    if (kSeq && !item_marked(aborted, item)) return;
-    uint32_t lo = 0;
+    const uint32_t v = blockIdx.x * (kReplayThreads / 64u) + wave_in_block();
+    if (v >= cm.wv0[cm.n]) return;
+    uint32_t ci = 0;  // the last i with wv0[i] <= v
     {
-        uint32_t hi = ncd;
+        uint32_t hi = cm.n;
+        while (hi - ci > 1) {
+            const uint32_t mid = (ci + hi) >> 1;
+            if (cm.wv0[mid] <= v) ci = mid;
+            else hi = mid;
+        }
+    }
+    const uint32_t c = cm.cand[ci];
+    const uint64_t item = (uint64_t)item_off[c * R] + (v - cm.wv0[ci]);
+    if (item >= item_off[(c + 1) * R]) return;
+    if (kSeq && !item_marked(aborted, item)) return;
+    uint32_t lo = c * R;  // the item's stream
+    {
+        uint32_t hi = (c + 1) * R;
         while (hi - lo > 1) {
             const uint32_t mid = (lo + hi) >> 1;
             if (item_off[mid] <= item) lo = mid;
@@ -1045,13 +1075,14 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
     }
     // kSeq: only the first marked segment of a run, which is never a stream's first item
     if (kSeq && (item == item_off[lo] || item_marked(aborted, item - 1))) return;
-    const uint32_t c = lo / R, d = lo % R;
+    const uint32_t d = lo - c * R;
     const uint32_t W = wa.W[c];
     if (slot_class(W) != (uint32_t)SL) return;
     if (!kSeq && wa.grp[c] > 1u) return;  // k_replay_grp's segments (its marked ones come here in kSeq)
     const uint32_t* go = grp_off + (uint64_t)c * (R + 1u);
     const uint32_t gs = go[d], cnt = go[d + 1] - gs;
     const uint32_t S = seg_len(W, wa.seg_min, wa.grp[c]);
+    const uint32_t nseg = item_off[lo + 1] - item_off[lo];
     // [s0, s1): the records this wavefront replays; [s0, sc) of them are replayed only to
     // reach the state at sc (the run's predecessor in the kSeq pass)
     uint64_t i0 = item, i1 = item + 1;
@@ -1059,12 +1090,9 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
         i0 = item - 1;
         while (i1 < item_off[lo + 1] && item_marked(aborted, i1)) ++i1;
     }
-    const uint64_t s0w = (i0 - item_off[lo]) * (uint64_t)S;
-    if (s0w > cnt) return;  // only if the partition used other slot counts
-    const uint32_t s0 = (uint32_t)s0w;
-    const uint32_t sc = kSeq ? s0 + S : s0;
-    const uint64_t s1w = (i1 - item_off[lo]) * (uint64_t)S;
-    const uint32_t s1 = s1w < cnt ? (uint32_t)s1w : cnt;
+    const uint32_t s0 = seg_start(i0 - item_off[lo], nseg, cnt);
+    const uint32_t sc = kSeq ? seg_start(item - item_off[lo], nseg, cnt) : s0;
+    const uint32_t s1 = seg_start(i1 - item_off[lo], nseg, cnt);
     const uint64_t* __restrict__ rl = rec + (uint64_t)c * n + gs;
 
     // Slot q of the rebuilt state is the q-th most recent key, which is already the
@@ -1338,11 +1366,9 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay_grp(
     const uint32_t S = seg_len(W, wa.seg_min, G);
     const uint32_t* go = grp_off + (uint64_t)c * (R + 1u);
     const uint32_t gs = live ? go[d] : 0u, cnt = live ? go[d + 1] - gs : 0u;
-    const uint64_t s0w = live ? (item - item_off[lo]) * (uint64_t)S : 0u;
-    live = live && s0w <= cnt;
-    const uint32_t s0 = live ? (uint32_t)s0w : 0u;
-    const uint64_t s1w = s0w + S;
-    const uint32_t s1 = live ? (s1w < cnt ? (uint32_t)s1w : cnt) : 0u;
+    const uint32_t nseg = live ? item_off[lo + 1] - item_off[lo] : 1u;
+    const uint32_t s0 = live ? seg_start(item - item_off[lo], nseg, cnt) : 0u;
+    const uint32_t s1 = live ? seg_start(item - item_off[lo] + 1u, nseg, cnt) : 0u;
     const uint64_t* __restrict__ rl = rec + (uint64_t)c * n + gs;
     uint32_t* __restrict__ stage = s_stage[wv] + g * kStride;
 
@@ -1558,7 +1584,6 @@ struct ReplayArgs {
     WArg wa;
     uint32_t classes;    // bit SL - 1: some candidate's list has SL registers
     uint32_t wclasses;   // the same, candidates replayed one list per wavefront only
-    uint32_t seg_short;  // the shortest segment of this call's candidates
     uint32_t groups;     // bit G: some candidate is replayed by k_replay_grp<G>
     uint64_t grp_waves;  // bound on k_replay_grp wavefronts
 };
@@ -1578,7 +1603,6 @@ inline cr_status replay_args(uint64_t n, uint32_t J, uint32_t P, uint32_t R, con
     ra->wa.seg_min = (uint32_t)(((uint64_t)n * P + kSegTarget - 1) / kSegTarget);
     ra->classes = 0;
     ra->wclasses = 0;
-    ra->seg_short = 0xFFFFFFFFu;
     ra->groups = 0;
     ra->grp_waves = 0;
     uint64_t small = 0;  // candidates k_replay_grp could take
@@ -1592,7 +1616,6 @@ inline cr_status replay_args(uint64_t n, uint32_t J, uint32_t P, uint32_t R, con
         ra->classes |= 1u << (slot_class(W[c]) - 1u);
         if (G == 1u) ra->wclasses |= 1u << (slot_class(W[c]) - 1u);
         const uint32_t S = seg_len(W[c], ra->wa.seg_min, G);
-        ra->seg_short = S < ra->seg_short ? S : ra->seg_short;
         if (G > 1u) {  // at most R + n / S work items, G per wavefront
             ra->groups |= 1u << G;
             ra->grp_waves += ((uint64_t)R + n / S) / G + 1u;
@@ -1711,21 +1734,37 @@ extern "C" cr_status cr_replay_lru(const uint32_t* prefix_len, uint32_t num_keys
         return CR_EINVAL;
     const ReplayWs w = replay_layout(ws_base(ws), n, P, R);
     const hipStream_t st = as_stream(stream);
-    // Work items: at most one per stream plus one per full segment, and no segment is shorter
-    // than seg_short, so P R + P n / seg_short bounds them (at most P R + 16,384 + 1, since
-    // seg_short >= n P / 16,384); the bitmap is sized by the looser max_items.
-    const uint64_t items = (uint64_t)P * R + (uint64_t)P * n / ra.seg_short + 1u;
-    const uint64_t blocks = (items + (kReplayThreads / 64) - 1) / (kReplayThreads / 64);
     const uint64_t gblocks = (ra.grp_waves + (kReplayThreads / 64) - 1) / (kReplayThreads / 64);
-    if (blocks > 0x7FFFFFFFull || gblocks > 0x7FFFFFFFull) return CR_EINVAL;
+    if (gblocks > 0x7FFFFFFFull) return CR_EINVAL;
+    // One k_replay launch per list size, with wavefronts for its own candidates only: a
+    // stream of cnt records has max(1, ceil(cnt / S)) work items, so a candidate has at most
+    // R + n / S of them.
+    CandMap cm;
+    auto cand_map = [&](uint32_t SL, bool seq) -> uint64_t {
+        uint64_t wv = 0;
+        cm.n = 0;
+        for (uint32_t c = 0; c < P; ++c) {
+            if (slot_class(W[c]) != SL || (!seq && ra.wa.grp[c] > 1u)) continue;
+            cm.cand[cm.n] = (uint16_t)c;
+            cm.wv0[cm.n++] = (uint32_t)wv;
+            wv += (uint64_t)R + n / seg_len(W[c], ra.wa.seg_min, ra.wa.grp[c]) + 1u;
+        }
+        cm.wv0[cm.n] = (uint32_t)wv;
+        return wv;
+    };
+    for (uint32_t SL = 1; SL <= 8; ++SL)
+        if (cand_map(SL, true) > 0x7FFFFFFFull) return CR_EINVAL;
     (void)hipGetLastError();
     hipLaunchKernelGGL(k_zero_u32, dim3(256), dim3(256), 0, st, w.aborted, w.flag_words);
 #define CR_REPLAY(SL, TWO, SEQ, NB)                                                                                 \
     hipLaunchKernelGGL((k_replay<SL, TWO, SEQ>), dim3((uint32_t)(NB)), dim3(kReplayThreads), 0, st, w.rec, n,        \
-                       w.grp_off, w.item_off, P, R, num_keys, J, prefix_len, ra.wa, max_W, lru_in, lru_out, stats,    \
-                       w.aborted, err)
-#define CR_CLASS(SL, SEQ) \
-    if ((SEQ ? ra.classes : ra.wclasses) & (1u << ((SL) - 1))) CR_REPLAY(SL, (SL) >= kTwoLevelFrom, SEQ, blocks)
+                       w.grp_off, w.item_off, P, R, num_keys, J, prefix_len, ra.wa, cm, max_W, lru_in, lru_out,       \
+                       stats, w.aborted, err)
+#define CR_CLASS(SL, SEQ)                                                                                           \
+    if ((SEQ ? ra.classes : ra.wclasses) & (1u << ((SL) - 1))) {                                                   \
+        const uint64_t nw = cand_map(SL, SEQ);                                                                      \
+        if (nw) CR_REPLAY(SL, (SL) >= kTwoLevelFrom, SEQ, (nw + (kReplayThreads / 64) - 1) / (kReplayThreads / 64)); \
+    }
     CR_CLASS(1, false); CR_CLASS(2, false); CR_CLASS(3, false); CR_CLASS(4, false);
     CR_CLASS(5, false); CR_CLASS(6, false); CR_CLASS(7, false); CR_CLASS(8, false);
     // several lists per wavefront; their marked segments join the kSeq pass of k_replay<1>
