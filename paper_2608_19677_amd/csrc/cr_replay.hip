@@ -844,15 +844,14 @@ __device__ __forceinline__ uint32_t rebuild_batch(uint32_t (&sk)[SL], const uint
 // wait states it needs after that register's last VALU write.
 __device__ __forceinline__ uint32_t il_core(uint32_t first, uint32_t last, uint64_t m, uint64_t& keep, uint32_t& l)
 {
-    uint32_t out;
-    asm("s_ff1_i32_b64 %1, %5\n\t"
+    asm("s_ff1_i32_b64 %1, %4\n\t"
         "s_lshl_b64 %2, -2, %1\n\t"
         "s_mov_b64 vcc, %2\n\t"
-        "v_cndmask_b32_dpp %0, %4, %3, vcc wave_shr:1 row_mask:0xf bank_mask:0xf"
-        : "=v"(out), "=&s"(l), "=&s"(keep)
-        : "v"(first), "v"(last), "s"(m)
+        "v_cndmask_b32_dpp %0, %3, %0, vcc wave_shr:1 row_mask:0xf bank_mask:0xf"
+        : "+v"(first), "=&s"(l), "=&s"(keep)
+        : "v"(last), "s"(m)
         : "vcc", "scc");  // s_lshl_b64 sets SCC
-    return out;
+    return first;
 }
 
 // Move-to-front access of key kk over the interleaved list (position SL lane + s in
@@ -910,10 +909,10 @@ __device__ __forceinline__ uint32_t mtf_batch_il(uint32_t (&sk)[SL], const uint6
 // key and ins the key the front pushed out (its old position 63). If kk is in the back, the
 // back positions before it move back by one; otherwise every back position does, dropping
 // the least recent key of a full list. ins takes back position 0. The interleaved move-to-
-// front of mtf_step_il over registers 1..SL-1, inserting ins instead of kk. Returns whether
-// kk was in the back.
+// front of mtf_step_il over registers 1..SL-1, inserting ins instead of kk. Returns the hit
+// mask of kk over the back (0 when kk was not there).
 template <int SL, bool kMasked>
-__device__ __forceinline__ bool back_step(uint32_t (&sk)[SL], uint32_t kk, uint32_t ins, const uint64_t (&vm)[SL])
+__device__ __forceinline__ uint64_t back_step(uint32_t (&sk)[SL], uint32_t kk, uint32_t ins, const uint64_t (&vm)[SL])
 {
     uint64_t mh[SL];
     uint64_t m = 0;
@@ -939,22 +938,22 @@ __device__ __forceinline__ bool back_step(uint32_t (&sk)[SL], uint32_t kk, uint3
             sk[s] = __builtin_amdgcn_inverse_ballot_w64(keep | before[s]) ? sk[s] : sk[s - 1];
         sk[1] = wrlane(r1, ins, 0u);
     }
-    return m != 0;
+    return m;
 }
 
 // Two-level list, 64 records (all valid). Every access changes the front alone until it
 // misses there, and the back changes only on those misses (its operation takes the key and
 // the key the front pushed out of position 63). Each record's front access is branch-free;
-// a front miss then runs its back operation at once, behind a branch the whole wavefront
-// takes together, so nothing is logged per record. The keys come by scalar loads, 8 records
+// a front miss runs its back operation first, behind a branch the whole wavefront takes
+// together, so nothing is logged per record. The keys come by scalar loads, 8 records
 // per load, and the 8 records of a load are unrolled with one copy of the back operation
-// each. The front's lane mask comes from the vector unit (mtf_core_v): this list's scalar
-// unit is the busier one. Returns lane t = 1 if record t hit (in the front or the back).
+// each. Each front miss writes its lane of a vector register with whether the back held the
+// key (one writelane). Returns lane t = 1 if record t hit (front or back).
 template <int SL, bool kMasked>
 __device__ __forceinline__ uint32_t mtf_batch_two(uint32_t (&sk)[SL], const uint64_t* __restrict__ rb,
                                                   const uint64_t (&vm)[SL], uint32_t lane)
 {
-    uint64_t fm = 0, bh = 0;  // records that missed the front; of those, the ones the back held
+    uint32_t missed = 0;  // lane t: 1 if record t was in neither part of the list
 #pragma unroll 1
     for (uint32_t g = 0; g < 8; ++g) {
         uint64_t rk[8];
@@ -965,15 +964,16 @@ __device__ __forceinline__ uint32_t mtf_batch_two(uint32_t (&sk)[SL], const uint
             const uint32_t key = (uint32_t)rk[t];
             const uint64_t m = ballot(sk[0] == key);
             if (m == 0) {  // the back operation first, while front position 63 still holds the key it pushes out
-                const uint64_t bit = 1ull << (8u * g + t);
-                fm |= bit;
-                if (back_step<SL, kMasked>(sk, key, rdlane(sk[0], 63u), vm)) bh |= bit;
+                const uint64_t mb = back_step<SL, kMasked>(sk, key, rdlane(sk[0], 63u), vm);
+                uint32_t miss;  // 1 when the back did not hold the key either, chosen by the scalar unit
+                asm("s_cmp_eq_u64 %1, 0\n\ts_cselect_b32 %0, 1, 0" : "=s"(miss) : "s"(mb) : "scc");
+                missed = wrlane(missed, miss, 8u * g + t);
             }
-            mtf_core_v(sk[0], m, lane);
+            mtf_core_v(sk[0], m, lane);  // with m = 0 every front position moves
             sk[0] = wrlane(sk[0], key, 0u);
         }
     }
-    return ((~fm | bh) >> lane) & 1ull ? 1u : 0u;
+    return missed ^ 1u;
 }
 
 // 64 records (lane t of kl = key of record t, all valid) through the move-to-front list;
@@ -1224,7 +1224,7 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
                         const uint32_t ev = rdlane(skey[0], 63u);
                         mtf_core(skey[0], m);
                         skey[0] = wrlane(skey[0], kk, 0u);
-                        if (m || back_step<SL, true>(skey, kk, ev, vm)) hit = wrlane(hit, 1u, t);
+                        if (m || back_step<SL, true>(skey, kk, ev, vm) != 0) hit = wrlane(hit, 1u, t);
                     }
                 }
                 hl = hit != 0u;
