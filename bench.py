@@ -77,6 +77,9 @@ def parse():
                          "per-stage times always come from an eager pass; studies and --opaque run eagerly)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-alone", action="store_true",
+                    help="sweep: skip timing count and routing alone after the timed steps (keeps a kernel trace "
+                         "to the steps' own launches)")
     ap.add_argument("--no-unbatched", action="store_true",
                     help="skip the single unbatched plan build (keeps a kernel trace to the step's own launches)")
     ap.add_argument("--calib-copy-mb", type=int, default=0,
@@ -230,17 +233,18 @@ def run_sweep(args):
             ts.append(a.elapsed_time(b))
         return float(np.median(ts))
 
-    if last.slice_count:
-        count_alone = alone(lambda: B.cr_count_slice(last.inp.keys, last.K, scratch, last.err, last.ws_count, None,
-                                                     n=last.n))
-    else:
-        count_alone = alone(lambda: B.cr_count_rates(last.inp.keys, last.inp.off, last.J, last.K, scratch, last.err,
-                                                     None, n=last.n))
-    for k, ms in (("count", count_alone), ("route", alone(last.route))):
-        v = kern[k]
-        v["ms_alone"] = ms
-        v["achieved_alone"] = v["work"] / (ms * 1e-3) / 1e9
-        v["frac_alone"] = v["achieved_alone"] / v["peak"]
+    if not args.no_alone:
+        if last.slice_count:
+            count_alone = alone(lambda: B.cr_count_slice(last.inp.keys, last.K, scratch, last.err, last.ws_count,
+                                                         None, n=last.n))
+        else:
+            count_alone = alone(lambda: B.cr_count_rates(last.inp.keys, last.inp.off, last.J, last.K, scratch,
+                                                         last.err, None, n=last.n))
+        for k, ms in (("count", count_alone), ("route", alone(last.route))):
+            v = kern[k]
+            v["ms_alone"] = ms
+            v["achieved_alone"] = v["work"] / (ms * 1e-3) / 1e9
+            v["frac_alone"] = v["achieved_alone"] / v["peak"]
     d = kern["lru"]
     out = {
         "metric": "requests/sec through count+route+LRU replay",
@@ -271,8 +275,10 @@ def run_sweep(args):
         "us_per_plan_build": (stage_ms["admit"] + stage_ms["place"]) * 1e3 / P,
         "stage_ms": stage_ms,
         "kernels": {k: {kk: vv for kk, vv in v.items() if kk != "work"} for k, v in kern.items()},
-        "hbm_frac": {"count": kern["count"]["frac_alone"], "route": kern["route"]["frac_alone"],
-                     "measured": "each call alone on the idle device after the timed steps"},
+        "hbm_frac": ({"count": kern["count"]["frac_alone"], "route": kern["route"]["frac_alone"],
+                      "measured": "each call alone on the idle device after the timed steps"} if not args.no_alone else
+                     {"count": kern["count"]["frac"], "route": kern["route"]["frac"],
+                      "measured": "HIP events of the timed steps"}),
         "hit_rate": {"min": float(hit.min()), "max": float(hit.max())},
     }
     if args.calib_copy_mb:
@@ -551,8 +557,7 @@ def main():
         "us_one_plan_build": one_build_us,
         "stage_ms": stage_ms,
         "kernels": {k: {kk: vv for kk, vv in v.items() if kk != "work"} for k, v in kern.items()},
-        "hbm_frac": {"count": kern["count"]["frac_alone"], "route": kern["route"]["frac_alone"],
-                     "measured": "each call alone on the idle device after the timed steps"},
+        "hbm_frac": {"count": kern["count"]["frac"], "route": kern["route"]["frac"]},
         "hit_rate": (tot[:, 1] / tot[:, 0]).tolist(),
     }
     out["config"]["plan_builds"] = n_plans
