@@ -45,7 +45,8 @@ struct WArg {
 // The candidates one k_replay launch serves and the first wavefront of each: wavefront v
 // takes work item v - wv0[i] of candidate cand[i] for wv0[i] <= v < wv0[i + 1]. Each
 // candidate gets as many wavefronts as it can have work items (one per stream plus one per
-// full segment), so a launch runs no wavefront for another list size's candidates.
+// full segment), so a launch runs no wavefront for another list size's candidates. n = 0
+// when the launch serves every candidate of the call: wavefront v then takes work item v.
 struct CandMap {
     uint32_t n;
     uint16_t cand[CR_MAX_CANDS];
@@ -53,13 +54,17 @@ struct CandMap {
 };
 
 // Segment i of a stream of cnt records cut into nseg = ceil(cnt / S) segments (at least one):
-// records [seg_start(i), seg_start(i + 1)). Lengths differ by at most one and none exceeds
-// S, so the wavefronts of a launch run for about as long as each other (with segments of
-// exactly S, a stream's last one was its remainder, and those short wavefronts left the
-// chip part empty near each launch's end).
-__host__ __device__ __forceinline__ uint32_t seg_start(uint64_t i, uint64_t nseg, uint64_t cnt)
+// records [seg_start(i), seg_start(i + 1)). The stream's ceil(cnt / 64) batches of 64 records
+// are dealt evenly, so segments differ by at most one batch and only the last one ends in a
+// partial batch (the replay takes a full batch in one unrolled pass, a partial one record by
+// record); the wavefronts of a launch thus run for about as long as each other (with
+// segments of exactly S, a stream's last one was its remainder, and those short wavefronts
+// left the chip part empty near each launch's end). One 32-bit division per bound.
+__host__ __device__ __forceinline__ uint32_t seg_start(uint32_t i, uint32_t nseg, uint32_t cnt)
 {
-    return (uint32_t)(i * cnt / nseg);
+    const uint32_t nb = (cnt + 63u) / 64u, L = nb / nseg, r = nb - L * nseg;
+    const uint32_t b = i * L + (i < r ? i : r);
+    return b < nb ? 64u * b : cnt;
 }
 
 // Segments the whole replay is cut into, a few rounds of wavefronts over the chip: a
@@ -1050,29 +1055,37 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
 {
     const uint32_t lane = lane_id();
     const uint32_t v = blockIdx.x * (kReplayThreads / 64u) + wave_in_block();
-    if (v >= cm.wv0[cm.n]) return;
-    uint32_t ci = 0;  // the last i with wv0[i] <= v
-    {
-        uint32_t hi = cm.n;
-        while (hi - ci > 1) {
-            const uint32_t mid = (ci + hi) >> 1;
-            if (cm.wv0[mid] <= v) ci = mid;
-            else hi = mid;
+    uint64_t item;
+    uint32_t lo, hi;  // the item's stream is searched for in [lo, hi)
+    if (cm.n == 0) {  // every candidate of the call: wavefront v takes work item v
+        item = v;
+        if (item >= item_off[P * R]) return;
+        lo = 0;
+        hi = P * R;
+    } else {
+        if (v >= cm.wv0[cm.n]) return;
+        uint32_t ci = 0;  // the last i with wv0[i] <= v
+        {
+            uint32_t h = cm.n;
+            while (h - ci > 1) {
+                const uint32_t mid = (ci + h) >> 1;
+                if (cm.wv0[mid] <= v) ci = mid;
+                else h = mid;
+            }
         }
+        const uint32_t cc = cm.cand[ci];
+        item = (uint64_t)item_off[cc * R] + (v - cm.wv0[ci]);
+        if (item >= item_off[(cc + 1) * R]) return;
+        lo = cc * R;
+        hi = (cc + 1) * R;
     }
-    const uint32_t c = cm.cand[ci];
-    const uint64_t item = (uint64_t)item_off[c * R] + (v - cm.wv0[ci]);
-    if (item >= item_off[(c + 1) * R]) return;
     if (kSeq && !item_marked(aborted, item)) return;
-    uint32_t lo = c * R;  // the item's stream
-    {
-        uint32_t hi = (c + 1) * R;
-        while (hi - lo > 1) {
-            const uint32_t mid = (lo + hi) >> 1;
-            if (item_off[mid] <= item) lo = mid;
-            else hi = mid;
-        }
+    while (hi - lo > 1) {
+        const uint32_t mid = (lo + hi) >> 1;
+        if (item_off[mid] <= item) lo = mid;
+        else hi = mid;
     }
+    const uint32_t c = lo / R;
     // kSeq: only the first marked segment of a run, which is never a stream's first item
     if (kSeq && (item == item_off[lo] || item_marked(aborted, item - 1))) return;
     const uint32_t d = lo - c * R;
@@ -1090,9 +1103,9 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay(
         i0 = item - 1;
         while (i1 < item_off[lo + 1] && item_marked(aborted, i1)) ++i1;
     }
-    const uint32_t s0 = seg_start(i0 - item_off[lo], nseg, cnt);
-    const uint32_t sc = kSeq ? seg_start(item - item_off[lo], nseg, cnt) : s0;
-    const uint32_t s1 = seg_start(i1 - item_off[lo], nseg, cnt);
+    const uint32_t s0 = seg_start((uint32_t)(i0 - item_off[lo]), nseg, cnt);
+    const uint32_t sc = kSeq ? seg_start((uint32_t)(item - item_off[lo]), nseg, cnt) : s0;
+    const uint32_t s1 = seg_start((uint32_t)(i1 - item_off[lo]), nseg, cnt);
     const uint64_t* __restrict__ rl = rec + (uint64_t)c * n + gs;
 
     // Slot q of the rebuilt state is the q-th most recent key, which is already the
@@ -1367,8 +1380,8 @@ __global__ __launch_bounds__(kReplayThreads) void k_replay_grp(
     const uint32_t* go = grp_off + (uint64_t)c * (R + 1u);
     const uint32_t gs = live ? go[d] : 0u, cnt = live ? go[d + 1] - gs : 0u;
     const uint32_t nseg = live ? item_off[lo + 1] - item_off[lo] : 1u;
-    const uint32_t s0 = live ? seg_start(item - item_off[lo], nseg, cnt) : 0u;
-    const uint32_t s1 = live ? seg_start(item - item_off[lo] + 1u, nseg, cnt) : 0u;
+    const uint32_t s0 = live ? seg_start((uint32_t)(item - item_off[lo]), nseg, cnt) : 0u;
+    const uint32_t s1 = live ? seg_start((uint32_t)(item - item_off[lo]) + 1u, nseg, cnt) : 0u;
     const uint64_t* __restrict__ rl = rec + (uint64_t)c * n + gs;
     uint32_t* __restrict__ stage = s_stage[wv] + g * kStride;
 
@@ -1750,6 +1763,7 @@ extern "C" cr_status cr_replay_lru(const uint32_t* prefix_len, uint32_t num_keys
             wv += (uint64_t)R + n / seg_len(W[c], ra.wa.seg_min, ra.wa.grp[c]) + 1u;
         }
         cm.wv0[cm.n] = (uint32_t)wv;
+        if (cm.n == P) cm.n = 0;  // every candidate, in order: work item v is wavefront v
         return wv;
     };
     for (uint32_t SL = 1; SL <= 8; ++SL)
