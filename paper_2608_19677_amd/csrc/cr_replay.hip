@@ -31,6 +31,8 @@
 // touched only when the front misses. No form needs a per-request search or reduction.
 #include "cr_common.h"
 
+#include <mutex>
+
 namespace cr {
 namespace {
 
@@ -1045,8 +1047,11 @@ __device__ __forceinline__ bool item_marked(const uint32_t* __restrict__ aborted
     return (aborted[it >> 5] >> (it & 31u)) & 1u;
 }
 
+// At most 96 scalar registers, so that eight wavefronts fit on a SIMD (the W = 512 list took
+// 104 and seven); the one- and two-register lists spill three of theirs to vector-register
+// lanes. The sweep's replay measured 117.6 -> 116.2 ms alone with the cap.
 template <int SL, bool kTwo, bool kSeq>
-__global__ __launch_bounds__(kReplayThreads) void k_replay(
+__global__ __launch_bounds__(kReplayThreads) __attribute__((amdgpu_num_sgpr(96))) void k_replay(
     const uint64_t* __restrict__ rec, uint64_t n, const uint32_t* __restrict__ grp_off,
     const uint32_t* __restrict__ item_off, uint32_t P, uint32_t R, uint32_t K, uint32_t J,
     const uint32_t* __restrict__ prefix_len, WArg wa, CandMap cm, uint32_t max_W,
@@ -1733,6 +1738,44 @@ extern "C" cr_status cr_replay_partition(const uint32_t* keys, const uint16_t* s
     return hipGetLastError() == hipSuccess ? CR_OK : CR_EHIP;
 }
 
+namespace cr {
+namespace {
+// Two side streams per device (default priority) for the list-size launches of a replay
+// call, created on a device's first call and kept until the process ends. A launch runs as
+// many wavefronts as its segments, and near its end the chip empties while its last
+// segments finish; on two streams one list size's launch fills the room another's leaves.
+// The calls that share them are serialised by a host mutex (fork, launches and join).
+#ifndef CR_REPLAY_SIDE_STREAMS
+#define CR_REPLAY_SIDE_STREAMS 1
+#endif
+constexpr int kSideDevices = 64;
+struct SideStreams {
+    bool ready = false;
+    hipStream_t s[2] = {nullptr, nullptr};
+    hipEvent_t fork = nullptr, join[2] = {nullptr, nullptr};
+};
+std::mutex g_side_mu;
+SideStreams g_side[kSideDevices];
+
+// The device's side streams, or nullptr (the launches then stay on the caller's stream).
+SideStreams* side_streams()
+{
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kSideDevices) return nullptr;
+    SideStreams& q = g_side[dev];
+    if (!q.ready) {
+        for (int i = 0; i < 2; ++i)
+            if (hipStreamCreateWithFlags(&q.s[i], hipStreamNonBlocking) != hipSuccess ||
+                hipEventCreateWithFlags(&q.join[i], hipEventDisableTiming) != hipSuccess)
+                return nullptr;
+        if (hipEventCreateWithFlags(&q.fork, hipEventDisableTiming) != hipSuccess) return nullptr;
+        q.ready = true;
+    }
+    return &q;
+}
+}  // namespace
+}  // namespace cr
+
 extern "C" cr_status cr_replay_lru(const uint32_t* prefix_len, uint32_t num_keys, uint64_t n, uint32_t J,
                                    uint32_t P, uint32_t R, const uint32_t* W, uint32_t max_W, const uint32_t* lru_in,
                                    uint32_t* lru_out, uint64_t* stats, void* ws, size_t ws_bytes, uint32_t* err,
@@ -1779,16 +1822,84 @@ extern "C" cr_status cr_replay_lru(const uint32_t* prefix_len, uint32_t num_keys
         const uint64_t nw = cand_map(SL, SEQ);                                                                      \
         if (nw) CR_REPLAY(SL, (SL) >= kTwoLevelFrom, SEQ, (nw + (kReplayThreads / 64) - 1) / (kReplayThreads / 64)); \
     }
-    CR_CLASS(1, false); CR_CLASS(2, false); CR_CLASS(3, false); CR_CLASS(4, false);
-    CR_CLASS(5, false); CR_CLASS(6, false); CR_CLASS(7, false); CR_CLASS(8, false);
-    // several lists per wavefront; their marked segments join the kSeq pass of k_replay<1>
-#define CR_GRP(G)                                                                                                   \
-    if (ra.groups & (1u << (G)))                                                                                     \
-    hipLaunchKernelGGL((k_replay_grp<G>), dim3((uint32_t)gblocks), dim3(kReplayThreads), 0, st, w.rec, n, w.grp_off, \
-                       w.item_off, w.gwave_off, P, R, num_keys, prefix_len, ra.wa, max_W, lru_in, lru_out, stats,     \
-                       w.aborted, err)
-    CR_GRP(4); CR_GRP(8);
+    // The list sizes' launches and the grouped ones are independent of each other (other
+    // candidates; the marked-segment bitmap takes atomic ORs); the kSeq passes read what all
+    // of them marked, so they follow on the caller's stream after the join. A call under
+    // stream capture keeps everything on the caller's stream.
+    uint32_t nlaunch = __builtin_popcount(ra.wclasses) + __builtin_popcount(ra.groups);
+    std::unique_lock<std::mutex> side_lock;
+    SideStreams* side = nullptr;
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    if (CR_REPLAY_SIDE_STREAMS && nlaunch >= 2 && hipStreamIsCapturing(st, &cap) == hipSuccess &&
+        cap == hipStreamCaptureStatusNone) {
+        side_lock = std::unique_lock<std::mutex>(g_side_mu);
+        side = side_streams();
+    }
+    hipStream_t lane_st[2] = {st, st};
+    if (side) {
+        if (hipEventRecord(side->fork, st) != hipSuccess || hipStreamWaitEvent(side->s[0], side->fork, 0) != hipSuccess ||
+            hipStreamWaitEvent(side->s[1], side->fork, 0) != hipSuccess)
+            return CR_EHIP;
+        lane_st[0] = side->s[0];
+        lane_st[1] = side->s[1];
+    }
+    // list sizes in order of their work (W times candidates), dealt to the two streams in turn
+    struct Launch { uint32_t kind; uint64_t work; };  // kind 1..8: k_replay<kind>; 100 + G: k_replay_grp<G>
+    Launch todo[10];
+    uint32_t nt = 0;
+    for (uint32_t SL = 1; SL <= 8; ++SL)
+        if (ra.wclasses & (1u << (SL - 1))) {
+            uint64_t wk = 0;
+            for (uint32_t c = 0; c < P; ++c)
+                if (slot_class(W[c]) == SL && ra.wa.grp[c] == 1u) wk += W[c];
+            todo[nt++] = Launch{SL, wk};
+        }
+    for (uint32_t G = 4; G <= 8; G += 4)
+        if (ra.groups & (1u << G)) {
+            uint64_t wk = 0;
+            for (uint32_t c = 0; c < P; ++c)
+                if (ra.wa.grp[c] == G) wk += 16u;  // about one 16-slot list's cost per candidate
+            todo[nt++] = Launch{100u + G, wk};
+        }
+    for (uint32_t a = 1; a < nt; ++a)  // insertion sort, heaviest first
+        for (uint32_t b = a; b > 0 && todo[b].work > todo[b - 1].work; --b) {
+            const Launch t = todo[b];
+            todo[b] = todo[b - 1];
+            todo[b - 1] = t;
+        }
+    uint64_t load[2] = {0, 0};
+    for (uint32_t t = 0; t < nt; ++t) {
+        const int li = load[1] < load[0] ? 1 : 0;  // the less loaded stream
+        load[li] += todo[t].work;
+        const hipStream_t ls = lane_st[li];
+        const uint32_t k = todo[t].kind;
+#define CR_ON(SL)                                                                                                  \
+        if (k == (SL)) {                                                                                          \
+            const uint64_t nw = cand_map(SL, false);                                                              \
+            if (nw)                                                                                               \
+                hipLaunchKernelGGL((k_replay<SL, (SL) >= kTwoLevelFrom, false>),                                  \
+                                   dim3((uint32_t)((nw + (kReplayThreads / 64) - 1) / (kReplayThreads / 64))),     \
+                                   dim3(kReplayThreads), 0, ls, w.rec, n, w.grp_off, w.item_off, P, R, num_keys, J, \
+                                   prefix_len, ra.wa, cm, max_W, lru_in, lru_out, stats, w.aborted, err);           \
+        }
+        CR_ON(1) CR_ON(2) CR_ON(3) CR_ON(4) CR_ON(5) CR_ON(6) CR_ON(7) CR_ON(8)
+#undef CR_ON
+        // several lists per wavefront; their marked segments join the kSeq pass of k_replay<1>
+#define CR_GRP(G)                                                                                                  \
+        if (k == 100u + (G))                                                                                       \
+            hipLaunchKernelGGL((k_replay_grp<G>), dim3((uint32_t)gblocks), dim3(kReplayThreads), 0, ls, w.rec, n,   \
+                               w.grp_off, w.item_off, w.gwave_off, P, R, num_keys, prefix_len, ra.wa, max_W, lru_in, \
+                               lru_out, stats, w.aborted, err);
+        CR_GRP(4) CR_GRP(8)
 #undef CR_GRP
+    }
+    if (side) {
+        for (int i = 0; i < 2; ++i)
+            if (hipEventRecord(side->join[i], side->s[i]) != hipSuccess ||
+                hipStreamWaitEvent(st, side->join[i], 0) != hipSuccess)
+                return CR_EHIP;
+        side_lock.unlock();
+    }
     CR_CLASS(1, true); CR_CLASS(2, true); CR_CLASS(3, true); CR_CLASS(4, true);
     CR_CLASS(5, true); CR_CLASS(6, true); CR_CLASS(7, true); CR_CLASS(8, true);
 #undef CR_CLASS
