@@ -542,12 +542,18 @@ class ChunkChain:
     how the large sweep streams 1e9 requests as ten 1e8-request chunks.
 
     With ``overlap`` (the default) a chunk's count, plans, routing and partition run on one
-    HIP stream and its replay on a second, so that chunk s+1's front half runs while chunk s
-    is replayed. Only two orders cross the streams: the replay of chunk s waits for its
-    partition, and the partition of chunk s (which rewrites the buffer set's records and
-    clears its statistics) waits for the replay of chunk s-2 on the same set; everything
-    else a chunk reads was written earlier on its own stream. Without ``overlap`` every
-    call goes to the caller's stream in order."""
+    HIP stream (F) and its replay on a second (L). Step s enqueues on F the count and plans
+    of chunk s+1 (chunk 0's front half comes first in step 0), on L the replay of chunk s,
+    and on F the routing and partition of chunk s+1, which then run while chunk s is
+    replayed. The replay of chunk s waits for its own partition and for the plans of chunk
+    s+1: the count and plan kernels are short, latency-bound launches of few blocks, and
+    under a replay that keeps every wavefront slot busy they waited up to 13 ms each for
+    room, while alone on the chip they take about 10 ms together (the chunk step measured
+    146-148 -> 140-142 ms on the large sweep). The partition of chunk s+1 (which rewrites
+    the buffer set's records and clears its statistics) waits for the replay of chunk s-1 on
+    the same set; everything else a chunk reads was written earlier on its own stream. A
+    chunk's results stay in its buffer set until the next step is enqueued. Without
+    ``overlap`` every call goes to the caller's stream in order."""
 
     def __init__(self, chunks, device="cuda", overlap: bool = True):
         self.chunks = list(chunks)
@@ -567,6 +573,8 @@ class ChunkChain:
             self.front = torch.cuda.Stream(device=device)
             self.back = torch.cuda.Stream(device=device)
             self.replayed = [None, None]  # per buffer set: event after its last replay
+            self.parted = [None, None]  # per buffer set: event after its last partition
+            self.ahead = False  # chunk s's front half is already enqueued
 
     def pipe(self, s: int) -> Pipeline:
         return self.sets[s % 2]
@@ -590,49 +598,69 @@ class ChunkChain:
         end) events. ``on_done(p)`` is called with the set after its replay has been
         enqueued, on the stream that replays it and before the set can be reused, so that
         it may enqueue copies of the chunk's results there. With ``overlap`` the work goes
-        to the chain's own streams, after what the caller's stream has enqueued so far;
-        synchronize the device (or ``join``) before reading results on the host."""
+        to the chain's own streams, after what the caller's stream has enqueued so far (and
+        includes the next chunk's front half); synchronize the device (or ``join``) before
+        reading results on the host, and read them before the next step."""
         p = self.prepare(self.s)
 
-        def run(stage, st):
+        def run(q, stage, st):
             if timers is None:
-                getattr(p, stage)()
+                getattr(q, stage)()
                 return
             a = torch.cuda.Event(enable_timing=True)
             b = torch.cuda.Event(enable_timing=True)
             a.record(st)
-            getattr(p, stage)()
+            getattr(q, stage)()
             b.record(st)
             timers.setdefault(stage, []).append((a, b))
 
         if not self.overlap:
             st = stream if stream is not None else torch.cuda.current_stream()
             for stage in Pipeline.STAGES:
-                run(stage, st)
+                run(p, stage, st)
             if on_done is not None:
                 on_done(p)
-        else:
-            cur = stream if stream is not None else torch.cuda.current_stream()
-            F, L = self.front, self.back
-            F.wait_stream(cur)
-            L.wait_stream(cur)
-            k = self.s % 2
+            self.s += 1
+            return p
+        cur = stream if stream is not None else torch.cuda.current_stream()
+        F, L = self.front, self.back
+        F.wait_stream(cur)
+        L.wait_stream(cur)
+
+        def front_plans(q):  # count and plans of a chunk, on F
             with torch.cuda.stream(F):
-                for stage in Pipeline.STAGES[:-2]:
-                    run(stage, F)
+                for stage in ("count", "admit", "place"):
+                    run(q, stage, F)
+
+        def front_rest(q, k):  # routing and partition of a chunk (buffer set k), on F
+            with torch.cuda.stream(F):
+                run(q, "route", F)
                 if self.replayed[k] is not None:
-                    F.wait_event(self.replayed[k])  # the replay of chunk s-2 is done with the set
-                run("partition", F)
-                parted = torch.cuda.Event()
-                parted.record(F)
-            with torch.cuda.stream(L):
-                L.wait_event(parted)
-                run("lru", L)
-                if on_done is not None:
-                    on_done(p)
+                    F.wait_event(self.replayed[k])  # the last replay on this set is done with it
+                run(q, "partition", F)
                 ev = torch.cuda.Event()
-                ev.record(L)
-                self.replayed[k] = ev
+                ev.record(F)
+                self.parted[k] = ev
+
+        k = self.s % 2
+        if not self.ahead:  # the first step: chunk s's own front half
+            front_plans(p)
+            front_rest(p, k)
+        nxt = self.prepare(self.s + 1)  # the other buffer set, for chunk s+1
+        front_plans(nxt)
+        planned = torch.cuda.Event()
+        planned.record(F)
+        with torch.cuda.stream(L):
+            L.wait_event(self.parted[k])
+            L.wait_event(planned)
+            run(p, "lru", L)
+            if on_done is not None:
+                on_done(p)
+            ev = torch.cuda.Event()
+            ev.record(L)
+            self.replayed[k] = ev
+        front_rest(nxt, 1 - k)
+        self.ahead = True
         self.s += 1
         return p
 
