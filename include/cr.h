@@ -10,7 +10,9 @@
  *  - Buffers are DEVICE pointers owned by the caller unless marked "host".
  *  - A call validates its scalar arguments on the host, enqueues kernels on `stream`
  *    (a hipStream_t passed as void*; NULL = the default stream) and returns. It
- *    never allocates, frees or synchronises, and keeps no state between calls.
+ *    never allocates device memory, frees or synchronises, and keeps no state between
+ *    calls, except where a call says otherwise (cr_replay_lru's side streams,
+ *    cr_admit_noalloc's scratch array, cr_replay_set_group_min_records).
  *    Calls are thread-compatible: concurrent calls must not share output buffers.
  *  - Return value: CR_OK, or a negative cr_status. On a negative status nothing
  *    has been enqueued.
@@ -321,7 +323,15 @@ cr_status cr_replay_partition(const uint32_t* keys, const uint16_t* suffix, cons
  * W distinct keys) is left to a second launch, in which one wavefront per run of such
  * segments replays the segment before the run (without counting it) and then the run, in
  * order. Each request is thus replayed at most twice and scanned at most nine times,
- * whatever the key mix; the results do not depend on which launch counts them. */
+ * whatever the key mix; the results do not depend on which launch counts them.
+ * The launches of the first pass (one per list size, ceil(W/64) registers, and one per
+ * grouped form) are independent of each other. When there are two or more and `stream`
+ * is not capturing, they run on two side streams of the device, forked from `stream`
+ * by an event and joined back to it before the second launch: the side streams and
+ * their three events are created by the first such call on a device (hipStreamCreate,
+ * default priority) and kept until the process ends, and calls from several host
+ * threads take a host mutex while they enqueue. Ordering on `stream` is as if every
+ * launch were on it. A failure to create them keeps the launches on `stream`. */
 cr_status cr_replay_lru(const uint32_t* prefix_len, uint32_t num_keys, uint64_t n, uint32_t J,
                         uint32_t P, uint32_t R, const uint32_t* W, uint32_t max_W,
                         const uint32_t* lru_in, uint32_t* lru_out, uint64_t* stats, void* ws,

@@ -1750,28 +1750,41 @@ namespace {
 #endif
 constexpr int kSideDevices = 64;
 struct SideStreams {
-    bool ready = false;
+    bool ready = false, failed = false;
     hipStream_t s[2] = {nullptr, nullptr};
     hipEvent_t fork = nullptr, join[2] = {nullptr, nullptr};
 };
 std::mutex g_side_mu;
 SideStreams g_side[kSideDevices];
 
-// The device's side streams, or nullptr (the launches then stay on the caller's stream).
+// The current device's side streams (caller holds g_side_mu), or nullptr: then the launches
+// stay on the caller's stream. A device whose streams or events could not all be created
+// releases what was made and is not tried again.
 SideStreams* side_streams()
 {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kSideDevices) return nullptr;
     SideStreams& q = g_side[dev];
-    if (!q.ready) {
-        for (int i = 0; i < 2; ++i)
-            if (hipStreamCreateWithFlags(&q.s[i], hipStreamNonBlocking) != hipSuccess ||
-                hipEventCreateWithFlags(&q.join[i], hipEventDisableTiming) != hipSuccess)
-                return nullptr;
-        if (hipEventCreateWithFlags(&q.fork, hipEventDisableTiming) != hipSuccess) return nullptr;
-        q.ready = true;
+    if (!q.ready && !q.failed) {
+        bool ok = hipEventCreateWithFlags(&q.fork, hipEventDisableTiming) == hipSuccess;
+        for (int i = 0; i < 2 && ok; ++i)
+            ok = hipStreamCreateWithFlags(&q.s[i], hipStreamNonBlocking) == hipSuccess &&
+                 hipEventCreateWithFlags(&q.join[i], hipEventDisableTiming) == hipSuccess;
+        if (!ok) {
+            for (int i = 0; i < 2; ++i) {
+                if (q.join[i]) (void)hipEventDestroy(q.join[i]);
+                if (q.s[i]) (void)hipStreamDestroy(q.s[i]);
+                q.join[i] = nullptr;
+                q.s[i] = nullptr;
+            }
+            if (q.fork) (void)hipEventDestroy(q.fork);
+            q.fork = nullptr;
+            (void)hipGetLastError();
+            q.failed = true;
+        }
+        q.ready = ok;
     }
-    return &q;
+    return q.ready ? &q : nullptr;
 }
 }  // namespace
 }  // namespace cr
