@@ -14,8 +14,9 @@
  *    calls, except where a call says otherwise (cr_replay_lru's side streams,
  *    cr_admit_noalloc's scratch array, cr_replay_set_group_min_records).
  *    Calls are thread-compatible: concurrent calls must not share output buffers.
- *  - Return value: CR_OK, or a negative cr_status. On a negative status nothing
- *    has been enqueued.
+ *  - Return value: CR_OK, or a negative cr_status. On CR_EINVAL or CR_ESIZE nothing
+ *    has been enqueued; CR_EHIP reports a failed HIP call, and launches of the same
+ *    call made before it may have been enqueued.
  *  - Data-dependent problems found on the device (a key >= num_keys, a destination
  *    >= R, an inconsistent plan spec) never abort a kernel: the offending item is
  *    skipped as documented per call, and a CR_ERR_* bit is OR-ed into the caller's

@@ -1856,7 +1856,12 @@ extern "C" cr_status cr_replay_lru(const uint32_t* prefix_len, uint32_t num_keys
         lane_st[0] = side->s[0];
         lane_st[1] = side->s[1];
     }
-    // list sizes in order of their work (W times candidates), dealt to the two streams in turn
+    // Launches in order of their work, each onto the stream with less work so far. A
+    // launch's work is its candidates times a cost per candidate and request by list form,
+    // in hundredths of the one-register list's (as measured alone on the 1e8-request sweep:
+    // 0.98, 1.96, 2.2, 2.8 and 3.75 ms per candidate for 1, 2, 3, 5 and 8 registers, 0.55 and
+    // 0.75 for the lists of 8 and 16 slots replayed 8 and 4 per wavefront).
+    static constexpr uint32_t kCost[9] = {0u, 100u, 200u, 225u, 255u, 285u, 320u, 350u, 385u};
     struct Launch { uint32_t kind; uint64_t work; };  // kind 1..8: k_replay<kind>; 100 + G: k_replay_grp<G>
     Launch todo[10];
     uint32_t nt = 0;
@@ -1864,14 +1869,14 @@ extern "C" cr_status cr_replay_lru(const uint32_t* prefix_len, uint32_t num_keys
         if (ra.wclasses & (1u << (SL - 1))) {
             uint64_t wk = 0;
             for (uint32_t c = 0; c < P; ++c)
-                if (slot_class(W[c]) == SL && ra.wa.grp[c] == 1u) wk += W[c];
+                if (slot_class(W[c]) == SL && ra.wa.grp[c] == 1u) wk += kCost[SL];
             todo[nt++] = Launch{SL, wk};
         }
     for (uint32_t G = 4; G <= 8; G += 4)
         if (ra.groups & (1u << G)) {
             uint64_t wk = 0;
             for (uint32_t c = 0; c < P; ++c)
-                if (ra.wa.grp[c] == G) wk += 16u;  // about one 16-slot list's cost per candidate
+                if (ra.wa.grp[c] == G) wk += G == 8u ? 56u : 77u;
             todo[nt++] = Launch{100u + G, wk};
         }
     for (uint32_t a = 1; a < nt; ++a)  // insertion sort, heaviest first
