@@ -245,6 +245,8 @@ def run_sweep(args):
             v["ms_alone"] = ms
             v["achieved_alone"] = v["work"] / (ms * 1e-3) / 1e9
             v["frac_alone"] = v["achieved_alone"] / v["peak"]
+        err = int(last.err.cpu().numpy().view(np.uint32)[0])
+        assert err == 0, f"device error word {err:#x} after the calls alone"
     d = kern["lru"]
     out = {
         "metric": "requests/sec through count+route+LRU replay",
