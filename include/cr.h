@@ -332,7 +332,10 @@ cr_status cr_replay_partition(const uint32_t* keys, const uint16_t* suffix, cons
  * their three events are created by the first such call on a device (hipStreamCreate,
  * default priority) and kept until the process ends, and calls from several host
  * threads take a host mutex while they enqueue. Ordering on `stream` is as if every
- * launch were on it. A failure to create them keeps the launches on `stream`. */
+ * launch were on it. A failure to create them keeps the launches on `stream`. The HIP
+ * runtime maps streams onto a few hardware queues (four per process by default); when
+ * the process already holds streams of its own, both side streams can land on one
+ * queue, and the launches then run one after another. */
 cr_status cr_replay_lru(const uint32_t* prefix_len, uint32_t num_keys, uint64_t n, uint32_t J,
                         uint32_t P, uint32_t R, const uint32_t* W, uint32_t max_W,
                         const uint32_t* lru_in, uint32_t* lru_out, uint64_t* stats, void* ws,
