@@ -82,6 +82,9 @@ def parse():
                          "to the steps' own launches)")
     ap.add_argument("--no-unbatched", action="store_true",
                     help="skip the single unbatched plan build (keeps a kernel trace to the step's own launches)")
+    ap.add_argument("--copy-ceiling", action="store_true",
+                    help="time plain device-to-device copies that move the count's and routing's "
+                         "algorithmic bytes at the 70B-like and sweep sizes, print one JSON line and exit")
     ap.add_argument("--calib-copy-mb", type=int, default=0,
                     help="after timing, copy this many MiB device-to-device once (a plain copy kernel of known "
                          "size, to scale the FETCH_SIZE / WRITE_SIZE counters)")
@@ -350,12 +353,50 @@ def sweep_cpu_baseline(args, w0):
                       + ", ".join(f"{k} {v:.2f}" for k, v in tm.items() if k in ("count", "plan", "route", "replay"))}
 
 
+def copy_ceiling():
+    """Plain device-to-device copies (the runtime's copy kernel behind torch's copy_) that move
+    as many bytes as the count and routing kernels' algorithmic traffic at the sizes they run
+    at: half read, half written. What a copy of that size reaches is a practical ceiling for
+    an HBM-bound kernel moving the same bytes in one launch."""
+    import numpy as np
+    import torch
+    torch.cuda.set_device(0)
+    cases = [("count, 70B-like: 1e7 requests x 4 B", 40e6), ("route, 70B-like: 1e7 x (4 + 2) B", 60e6),
+             ("count, sweep chunk: 1e8 x 4 B", 4e8), ("route, sweep chunk: 1e8 x (4 + 2 x 64) B", 13.2e9)]
+    out = []
+    for name, moved in cases:
+        nb = int(moved) // 2
+        src = torch.empty(nb, dtype=torch.uint8, device="cuda:0")
+        src.fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(20 if moved < 1e9 else 5):
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record()
+            dst.copy_(src)
+            b.record()
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b))
+        ms = float(np.median(ts))
+        out.append({"case": name, "bytes_moved": 2 * nb, "us_events": ms * 1e3,
+                    "frac_of_8TB_s": 2 * nb / (ms * 1e-3) / (HBM_PEAK_GBS * 1e9)})
+        del src, dst
+    return {"copy_ceiling": out, "peak_GB_s": HBM_PEAK_GBS}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
         print(json.dumps({"error": "one GPU only: the path runs on a single MI355X and has no multi-GPU "
                                    "sharding", "n_gpus": args.gpus}), flush=True)
         sys.exit(2)
+    if args.copy_ceiling:
+        print(json.dumps(copy_ceiling()), flush=True)
+        return
     if args.workload == "sweep":
         from paper_2608_19677_amd import build as hip_build
         if not os.path.exists(hip_build.LIB):
